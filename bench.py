@@ -1,0 +1,277 @@
+"""Decode-attention benchmark on one MI355X.
+
+A step is one pass of the whole decode hot path over one batch: the
+reference estimate, the gated split-KV scan of every level, and the additive
+combine.  The default workload is the Llama-3-8B-shaped GQA decode (batch 16,
+32 query / 8 kv heads, head dim 128, 8192 cached keys per request, paged BF16
+cache of 16-key pages).  Inputs are synthetic, seeded and resident in HBM
+before timing.  Before every timed step a 1 GiB buffer is written so that no
+cache (4 MB L2 per XCD, 256 MB MALL) holds any of the step's data; each step
+is bracketed by HIP events on the stream the kernels are launched on.
+
+Prints ONE JSON line (rank 0).  ``--all`` adds one JSON line per workload and
+depth on stderr (used for the design notes' tables).
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "decode-attn us/call + achieved HBM GB/s (% of peak) at T=16 and T=inf"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--all", action="store_true", help="also time workloads 1-5 (stderr)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    return ap.parse_args()
+
+
+class Path:
+    """The decode path of one workload, bound to preallocated device buffers."""
+
+    def __init__(self, wl, F, torch):
+        self.wl, self.F, self.torch = wl, F, torch
+        dev = wl.q.device
+        self.levels = [F.kv_view(wl.k, wl.v, lv.seq_lens, num_kv_heads=wl.num_kv_heads,
+                                 max_seq_len=lv.max_seq_len, block_table=lv.block_table,
+                                 row_indptr=lv.row_indptr, row_req=lv.row_req,
+                                 max_reqs_per_seq=lv.max_reqs_per_seq) for lv in wl.levels]
+        self.flat = F.kv_view(wl.k, None, wl.flat.seq_lens, num_kv_heads=wl.num_kv_heads,
+                              max_seq_len=wl.flat.max_seq_len, block_table=wl.flat.block_table)
+        self.qv = F.q_view(wl.q)
+        b, h, d = wl.q.shape
+        self.splits = list(wl.level_splits)
+        total = sum(self.splits)
+        self.z = torch.empty(b, h, dtype=torch.float32, device=dev)
+        self.part_A = torch.empty(total, b, h, d, dtype=torch.float32, device=dev)
+        self.part_L = torch.empty(total, b, h, dtype=torch.float32, device=dev)
+        self.out = torch.empty(b, h, d, dtype=torch.float32, device=dev)
+
+    def estimate(self, stream):
+        self.F.fold_ref_estimate(self.flat, self.qv, self.wl.sm_scale, self.z, stream=stream)
+
+    def decode(self, T, stream):
+        off = 0
+        for kv, s in zip(self.levels, self.splits):
+            self.F.fold_decode_split(kv, self.qv, self.wl.sm_scale, self.z, T, s, off,
+                                     self.part_A, self.part_L, stream=stream)
+            off += s
+
+    def combine(self, stream):
+        self.F.fold_combine(self.part_A, self.part_L, self.out, stream=stream)
+
+    def read_fraction(self, T):
+        """Fraction of (kv seq, kv head, key) value rows the scan reads at depth T
+        (from the kernel's own read-gate export; untimed)."""
+        torch, F = self.torch, self.F
+        if math.isinf(T):
+            return 1.0
+        dev = self.wl.q.device
+        read = total = 0
+        off = 0
+        b, h, d = self.wl.q.shape
+        for lv, kv, s in zip(self.wl.levels, self.levels, self.splits):
+            rg = F.fold_decode_row_groups(kv, self.qv)
+            kg = torch.zeros(lv.num_seqs, self.wl.num_kv_heads, rg, lv.max_seq_len,
+                             dtype=torch.uint8, device=dev)
+            F.fold_decode_split(kv, self.qv, self.wl.sm_scale, self.z, T, s, off, self.part_A,
+                                self.part_L, key_gate_out=kg)
+            off += s
+            read += int(kg.sum().item())
+            total += sum(lv.seq_lens_host) * self.wl.num_kv_heads * rg
+        return read / max(total, 1)
+
+
+def kv_bytes(wl, lam):
+    """Algorithmic bytes of one decode scan (all levels): every key row, the
+    value rows the read gates keep (fraction lam of read-group key rows), the
+    query rows, references, block-table entries and partials written."""
+    d = wl.head_dim
+    b, h, _ = wl.q.shape
+    keys = sum(sum(lv.seq_lens_host) for lv in wl.levels) * wl.num_kv_heads
+    total = keys * 2 * d + lam * keys * 2 * d
+    total += 2 * b * h * d + 4 * b * h
+    if wl.page_size:
+        total += 4 * sum(sum((n + wl.page_size - 1) // wl.page_size for n in lv.seq_lens_host)
+                         for lv in wl.levels)
+    total += 4 * sum(wl.level_splits) * b * h * (d + 1)
+    return total, keys
+
+
+def time_variant(path, T, steps, warmup, flush, torch):
+    """Median per-kernel and per-step durations (ms) with a cache flush before
+    every step; events are recorded on the launch stream."""
+    stream = torch.cuda.current_stream()
+    res = {"est": [], "dec": [], "comb": [], "step": []}
+    for it in range(warmup + steps):
+        flush.fill_(it & 0xff)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record(stream)
+        path.estimate(stream)
+        ev[1].record(stream)
+        path.decode(T, stream)
+        ev[2].record(stream)
+        path.combine(stream)
+        ev[3].record(stream)
+        if it >= warmup:
+            ev[3].synchronize()
+            res["est"].append(ev[0].elapsed_time(ev[1]))
+            res["dec"].append(ev[1].elapsed_time(ev[2]))
+            res["comb"].append(ev[2].elapsed_time(ev[3]))
+            res["step"].append(ev[0].elapsed_time(ev[3]))
+    torch.cuda.synchronize()
+    return {k: statistics.median(v) for k, v in res.items()}, res
+
+
+def cpu_baseline(wl, budget_s):
+    """The FP64 oracle timed on this host on a bounded sample of the workload's
+    (kv sequence, kv head) chunks; scaled to one whole call."""
+    import numpy as np
+
+    import oracle
+    from workloads import host_bits
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    cores = len(os.sched_getaffinity(0))
+    q_bits, k_bits, v_bits = host_bits(wl.q), host_bits(wl.k), host_bits(wl.v)
+    lv = wl.levels[0]
+    bt = None if lv.block_table is None else lv.block_table.cpu().numpy()
+    z = np.zeros((wl.batch, wl.num_heads))
+    chunks_all = [(s, g) for s in range(lv.num_seqs) for g in range(wl.num_kv_heads)]
+    done = 0
+    t0 = time.perf_counter()
+    for c in chunks_all:
+        oracle.decode_level(q_bits, k_bits, v_bits, num_kv_heads=wl.num_kv_heads,
+                            page_size=wl.page_size, sm_scale=wl.sm_scale,
+                            seq_lens=lv.seq_lens_host, block_table=bt, z=z, T=math.inf,
+                            num_splits=wl.level_splits[0], chunks=[c])
+        done += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    per_call_s = dt * len(chunks_all) / done
+    keys = sum(lv.seq_lens_host) * wl.num_kv_heads
+    return {"value": per_call_s * 1e6, "unit": "us/call", "cores": threads,
+            "host_cores_visible": cores, "kind": "oracle",
+            "keys_per_s": keys / per_call_s,
+            "sample": f"FP64 oracle decode (T=inf) of {done} of {len(chunks_all)} "
+                      f"(request, kv head) chunks in {dt:.1f} s, scaled to the whole call"}
+
+
+def run_workload(i, args, torch, F, make_config, flush, steps, warmup):
+    wl = make_config(i, device="cuda")
+    path = Path(wl, F, torch)
+    stream = torch.cuda.current_stream()
+    path.estimate(stream)
+    out = {}
+    for T in (math.inf, 16.0) + ((24.0, 12.0) if i == 3 else ()):
+        lam = path.read_fraction(T)
+        med, _ = time_variant(path, T, steps, warmup, flush, torch)
+        nbytes, keys = kv_bytes(wl, lam)
+        out[T] = {"med": med, "lam": lam, "bytes": nbytes, "keys": keys}
+    return wl, out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the decode path has no multi-GPU leg in this build)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2609_33410_amd as F
+    from workloads import CONFIG_NAMES, make_config
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    F.load_library()
+    flush = torch.empty(1 << 28, dtype=torch.int32, device="cuda")  # 1 GiB
+
+    wall0 = time.perf_counter()
+    wl, res = run_workload(args.config, args, torch, F, make_config, flush, args.steps,
+                           args.warmup)
+    wall = time.perf_counter() - wall0
+    dense, t16 = res[math.inf], res[16.0]
+    dec_ms = dense["med"]["dec"]
+    achieved = dense["bytes"] / (dec_ms * 1e-3) / 1e9
+    step_ms = dense["med"]["step"]
+    line = {
+        "metric": METRIC,
+        "value": round(step_ms * 1e3, 2),
+        "unit": "us/call",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": CONFIG_NAMES[args.config], "batch": wl.batch,
+                   "q_heads": wl.num_heads, "kv_heads": wl.num_kv_heads,
+                   "head_dim": wl.head_dim, "keys_per_request": wl.flat.seq_lens_host[0],
+                   "page_size": wl.page_size, "splits": wl.level_splits,
+                   "step": "estimate + split scan + combine, T=inf",
+                   "timing": "median of per-step HIP events, 1 GiB cache flush before each step"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": None, "kernel": "decode_split_kernel",
+                     "algorithmic_bytes_per_launch": int(dense["bytes"]),
+                     "avg_launch_us": round(dec_ms * 1e3, 2)},
+        "breakdown_us": {"T=inf": {k: round(v * 1e3, 2) for k, v in dense["med"].items()},
+                         "T=16": {k: round(v * 1e3, 2) for k, v in t16["med"].items()}},
+        "t16_us_per_call": round(t16["med"]["step"] * 1e3, 2),
+        "t16_decode_gbps": round(t16["bytes"] / (t16["med"]["dec"] * 1e-3) / 1e9, 1),
+        "t16_value_read_fraction": round(t16["lam"], 5),
+        "t16_speedup_decode": round(dense["med"]["dec"] / t16["med"]["dec"], 3),
+        "keys_per_s": round(dense["keys"] / (step_ms * 1e-3), 1),
+        "wall_s": round(wall, 2),
+    }
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+    if args.all:
+        for i in (1, 2, 3, 4, 5):
+            wl_i, r = run_workload(i, args, torch, F, make_config, flush, args.steps,
+                                   args.warmup)
+            for T, v in r.items():
+                rec = {"workload": CONFIG_NAMES[i], "T": "inf" if math.isinf(T) else T,
+                       "us_per_call": round(v["med"]["step"] * 1e3, 2),
+                       "decode_us": round(v["med"]["dec"] * 1e3, 2),
+                       "estimate_us": round(v["med"]["est"] * 1e3, 2),
+                       "combine_us": round(v["med"]["comb"] * 1e3, 2),
+                       "decode_bytes": int(v["bytes"]),
+                       "decode_gbps": round(v["bytes"] / (v["med"]["dec"] * 1e-3) / 1e9, 1),
+                       "value_read_fraction": round(v["lam"], 5),
+                       "keys_per_s": round(v["keys"] / (v["med"]["step"] * 1e-3), 1)}
+                print(json.dumps(rec), file=sys.stderr, flush=True)
+            del wl_i
+            torch.cuda.empty_cache()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,197 @@
+/*
+ * fold.h - C ABI of the FoldAttention decode hot path for MI355X (gfx950).
+ *
+ * Declared-reference softmax attention over a BF16 KV cache (FoldAttention,
+ * arXiv 2609.33410).  For query row i a finite reference Z_i is fixed before
+ * any key is read (Section 3, Eq. fold).  Every weight 2^(s_ij - Z_i) is then
+ * final when computed, so a scan over any key subset yields an FP32 pair
+ *     A_i = sum_{live j} 2^(s_ij - Z_i) v_j,   L_i = sum_{j} 2^(s_ij - Z_i)
+ * and pairs from disjoint key ranges (split-KV slots, cascade levels) are
+ * combined by plain addition, o_i = sum A_i / sum L_i (Proposition 1; Section
+ * 4; Algorithm 1).  A per-call depth T cuts keys with s_ij - Z_i < -T from A
+ * while their weight stays in L (Section 4, "Depth as a dial").
+ *
+ * Scores are base 2: s_ij = log2(e) * sm_scale * (q_i . k_j) (Section 2),
+ * with sm_scale in natural-log units (1/sqrt(D) for standard attention).
+ *
+ * Conventions shared by every call:
+ *   - Every pointer except the view structs themselves and fold_debug is a
+ *     DEVICE pointer owned by the caller.  The library keeps no pointer after
+ *     a call returns, allocates nothing, and never synchronises: work is
+ *     enqueued on `stream` (a hipStream_t; NULL = the default stream).
+ *   - Arguments are validated on the host before anything is launched.  A
+ *     failed check returns FOLD_E_INVAL (or FOLD_E_UNSUPPORTED) and launches
+ *     nothing; fold_last_error() then returns a thread-local message.  A launch
+ *     failure returns FOLD_E_HIP.  No C++ exception crosses this boundary.
+ *   - BF16 arrays hold raw bfloat16 bit patterns; q, k and v must be 16-byte
+ *     aligned.
+ *   - Device-side bounds: a kv sequence's length is clamped to what its view
+ *     can address (max_seq_len, or max_pages_per_seq * page_size); a page id
+ *     outside [0, num_pages) and a row request outside [0, batch) are skipped
+ *     (they contribute nothing and are never dereferenced).
+ *   - Results are deterministic: no atomics; every sum has a fixed order.
+ */
+#ifndef FOLD_H
+#define FOLD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FOLD_ABI_VERSION 1
+
+typedef enum fold_status {
+  FOLD_OK = 0,
+  FOLD_E_INVAL = 1,       /* an argument failed validation; nothing launched */
+  FOLD_E_UNSUPPORTED = 2, /* a valid request this build does not implement */
+  FOLD_E_HIP = 3          /* the HIP runtime reported a launch error */
+} fold_status;
+
+typedef enum fold_dtype { FOLD_DTYPE_F32 = 0, FOLD_DTYPE_BF16 = 1 } fold_dtype;
+
+/*
+ * One scan level's view of the KV cache (Section 4: paged cache with a
+ * per-request block table; value-product paragraph: a shared prefix is one
+ * kv sequence attended by the stacked query rows of every request holding it).
+ *
+ * Paged (block_table != NULL): k and v are [num_pages][num_kv_heads]
+ *   [page_size][head_dim] bf16; key j of kv sequence s, head g, lives at page
+ *   block_table[s * max_pages_per_seq + j / page_size], slot j % page_size.
+ *   page_size must be a positive multiple of 16.
+ * Contiguous (block_table == NULL): k and v are [num_seqs][num_kv_heads]
+ *   [max_seq_len][head_dim] bf16.
+ * seq_lens [num_seqs] int32 (device): keys per kv sequence.
+ * Rows: with row_indptr == row_req == NULL, kv sequence s is attended by
+ *   request s (num_seqs <= batch).  Otherwise kv sequence s is attended by the
+ *   requests row_req[row_indptr[s] .. row_indptr[s+1]) (CSR, device arrays),
+ *   and max_reqs_per_seq bounds row_indptr[s+1] - row_indptr[s] on the host.
+ * Query head h reads kv head h / (num_heads / num_kv_heads).
+ */
+typedef struct fold_kv_view {
+  const void* k;
+  const void* v;
+  const int32_t* block_table;
+  const int32_t* seq_lens;
+  const int32_t* row_indptr;
+  const int32_t* row_req;
+  int32_t num_seqs;
+  int32_t num_kv_heads;
+  int32_t head_dim;          /* 64 or 128 */
+  int32_t page_size;         /* ignored when contiguous */
+  int32_t max_pages_per_seq; /* row stride of block_table */
+  int32_t num_pages;         /* pages in k / v (paged) */
+  int32_t max_seq_len;       /* host bound on seq_lens; contiguous row stride */
+  int32_t max_reqs_per_seq;  /* host bound for CSR rows; ignored otherwise */
+} fold_kv_view;
+
+/* Query rows: q is [batch][num_heads][head_dim] bf16; row i = r * num_heads + h. */
+typedef struct fold_q_view {
+  const void* q;
+  int32_t batch;
+  int32_t num_heads;
+} fold_q_view;
+
+/* Estimator constants (Section 3, "Choosing the reference"): the first `sink`
+ * keys and the last `recent` keys are scored exactly; the keys in between are
+ * cut into `strata` contiguous strata represented by their centres, whose
+ * weights are sorted and trimmed by `trim_lo` / `trim_hi` before their mean
+ * stands for the whole middle range.  Rows of at most sink+recent+strata keys
+ * get their exact log-sum-exp.  NULL selects {1, 63, 128, 8, 8}. */
+typedef struct fold_est_params {
+  int32_t sink;
+  int32_t recent;
+  int32_t strata;
+  int32_t trim_lo;
+  int32_t trim_hi;
+} fold_est_params;
+
+/* Optional exports of exactly the values the scan compared (not timed).
+ * x_out [batch][num_heads][max_seq_len] fp32: x_ij = s_ij - Z_i.
+ * key_gate_out [num_seqs][num_kv_heads][row_groups][max_seq_len] u8: 1 if the
+ *   value row was read (some row of the read group is live on key j).
+ * page_gate_out [num_seqs][num_kv_heads][row_groups][ceil(max_seq_len/16)] u8:
+ *   1 if any key of the 16-key page was read.
+ * row_groups = fold_decode_row_groups(kv, q).  The rows attending one
+ * (kv sequence s, kv head g) are numbered rho = c * G + (h mod G), where c is
+ * the position of the row's request in the sequence's row list (0 without CSR
+ * rows) and G = num_heads / num_kv_heads; read group u holds the rows
+ * rho in [u * R, (u + 1) * R) with R = fold_decode_rows_per_group(kv, q).
+ * Entries of read groups that hold no row are left unwritten.  Any pointer
+ * may be NULL. */
+typedef struct fold_debug {
+  float* x_out;
+  uint8_t* key_gate_out;
+  uint8_t* page_gate_out;
+} fold_debug;
+
+/* FOLD_ABI_VERSION of the built library. */
+int fold_abi_version(void);
+
+/* Static text for a status code. */
+const char* fold_status_string(fold_status s);
+
+/* Thread-local message describing the last failed call on this thread. */
+const char* fold_last_error(void);
+
+/* Rows per read group and number of read groups per (kv sequence, kv head)
+ * that fold_decode_split uses for this view (the group over which read
+ * verdicts are ORed, Section 4 "Weight-gated reads").  Returns -1 on an
+ * invalid view. */
+int32_t fold_decode_rows_per_group(const fold_kv_view* kv, const fold_q_view* q);
+int32_t fold_decode_row_groups(const fold_kv_view* kv, const fold_q_view* q);
+
+/*
+ * fold_ref_estimate - per-row finite reference Z_i (Section 3, "Choosing the
+ * reference"): a base-2 log-sum-exp estimate from the sink, the most recent
+ * keys and trimmed stratified centres, with no state carried between calls.
+ *   kv      per-request view (row_indptr must be NULL; a cascade passes its
+ *           flat prefix ++ suffix tables)
+ *   q       query rows
+ *   z_out   [batch][num_heads] fp32 (device).  Requests r >= num_seqs and
+ *           rows of empty sequences get Z = 0.
+ */
+fold_status fold_ref_estimate(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
+                              const fold_est_params* params, float* z_out, void* stream);
+
+/*
+ * fold_decode_split - gated split-KV scan of one level (Section 4; Algorithm 1).
+ * Split s of num_splits walks the 64-key tiles t with t mod num_splits == s,
+ * reads every key row, scores it against the fixed Z_i, ORs the live verdicts
+ * over the read group, reads only live value rows, and writes its FP32 pair to
+ * slot slot_offset + s:
+ *   part_A [num_slots][batch][num_heads][head_dim] fp32,
+ *   part_L [num_slots][batch][num_heads] fp32.
+ * A split with no keys writes zeros.  Only the rows this view covers are
+ * written.
+ *   z        [batch][num_heads] fp32, the declared references
+ *   depth_T  +INFINITY for dense decode, else a finite T >= 0 (NaN or negative
+ *            is FOLD_E_INVAL); a key is live for row i iff x_ij >= -T
+ *   dbg      NULL, or the optional exports above
+ */
+fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
+                              const float* z, float depth_T, int32_t num_splits,
+                              int32_t slot_offset, int32_t num_slots, float* part_A,
+                              float* part_L, const fold_debug* dbg, void* stream);
+
+/*
+ * fold_combine - additive combine (Algorithm 1, last step; Section 4): for
+ * each row, sum the slots in increasing slot order and take the quotient
+ * o = sum A / sum L.  No maximum is compared and nothing is rescaled.
+ *   part_A [num_slots][num_rows][head_dim], part_L [num_slots][num_rows] fp32
+ *   out     [num_rows][head_dim], fp32 or bf16 (round to nearest even)
+ *   z       [num_rows] fp32; needed only when lse_out is requested
+ *   lse_out [num_rows] fp32 or NULL: base-2 log-sum-exp Z + log2(sum L)
+ *   cert_out [num_rows] u8 or NULL: range certificate of Section 3,
+ *            bit0 sum L < 2^-1, bit1 sum L > 2^100, bit2 a non-finite output
+ */
+fold_status fold_combine(const float* part_A, const float* part_L, int32_t num_slots,
+                         int32_t num_rows, int32_t head_dim, const float* z, void* out,
+                         fold_dtype out_dtype, float* lse_out, uint8_t* cert_out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FOLD_H */

@@ -1,0 +1,28 @@
+"""FoldAttention decode hot path for MI355X (gfx950).
+
+The compute path is ``libfold.so`` (hand-written HIP kernels behind the C ABI
+of ``include/fold.h``); :mod:`paper_2609_33410_amd.fold` is its ctypes
+binding.  PyTorch supplies device memory and streams only.
+"""
+
+from .fold import (  # noqa: F401
+    EXPORTED,
+    FOLD_DTYPE_BF16,
+    FOLD_DTYPE_F32,
+    FOLD_E_HIP,
+    FOLD_E_INVAL,
+    FOLD_E_UNSUPPORTED,
+    FOLD_OK,
+    LIB_PATH,
+    FoldError,
+    FoldLibraryMissing,
+    fold_combine,
+    fold_decode,
+    fold_decode_row_groups,
+    fold_decode_rows_per_group,
+    fold_decode_split,
+    fold_ref_estimate,
+    kv_view,
+    load_library,
+    q_view,
+)

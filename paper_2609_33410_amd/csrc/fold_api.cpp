@@ -1,0 +1,218 @@
+// Host side of the C ABI declared in include/fold.h: argument validation and
+// kernel launches.  Nothing here allocates, synchronises or keeps a pointer.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "fold.h"
+#include "fold_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+fold_status fail(fold_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+fold_status ok() {
+  g_last_error.clear();
+  return FOLD_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+const float kLog2e = 1.4426950408889634f;
+
+// Checks shared by the calls that read the cache; fills the geometry.
+fold_status check_view(const fold_kv_view* kv, const fold_q_view* q, fold::ScanGeometry* g,
+                       bool need_v) {
+  if (!kv || !q) return fail(FOLD_E_INVAL, "kv view and q view are required");
+  if (!kv->k || (need_v && !kv->v) || !kv->seq_lens || !q->q)
+    return fail(FOLD_E_INVAL, "k%s, seq_lens and q pointers are required", need_v ? ", v" : "");
+  if (kv->head_dim != 64 && kv->head_dim != 128)
+    return fail(FOLD_E_INVAL, "head_dim %d: must be 64 or 128", kv->head_dim);
+  if (kv->num_kv_heads < 1 || q->num_heads < 1 || q->num_heads % kv->num_kv_heads != 0)
+    return fail(FOLD_E_INVAL, "num_heads %d must be a positive multiple of num_kv_heads %d",
+                q->num_heads, kv->num_kv_heads);
+  if (kv->num_seqs < 0 || q->batch < 0 || kv->max_seq_len < 0)
+    return fail(FOLD_E_INVAL, "negative size");
+  if (!aligned16(kv->k) || (need_v && !aligned16(kv->v)) || !aligned16(q->q))
+    return fail(FOLD_E_INVAL, "q, k and v must be 16-byte aligned");
+  if (kv->block_table) {
+    if (kv->page_size <= 0 || kv->page_size % fold::kChunk != 0)
+      return fail(FOLD_E_INVAL, "page_size %d: must be a positive multiple of 16", kv->page_size);
+    if (kv->max_pages_per_seq < 1 || kv->num_pages < 1)
+      return fail(FOLD_E_INVAL, "max_pages_per_seq and num_pages must be positive");
+  }
+  if ((kv->row_indptr == nullptr) != (kv->row_req == nullptr))
+    return fail(FOLD_E_INVAL, "row_indptr and row_req must both be set or both be NULL");
+  if (kv->row_indptr && kv->max_reqs_per_seq < 1)
+    return fail(FOLD_E_INVAL, "max_reqs_per_seq must be positive with CSR rows");
+  if (!kv->row_indptr && kv->num_seqs > q->batch)
+    return fail(FOLD_E_INVAL, "num_seqs %d exceeds batch %d (request s attends kv sequence s)",
+                kv->num_seqs, q->batch);
+  g->k = static_cast<const uint16_t*>(kv->k);
+  g->v = static_cast<const uint16_t*>(kv->v);
+  g->block_table = kv->block_table;
+  g->seq_lens = kv->seq_lens;
+  g->row_indptr = kv->row_indptr;
+  g->row_req = kv->row_req;
+  g->num_seqs = kv->num_seqs;
+  g->hkv = kv->num_kv_heads;
+  g->page_size = kv->block_table ? kv->page_size : 0;
+  g->max_pages = kv->block_table ? kv->max_pages_per_seq : 0;
+  g->num_pages = kv->block_table ? kv->num_pages : 0;
+  g->max_seq_len = kv->max_seq_len;
+  g->batch = q->batch;
+  g->heads = q->num_heads;
+  g->group = q->num_heads / kv->num_kv_heads;
+  return FOLD_OK;
+}
+
+int rows_per_seq(const fold_kv_view* kv, const fold_q_view* q) {
+  const int group = q->num_heads / kv->num_kv_heads;
+  const long long reqs = kv->row_indptr ? kv->max_reqs_per_seq : 1;
+  const long long rows = reqs * group;
+  return rows > (1 << 30) ? (1 << 30) : static_cast<int>(rows);
+}
+
+}  // namespace
+
+extern "C" {
+
+int fold_abi_version(void) { return FOLD_ABI_VERSION; }
+
+const char* fold_status_string(fold_status s) {
+  switch (s) {
+    case FOLD_OK: return "FOLD_OK";
+    case FOLD_E_INVAL: return "FOLD_E_INVAL: invalid argument";
+    case FOLD_E_UNSUPPORTED: return "FOLD_E_UNSUPPORTED: not supported by this build";
+    case FOLD_E_HIP: return "FOLD_E_HIP: HIP launch error";
+  }
+  return "unknown fold_status";
+}
+
+const char* fold_last_error(void) { return g_last_error.c_str(); }
+
+int32_t fold_decode_rows_per_group(const fold_kv_view* kv, const fold_q_view* q) {
+  fold::ScanGeometry g;
+  if (check_view(kv, q, &g, false) != FOLD_OK) return -1;
+  return fold::decode_rows_per_group(rows_per_seq(kv, q));
+}
+
+int32_t fold_decode_row_groups(const fold_kv_view* kv, const fold_q_view* q) {
+  fold::ScanGeometry g;
+  if (check_view(kv, q, &g, false) != FOLD_OK) return -1;
+  const int rows = rows_per_seq(kv, q);
+  const int gr = fold::decode_rows_per_group(rows);
+  return (rows + gr - 1) / gr;
+}
+
+fold_status fold_ref_estimate(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
+                              const fold_est_params* params, float* z_out, void* stream) {
+  fold::EstimateArgs a;
+  fold_status st = check_view(kv, q, &a.geo, false);
+  if (st != FOLD_OK) return st;
+  if (!z_out) return fail(FOLD_E_INVAL, "z_out is required");
+  if (kv->row_indptr) return fail(FOLD_E_INVAL, "the estimate needs a per-request view (no CSR rows)");
+  if (!isfinite(sm_scale)) return fail(FOLD_E_INVAL, "sm_scale must be finite");
+  if (a.geo.group > fold::kMaxEstRows)
+    return fail(FOLD_E_UNSUPPORTED, "GQA group %d exceeds %d", a.geo.group, fold::kMaxEstRows);
+  fold_est_params p = {1, 63, 128, 8, 8};
+  if (params) p = *params;
+  if (p.sink < 0 || p.recent < 0 || p.strata < 1 || p.trim_lo < 0 || p.trim_hi < 0 ||
+      p.trim_lo + p.trim_hi >= p.strata ||
+      static_cast<long long>(p.sink) + p.recent + p.strata > fold::kMaxEstSamples)
+    return fail(FOLD_E_INVAL, "estimator parameters out of range");
+  a.q = static_cast<const uint16_t*>(q->q);
+  a.z_out = z_out;
+  a.score_scale = kLog2e * sm_scale;
+  a.sink = p.sink;
+  a.recent = p.recent;
+  a.strata = p.strata;
+  a.trim_lo = p.trim_lo;
+  a.trim_hi = p.trim_hi;
+  if (static_cast<long long>(q->batch) * kv->num_kv_heads > 0x7fffffffLL)
+    return fail(FOLD_E_INVAL, "grid too large");
+  hipError_t e = fold::launch_estimate(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "estimate launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
+                              const float* z, float depth_T, int32_t num_splits,
+                              int32_t slot_offset, int32_t num_slots, float* part_A,
+                              float* part_L, const fold_debug* dbg, void* stream) {
+  fold::DecodeArgs a;
+  fold_status st = check_view(kv, q, &a.geo, true);
+  if (st != FOLD_OK) return st;
+  if (!z || !part_A || !part_L) return fail(FOLD_E_INVAL, "z, part_A and part_L are required");
+  if (isnan(depth_T) || depth_T < 0.0f)
+    return fail(FOLD_E_INVAL, "depth_T must be +INFINITY or a finite value >= 0");
+  if (!isfinite(sm_scale)) return fail(FOLD_E_INVAL, "sm_scale must be finite");
+  if (num_splits < 1) return fail(FOLD_E_INVAL, "num_splits must be >= 1");
+  if (slot_offset < 0 || static_cast<long long>(slot_offset) + num_splits > num_slots)
+    return fail(FOLD_E_INVAL, "slots [%d, %d) exceed num_slots %d", slot_offset,
+                slot_offset + num_splits, num_slots);
+  const int rows = rows_per_seq(kv, q);
+  const int gr = fold::decode_rows_per_group(rows);
+  const int groups = (rows + gr - 1) / gr;
+  const long long blocks = static_cast<long long>(kv->num_seqs) * kv->num_kv_heads * num_splits * groups;
+  if (blocks > 0x7fffffffLL) return fail(FOLD_E_INVAL, "grid too large");
+  a.q = static_cast<const uint16_t*>(q->q);
+  a.z = z;
+  a.part_A = part_A;
+  a.part_L = part_L;
+  a.x_out = dbg ? dbg->x_out : nullptr;
+  a.key_gate_out = dbg ? dbg->key_gate_out : nullptr;
+  a.page_gate_out = dbg ? dbg->page_gate_out : nullptr;
+  a.score_scale = kLog2e * sm_scale;
+  a.dense = isinf(depth_T) ? 1 : 0;
+  a.neg_T = a.dense ? 0.0f : -depth_T;
+  a.num_splits = num_splits;
+  a.slot_offset = slot_offset;
+  a.rows_per_seq = rows;
+  a.rows_per_group = gr;
+  a.row_groups = groups;
+  hipError_t e = fold::launch_decode(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "decode launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_combine(const float* part_A, const float* part_L, int32_t num_slots,
+                         int32_t num_rows, int32_t head_dim, const float* z, void* out,
+                         fold_dtype out_dtype, float* lse_out, uint8_t* cert_out, void* stream) {
+  if (!part_A || !part_L || !out) return fail(FOLD_E_INVAL, "part_A, part_L and out are required");
+  if (num_slots < 1 || num_rows < 0) return fail(FOLD_E_INVAL, "num_slots >= 1, num_rows >= 0");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(FOLD_E_INVAL, "head_dim %d: must be 64 or 128", head_dim);
+  if (out_dtype != FOLD_DTYPE_F32 && out_dtype != FOLD_DTYPE_BF16)
+    return fail(FOLD_E_INVAL, "unknown out_dtype");
+  if (lse_out && !z) return fail(FOLD_E_INVAL, "lse_out needs z");
+  fold::CombineArgs a;
+  a.part_A = part_A;
+  a.part_L = part_L;
+  a.z = z;
+  a.out = out;
+  a.lse_out = lse_out;
+  a.cert_out = cert_out;
+  a.num_slots = num_slots;
+  a.num_rows = num_rows;
+  a.head_dim = head_dim;
+  a.out_bf16 = out_dtype == FOLD_DTYPE_BF16 ? 1 : 0;
+  hipError_t e = fold::launch_combine(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "combine launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

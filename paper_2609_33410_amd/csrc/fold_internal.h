@@ -1,0 +1,96 @@
+// Internal launch interface between the C ABI (fold_api.cpp) and the HIP
+// kernels.  Not installed; the public contract is include/fold.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fold {
+
+// Keys per split-interleave tile and per page-gate bit (Section 4: splits
+// interleave by 64-key tiles; pages are 16 keys).
+constexpr int kTile = 64;
+constexpr int kChunk = 16;
+
+struct ScanGeometry {
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* block_table;
+  const int32_t* seq_lens;
+  const int32_t* row_indptr;
+  const int32_t* row_req;
+  int num_seqs;
+  int hkv;
+  int page_size;   // 0 => contiguous
+  int max_pages;
+  int num_pages;
+  int max_seq_len;
+  int batch;
+  int heads;
+  int group;       // heads / hkv
+};
+
+struct DecodeArgs {
+  ScanGeometry geo;
+  const uint16_t* q;
+  const float* z;
+  float* part_A;
+  float* part_L;
+  float* x_out;
+  uint8_t* key_gate_out;
+  uint8_t* page_gate_out;
+  float score_scale;  // log2(e) * sm_scale
+  float neg_T;        // -T (finite depth) ; unused when dense
+  int dense;          // T == +inf
+  int num_splits;
+  int slot_offset;
+  int rows_per_seq;   // bound on rows attending one (kv seq, kv head)
+  int rows_per_group; // rows one workgroup serves (template GR)
+  int row_groups;
+};
+
+struct EstimateArgs {
+  ScanGeometry geo;
+  const uint16_t* q;
+  float* z_out;
+  float score_scale;
+  int sink, recent, strata, trim_lo, trim_hi;
+};
+
+struct CombineArgs {
+  const float* part_A;
+  const float* part_L;
+  const float* z;
+  void* out;
+  float* lse_out;
+  uint8_t* cert_out;
+  int num_slots;
+  int num_rows;
+  int head_dim;
+  int out_bf16;
+};
+
+// Keys a kv sequence of this view can hold: max_seq_len, and for a paged view
+// also max_pages * page_size.  Device-supplied lengths are clamped to it.
+__host__ __device__ inline int view_capacity(const ScanGeometry& g) {
+  if (g.page_size > 0) {
+    const long long paged = static_cast<long long>(g.max_pages) * g.page_size;
+    return paged < g.max_seq_len ? static_cast<int>(paged) : g.max_seq_len;
+  }
+  return g.max_seq_len;
+}
+
+// Each returns hipSuccess or the launch error.
+hipError_t launch_decode(const DecodeArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_estimate(const EstimateArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
+
+// Rows per read group the decode kernel is instantiated for, given the rows
+// that attend one (kv sequence, kv head).
+int decode_rows_per_group(int rows_per_seq);
+
+// Largest estimator sample the kernel's LDS holds.
+constexpr int kMaxEstSamples = 512;
+constexpr int kMaxEstRows = 16;
+
+}  // namespace fold

@@ -1,0 +1,289 @@
+"""ctypes binding of ``libfold.so`` (the C ABI in ``include/fold.h``).
+
+Argument marshalling only: torch tensors supply device memory and
+``torch.cuda.current_stream()`` supplies the HIP stream; every step of the
+decode path runs in the library's HIP kernels.  The library must be built
+(``python -m paper_2609_33410_amd.build_lib``); without it every entry point
+raises ``FoldLibraryMissing``.  There is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfold.so")
+
+FOLD_OK, FOLD_E_INVAL, FOLD_E_UNSUPPORTED, FOLD_E_HIP = 0, 1, 2, 3
+FOLD_DTYPE_F32, FOLD_DTYPE_BF16 = 0, 1
+
+EXPORTED = (
+    "fold_abi_version",
+    "fold_status_string",
+    "fold_last_error",
+    "fold_decode_rows_per_group",
+    "fold_decode_row_groups",
+    "fold_ref_estimate",
+    "fold_decode_split",
+    "fold_combine",
+)
+
+
+class FoldLibraryMissing(RuntimeError):
+    pass
+
+
+class FoldError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+class fold_kv_view(ctypes.Structure):
+    _fields_ = [
+        ("k", ctypes.c_void_p),
+        ("v", ctypes.c_void_p),
+        ("block_table", ctypes.c_void_p),
+        ("seq_lens", ctypes.c_void_p),
+        ("row_indptr", ctypes.c_void_p),
+        ("row_req", ctypes.c_void_p),
+        ("num_seqs", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("max_pages_per_seq", ctypes.c_int32),
+        ("num_pages", ctypes.c_int32),
+        ("max_seq_len", ctypes.c_int32),
+        ("max_reqs_per_seq", ctypes.c_int32),
+    ]
+
+
+class fold_q_view(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("batch", ctypes.c_int32), ("num_heads", ctypes.c_int32)]
+
+
+class fold_est_params(ctypes.Structure):
+    _fields_ = [("sink", ctypes.c_int32), ("recent", ctypes.c_int32), ("strata", ctypes.c_int32),
+                ("trim_lo", ctypes.c_int32), ("trim_hi", ctypes.c_int32)]
+
+
+class fold_debug(ctypes.Structure):
+    _fields_ = [("x_out", ctypes.c_void_p), ("key_gate_out", ctypes.c_void_p),
+                ("page_gate_out", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the library once.  torch is imported first so that the library
+    binds to the HIP runtime torch already loaded (same soname)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise FoldLibraryMissing(
+            f"{path} is not built; run `python -m paper_2609_33410_amd.build_lib`")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER
+    lib.fold_abi_version.restype = ctypes.c_int
+    lib.fold_abi_version.argtypes = []
+    lib.fold_status_string.restype = ctypes.c_char_p
+    lib.fold_status_string.argtypes = [ctypes.c_int]
+    lib.fold_last_error.restype = ctypes.c_char_p
+    lib.fold_last_error.argtypes = []
+    for name in ("fold_decode_rows_per_group", "fold_decode_row_groups"):
+        fn = getattr(lib, name)
+        fn.restype = ctypes.c_int32
+        fn.argtypes = [P(fold_kv_view), P(fold_q_view)]
+    lib.fold_ref_estimate.restype = ctypes.c_int
+    lib.fold_ref_estimate.argtypes = [P(fold_kv_view), P(fold_q_view), ctypes.c_float,
+                                      P(fold_est_params), ctypes.c_void_p, ctypes.c_void_p]
+    lib.fold_decode_split.restype = ctypes.c_int
+    lib.fold_decode_split.argtypes = [P(fold_kv_view), P(fold_q_view), ctypes.c_float,
+                                      ctypes.c_void_p, ctypes.c_float, ctypes.c_int32,
+                                      ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                      ctypes.c_void_p, P(fold_debug), ctypes.c_void_p]
+    lib.fold_combine.restype = ctypes.c_int
+    lib.fold_combine.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                 ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    _lib = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != FOLD_OK:
+        lib = load_library()
+        msg = lib.fold_last_error().decode(errors="replace")
+        raise FoldError(status, f"{lib.fold_status_string(status).decode()}: {msg}")
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype) -> None:
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+@dataclass
+class KV:
+    """A cache view plus the tensors it points into (kept alive here)."""
+    view: fold_kv_view
+    tensors: tuple
+
+
+@dataclass
+class Q:
+    view: fold_q_view
+    tensor: torch.Tensor
+
+
+def kv_view(k: torch.Tensor, v: Optional[torch.Tensor], seq_lens: torch.Tensor, *,
+            num_kv_heads: int, max_seq_len: int, block_table: Optional[torch.Tensor] = None,
+            row_indptr: Optional[torch.Tensor] = None, row_req: Optional[torch.Tensor] = None,
+            max_reqs_per_seq: int = 1) -> KV:
+    """Describe one scan level.  Paged: ``k, v [num_pages, Hkv, P, D]`` with
+    ``block_table [num_seqs, max_pages]``; contiguous: ``k, v [num_seqs, Hkv,
+    max_seq_len, D]``."""
+    _need(k, "k", torch.bfloat16)
+    if v is not None:
+        _need(v, "v", torch.bfloat16)
+    _need(seq_lens, "seq_lens", torch.int32)
+    d = int(k.shape[-1])
+    s = fold_kv_view()
+    s.k, s.v = _ptr(k), _ptr(v)
+    s.seq_lens = _ptr(seq_lens)
+    s.num_seqs = int(seq_lens.shape[0])
+    s.num_kv_heads = num_kv_heads
+    s.head_dim = d
+    s.max_seq_len = max_seq_len
+    if block_table is not None:
+        _need(block_table, "block_table", torch.int32)
+        s.block_table = _ptr(block_table)
+        s.page_size = int(k.shape[2])
+        s.max_pages_per_seq = int(block_table.shape[1])
+        s.num_pages = int(k.shape[0])
+    if row_indptr is not None:
+        _need(row_indptr, "row_indptr", torch.int32)
+        _need(row_req, "row_req", torch.int32)
+        s.row_indptr, s.row_req = _ptr(row_indptr), _ptr(row_req)
+        s.max_reqs_per_seq = max_reqs_per_seq
+    return KV(s, (k, v, seq_lens, block_table, row_indptr, row_req))
+
+
+def q_view(q: torch.Tensor) -> Q:
+    _need(q, "q", torch.bfloat16)
+    s = fold_q_view()
+    s.q = _ptr(q)
+    s.batch, s.num_heads = int(q.shape[0]), int(q.shape[1])
+    return Q(s, q)
+
+
+def fold_decode_rows_per_group(kv: KV, q: Q) -> int:
+    return load_library().fold_decode_rows_per_group(ctypes.byref(kv.view), ctypes.byref(q.view))
+
+
+def fold_decode_row_groups(kv: KV, q: Q) -> int:
+    return load_library().fold_decode_row_groups(ctypes.byref(kv.view), ctypes.byref(q.view))
+
+
+def fold_ref_estimate(kv: KV, q: Q, sm_scale: float, z_out: torch.Tensor, params=None,
+                      stream=None) -> torch.Tensor:
+    _need(z_out, "z_out", torch.float32)
+    p = None
+    if params is not None:
+        p = fold_est_params(params["sink"], params["recent"], params["strata"],
+                            params["trim_lo"], params["trim_hi"])
+    _check(load_library().fold_ref_estimate(ctypes.byref(kv.view), ctypes.byref(q.view),
+                                            sm_scale, None if p is None else ctypes.byref(p),
+                                            _ptr(z_out), _stream(stream)))
+    return z_out
+
+
+def fold_decode_split(kv: KV, q: Q, sm_scale: float, z: torch.Tensor, depth_T: float,
+                      num_splits: int, slot_offset: int, part_A: torch.Tensor,
+                      part_L: torch.Tensor, x_out: Optional[torch.Tensor] = None,
+                      key_gate_out: Optional[torch.Tensor] = None,
+                      page_gate_out: Optional[torch.Tensor] = None, stream=None) -> None:
+    _need(z, "z", torch.float32)
+    _need(part_A, "part_A", torch.float32)
+    _need(part_L, "part_L", torch.float32)
+    dbg = None
+    if x_out is not None or key_gate_out is not None or page_gate_out is not None:
+        for t, nm, dt in ((x_out, "x_out", torch.float32), (key_gate_out, "key_gate_out", torch.uint8),
+                          (page_gate_out, "page_gate_out", torch.uint8)):
+            if t is not None:
+                _need(t, nm, dt)
+        dbg = fold_debug(_ptr(x_out), _ptr(key_gate_out), _ptr(page_gate_out))
+    _check(load_library().fold_decode_split(
+        ctypes.byref(kv.view), ctypes.byref(q.view), sm_scale, _ptr(z), depth_T, num_splits,
+        slot_offset, int(part_A.shape[0]), _ptr(part_A), _ptr(part_L),
+        None if dbg is None else ctypes.byref(dbg), _stream(stream)))
+
+
+def fold_combine(part_A: torch.Tensor, part_L: torch.Tensor, out: torch.Tensor,
+                 z: Optional[torch.Tensor] = None, lse_out: Optional[torch.Tensor] = None,
+                 cert_out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    _need(part_A, "part_A", torch.float32)
+    _need(part_L, "part_L", torch.float32)
+    if out.dtype == torch.float32:
+        odt = FOLD_DTYPE_F32
+    elif out.dtype == torch.bfloat16:
+        odt = FOLD_DTYPE_BF16
+    else:
+        raise TypeError("out must be float32 or bfloat16")
+    if not out.is_contiguous():
+        raise ValueError("out must be contiguous")
+    num_slots = int(part_A.shape[0])
+    d = int(part_A.shape[-1])
+    rows = part_A[0].numel() // d if num_slots else 0
+    _check(load_library().fold_combine(_ptr(part_A), _ptr(part_L), num_slots, rows, d, _ptr(z),
+                                       _ptr(out), odt, _ptr(lse_out), _ptr(cert_out),
+                                       _stream(stream)))
+    return out
+
+
+def fold_decode(levels, q: torch.Tensor, z: torch.Tensor, depth_T: float, splits,
+                sm_scale: float, out_dtype=torch.float32, lse: bool = False, cert: bool = False,
+                stream=None):
+    """Every level's split scan into one slot array, then the combine.
+
+    ``levels`` is a list of ``KV`` views; ``splits`` their split counts.  Returns
+    ``(out, part_A, part_L, lse_out, cert_out)``.
+    """
+    b, h, d = q.shape
+    qv = q_view(q)
+    total = sum(splits)
+    part_A = torch.empty(total, b, h, d, dtype=torch.float32, device=q.device)
+    part_L = torch.empty(total, b, h, dtype=torch.float32, device=q.device)
+    off = 0
+    for kv, s in zip(levels, splits):
+        fold_decode_split(kv, qv, sm_scale, z, depth_T, s, off, part_A, part_L, stream=stream)
+        off += s
+    out = torch.empty(b, h, d, dtype=out_dtype, device=q.device)
+    lse_out = torch.empty(b, h, dtype=torch.float32, device=q.device) if lse else None
+    cert_out = torch.empty(b, h, dtype=torch.uint8, device=q.device) if cert else None
+    fold_combine(part_A, part_L, out, z=z if lse else None, lse_out=lse_out, cert_out=cert_out,
+                 stream=stream)
+    return out, part_A, part_L, lse_out, cert_out
+
+
+def depth_value(T) -> float:
+    """``None`` / ``inf`` -> +INFINITY (dense decode); otherwise float(T)."""
+    return math.inf if T is None else float(T)

@@ -1,0 +1,137 @@
+"""The C ABI library loads, exports every declared entry point, and rejects
+invalid arguments on the host before launching anything (CPU only)."""
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2609_33410_amd as F
+from paper_2609_33410_amd import build_lib
+from paper_2609_33410_amd.fold import fold_debug, fold_kv_view, fold_q_view
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(F.LIB_PATH):
+        build_lib.build()
+    return F.load_library()
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "fold.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(fold_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert len(names) >= 8
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(F.EXPORTED)
+
+
+def test_version_and_status_strings(lib):
+    assert lib.fold_abi_version() == 1
+    for code, word in ((0, b"FOLD_OK"), (1, b"FOLD_E_INVAL"), (2, b"FOLD_E_UNSUPPORTED"),
+                       (3, b"FOLD_E_HIP")):
+        assert lib.fold_status_string(code).startswith(word)
+
+
+FAKE = 1 << 20  # a 16-byte aligned, never dereferenced address: validation fails first
+
+
+def _kv(**over):
+    kv = fold_kv_view()
+    kv.k = kv.v = kv.seq_lens = FAKE
+    kv.block_table = FAKE
+    kv.num_seqs, kv.num_kv_heads, kv.head_dim = 2, 2, 128
+    kv.page_size, kv.max_pages_per_seq, kv.num_pages = 16, 4, 8
+    kv.max_seq_len, kv.max_reqs_per_seq = 64, 1
+    for k, v in over.items():
+        setattr(kv, k, v)
+    return kv
+
+
+def _q(**over):
+    q = fold_q_view()
+    q.q, q.batch, q.num_heads = FAKE, 2, 8
+    for k, v in over.items():
+        setattr(q, k, v)
+    return q
+
+
+def _decode(lib, kv, q, T=math.inf, splits=1, slot_offset=0, num_slots=1, z=FAKE):
+    return lib.fold_decode_split(ctypes.byref(kv), ctypes.byref(q), 0.125, z, T, splits,
+                                 slot_offset, num_slots, FAKE, FAKE, None, None)
+
+
+@pytest.mark.parametrize("case", [
+    ("head_dim", {"head_dim": 96}, {}),
+    ("heads % kv_heads", {"num_kv_heads": 3}, {}),
+    ("page_size", {"page_size": 8}, {}),
+    ("misaligned k", {"k": FAKE + 2}, {}),
+    ("misaligned q", {}, {"q": FAKE + 8}),
+    ("null v", {"v": None}, {}),
+    ("num_seqs > batch", {"num_seqs": 3}, {}),
+    ("csr half set", {"row_indptr": FAKE}, {}),
+])
+def test_decode_rejects_bad_views(lib, case):
+    _, kvo, qo = case
+    assert _decode(lib, _kv(**kvo), _q(**qo)) == F.FOLD_E_INVAL
+    assert len(lib.fold_last_error()) > 0
+
+
+@pytest.mark.parametrize("kw", [
+    {"T": float("nan")}, {"T": -1.0}, {"splits": 0}, {"slot_offset": 1, "num_slots": 1},
+    {"z": None},
+])
+def test_decode_rejects_bad_call_args(lib, kw):
+    assert _decode(lib, _kv(), _q(), **kw) == F.FOLD_E_INVAL
+
+
+def test_estimate_rejects_csr_view_and_bad_params(lib):
+    from paper_2609_33410_amd.fold import fold_est_params
+    kv = _kv(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=4)
+    assert lib.fold_ref_estimate(ctypes.byref(kv), ctypes.byref(_q()), 0.1, None, FAKE,
+                                 None) == F.FOLD_E_INVAL
+    p = fold_est_params(1, 63, 128, 64, 64)
+    assert lib.fold_ref_estimate(ctypes.byref(_kv()), ctypes.byref(_q()), 0.1, ctypes.byref(p),
+                                 FAKE, None) == F.FOLD_E_INVAL
+    p = fold_est_params(1, 63, 500, 8, 8)
+    assert lib.fold_ref_estimate(ctypes.byref(_kv()), ctypes.byref(_q()), 0.1, ctypes.byref(p),
+                                 FAKE, None) == F.FOLD_E_INVAL
+
+
+def test_combine_rejects_bad_args(lib):
+    assert lib.fold_combine(FAKE, FAKE, 0, 4, 128, None, FAKE, 0, None, None, None) == F.FOLD_E_INVAL
+    assert lib.fold_combine(FAKE, FAKE, 2, 4, 80, None, FAKE, 0, None, None, None) == F.FOLD_E_INVAL
+    assert lib.fold_combine(FAKE, FAKE, 2, 4, 128, None, FAKE, 7, None, None, None) == F.FOLD_E_INVAL
+    assert lib.fold_combine(FAKE, FAKE, 2, 4, 128, None, FAKE, 0, FAKE, None, None) == F.FOLD_E_INVAL
+
+
+def test_row_group_queries(lib):
+    kv = _kv()
+    assert lib.fold_decode_rows_per_group(ctypes.byref(kv), ctypes.byref(_q())) == 4
+    assert lib.fold_decode_row_groups(ctypes.byref(kv), ctypes.byref(_q())) == 1
+    csr = _kv(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=64, num_kv_heads=1)
+    assert lib.fold_decode_rows_per_group(ctypes.byref(csr), ctypes.byref(_q())) == 8
+    assert lib.fold_decode_row_groups(ctypes.byref(csr), ctypes.byref(_q())) == 64
+    assert lib.fold_decode_row_groups(ctypes.byref(_kv(head_dim=5)), ctypes.byref(_q())) == -1
+
+
+def test_binding_raises_when_library_missing(tmp_path):
+    import importlib
+    from paper_2609_33410_amd import fold as fmod
+    saved = fmod._lib
+    try:
+        fmod._lib = None
+        with pytest.raises(F.FoldLibraryMissing):
+            fmod.load_library(str(tmp_path / "libfold.so"))
+    finally:
+        fmod._lib = saved
