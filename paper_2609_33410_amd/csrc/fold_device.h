@@ -14,17 +14,18 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// Reinterpret a 32-bit word as two BF16 values.  The word must arrive as a
+// scalar: clang lowers __builtin_bit_cast applied directly to an ext-vector
+// component (v.y, v.z, ...) to a read of component 0.
+__device__ __forceinline__ bf16x2 as_bf16x2(uint32_t w) { return __builtin_bit_cast(bf16x2, w); }
+
 // sum_{e<8} k[e] * q[e] + acc over 8 packed BF16 values, FP32 accumulation
 // (v_dot2_f32_bf16: two exact BF16 products per instruction).
 __device__ __forceinline__ float dot8_bf16(u32x4 k, u32x4 q, float acc) {
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, k.x),
-                                        __builtin_bit_cast(bf16x2, q.x), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, k.y),
-                                        __builtin_bit_cast(bf16x2, q.y), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, k.z),
-                                        __builtin_bit_cast(bf16x2, q.z), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, k.w),
-                                        __builtin_bit_cast(bf16x2, q.w), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(k.x), as_bf16x2(q.x), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(k.y), as_bf16x2(q.y), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(k.z), as_bf16x2(q.z), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(k.w), as_bf16x2(q.w), acc, false);
   return acc;
 }
 

@@ -234,8 +234,13 @@ def test_certificate_forced_bad_reference_and_rerun():
     base = _gpu.run(wl, INF, splits=[1])
     assert (base["cert"] == 0).all()
     z = base["z"].cuda()
-    for shift, bit in ((140.0, 1), (-110.0, 2)):
-        bad = _gpu.run(wl, INF, splits=[1], z=(z + shift).contiguous())
+    # +140 binades flushes every FP32 weight (L = 0): the flag fires, but lse is
+    # -inf and cannot seed a rerun.  lse + 20 and lse - 110 keep L representable.
+    bad = _gpu.run(wl, INF, splits=[1], z=(z + 140.0).contiguous())
+    assert ((bad["cert"].numpy() & 1) != 0).all()
+    lse = base["lse"].cuda()
+    for shift, bit in ((20.0, 1), (-110.0, 2)):
+        bad = _gpu.run(wl, INF, splits=[1], z=(lse + shift).contiguous())
         assert ((bad["cert"].numpy() & bit) != 0).all()
         rerun = _gpu.run(wl, INF, splits=[1], z=bad["lse"].cuda().contiguous())
         assert (rerun["cert"] == 0).all()
