@@ -5,9 +5,10 @@ reference estimate, the gated split-KV scan of every level, and the additive
 combine.  The default workload is the Llama-3-8B-shaped GQA decode (batch 16,
 32 query / 8 kv heads, head dim 128, 8192 cached keys per request, paged BF16
 cache of 16-key pages).  Inputs are synthetic, seeded and resident in HBM
-before timing.  Before every timed step a 1 GiB buffer is written so that no
-cache (4 MB L2 per XCD, 256 MB MALL) holds any of the step's data; each step
-is bracketed by HIP events on the stream the kernels are launched on.
+before timing.  Before every timed step a 1 GiB buffer is read, so that no
+cache (4 MB L2 per XCD, 256 MB MALL) holds any of the step's data and no dirty
+line is left to drain during the step; each step is bracketed by HIP events on
+the stream the kernels are launched on.
 
 Prints ONE JSON line (rank 0).  ``--all`` adds one JSON line per workload and
 depth on stderr (used for the design notes' tables).
@@ -39,6 +40,7 @@ def parse():
     ap.add_argument("--all", action="store_true", help="also time workloads 1-5 (stderr)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--splits", type=int, default=None, help="override the split count")
     return ap.parse_args()
 
 
@@ -114,13 +116,19 @@ def kv_bytes(wl, lam):
     return total, keys
 
 
+def evict_caches(flush):
+    """Read (not write) a 1 GiB buffer: every cache line of the step's data is
+    evicted, and no dirty line is left to be written back during the step."""
+    return flush.sum(dtype=flush.dtype)
+
+
 def time_variant(path, T, steps, warmup, flush, torch):
-    """Median per-kernel and per-step durations (ms) with a cache flush before
-    every step; events are recorded on the launch stream."""
+    """Median per-kernel and per-step durations (ms) with a cache eviction
+    before every step; events are recorded on the launch stream."""
     stream = torch.cuda.current_stream()
     res = {"est": [], "dec": [], "comb": [], "step": []}
     for it in range(warmup + steps):
-        flush.fill_(it & 0xff)
+        evict_caches(flush)
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
         ev[0].record(stream)
         path.estimate(stream)
@@ -178,8 +186,10 @@ def cpu_baseline(wl, budget_s):
                       f"(request, kv head) chunks in {dt:.1f} s, scaled to the whole call"}
 
 
-def run_workload(i, args, torch, F, make_config, flush, steps, warmup):
+def run_workload(i, args, torch, F, make_config, flush, steps, warmup, splits=None):
     wl = make_config(i, device="cuda")
+    if splits is not None and len(wl.level_splits) == 1:
+        wl.level_splits = [splits]
     path = Path(wl, F, torch)
     stream = torch.cuda.current_stream()
     path.estimate(stream)
@@ -207,11 +217,11 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     F.load_library()
-    flush = torch.empty(1 << 28, dtype=torch.int32, device="cuda")  # 1 GiB
+    flush = torch.ones(1 << 28, dtype=torch.int32, device="cuda")  # 1 GiB
 
     wall0 = time.perf_counter()
     wl, res = run_workload(args.config, args, torch, F, make_config, flush, args.steps,
-                           args.warmup)
+                           args.warmup, splits=args.splits)
     wall = time.perf_counter() - wall0
     dense, t16 = res[math.inf], res[16.0]
     dec_ms = dense["med"]["dec"]
@@ -235,7 +245,7 @@ def main():
                    "head_dim": wl.head_dim, "keys_per_request": wl.flat.seq_lens_host[0],
                    "page_size": wl.page_size, "splits": wl.level_splits,
                    "step": "estimate + split scan + combine, T=inf",
-                   "timing": "median of per-step HIP events, 1 GiB cache flush before each step"},
+                   "timing": "median of per-step HIP events, 1 GiB read before each step evicts all caches"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": None, "kernel": "decode_split_kernel",

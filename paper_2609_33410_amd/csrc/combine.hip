@@ -17,7 +17,24 @@ __global__ __launch_bounds__(128) void combine_kernel(const CombineArgs a) {
   const int D = a.head_dim;
   float acc = 0.0f;
   float l = 0.0f;
-  for (int s = 0; s < a.num_slots; ++s) {
+  // Slots are added in increasing order; loads are batched eight at a time so
+  // they are in flight together.
+  int s = 0;
+  for (; s + 8 <= a.num_slots; s += 8) {
+    float av[8], lv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const size_t sr = static_cast<size_t>(s + u) * a.num_rows + row;
+      av[u] = a.part_A[sr * D + d];
+      lv[u] = a.part_L[sr];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      acc += av[u];
+      l += lv[u];
+    }
+  }
+  for (; s < a.num_slots; ++s) {
     const size_t sr = static_cast<size_t>(s) * a.num_rows + row;
     acc += a.part_A[sr * D + d];
     l += a.part_L[sr];

@@ -3,231 +3,245 @@
 //
 // One workgroup = one (kv sequence, kv head, split, read group of GR query
 // rows); four wave64s.  The split walks the 64-key tiles t == split (mod S);
-// wave w of the workgroup owns the 16-key chunk 4t + w of each tile, which is
-// a contiguous [16][D] bf16 slab in both cache layouts (pages hold a multiple
-// of 16 keys).  Per chunk a wave:
-//   1. issues the 128-bit loads of the NEXT chunk's keys (prefetch),
-//   2. scores this chunk's keys against the GR rows: D/8 lanes hold one key
-//      row (8 channels each, v_dot2_f32_bf16), a DPP row reduction gives every
-//      lane of the key the full dot product; x = s - Z_i in FP32,
-//   3. takes the verdict live = (T infinite) or (x >= -T), ORs it over the
-//      rows, and issues the value loads of live keys only (lanes of cut keys
-//      are masked off, so their bytes are never requested; a chunk with no
-//      live key issues none),
-//   4. accumulates A += [live] 2^x v and L += 2^x in FP32 registers.
-// Waves never synchronise inside the loop.  At the end the lanes of a wave
-// and then the four waves are reduced in a fixed order and the pair (A, L) of
-// every row is written to its split's slot.
-#include "fold_device.h"
-#include "fold_internal.h"
+// wave w owns the 16-key chunk 4t + w of each tile, a contiguous [16][D] bf16
+// slab in both cache layouts (pages hold a multiple of 16 keys).  D/8 lanes
+// hold one key row (8 channels each), so one wave-wide 128-bit load covers
+// 64/(D/8) keys and 1 KiB of contiguous bytes.
+//
+// Loads go through buffer resources whose size is the chunk's valid bytes:
+// keys past the sequence end and value rows of cut keys are given an offset
+// outside the resource, so the hardware returns zero without touching memory.
+// No load sits under a branch, which keeps the memory counters exact.
+//
+// Gated scan (finite T), software-pipelined three chunks deep per wave:
+//   iteration t: issue K loads of chunk t+2;
+//                score chunk t+1 (v_dot2_f32_bf16 + DPP row sums, x = s - Z in
+//                FP32, live = x >= -T, ORed over the read group's rows) and
+//                issue the value loads of its live keys only;
+//                accumulate chunk t: A += [live] 2^x v, L += 2^x (FP32).
+// Dense scan (T = inf): every key is live, so K and V of chunk t+1 are issued
+// together before chunk t is scored and accumulated.
+// At the end the lanes of a wave and then the four waves are reduced in a fixed
+// order and the pair (A, L) of every row is written to its split's slot.
+#include "decode_common.h"
 
 namespace fold {
 namespace {
 
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
+constexpr int kWaves = kScanWaves;
+constexpr int kThreads = kScanThreads;
 
-// First element of the 16-key chunk `c` of (seq, head), or nullptr when the
-// chunk's page id is out of range.
-__device__ __forceinline__ const uint16_t* chunk_base(const uint16_t* base, const ScanGeometry& g,
-                                                      int seq, int head, int c, int D) {
-  if (g.page_size > 0) {
-    const int key0 = c * kChunk;
-    const int page = key0 / g.page_size;
-    const int off = key0 - page * g.page_size;
-    const int phys = g.block_table[static_cast<size_t>(seq) * g.max_pages + page];
-    if (phys < 0 || phys >= g.num_pages) return nullptr;
-    return base + ((static_cast<size_t>(phys) * g.hkv + head) * g.page_size + off) * D;
-  }
-  return base + ((static_cast<size_t>(seq) * g.hkv + head) * g.max_seq_len +
-                 static_cast<size_t>(c) * kChunk) * D;
-}
+template <int D, int GR, bool DENSE, bool DBG>
+struct Scan {
+  static constexpr int LPK = D / 8;        // lanes per key row
+  static constexpr int KPI = 64 / LPK;     // keys per wave-wide 128-bit load
+  static constexpr int NI = kChunk / KPI;  // loads per lane per 16-key chunk
 
-struct RowInfo {
-  int req;
-  int head;
-  bool ok;
-};
-
-__device__ __forceinline__ RowInfo row_info(const ScanGeometry& g, int seq, int kvh, int rho,
-                                            int nrows, int req0) {
-  RowInfo ri;
-  ri.ok = rho < nrows;
-  const int rr = ri.ok ? rho : 0;
-  ri.req = g.row_indptr ? g.row_req[req0 + rr / g.group] : seq;
-  ri.head = kvh * g.group + rr % g.group;
-  ri.ok = ri.ok && ri.req >= 0 && ri.req < g.batch;
-  return ri;
-}
-
-template <int D, int GR>
-__global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs a) {
-  constexpr int LPK = D / 8;         // lanes per key row
-  constexpr int KPI = 64 / LPK;      // keys per wave-wide 128-bit load
-  constexpr int NI = kChunk / KPI;   // loads per lane per 16-key chunk
-  const ScanGeometry& g = a.geo;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int part = lane % LPK;
-  const int kslot = lane / LPK;
-
-  int bid = blockIdx.x;
-  const int seq = bid % g.num_seqs;
-  bid /= g.num_seqs;
-  const int kvh = bid % g.hkv;
-  bid /= g.hkv;
-  const int split = bid % a.num_splits;
-  const int rg = bid / a.num_splits;
-
-  int req0 = seq, nreq = 1;
-  if (g.row_indptr) {
-    req0 = g.row_indptr[seq];
-    nreq = g.row_indptr[seq + 1] - req0;
-  }
-  const int nrows = nreq * g.group;
-  if (rg * GR >= nrows) return;  // uniform: this read group has no rows
-
-  const int n = clamp_len(g.seq_lens[seq], view_capacity(g));
-  const int nchunks = (n + kChunk - 1) / kChunk;
-
-  // Query rows of the read group: 8 BF16 channels per lane, and Z_i.
+  const DecodeArgs& a;
+  const ScanGeometry& g;
+  int seq, kvh, rg, nrows, req0, n, nchunks, lane, part, kslot;
+  size_t gate_row;
+  int gate_pages;
   u32x4 qv[GR];
   float zr[GR];
   bool rok[GR];
-#pragma unroll
-  for (int r = 0; r < GR; ++r) {
-    const RowInfo ri = row_info(g, seq, kvh, rg * GR + r, nrows, req0);
-    rok[r] = ri.ok;
-    const size_t row = static_cast<size_t>(ri.req) * g.heads + ri.head;
-    qv[r] = ri.ok ? *reinterpret_cast<const u32x4*>(a.q + row * D + 8 * part) : u32x4{0, 0, 0, 0};
-    zr[r] = ri.ok ? a.z[row] : 0.0f;
-  }
-
+  size_t xrow[GR];  // query row index req * heads + head (debug export)
   float acc[GR][8];
   float lsum[GR];
+
+  __device__ Scan(const DecodeArgs& a_) : a(a_), g(a_.geo) {}
+
+  __device__ __forceinline__ void load(rsrc_t r, u32x4 (&dst)[NI]) const {
 #pragma unroll
-  for (int r = 0; r < GR; ++r) {
-    lsum[r] = 0.0f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[r][e] = 0.0f;
+    for (int i = 0; i < NI; ++i) dst[i] = buf_load(r, 1024u * i + 16u * lane);
   }
 
-  const int cstride = kWaves * a.num_splits;
-  int c = kWaves * split + wave;
-  const size_t gate_row = (static_cast<size_t>(seq) * g.hkv + kvh) * a.row_groups + rg;
-  const int gate_pages = (g.max_seq_len + kChunk - 1) / kChunk;
-
-  u32x4 kcur[NI];
-  const uint16_t* kbase = c < nchunks ? chunk_base(g.k, g, seq, kvh, c, D) : nullptr;
+  __device__ __forceinline__ void load_gated(rsrc_t r, const bool (&live)[NI], u32x4 (&dst)[NI]) const {
 #pragma unroll
-  for (int i = 0; i < NI; ++i) {
-    const int j = c * kChunk + KPI * i + kslot;
-    kcur[i] = (kbase && j < n) ? *reinterpret_cast<const u32x4*>(kbase + 512 * i + 8 * lane)
-                               : u32x4{0, 0, 0, 0};
+    for (int i = 0; i < NI; ++i) dst[i] = buf_load(r, live[i] ? 1024u * i + 16u * lane : kOutOfRange);
   }
 
-  for (; c < nchunks; c += cstride) {
-    const bool have_k = kbase != nullptr;
-    // 1. prefetch the next chunk's keys
-    const int cn = c + cstride;
-    const uint16_t* kbase_n = cn < nchunks ? chunk_base(g.k, g, seq, kvh, cn, D) : nullptr;
-    u32x4 knext[NI];
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int j = cn * kChunk + KPI * i + kslot;
-      knext[i] = (kbase_n && j < n) ? *reinterpret_cast<const u32x4*>(kbase_n + 512 * i + 8 * lane)
-                                    : u32x4{0, 0, 0, 0};
-    }
-
-    // 2-3. scores, verdicts and the read mask of this chunk
-    float p[NI][GR];
-    bool anyl[NI];
+  // Scores, verdicts, L; the A-weights of live keys go to p.  Returns whether
+  // any key of the chunk is read (wave-uniform).
+  __device__ __forceinline__ bool score(int c, const u32x4 (&kv)[NI], float (&p)[NI][GR],
+                                        bool (&anyl)[NI]) {
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int j = c * kChunk + KPI * i + kslot;
-      const bool kok = have_k && j < n;
+      const bool kok = c < nchunks && j < n;
       anyl[i] = false;
 #pragma unroll
       for (int r = 0; r < GR; ++r) {
-        const float dot = group_sum<LPK>(dot8_bf16(kcur[i], qv[r], 0.0f));
-        const float x = dot * a.score_scale - zr[r];
+        const float dot = group_sum<LPK>(dot8_bf16(kv[i], qv[r], 0.0f));
+        const float x = __builtin_fmaf(dot, a.score_scale, -zr[r]);
         const bool ok = kok && rok[r];
-        const bool live = ok && (a.dense || x >= a.neg_T);
+        const bool live = ok && (DENSE || x >= a.neg_T);
         const float w = ok ? exp2_fast(x) : 0.0f;
         lsum[r] += w;
         p[i][r] = live ? w : 0.0f;
         anyl[i] = anyl[i] || live;
-        if (a.x_out && ok && part == 0) {
-          const RowInfo ri = row_info(g, seq, kvh, rg * GR + r, nrows, req0);
-          a.x_out[(static_cast<size_t>(ri.req) * g.heads + ri.head) * g.max_seq_len + j] = x;
-        }
+        if (DBG && a.x_out && ok && part == 0) a.x_out[xrow[r] * g.max_seq_len + j] = x;
       }
-      if (a.key_gate_out && kok && part == 0)
+      if (DBG && a.key_gate_out && kok && part == 0)
         a.key_gate_out[gate_row * g.max_seq_len + j] = anyl[i] ? 1 : 0;
     }
     bool lane_any = false;
 #pragma unroll
     for (int i = 0; i < NI; ++i) lane_any = lane_any || anyl[i];
     const bool chunk_any = __ballot(lane_any) != 0;
-    if (a.page_gate_out && lane == 0 && have_k)
+    if (DBG && a.page_gate_out && lane == 0 && c < nchunks)
       a.page_gate_out[gate_row * gate_pages + c] = chunk_any ? 1 : 0;
+    return chunk_any;
+  }
 
-    // 4. gated value reads and accumulation
-    if (chunk_any) {
-      const uint16_t* vbase = chunk_base(g.v, g, seq, kvh, c, D);
-      u32x4 vv[NI];
+  __device__ __forceinline__ void accumulate(const u32x4 (&vv)[NI], const float (&p)[NI][GR]) {
 #pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        vv[i] = u32x4{0, 0, 0, 0};
-        if (anyl[i]) vv[i] = *reinterpret_cast<const u32x4*>(vbase + 512 * i + 8 * lane);
-      }
+    for (int i = 0; i < NI; ++i) {
+      const float v0 = bf16_lo(vv[i].x), v1 = bf16_hi(vv[i].x);
+      const float v2 = bf16_lo(vv[i].y), v3 = bf16_hi(vv[i].y);
+      const float v4 = bf16_lo(vv[i].z), v5 = bf16_hi(vv[i].z);
+      const float v6 = bf16_lo(vv[i].w), v7 = bf16_hi(vv[i].w);
 #pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        const float v0 = bf16_lo(vv[i].x), v1 = bf16_hi(vv[i].x);
-        const float v2 = bf16_lo(vv[i].y), v3 = bf16_hi(vv[i].y);
-        const float v4 = bf16_lo(vv[i].z), v5 = bf16_hi(vv[i].z);
-        const float v6 = bf16_lo(vv[i].w), v7 = bf16_hi(vv[i].w);
-#pragma unroll
-        for (int r = 0; r < GR; ++r) {
-          const float pr = p[i][r];
-          acc[r][0] += pr * v0;
-          acc[r][1] += pr * v1;
-          acc[r][2] += pr * v2;
-          acc[r][3] += pr * v3;
-          acc[r][4] += pr * v4;
-          acc[r][5] += pr * v5;
-          acc[r][6] += pr * v6;
-          acc[r][7] += pr * v7;
-        }
+      for (int r = 0; r < GR; ++r) {
+        const float pr = p[i][r];
+        acc[r][0] += pr * v0;
+        acc[r][1] += pr * v1;
+        acc[r][2] += pr * v2;
+        acc[r][3] += pr * v3;
+        acc[r][4] += pr * v4;
+        acc[r][5] += pr * v5;
+        acc[r][6] += pr * v6;
+        acc[r][7] += pr * v7;
       }
     }
+  }
+};
+
+template <int D, int GR, bool DENSE, bool DBG>
+__global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs a) {
+  using S = Scan<D, GR, DENSE, DBG>;
+  constexpr int NI = S::NI;
+  const ScanGeometry& g = a.geo;
+  S sc(a);
+  sc.lane = threadIdx.x & 63;
+  // wave-uniform (an SGPR), so chunk indices and buffer resources are scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  sc.part = sc.lane % S::LPK;
+  sc.kslot = sc.lane / S::LPK;
+
+  const ScanPlace pl = scan_place(a);
+  sc.seq = pl.seq;
+  sc.kvh = pl.kvh;
+  const int split = pl.split;
+  sc.rg = pl.rg;
+  sc.req0 = pl.req0;
+  sc.nrows = pl.nrows;
+  if (sc.rg * GR >= sc.nrows) return;  // uniform: this read group has no rows
+  sc.n = pl.n;
+  sc.nchunks = pl.nchunks;
+  sc.gate_row = (static_cast<size_t>(sc.seq) * g.hkv + sc.kvh) * a.row_groups + sc.rg;
+  sc.gate_pages = (g.max_seq_len + kChunk - 1) / kChunk;
+
 #pragma unroll
-    for (int i = 0; i < NI; ++i) kcur[i] = knext[i];
-    kbase = kbase_n;
+  for (int r = 0; r < GR; ++r) {
+    const RowInfo ri = row_info(g, sc.seq, sc.kvh, sc.rg * GR + r, sc.nrows, sc.req0);
+    sc.rok[r] = ri.ok;
+    const size_t row = static_cast<size_t>(ri.req) * g.heads + ri.head;
+    sc.qv[r] = ri.ok ? *reinterpret_cast<const u32x4*>(a.q + row * D + 8 * sc.part)
+                     : u32x4{0, 0, 0, 0};
+    sc.zr[r] = ri.ok ? a.z[row] : 0.0f;
+    sc.xrow[r] = row;
+    sc.lsum[r] = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sc.acc[r][e] = 0.0f;
+  }
+
+  // Chunks of this wave: c_t = c0 + t * cstride, t < m.
+  const int cstride = kWaves * a.num_splits;
+  const int c0 = kWaves * split + wave;
+  const int m = sc.nchunks > c0 ? (sc.nchunks - c0 + cstride - 1) / cstride : 0;
+
+  if (DENSE) {
+    u32x4 kA[NI], vA[NI], kB[NI], vB[NI];
+    float p[NI][GR];
+    bool anyl[NI];
+    rsrc_t rk, rv;
+    chunk_rsrc<D>(g, pl, c0, &rk, &rv);
+    sc.load(rk, kA);
+    sc.load(rv, vA);
+    for (int t = 0; t < m; t += 2) {
+      chunk_rsrc<D>(g, pl, c0 + (t + 1) * cstride, &rk, &rv);
+      sc.load(rk, kB);
+      sc.load(rv, vB);
+      sc.score(c0 + t * cstride, kA, p, anyl);
+      sc.accumulate(vA, p);
+      if (t + 1 >= m) break;
+      chunk_rsrc<D>(g, pl, c0 + (t + 2) * cstride, &rk, &rv);
+      sc.load(rk, kA);
+      sc.load(rv, vA);
+      sc.score(c0 + (t + 1) * cstride, kB, p, anyl);
+      sc.accumulate(vB, p);
+    }
+  } else {
+    // kX: keys of chunk t+1 (scored this iteration); kY: keys of chunk t+2
+    u32x4 kA[NI], kB[NI], vA[NI], vB[NI];
+    float pA[NI][GR], pB[NI][GR];
+    bool lA[NI], lB[NI];
+    bool anyA = false, anyB = false;
+    rsrc_t rk, rv;
+    if (m > 0) {
+      chunk_rsrc<D>(g, pl, c0, &rk, &rv);
+      sc.load(rk, kA);
+      rsrc_t rk1, rv1;
+      chunk_rsrc<D>(g, pl, c0 + cstride, &rk1, &rv1);
+      sc.load(rk1, kB);
+      anyA = sc.score(c0, kA, pA, lA);
+      sc.load_gated(rv, lA, vA);
+    }
+    for (int t = 0; t < m; t += 2) {
+      // chunk t: V in vA / weights in pA; chunk t+1: K in kB
+      rsrc_t rv1;
+      chunk_rsrc<D>(g, pl, c0 + (t + 2) * cstride, &rk, &rv);
+      sc.load(rk, kA);
+      {
+        rsrc_t rk1;
+        chunk_rsrc<D>(g, pl, c0 + (t + 1) * cstride, &rk1, &rv1);
+      }
+      anyB = sc.score(c0 + (t + 1) * cstride, kB, pB, lB);
+      sc.load_gated(rv1, lB, vB);
+      if (anyA) sc.accumulate(vA, pA);
+      if (t + 1 >= m) break;
+      // chunk t+1: V in vB / weights in pB; chunk t+2: K in kA
+      chunk_rsrc<D>(g, pl, c0 + (t + 3) * cstride, &rk, &rv1);
+      sc.load(rk, kB);
+      anyA = sc.score(c0 + (t + 2) * cstride, kA, pA, lA);
+      sc.load_gated(rv, lA, vA);
+      if (anyB) sc.accumulate(vB, pB);
+    }
   }
 
   // Reduce over the key slots of the wave (lanes with equal `part`).
 #pragma unroll
-  for (int off = LPK; off < 64; off <<= 1) {
+  for (int off = S::LPK; off < 64; off <<= 1) {
 #pragma unroll
     for (int r = 0; r < GR; ++r) {
-      lsum[r] += __shfl_xor(lsum[r], off, 64);
+      sc.lsum[r] += __shfl_xor(sc.lsum[r], off, 64);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[r][e] += __shfl_xor(acc[r][e], off, 64);
+      for (int e = 0; e < 8; ++e) sc.acc[r][e] += __shfl_xor(sc.acc[r][e], off, 64);
     }
   }
 
   __shared__ float red_a[kWaves][GR][D];
   __shared__ float red_l[kWaves][GR];
-  if (kslot == 0) {
+  if (sc.kslot == 0) {
 #pragma unroll
     for (int r = 0; r < GR; ++r)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) red_a[wave][r][8 * part + e] = acc[r][e];
+      for (int e = 0; e < 8; ++e) red_a[wave][r][8 * sc.part + e] = sc.acc[r][e];
   }
-  if (lane == 0) {
+  if (sc.lane == 0) {
 #pragma unroll
-    for (int r = 0; r < GR; ++r) red_l[wave][r] = lsum[r];
+    for (int r = 0; r < GR; ++r) red_l[wave][r] = sc.lsum[r];
   }
   __syncthreads();
 
@@ -235,7 +249,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs
   for (int idx = threadIdx.x; idx < GR * D; idx += kThreads) {
     const int r = idx / D;
     const int d = idx - r * D;
-    const RowInfo ri = row_info(g, seq, kvh, rg * GR + r, nrows, req0);
+    const RowInfo ri = row_info(g, sc.seq, sc.kvh, sc.rg * GR + r, sc.nrows, sc.req0);
     if (!ri.ok) continue;
     const size_t row = (slot * g.batch + ri.req) * g.heads + ri.head;
     float s = red_a[0][r][d];
@@ -251,39 +265,46 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs
   }
 }
 
-template <int D, int GR>
-hipError_t launch_dg(const DecodeArgs& a, hipStream_t stream) {
-  const long long blocks = static_cast<long long>(a.geo.num_seqs) * a.geo.hkv * a.num_splits *
-                           a.row_groups;
-  if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((decode_split_kernel<D, GR>), dim3(static_cast<unsigned>(blocks)),
-                     dim3(kThreads), 0, stream, a);
-  return hipGetLastError();
-}
-
 template <int D>
-hipError_t launch_d(const DecodeArgs& a, hipStream_t stream) {
-  switch (a.rows_per_group) {
-    case 1: return launch_dg<D, 1>(a, stream);
-    case 2: return launch_dg<D, 2>(a, stream);
-    case 4: return launch_dg<D, 4>(a, stream);
-    case 8: return launch_dg<D, 8>(a, stream);
-    default: return hipErrorInvalidValue;
+hipError_t launch_valu(const DecodeArgs& a, unsigned blocks, hipStream_t stream) {
+  const bool dbg = a.x_out || a.key_gate_out || a.page_gate_out;
+  if (a.dense) {
+    if (dbg)
+      hipLaunchKernelGGL((decode_split_kernel<D, 1, true, true>), dim3(blocks), dim3(kThreads), 0,
+                         stream, a);
+    else
+      hipLaunchKernelGGL((decode_split_kernel<D, 1, true, false>), dim3(blocks), dim3(kThreads), 0,
+                         stream, a);
+  } else {
+    if (dbg)
+      hipLaunchKernelGGL((decode_split_kernel<D, 1, false, true>), dim3(blocks), dim3(kThreads), 0,
+                         stream, a);
+    else
+      hipLaunchKernelGGL((decode_split_kernel<D, 1, false, false>), dim3(blocks), dim3(kThreads), 0,
+                         stream, a);
   }
+  return hipGetLastError();
 }
 
 }  // namespace
 
+// Rows per read group: one row (MHA, VALU scan) or 16 / 32 rows (matrix-core
+// scan for GQA groups and stacked cascade rows).
 int decode_rows_per_group(int rows_per_seq) {
   if (rows_per_seq <= 1) return 1;
-  if (rows_per_seq <= 2) return 2;
-  if (rows_per_seq <= 4) return 4;
-  return 8;
+  if (rows_per_seq <= 16) return 16;
+  return 32;
 }
 
+hipError_t launch_decode_mfma(const DecodeArgs& a, int head_dim, hipStream_t stream);
+
 hipError_t launch_decode(const DecodeArgs& a, int head_dim, hipStream_t stream) {
-  if (head_dim == 128) return launch_d<128>(a, stream);
-  if (head_dim == 64) return launch_d<64>(a, stream);
+  if (a.rows_per_group > 1) return launch_decode_mfma(a, head_dim, stream);
+  const long long blocks = static_cast<long long>(a.geo.num_seqs) * a.geo.hkv * a.num_splits *
+                           a.row_groups;
+  if (blocks == 0) return hipSuccess;
+  if (head_dim == 128) return launch_valu<128>(a, static_cast<unsigned>(blocks), stream);
+  if (head_dim == 64) return launch_valu<64>(a, static_cast<unsigned>(blocks), stream);
   return hipErrorInvalidValue;
 }
 

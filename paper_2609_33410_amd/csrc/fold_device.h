@@ -72,6 +72,15 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   return static_cast<uint16_t>(u >> 16);
 }
 
+// Read-only metadata (block tables, lengths, row lists) viewed through the
+// constant address space: a wave-uniform index then compiles to a scalar load,
+// whose completion is tracked apart from the vector loads of K and V.  The
+// caller must not modify these arrays while a call is in flight.
+typedef __attribute__((address_space(4))) const int32_t const_i32;
+__device__ __forceinline__ int32_t ld_uniform(const int32_t* p, size_t i) {
+  return ((const const_i32*)p)[i];  // address-space cast (C-style is required)
+}
+
 // Clamp a device-supplied sequence length to what the view can address.
 __device__ __forceinline__ int clamp_len(int n, int cap) { return n < 0 ? 0 : (n > cap ? cap : n); }
 

@@ -25,7 +25,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const EstimateArgs a
   constexpr int KPI = 64 / LPK;
   const ScanGeometry& g = a.geo;
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int part = lane % LPK;
   const int kslot = lane / LPK;
   const int req = blockIdx.x / g.hkv;
@@ -75,26 +75,51 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const EstimateArgs a
   }
   __syncthreads();
 
-  // Score every sampled key against every row.
-  for (int t0 = 0; t0 < m; t0 += kThreads / LPK) {
-    const int t = t0 + wave * KPI + kslot;
-    u32x4 kv = {0, 0, 0, 0};
-    if (t < m) {
-      const int j = sidx[t];
-      const uint16_t* p = nullptr;
+  // Score every sampled key against every row.  Each lane scores up to
+  // kBatch keys per pass; their block-table entries and key bytes are each
+  // requested together (branch-free, always in-bounds indices), so a pass
+  // costs two memory round trips.
+  constexpr int kBatch = 12;
+  constexpr int kKeysPerPass = kThreads / LPK;
+  for (int t0 = 0; t0 < m; t0 += kKeysPerPass * kBatch) {
+    int jb[kBatch];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int t = t0 + b * kKeysPerPass + wave * KPI + kslot;
+      jb[b] = sidx[t < m ? t : m - 1];
+    }
+    int phys[kBatch];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b)
+      phys[b] = g.page_size > 0
+                    ? g.block_table[static_cast<size_t>(req) * g.max_pages + jb[b] / g.page_size]
+                    : 0;
+    u32x4 kv[kBatch];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int t = t0 + b * kKeysPerPass + wave * KPI + kslot;
+      const int j = jb[b];
+      size_t off;
+      bool ok = t < m;
       if (g.page_size > 0) {
-        const int page = j / g.page_size;
-        const int phys = g.block_table[static_cast<size_t>(req) * g.max_pages + page];
-        if (phys >= 0 && phys < g.num_pages)
-          p = g.k + ((static_cast<size_t>(phys) * g.hkv + kvh) * g.page_size + (j - page * g.page_size)) * D;
+        ok = ok && phys[b] >= 0 && phys[b] < g.num_pages;
+        off = ((static_cast<size_t>(ok ? phys[b] : 0) * g.hkv + kvh) * g.page_size +
+               (j % g.page_size)) * D;
       } else {
-        p = g.k + ((static_cast<size_t>(req) * g.hkv + kvh) * g.max_seq_len + j) * D;
+        off = ((static_cast<size_t>(req) * g.hkv + kvh) * g.max_seq_len + j) * D;
       }
-      if (p) kv = *reinterpret_cast<const u32x4*>(p + 8 * part);
+      const u32x4 v = *reinterpret_cast<const u32x4*>(g.k + (ok ? off : 0) + 8 * part);
+      kv[b] = ok ? v : u32x4{0, 0, 0, 0};
     }
     for (int r = 0; r < G; ++r) {
-      const float dot = group_sum<LPK>(dot8_bf16(kv, qs[r][part], 0.0f));
-      if (t < m && part == 0) sc[r][t] = dot * a.score_scale;
+      const u32x4 qf = qs[r][part];
+#pragma unroll
+      for (int b = 0; b < kBatch; ++b) {
+        const int t = t0 + b * kKeysPerPass + wave * KPI + kslot;
+        if (t0 + b * kKeysPerPass >= m) break;  // uniform
+        const float dot = group_sum<LPK>(dot8_bf16(kv[b], qf, 0.0f));
+        if (t < m && part == 0) sc[r][t] = dot * a.score_scale;
+      }
     }
   }
   __syncthreads();
@@ -110,15 +135,41 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const EstimateArgs a
     if (stratified) {
       const float* cs = &sc[r][a.sink + a.recent];
       float kept = 0.0f;
-      for (int b = lane; b < a.strata; b += 64) {
-        const float sb = cs[b];
-        int rank = 0;
-        for (int b2 = 0; b2 < a.strata; ++b2) {
-          const float s2 = cs[b2];
-          rank += (s2 < sb || (s2 == sb && b2 < b)) ? 1 : 0;
-        }
-        if (rank >= a.trim_lo && rank < a.strata - a.trim_hi) kept += exp2_fast(sb - mx);
+      // Trim: remove the trim_hi largest and the trim_lo smallest centre scores
+      // one at a time (wave-wide max / min; among equal scores the lowest
+      // stratum index goes first), then add the weights of the rest.  Ranking
+      // by score equals ranking by weight because 2^x is monotone.
+      constexpr int kPerLane = kMaxEstSamples / 64;
+      const int nu = (a.strata + 63) / 64;
+      float sv[kPerLane];
+      bool keep[kPerLane];
+#pragma unroll
+      for (int u = 0; u < kPerLane; ++u) {
+        const int b = lane + 64 * u;
+        keep[u] = u < nu && b < a.strata;
+        sv[u] = keep[u] ? cs[b] : 0.0f;
       }
+      for (int k = 0; k < a.trim_hi + a.trim_lo; ++k) {
+        const bool top = k < a.trim_hi;
+        float ext = top ? -INFINITY : INFINITY;
+#pragma unroll
+        for (int u = 0; u < kPerLane; ++u)
+          if (u < nu && keep[u]) ext = top ? fmaxf(ext, sv[u]) : fminf(ext, sv[u]);
+        ext = top ? wave_max(ext) : -wave_max(-ext);
+        bool removed = false;  // uniform
+#pragma unroll
+        for (int u = 0; u < kPerLane; ++u) {
+          if (u >= nu || removed) break;
+          const uint64_t hit = __ballot(keep[u] && sv[u] == ext);
+          if (hit) {
+            if (lane == __builtin_ctzll(hit)) keep[u] = false;
+            removed = true;
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kPerLane; ++u)
+        if (u < nu && keep[u]) kept += exp2_fast(sv[u] - mx);
       kept = wave_sum(kept);
       const int nkept = a.strata - a.trim_lo - a.trim_hi;
       mass = (static_cast<float>(rmid) / static_cast<float>(nkept)) * kept;

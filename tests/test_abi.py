@@ -117,11 +117,16 @@ def test_combine_rejects_bad_args(lib):
 
 def test_row_group_queries(lib):
     kv = _kv()
-    assert lib.fold_decode_rows_per_group(ctypes.byref(kv), ctypes.byref(_q())) == 4
+    # GQA group of 4: one matrix-core read group of 16 rows
+    assert lib.fold_decode_rows_per_group(ctypes.byref(kv), ctypes.byref(_q())) == 16
     assert lib.fold_decode_row_groups(ctypes.byref(kv), ctypes.byref(_q())) == 1
+    # MHA: one row per read group (VALU scan)
+    mha = _kv(num_kv_heads=8)
+    assert lib.fold_decode_rows_per_group(ctypes.byref(mha), ctypes.byref(_q())) == 1
+    # 64 requests x 8 heads stacked on one kv sequence: 512 rows in groups of 32
     csr = _kv(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=64, num_kv_heads=1)
-    assert lib.fold_decode_rows_per_group(ctypes.byref(csr), ctypes.byref(_q())) == 8
-    assert lib.fold_decode_row_groups(ctypes.byref(csr), ctypes.byref(_q())) == 64
+    assert lib.fold_decode_rows_per_group(ctypes.byref(csr), ctypes.byref(_q())) == 32
+    assert lib.fold_decode_row_groups(ctypes.byref(csr), ctypes.byref(_q())) == 16
     assert lib.fold_decode_row_groups(ctypes.byref(_kv(head_dim=5)), ctypes.byref(_q())) == -1
 
 

@@ -195,6 +195,19 @@ def test_mass_kept_L_independent_of_T():
         assert torch.equal(a["part_L"], b["part_L"])
 
 
+@pytest.mark.parametrize("cfg,T", [(1, INF), (1, 16.0), (2, INF), (2, 16.0), (5, 16.0)])
+def test_debug_exports_do_not_change_results(cfg, T):
+    """The kernel variant that exports x and read gates computes the same bits
+    as the production variant, so the exported decisions are the production
+    kernel's decisions."""
+    wl = make_config(cfg, device="cuda", batch=None if cfg == 1 else 4,
+                     seq_len=None if cfg == 1 else 1500)
+    z = _gpu.estimate(wl)
+    a = _gpu.run(wl, T, z=z, debug=False)
+    b = _gpu.run(wl, T, z=z, debug=True)
+    assert torch.equal(a["part_A"], b["part_A"]) and torch.equal(a["part_L"], b["part_L"])
+
+
 def test_repeat_bits_and_batch_invariance():
     wl = make_config(2, batch=4, seq_len=2000, device="cuda")
     z = _gpu.estimate(wl)

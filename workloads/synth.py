@@ -300,10 +300,10 @@ def make_config(i: int, seed: int = 0, device: str = "cpu", *, batch: Optional[i
                          depths=[INF, 16.0], keep_logical=keep_logical)
     if i == 5:
         reqs = batch or 64
-        pre = seq_len or 16384
+        pre = 16384 if seq_len is None else max(16, (seq_len // 16) * 16)
         return _generate_cascade(name=CONFIG_NAMES[5], requests=reqs, heads=8, kv_heads=1,
                                  dim=128, prefix_len=pre, suffix_len=1024 if seq_len is None
-                                 else max(16, seq_len // 16), page_size=16, seed=seed,
+                                 else max(16, (seq_len // 256) * 16), page_size=16, seed=seed,
                                  device=device, level_splits=[8, 4], depths=[INF, 16.0],
                                  keep_logical=keep_logical)
     raise ValueError(f"no workload {i}")
