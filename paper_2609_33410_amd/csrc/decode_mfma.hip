@@ -33,20 +33,8 @@
 namespace fold {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ f32x4 mfma_qk(u32x4 a, u32x4 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
-
-__device__ __forceinline__ f32x4 mfma_pv(u32x2 a, u32x2 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a),
-                                                   __builtin_bit_cast(s16x4, b), c, 0, 0, 0);
-}
+__device__ __forceinline__ f32x4 mfma_qk(u32x4 a, u32x4 b, f32x4 c) { return mfma_16x16x32(a, b, c); }
+__device__ __forceinline__ f32x4 mfma_pv(u32x2 a, u32x2 b, f32x4 c) { return mfma_16x16x16(a, b, c); }
 
 template <int D, int RB, bool DENSE, bool DBG>
 struct MfmaScan {
@@ -165,7 +153,7 @@ __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeA
   constexpr int NK = S::NK;
   constexpr int R = S::R;
   constexpr int kTileBytes = kScanWaves * 16 * S::VSTRIDE;
-  constexpr int kRedBytes = (R * D + R) * 4;
+  constexpr int kRedBytes = (R * D + RB * 64) * 4;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kTileBytes > kRedBytes ? kTileBytes : kRedBytes];
 
   const ScanGeometry& g = a.geo;
@@ -201,24 +189,35 @@ __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeA
   const int m = sc.p.nchunks > c0 ? (sc.p.nchunks - c0 + cstride - 1) / cstride : 0;
 
   if (DENSE) {
-    u32x4 kA[NK], vA[NK], kB[NK], vB[NK];
+    // three chunks in flight per wave: keys and values of t+1 and t+2 load
+    // while chunk t is scored and multiplied
+    u32x4 kA[NK], vA[NK], kB[NK], vB[NK], kC[NK], vC[NK];
     u32x2 phi[RB], plo[RB];
     rsrc_t rk, rv;
     chunk_rsrc<D>(g, sc.p, c0, &rk, &rv);
     sc.kload(rk, kA);
     sc.vload(rv, 0xffffu, vA);
-    for (int t = 0; t < m; t += 2) {
-      chunk_rsrc<D>(g, sc.p, c0 + (t + 1) * cstride, &rk, &rv);
-      sc.kload(rk, kB);
-      sc.vload(rv, 0xffffu, vB);
+    chunk_rsrc<D>(g, sc.p, c0 + cstride, &rk, &rv);
+    sc.kload(rk, kB);
+    sc.vload(rv, 0xffffu, vB);
+    for (int t = 0; t < m; t += 3) {
+      chunk_rsrc<D>(g, sc.p, c0 + (t + 2) * cstride, &rk, &rv);
+      sc.kload(rk, kC);
+      sc.vload(rv, 0xffffu, vC);
       uint32_t mk = sc.score(c0 + t * cstride, kA, phi, plo);
       sc.product(mk, vA, phi, plo);
       if (t + 1 >= m) break;
-      chunk_rsrc<D>(g, sc.p, c0 + (t + 2) * cstride, &rk, &rv);
+      chunk_rsrc<D>(g, sc.p, c0 + (t + 3) * cstride, &rk, &rv);
       sc.kload(rk, kA);
       sc.vload(rv, 0xffffu, vA);
       mk = sc.score(c0 + (t + 1) * cstride, kB, phi, plo);
       sc.product(mk, vB, phi, plo);
+      if (t + 2 >= m) break;
+      chunk_rsrc<D>(g, sc.p, c0 + (t + 4) * cstride, &rk, &rv);
+      sc.kload(rk, kB);
+      sc.vload(rv, 0xffffu, vB);
+      mk = sc.score(c0 + (t + 2) * cstride, kC, phi, plo);
+      sc.product(mk, vC, phi, plo);
     }
   } else if (m > 0) {
     u32x4 kA[NK], kB[NK], vA[NK], vB[NK];
@@ -255,10 +254,11 @@ __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeA
     sc.lsum[b] += __shfl_xor(sc.lsum[b], 32, 64);
   }
 
-  // Add the four waves in order through LDS (the value tiles are dead now).
+  // Add the four waves in order through LDS (the value tiles are dead now),
+  // in the accumulators' own lane order so that no two lanes share a bank.
   __syncthreads();
-  float* red = reinterpret_cast<float*>(smem);  // [R][D]
-  float* redl = red + R * D;                    // [R]
+  float* red = reinterpret_cast<float*>(smem);  // [RB][NB][4][64]
+  float* redl = red + RB * S::NB * 4 * 64;      // [RB][64]
   for (int w = 0; w < kScanWaves; ++w) {
     if (wave == w) {
 #pragma unroll
@@ -267,13 +267,11 @@ __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeA
         for (int blk = 0; blk < S::NB; ++blk)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int idx = (16 * b + sc.n16) * D + 16 * blk + 4 * sc.grp + i;
-            red[idx] = (w == 0 ? 0.0f : red[idx]) + sc.acc[b][blk][i];
+            float* r = red + ((b * S::NB + blk) * 4 + i) * 64 + sc.lane;
+            *r = (w == 0 ? 0.0f : *r) + sc.acc[b][blk][i];
           }
-        if (sc.grp == 0) {
-          const int r = 16 * b + sc.n16;
-          redl[r] = (w == 0 ? 0.0f : redl[r]) + sc.lsum[b];
-        }
+        float* rl = redl + b * 64 + sc.lane;
+        *rl = (w == 0 ? 0.0f : *rl) + sc.lsum[b];
       }
     }
     __syncthreads();
@@ -281,13 +279,18 @@ __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeA
 
   const size_t slot = static_cast<size_t>(a.slot_offset) + sc.p.split;
   for (int idx = threadIdx.x; idx < R * D; idx += kScanThreads) {
-    const int r = idx / D;
-    const int d = idx - r * D;
+    // idx = ((b * NB + blk) * 4 + i) * 64 + l  ->  row 16 b + l % 16, channel 16 blk + 4 (l / 16) + i
+    const int l = idx & 63;
+    const int i = (idx >> 6) & 3;
+    const int blk = (idx >> 8) % S::NB;
+    const int b = (idx >> 8) / S::NB;
+    const int r = 16 * b + (l & 15);
+    const int d = 16 * blk + 4 * (l >> 4) + i;
     const RowInfo ri = row_info(g, sc.p.seq, sc.p.kvh, sc.p.rg * R + r, sc.p.nrows, sc.p.req0);
     if (!ri.ok) continue;
     const size_t row = (slot * g.batch + ri.req) * g.heads + ri.head;
     a.part_A[row * D + d] = red[idx];
-    if (d == 0) a.part_L[row] = redl[r];
+    if (d == 0) a.part_L[row] = redl[b * 64 + (l & 15)];
   }
 }
 

@@ -4,13 +4,20 @@
 // the first `sink` keys, the last `recent` keys and the centre of each of
 // `strata` contiguous strata of the keys in between (every key when the row is
 // short).  They are scored against all query rows of the GQA group with the
-// same BF16 dot products as the decode scan, kept in LDS, and then one wave
-// per row forms
+// same BF16 dot products as the decode scan and kept in LDS; then one wave per
+// row forms
 //     Z = M + log2( sum_exact 2^(s - M) + (r / kept) * sum_kept 2^(s_c - M) )
-// where M is the largest sampled score and the kept centres are those whose
-// rank (by score, ties broken by stratum index) lies in
-// [trim_lo, strata - trim_hi).  Ranking by score equals ranking by weight
-// because 2^x is monotone.  All sums use fixed-order wave reductions.
+// where M is the largest sampled score and the kept centres are those left
+// after removing the trim_hi largest and the trim_lo smallest centre scores
+// (ranking by score equals ranking by weight because 2^x is monotone).
+//
+// Latency, not bandwidth, bounds this kernel (48 KiB per (request, kv head) at
+// D = 128).  Scores come from the matrix cores, 16 samples x 16 rows per
+// v_mfma_f32_16x16x32_bf16 (the decode scan's layout); every lane issues the
+// block-table reads of all its samples at once and then all their key loads,
+// so scoring costs two memory round trips.  The trim sorts the centre scores
+// with a bitonic network across the wave; wave reductions use DPP and
+// v_readlane.  Every sum has a fixed order, so the result is deterministic.
 #include "fold_device.h"
 #include "fold_internal.h"
 
@@ -21,25 +28,21 @@ constexpr int kThreads = 256;
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void estimate_kernel(const EstimateArgs a) {
-  constexpr int LPK = D / 8;
-  constexpr int KPI = 64 / LPK;
+  constexpr int NK = D / 32;            // 16-byte key loads per lane per sample tile
+  constexpr int kTilesPerPass = 4;      // sample tiles per wave whose loads fly together
+  constexpr int kScanWavesEst = kThreads / 64;
   const ScanGeometry& g = a.geo;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int part = lane % LPK;
-  const int kslot = lane / LPK;
   const int req = blockIdx.x / g.hkv;
   const int kvh = blockIdx.x % g.hkv;
   const int G = g.group;
 
-  __shared__ u32x4 qs[kMaxEstRows][D / 8];
   __shared__ float sc[kMaxEstRows][kMaxEstSamples];
   __shared__ int sidx[kMaxEstSamples];
 
   int n = 0;
-  if (req < g.num_seqs) {
-    n = clamp_len(g.seq_lens[req], view_capacity(g));
-  }
+  if (req < g.num_seqs) n = clamp_len(ld_uniform(g.seq_lens, req), view_capacity(g));
   if (n == 0) {
     for (int r = threadIdx.x; r < G; r += kThreads)
       a.z_out[static_cast<size_t>(req) * g.heads + kvh * G + r] = 0.0f;
@@ -51,6 +54,20 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const EstimateArgs a
   const int n_exact = stratified ? a.sink + a.recent : n;
   const long long rmid = static_cast<long long>(n) - a.sink - a.recent;
 
+  // Q^T operand of the score product: lane l holds channels 32c + 8(l/16) .. +8
+  // of query row l%16 (rows past the group are zero).
+  const int n16 = lane & 15;
+  const int grp = lane >> 4;
+  u32x4 qb[NK];
+#pragma unroll
+  for (int c = 0; c < NK; ++c) {
+    qb[c] = u32x4{0, 0, 0, 0};
+    if (n16 < G) {
+      const size_t row = static_cast<size_t>(req) * g.heads + kvh * G + n16;
+      qb[c] = *reinterpret_cast<const u32x4*>(a.q + row * D + 32 * c + 8 * grp);
+    }
+  }
+
   for (int t = threadIdx.x; t < m; t += kThreads) {
     int j;
     if (!stratified) {
@@ -60,117 +77,155 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const EstimateArgs a
     } else if (t < a.sink + a.recent) {
       j = n - a.recent + (t - a.sink);
     } else {
-      const long long b = t - a.sink - a.recent;
-      const long long lo = a.sink + (b * rmid) / a.strata;
-      const long long hi = a.sink + ((b + 1) * rmid) / a.strata;
-      j = static_cast<int>((lo + hi - 1) / 2);
+      // floor(b r / strata) in double: b r < 2^53 is exact, and a quotient that
+      // is not an integer sits at least 1/strata above its floor, far more than
+      // the division's rounding error.
+      const int b = t - a.sink - a.recent;
+      const int lo = a.sink + static_cast<int>(floor(static_cast<double>(b) * rmid / a.strata));
+      const int hi = a.sink + static_cast<int>(floor(static_cast<double>(b + 1) * rmid / a.strata));
+      j = (lo + hi - 1) / 2;
     }
     sidx[t] = j;
   }
-  for (int t = threadIdx.x; t < G * (D / 8); t += kThreads) {
-    const int r = t / (D / 8);
-    const int c = t - r * (D / 8);
-    const size_t row = static_cast<size_t>(req) * g.heads + kvh * G + r;
-    qs[r][c] = *reinterpret_cast<const u32x4*>(a.q + row * D + 8 * c);
-  }
   __syncthreads();
 
-  // Score every sampled key against every row.  Each lane scores up to
-  // kBatch keys per pass; their block-table entries and key bytes are each
-  // requested together (branch-free, always in-bounds indices), so a pass
-  // costs two memory round trips.
-  constexpr int kBatch = 12;
-  constexpr int kKeysPerPass = kThreads / LPK;
-  for (int t0 = 0; t0 < m; t0 += kKeysPerPass * kBatch) {
-    int jb[kBatch];
+  // Tiles of 16 samples; wave w scores tiles w, w+4, ...; lane l loads sample l%16.
+  const int ntiles = (m + 15) / 16;
+  for (int tau0 = wave; tau0 < ntiles; tau0 += kScanWavesEst * kTilesPerPass) {
+    int jb[kTilesPerPass];
 #pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int t = t0 + b * kKeysPerPass + wave * KPI + kslot;
-      jb[b] = sidx[t < m ? t : m - 1];
+    for (int u = 0; u < kTilesPerPass; ++u) {
+      const int t = 16 * (tau0 + kScanWavesEst * u) + n16;
+      jb[u] = sidx[t < m ? t : m - 1];
     }
-    int phys[kBatch];
+    int phys[kTilesPerPass];
 #pragma unroll
-    for (int b = 0; b < kBatch; ++b)
-      phys[b] = g.page_size > 0
-                    ? g.block_table[static_cast<size_t>(req) * g.max_pages + jb[b] / g.page_size]
+    for (int u = 0; u < kTilesPerPass; ++u)
+      phys[u] = g.page_size > 0
+                    ? g.block_table[static_cast<size_t>(req) * g.max_pages + jb[u] / g.page_size]
                     : 0;
-    u32x4 kv[kBatch];
+    u32x4 kv[kTilesPerPass][NK];
 #pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int t = t0 + b * kKeysPerPass + wave * KPI + kslot;
-      const int j = jb[b];
+    for (int u = 0; u < kTilesPerPass; ++u) {
+      const int t = 16 * (tau0 + kScanWavesEst * u) + n16;
+      const int j = jb[u];
       size_t off;
       bool ok = t < m;
       if (g.page_size > 0) {
-        ok = ok && phys[b] >= 0 && phys[b] < g.num_pages;
-        off = ((static_cast<size_t>(ok ? phys[b] : 0) * g.hkv + kvh) * g.page_size +
+        ok = ok && phys[u] >= 0 && phys[u] < g.num_pages;
+        off = ((static_cast<size_t>(ok ? phys[u] : 0) * g.hkv + kvh) * g.page_size +
                (j % g.page_size)) * D;
       } else {
         off = ((static_cast<size_t>(req) * g.hkv + kvh) * g.max_seq_len + j) * D;
       }
-      const u32x4 v = *reinterpret_cast<const u32x4*>(g.k + (ok ? off : 0) + 8 * part);
-      kv[b] = ok ? v : u32x4{0, 0, 0, 0};
-    }
-    for (int r = 0; r < G; ++r) {
-      const u32x4 qf = qs[r][part];
 #pragma unroll
-      for (int b = 0; b < kBatch; ++b) {
-        const int t = t0 + b * kKeysPerPass + wave * KPI + kslot;
-        if (t0 + b * kKeysPerPass >= m) break;  // uniform
-        const float dot = group_sum<LPK>(dot8_bf16(kv[b], qf, 0.0f));
-        if (t < m && part == 0) sc[r][t] = dot * a.score_scale;
+      for (int c = 0; c < NK; ++c) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(g.k + (ok ? off : 0) + 32 * c + 8 * grp);
+        kv[u][c] = ok ? v : u32x4{0, 0, 0, 0};
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kTilesPerPass; ++u) {
+      const int tau = tau0 + kScanWavesEst * u;
+      if (tau >= ntiles) break;  // uniform
+      f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int c = 0; c < NK; ++c) s = mfma_16x16x32(kv[u][c], qb[c], s);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = 16 * tau + 4 * grp + i;
+        if (n16 < G && t < m) sc[n16][t] = s[i] * a.score_scale;
       }
     }
   }
   __syncthreads();
 
+  constexpr int kPerLane = kMaxEstSamples / 64;
+  const int nu_all = (m + 63) / 64;
+  const int nu = (a.strata + 63) / 64;
   for (int r = wave; r < G; r += kThreads / 64) {
     float mx = -INFINITY;
-    for (int t = lane; t < m; t += 64) mx = fmaxf(mx, sc[r][t]);
-    mx = wave_max(mx);
+#pragma unroll
+    for (int u = 0; u < kPerLane; ++u) {
+      const int t = lane + 64 * u;
+      if (u < nu_all && t < m) mx = fmaxf(mx, sc[r][t]);
+    }
+    mx = wave_max_dpp(mx);
     float ex = 0.0f;
-    for (int t = lane; t < n_exact; t += 64) ex += exp2_fast(sc[r][t] - mx);
-    ex = wave_sum(ex);
+#pragma unroll
+    for (int u = 0; u < kPerLane; ++u) {
+      const int t = lane + 64 * u;
+      if (u < nu_all && t < n_exact) ex += exp2_fast(sc[r][t] - mx);
+    }
+    ex = wave_sum_dpp(ex);
     float mass = 0.0f;
     if (stratified) {
       const float* cs = &sc[r][a.sink + a.recent];
       float kept = 0.0f;
-      // Trim: remove the trim_hi largest and the trim_lo smallest centre scores
-      // one at a time (wave-wide max / min; among equal scores the lowest
-      // stratum index goes first), then add the weights of the rest.  Ranking
-      // by score equals ranking by weight because 2^x is monotone.
-      constexpr int kPerLane = kMaxEstSamples / 64;
-      const int nu = (a.strata + 63) / 64;
-      float sv[kPerLane];
-      bool keep[kPerLane];
-#pragma unroll
-      for (int u = 0; u < kPerLane; ++u) {
-        const int b = lane + 64 * u;
-        keep[u] = u < nu && b < a.strata;
-        sv[u] = keep[u] ? cs[b] : 0.0f;
-      }
-      for (int k = 0; k < a.trim_hi + a.trim_lo; ++k) {
-        const bool top = k < a.trim_hi;
-        float ext = top ? -INFINITY : INFINITY;
-#pragma unroll
-        for (int u = 0; u < kPerLane; ++u)
-          if (u < nu && keep[u]) ext = top ? fmaxf(ext, sv[u]) : fminf(ext, sv[u]);
-        ext = top ? wave_max(ext) : -wave_max(-ext);
-        bool removed = false;  // uniform
-#pragma unroll
-        for (int u = 0; u < kPerLane; ++u) {
-          if (u >= nu || removed) break;
-          const uint64_t hit = __ballot(keep[u] && sv[u] == ext);
-          if (hit) {
-            if (lane == __builtin_ctzll(hit)) keep[u] = false;
-            removed = true;
+      if (a.strata <= 128) {
+        // Bitonic sort of the (at most 128) centre scores across the wave, two
+        // per lane (element e = 2 * lane + u), padded with +inf; sorted
+        // positions [trim_lo, strata - trim_hi) are kept.  A fixed network:
+        // the kept multiset, hence the sum, does not depend on tie order.
+        float v0 = 2 * lane < a.strata ? cs[2 * lane] : INFINITY;
+        float v1 = 2 * lane + 1 < a.strata ? cs[2 * lane + 1] : INFINITY;
+        for (int k = 2; k <= 128; k <<= 1) {
+          for (int j = k >> 1; j >= 1; j >>= 1) {
+            const bool asc = ((2 * lane) & k) == 0;  // both elements of a lane share it
+            if (j == 1) {
+              const float lo = fminf(v0, v1), hi = fmaxf(v0, v1);
+              v0 = asc ? lo : hi;
+              v1 = asc ? hi : lo;
+            } else {
+              const int d = j >> 1;  // partner lane = lane ^ d
+              const float p0 = __shfl_xor(v0, d, 64);
+              const float p1 = __shfl_xor(v1, d, 64);
+              const bool keep_min = ((lane & d) == 0) == asc;
+              v0 = keep_min ? fminf(v0, p0) : fmaxf(v0, p0);
+              v1 = keep_min ? fminf(v1, p1) : fmaxf(v1, p1);
+            }
           }
         }
-      }
+        const int hi_pos = a.strata - a.trim_hi;
+        const int e0 = 2 * lane, e1 = 2 * lane + 1;
+        if (e0 >= a.trim_lo && e0 < hi_pos) kept += exp2_fast(v0 - mx);
+        if (e1 >= a.trim_lo && e1 < hi_pos) kept += exp2_fast(v1 - mx);
+      } else {
+        // Larger stratifications: remove the trim_hi largest and the trim_lo
+        // smallest scores one at a time (among equal scores the lowest
+        // stratum index goes first), then add what is left.
+        float sv[kPerLane];
+        bool keep[kPerLane];
 #pragma unroll
-      for (int u = 0; u < kPerLane; ++u)
-        if (u < nu && keep[u]) kept += exp2_fast(sv[u] - mx);
-      kept = wave_sum(kept);
+        for (int u = 0; u < kPerLane; ++u) {
+          const int b = lane + 64 * u;
+          keep[u] = u < nu && b < a.strata;
+          sv[u] = keep[u] ? cs[b] : 0.0f;
+        }
+        for (int k = 0; k < a.trim_hi + a.trim_lo; ++k) {
+          const bool top = k < a.trim_hi;  // uniform
+          float ext = -INFINITY;
+#pragma unroll
+          for (int u = 0; u < kPerLane; ++u)
+            if (u < nu && keep[u]) ext = fmaxf(ext, top ? sv[u] : -sv[u]);
+          ext = wave_max_dpp(ext);
+          if (!top) ext = -ext;
+          bool removed = false;  // uniform
+#pragma unroll
+          for (int u = 0; u < kPerLane; ++u) {
+            if (u >= nu || removed) break;
+            const uint64_t hit = __ballot(keep[u] && sv[u] == ext);
+            if (hit) {
+              if (lane == __builtin_ctzll(hit)) keep[u] = false;
+              removed = true;
+            }
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kPerLane; ++u)
+          if (u < nu && keep[u]) kept += exp2_fast(sv[u] - mx);
+      }
+      kept = wave_sum_dpp(kept);
       const int nkept = a.strata - a.trim_lo - a.trim_hi;
       mass = (static_cast<float>(rmid) / static_cast<float>(nkept)) * kept;
     }

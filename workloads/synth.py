@@ -286,7 +286,7 @@ def make_config(i: int, seed: int = 0, device: str = "cpu", *, batch: Optional[i
                          lens=[n] * b, paged=True, page_size=16,
                          spike_count=lambda m: int(round(0.01 * m)), alpha_spike=3.0, n_sink=4,
                          alpha_sink=6.0, seed=seed, device=device,
-                         level_splits=[8 if i == 2 else 16],
+                         level_splits=[4 if i == 2 else 16],
                          depths=[INF, 16.0] if i == 2 else [INF, 24.0, 16.0, 12.0],
                          keep_logical=keep_logical)
     if i == 4:
@@ -304,7 +304,7 @@ def make_config(i: int, seed: int = 0, device: str = "cpu", *, batch: Optional[i
         return _generate_cascade(name=CONFIG_NAMES[5], requests=reqs, heads=8, kv_heads=1,
                                  dim=128, prefix_len=pre, suffix_len=1024 if seq_len is None
                                  else max(16, (seq_len // 256) * 16), page_size=16, seed=seed,
-                                 device=device, level_splits=[8, 4], depths=[INF, 16.0],
+                                 device=device, level_splits=[32, 8], depths=[INF, 16.0],
                                  keep_logical=keep_logical)
     raise ValueError(f"no workload {i}")
 
