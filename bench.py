@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--splits", type=int, default=None, help="override the split count")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="end with one 1 GiB device copy (byte-counter calibration under rocprofv3)")
     return ap.parse_args()
 
 
@@ -147,6 +149,63 @@ def time_variant(path, T, steps, warmup, flush, torch):
     return {k: statistics.median(v) for k, v in res.items()}, res
 
 
+def time_graph(path, T, steps, warmup, flush, torch):
+    """Median duration (ms) of one whole step replayed as a captured HIP graph
+    (estimate, every level's scan, combine), caches evicted before each replay."""
+    stream = torch.cuda.current_stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        cs = torch.cuda.current_stream()
+        path.estimate(cs)
+        path.decode(T, cs)
+        path.combine(cs)
+    ts = []
+    for it in range(warmup + steps):
+        evict_caches(flush)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        if it >= warmup:
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+    torch.cuda.synchronize()
+    return statistics.median(ts)
+
+
+def kernel_sources_sha():
+    """SHA-256 over the HIP sources of the library (identifies the kernels)."""
+    import glob
+    import hashlib
+
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_33410_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def counter_traffic(workload_name):
+    """HBM bytes per dense decode launch from the committed counter summary,
+    or None when it is absent or was taken on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", "decode_traffic_counters.txt")
+    if not os.path.exists(path):
+        return None, None
+    rec = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("record:"):
+                r = json.loads(line[len("record:"):])
+                rec[r["workload"]] = r
+    r = rec.get(workload_name)
+    if r is None or r.get("source_sha256") != kernel_sources_sha():
+        return None, r
+    kib = r["fetch_kib"] * r["fetch_scale"] + r["write_kib"] * r["write_scale"]
+    return kib * 1024.0, r
+
+
 def cpu_baseline(wl, budget_s):
     """The FP64 oracle timed on this host on a bounded sample of the workload's
     (kv sequence, kv head) chunks; scaled to one whole call."""
@@ -168,22 +227,26 @@ def cpu_baseline(wl, budget_s):
     chunks_all = [(s, g) for s in range(lv.num_seqs) for g in range(wl.num_kv_heads)]
     done = 0
     t0 = time.perf_counter()
-    for c in chunks_all:
-        oracle.decode_level(q_bits, k_bits, v_bits, num_kv_heads=wl.num_kv_heads,
-                            page_size=wl.page_size, sm_scale=wl.sm_scale,
-                            seq_lens=lv.seq_lens_host, block_table=bt, z=z, T=math.inf,
-                            num_splits=wl.level_splits[0], chunks=[c])
-        done += 1
+    while True:  # whole calls (or a prefix of one) until the time budget is used
+        for c in chunks_all:
+            oracle.decode_level(q_bits, k_bits, v_bits, num_kv_heads=wl.num_kv_heads,
+                                page_size=wl.page_size, sm_scale=wl.sm_scale,
+                                seq_lens=lv.seq_lens_host, block_table=bt, z=z, T=math.inf,
+                                num_splits=wl.level_splits[0], chunks=[c])
+            done += 1
+            if time.perf_counter() - t0 > budget_s:
+                break
         if time.perf_counter() - t0 > budget_s:
             break
     dt = time.perf_counter() - t0
     per_call_s = dt * len(chunks_all) / done
     keys = sum(lv.seq_lens_host) * wl.num_kv_heads
-    return {"value": per_call_s * 1e6, "unit": "us/call", "cores": threads,
+    return {"value": round(per_call_s * 1e6, 1), "unit": "us/call", "cores": threads,
             "host_cores_visible": cores, "kind": "oracle",
-            "keys_per_s": keys / per_call_s,
-            "sample": f"FP64 oracle decode (T=inf) of {done} of {len(chunks_all)} "
-                      f"(request, kv head) chunks in {dt:.1f} s, scaled to the whole call"}
+            "keys_per_s": round(keys / per_call_s, 1),
+            "sample": f"FP64 oracle decode (T=inf, gather + scores + fold + splits) of "
+                      f"{done} (request, kv head) chunks = {done / len(chunks_all):.2f} whole "
+                      f"calls in {dt:.1f} s, scaled to one call"}
 
 
 def run_workload(i, args, torch, F, make_config, flush, steps, warmup, splits=None):
@@ -197,8 +260,9 @@ def run_workload(i, args, torch, F, make_config, flush, steps, warmup, splits=No
     for T in (math.inf, 16.0) + ((24.0, 12.0) if i == 3 else ()):
         lam = path.read_fraction(T)
         med, _ = time_variant(path, T, steps, warmup, flush, torch)
+        graph_ms = time_graph(path, T, steps, warmup, flush, torch)
         nbytes, keys = kv_bytes(wl, lam)
-        out[T] = {"med": med, "lam": lam, "bytes": nbytes, "keys": keys}
+        out[T] = {"med": med, "graph": graph_ms, "lam": lam, "bytes": nbytes, "keys": keys}
     return wl, out
 
 
@@ -227,6 +291,7 @@ def main():
     dec_ms = dense["med"]["dec"]
     achieved = dense["bytes"] / (dec_ms * 1e-3) / 1e9
     step_ms = dense["med"]["step"]
+    traffic, trec = counter_traffic(CONFIG_NAMES[args.config])
     line = {
         "metric": METRIC,
         "value": round(step_ms * 1e3, 2),
@@ -244,25 +309,39 @@ def main():
                    "q_heads": wl.num_heads, "kv_heads": wl.num_kv_heads,
                    "head_dim": wl.head_dim, "keys_per_request": wl.flat.seq_lens_host[0],
                    "page_size": wl.page_size, "splits": wl.level_splits,
-                   "step": "estimate + split scan + combine, T=inf",
-                   "timing": "median of per-step HIP events, 1 GiB read before each step evicts all caches"},
+                   "step": "estimate + split scan + combine at T=inf, launched on one stream",
+                   "timing": "median over steps of HIP events around the step on its stream; "
+                             "a 1 GiB read before each step evicts all caches"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": None, "kernel": "decode_split_kernel",
+                     "traffic": None if traffic is None else int(traffic),
+                     "kernel": "decode_mfma_kernel" if wl.group > 1 else "decode_split_kernel",
                      "algorithmic_bytes_per_launch": int(dense["bytes"]),
-                     "avg_launch_us": round(dec_ms * 1e3, 2)},
-        "breakdown_us": {"T=inf": {k: round(v * 1e3, 2) for k, v in dense["med"].items()},
-                         "T=16": {k: round(v * 1e3, 2) for k, v in t16["med"].items()}},
+                     "avg_launch_us": round(dec_ms * 1e3, 2),
+                     "launch_timing": "HIP events around the eager launch on its stream"},
         "t16_us_per_call": round(t16["med"]["step"] * 1e3, 2),
+        "graph_replay_us_per_call": {"T=inf": round(dense["graph"] * 1e3, 2),
+                                     "T=16": round(t16["graph"] * 1e3, 2)},
+        "breakdown_us_eager": {"T=inf": {k: round(v * 1e3, 2) for k, v in dense["med"].items()},
+                               "T=16": {k: round(v * 1e3, 2) for k, v in t16["med"].items()}},
         "t16_decode_gbps": round(t16["bytes"] / (t16["med"]["dec"] * 1e-3) / 1e9, 1),
         "t16_value_read_fraction": round(t16["lam"], 5),
         "t16_speedup_decode": round(dense["med"]["dec"] / t16["med"]["dec"], 3),
+        "t16_speedup_step": round(dense["med"]["step"] / t16["med"]["step"], 3),
         "keys_per_s": round(dense["keys"] / (step_ms * 1e-3), 1),
         "wall_s": round(wall, 2),
     }
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(line), flush=True)
+
+    if args.calibrate_copy:  # a plain copy of known size for byte-counter calibration
+        src = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        evict_caches(flush)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     if args.all:
         for i in (1, 2, 3, 4, 5):
@@ -271,6 +350,7 @@ def main():
             for T, v in r.items():
                 rec = {"workload": CONFIG_NAMES[i], "T": "inf" if math.isinf(T) else T,
                        "us_per_call": round(v["med"]["step"] * 1e3, 2),
+                       "us_per_call_graph": round(v["graph"] * 1e3, 2),
                        "decode_us": round(v["med"]["dec"] * 1e3, 2),
                        "estimate_us": round(v["med"]["est"] * 1e3, 2),
                        "combine_us": round(v["med"]["comb"] * 1e3, 2),
