@@ -137,8 +137,9 @@ const char* fold_last_error(void);
 
 /* Rows per read group and number of read groups per (kv sequence, kv head)
  * that fold_decode_split uses for this view (the group over which read
- * verdicts are ORed, Section 4 "Weight-gated reads").  Returns -1 on an
- * invalid view. */
+ * verdicts are ORed, Section 4 "Weight-gated reads"): 1 when one row attends
+ * a (kv sequence, kv head), 16 for up to 16 rows, 32 for up to 32, and 64 above
+ * that (stacked rows, Appendix E).  Returns -1 on an invalid view. */
 int32_t fold_decode_rows_per_group(const fold_kv_view* kv, const fold_q_view* q);
 int32_t fold_decode_row_groups(const fold_kv_view* kv, const fold_q_view* q);
 

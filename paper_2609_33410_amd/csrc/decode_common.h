@@ -75,11 +75,21 @@ __device__ __forceinline__ ScanPlace scan_place(const DecodeArgs& a) {
   return p;
 }
 
-// Buffer resources over the valid keys of 16-key chunk c of (seq, kvh):
-// empty past the sequence end or for a page id outside [0, num_pages).
+// Block-table entry of the page holding 16-key chunk c of the sequence (0 for
+// a contiguous view or past the sequence end).  A scalar load: issuing it well
+// before chunk_rsrc_at() hides its latency.
+__device__ __forceinline__ int chunk_page(const ScanGeometry& g, const ScanPlace& p, int c) {
+  if (g.page_size <= 0 || c >= p.nchunks) return 0;
+  return ld_uniform(g.block_table,
+                    static_cast<size_t>(p.seq) * g.max_pages + (c * kChunk) / g.page_size);
+}
+
+// Buffer resources over the valid keys of 16-key chunk c of (seq, kvh), given
+// the chunk's block-table entry: empty past the sequence end or for a page id
+// outside [0, num_pages).
 template <int D>
-__device__ __forceinline__ void chunk_rsrc(const ScanGeometry& g, const ScanPlace& p, int c,
-                                           rsrc_t* rk, rsrc_t* rv) {
+__device__ __forceinline__ void chunk_rsrc_at(const ScanGeometry& g, const ScanPlace& p, int c,
+                                              int phys, rsrc_t* rk, rsrc_t* rv) {
   const uint16_t* kb = g.k;
   const uint16_t* vb = g.v;
   uint32_t bytes = 0;
@@ -90,7 +100,6 @@ __device__ __forceinline__ void chunk_rsrc(const ScanGeometry& g, const ScanPlac
     bool ok = true;
     if (g.page_size > 0) {
       const int page = key0 / g.page_size;
-      const int phys = ld_uniform(g.block_table, static_cast<size_t>(p.seq) * g.max_pages + page);
       ok = phys >= 0 && phys < g.num_pages;
       off = ((static_cast<size_t>(ok ? phys : 0) * g.hkv + p.kvh) * g.page_size +
              (key0 - page * g.page_size)) * D;
@@ -105,6 +114,12 @@ __device__ __forceinline__ void chunk_rsrc(const ScanGeometry& g, const ScanPlac
   }
   *rk = make_rsrc(kb, bytes);
   *rv = make_rsrc(vb, bytes);
+}
+
+template <int D>
+__device__ __forceinline__ void chunk_rsrc(const ScanGeometry& g, const ScanPlace& p, int c,
+                                           rsrc_t* rk, rsrc_t* rv) {
+  chunk_rsrc_at<D>(g, p, c, chunk_page(g, p, c), rk, rv);
 }
 
 }  // namespace fold

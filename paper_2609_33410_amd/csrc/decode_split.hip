@@ -288,17 +288,21 @@ hipError_t launch_valu(const DecodeArgs& a, unsigned blocks, hipStream_t stream)
 
 }  // namespace
 
-// Rows per read group: one row (MHA, VALU scan) or 16 / 32 rows (matrix-core
-// scan for GQA groups and stacked cascade rows).
+// Rows per read group: one row (MHA, VALU scan), 16 / 32 rows (matrix-core
+// scan for GQA groups and small stacks), or 64 rows (the stacked-row scan for
+// more than 32 rows on one kv sequence).
 int decode_rows_per_group(int rows_per_seq) {
   if (rows_per_seq <= 1) return 1;
   if (rows_per_seq <= 16) return 16;
-  return 32;
+  if (rows_per_seq <= 32) return 32;
+  return 64;
 }
 
 hipError_t launch_decode_mfma(const DecodeArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_decode_stacked(const DecodeArgs& a, int head_dim, hipStream_t stream);
 
 hipError_t launch_decode(const DecodeArgs& a, int head_dim, hipStream_t stream) {
+  if (a.rows_per_group == 64) return launch_decode_stacked(a, head_dim, stream);
   if (a.rows_per_group > 1) return launch_decode_mfma(a, head_dim, stream);
   const long long blocks = static_cast<long long>(a.geo.num_seqs) * a.geo.hkv * a.num_splits *
                            a.row_groups;

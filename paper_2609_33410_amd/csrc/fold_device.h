@@ -107,6 +107,13 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Two FP32 values rounded to nearest even BF16 and packed, a in the low half
+// (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16_rne(float a, float b) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2));
+}
+
 // Round-to-nearest-even FP32 -> BF16 bits (NaN stays a quiet NaN).
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);

@@ -123,10 +123,16 @@ def test_row_group_queries(lib):
     # MHA: one row per read group (VALU scan)
     mha = _kv(num_kv_heads=8)
     assert lib.fold_decode_rows_per_group(ctypes.byref(mha), ctypes.byref(_q())) == 1
-    # 64 requests x 8 heads stacked on one kv sequence: 512 rows in groups of 32
+    # 64 requests x 8 heads stacked on one kv sequence: 512 rows in groups of 64
     csr = _kv(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=64, num_kv_heads=1)
-    assert lib.fold_decode_rows_per_group(ctypes.byref(csr), ctypes.byref(_q())) == 32
-    assert lib.fold_decode_row_groups(ctypes.byref(csr), ctypes.byref(_q())) == 16
+    assert lib.fold_decode_rows_per_group(ctypes.byref(csr), ctypes.byref(_q())) == 64
+    assert lib.fold_decode_row_groups(ctypes.byref(csr), ctypes.byref(_q())) == 8
+    # 4 requests x 8 heads: 32 rows, one matrix-core group; 5 requests: 40 rows, stacked
+    csr4 = _kv(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=4, num_kv_heads=1)
+    assert lib.fold_decode_rows_per_group(ctypes.byref(csr4), ctypes.byref(_q())) == 32
+    csr5 = _kv(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=5, num_kv_heads=1)
+    assert lib.fold_decode_rows_per_group(ctypes.byref(csr5), ctypes.byref(_q())) == 64
+    assert lib.fold_decode_row_groups(ctypes.byref(csr5), ctypes.byref(_q())) == 1
     assert lib.fold_decode_row_groups(ctypes.byref(_kv(head_dim=5)), ctypes.byref(_q())) == -1
 
 

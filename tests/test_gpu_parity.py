@@ -14,7 +14,7 @@ import torch
 
 import oracle
 from tests import _adapt, _gpu
-from workloads import host_bits, make_config, make_custom
+from workloads import host_bits, make_cascade, make_config, make_custom
 
 pytestmark = pytest.mark.gpu
 INF = float("inf")
@@ -185,6 +185,31 @@ def test_page_size_64_and_dim64_gqa8():
         _full_parity(wl, T, splits=[2])
 
 
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("requests,prefix,splits,shallow", [(5, 1488, (3, 2), 6.0),
+                                                            (8, 1024, (1, 1), 6.0),
+                                                            (12, 2000, (4, 3), 6.0),
+                                                            (17, 80, (2, 1), 4.0)])
+def test_stacked_rows_cascade(d, requests, prefix, splits, shallow):
+    """Prefix levels of more than 32 stacked rows (the stacked-row scan): 40 rows
+    (one partial read group), 64 (one full group), 96 (a full and a partial group)
+    and 136 (three groups); prefixes ending inside a 64-key tile and fewer tiles
+    than splits.  At the shallow depth most 32-key halves of a tile are unread
+    while a quarter to half of the rows keep live keys."""
+    wl = make_cascade(requests=requests, heads=8, kv_heads=1, dim=d, prefix_len=prefix,
+                      suffix_len=48, splits=splits, seed=requests + d, device="cuda")
+    for T in (INF, 16.0, shallow):
+        _full_parity(wl, T)
+
+
+def test_stacked_rows_two_kv_heads():
+    """Eight heads on two kv heads with 24 requests: 96 stacked rows per (prefix, kv head)."""
+    wl = make_cascade(requests=24, heads=8, kv_heads=2, dim=128, prefix_len=784, suffix_len=32,
+                      splits=(2, 1), seed=3, device="cuda")
+    for T in (INF, 6.0):
+        _full_parity(wl, T)
+
+
 # ------------------------------------------------------- invariants ---------
 def test_mass_kept_L_independent_of_T():
     wl = make_config(2, batch=2, seq_len=3000, device="cuda")
@@ -195,13 +220,14 @@ def test_mass_kept_L_independent_of_T():
         assert torch.equal(a["part_L"], b["part_L"])
 
 
-@pytest.mark.parametrize("cfg,T", [(1, INF), (1, 16.0), (2, INF), (2, 16.0), (5, 16.0)])
-def test_debug_exports_do_not_change_results(cfg, T):
+@pytest.mark.parametrize("cfg,T,batch", [(1, INF, None), (1, 16.0, None), (2, INF, 4),
+                                         (2, 16.0, 4), (5, 16.0, 4), (5, INF, 12), (5, 6.0, 12)])
+def test_debug_exports_do_not_change_results(cfg, T, batch):
     """The kernel variant that exports x and read gates computes the same bits
     as the production variant, so the exported decisions are the production
-    kernel's decisions."""
-    wl = make_config(cfg, device="cuda", batch=None if cfg == 1 else 4,
-                     seq_len=None if cfg == 1 else 1500)
+    kernel's decisions.  Config 5 with 4 requests stacks 32 rows on the prefix;
+    with 12 requests, 96 rows (the stacked-row scan, two read groups)."""
+    wl = make_config(cfg, device="cuda", batch=batch, seq_len=None if cfg == 1 else 1500)
     z = _gpu.estimate(wl)
     a = _gpu.run(wl, T, z=z, debug=False)
     b = _gpu.run(wl, T, z=z, debug=True)

@@ -12,6 +12,7 @@ from .synth import (  # noqa: F401
     KVView,
     Workload,
     host_bits,
+    make_cascade,
     make_config,
     make_custom,
 )

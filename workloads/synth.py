@@ -28,7 +28,7 @@ from __future__ import annotations
 
 import math
 from dataclasses import dataclass, field
-from typing import Dict, List, Optional
+from typing import Dict, List, Optional, Tuple
 
 import numpy as np
 import torch
@@ -307,6 +307,17 @@ def make_config(i: int, seed: int = 0, device: str = "cpu", *, batch: Optional[i
                                  device=device, level_splits=[32, 8], depths=[INF, 16.0],
                                  keep_logical=keep_logical)
     raise ValueError(f"no workload {i}")
+
+
+def make_cascade(*, requests: int, heads: int, kv_heads: int, dim: int, prefix_len: int,
+                 suffix_len: int, splits: Tuple[int, int] = (1, 1), seed: int = 0,
+                 device: str = "cpu", keep_logical: bool = False) -> Workload:
+    """A small shared-prefix cascade of any shape for tests (lengths multiples of 16)."""
+    return _generate_cascade(name="custom-cascade", requests=requests, heads=heads,
+                             kv_heads=kv_heads, dim=dim, prefix_len=prefix_len,
+                             suffix_len=suffix_len, page_size=16, seed=seed, device=device,
+                             level_splits=list(splits), depths=[INF, 16.0],
+                             keep_logical=keep_logical)
 
 
 def make_custom(*, batch: int, heads: int, kv_heads: int, dim: int, lens: List[int],
