@@ -277,20 +277,22 @@ __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeA
     __syncthreads();
   }
 
-  const size_t slot = static_cast<size_t>(a.slot_offset) + sc.p.split;
-  for (int idx = threadIdx.x; idx < R * D; idx += kScanThreads) {
-    // idx = ((b * NB + blk) * 4 + i) * 64 + l  ->  row 16 b + l % 16, channel 16 blk + 4 (l / 16) + i
-    const int l = idx & 63;
-    const int i = (idx >> 6) & 3;
-    const int blk = (idx >> 8) % S::NB;
-    const int b = (idx >> 8) / S::NB;
-    const int r = 16 * b + (l & 15);
-    const int d = 16 * blk + 4 * (l >> 4) + i;
-    const RowInfo ri = row_info(g, sc.p.seq, sc.p.kvh, sc.p.rg * R + r, sc.p.nrows, sc.p.req0);
-    if (!ri.ok) continue;
-    const size_t row = (slot * g.batch + ri.req) * g.heads + ri.head;
-    a.part_A[row * D + d] = red[idx];
-    if (d == 0) a.part_L[row] = redl[b * 64 + (l & 15)];
+  // The LDS sums sit at ((b * NB + blk) * 4 + i) * 64 + l for row 16 b + l%16
+  // and channel 16 blk + 4 (l/16) + i.  Wave i, lane l writes those entries of
+  // every (b, blk): the rows its lane held during the scan, whose query-row
+  // indices are already known.  No load is issued here: on gfx9 a wait for one
+  // would also wait for the partial stores already in flight.
+  const size_t slot_rows = (static_cast<size_t>(a.slot_offset) + sc.p.split) * g.batch * g.heads;
+  const int wl = threadIdx.x & 63;
+  const int wi = threadIdx.x >> 6;
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+    if (!sc.rok[b]) continue;
+    const size_t row = slot_rows + sc.xrow[b];
+#pragma unroll
+    for (int blk = 0; blk < S::NB; ++blk)
+      a.part_A[row * D + 16 * blk + 4 * (wl >> 4) + wi] = red[((b * S::NB + blk) * 4 + wi) * 64 + wl];
+    if (wi == 0 && wl < 16) a.part_L[row] = redl[b * 64 + wl];
   }
 }
 

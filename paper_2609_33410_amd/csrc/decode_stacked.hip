@@ -104,6 +104,29 @@ __device__ __forceinline__ void dma16(const u32x4& r, uint32_t lds_base, uint32_
                : "memory", "m0");
 }
 
+// Global loads issued from assembly, like the DMAs: the compiler does not
+// track them, so they may overlap the first tile DMAs; the caller waits for
+// them with an explicit s_waitcnt and then passes the registers through
+// tie_regs() so that no use is scheduled before that wait.
+__device__ __forceinline__ u32x4 gload16(const void* p) {
+  u32x4 r;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(p) : "memory");
+  return r;
+}
+__device__ __forceinline__ uint32_t gload4(const void* p) {
+  uint32_t r;
+  asm volatile("global_load_dword %0, %1, off" : "=v"(r) : "v"(p) : "memory");
+  return r;
+}
+template <int N>
+__device__ __forceinline__ void tie_regs(u32x4 (&q)[N], uint32_t& z) {
+  static_assert(N == 2 || N == 4, "operand count");
+  if constexpr (N == 4)
+    asm volatile("" : "+v"(q[0]), "+v"(q[1]), "+v"(q[2]), "+v"(q[3]), "+v"(z) : : "memory");
+  else
+    asm volatile("" : "+v"(q[0]), "+v"(q[1]), "+v"(z) : : "memory");
+}
+
 // Workgroup barrier for LDS traffic only: this wave's LDS operations complete,
 // then s_barrier.  __syncthreads() would also wait for every outstanding
 // vector-memory load; the DMA of the data about to be read is waited for
@@ -183,21 +206,38 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
     return __builtin_amdgcn_readlane(ptab, j & (kWaveSize - 1));
   };
 
-  // Prologue loads: the first page-table window, then the row's query and
-  // reference; all complete before the first DMA, so that inside the loops the
-  // only outstanding vector-memory operations are the DMAs counted below.
+  // Prologue loads: the first page-table window and the row list (the
+  // compiler waits for both before their values are used), then the row's
+  // query and reference from assembly: they are in flight together with the
+  // first tile DMAs and have landed once the first key tile has.
   if (g.page_size > 0 && m > 0) load_ptab(0);
   const RowInfo ri = row_info(g, p.seq, p.kvh, p.rg * kStkRows + 16 * rb + n16, p.nrows, p.req0);
   const size_t qrow = static_cast<size_t>(ri.req) * g.heads + ri.head;
-  // A row outside the group gets Z = +inf (and q = 0): x = -inf, its weights
-  // are exactly 0 and it is never live, without per-key selects.
-  const float zr = ri.ok ? a.z[qrow] : INFINITY;
+  // Block-table entries of tiles 0..4, read (and the page-table load waited
+  // for) before the assembly loads below are issued; the empty asm pins that
+  // order.
+  const int pg0 = page_of(0), pg1 = page_of(1), pg2 = page_of(2), pg3 = page_of(3),
+            pg4 = page_of(4);
+  asm volatile("" : : "s"(pg0), "s"(pg1), "s"(pg2), "s"(pg3), "s"(pg4));
   u32x4 qb[NK];
+  uint32_t zbits;
+  {
+    // a row outside the group reads row 0 (there is at least one row) and is
+    // replaced below
+    const uint16_t* qp = a.q + (ri.ok ? qrow * D : 0) + 8 * grp;
 #pragma unroll
-  for (int c = 0; c < NK; ++c)
-    qb[c] = ri.ok ? *reinterpret_cast<const u32x4*>(a.q + qrow * D + 32 * c + 8 * grp)
-                  : u32x4{0, 0, 0, 0};
-  wait_vmcnt<0>();
+    for (int c = 0; c < NK; ++c) qb[c] = gload16(qp + 32 * c);
+    zbits = gload4(a.z + (ri.ok ? qrow : 0));
+  }
+  float zr = 0.0f;
+  auto settle_row = [&]() {
+    tie_regs(qb, zbits);
+    // A row outside the group gets Z = +inf and q = 0: x = -inf, its weights
+    // are exactly 0 and it is never live, without per-key selects.
+    zr = ri.ok ? __uint_as_float(zbits) : INFINITY;
+#pragma unroll
+    for (int c = 0; c < NK; ++c) qb[c] = ri.ok ? qb[c] : u32x4{0, 0, 0, 0};
+  };
 
   // Slot permutation of a key row.  With 256-byte rows (D = 128) the 16 keys a
   // K-operand read covers need 16 distinct slots: f = k & 15; the two 16-lane
@@ -382,7 +422,6 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
   if (DENSE && m > 0) {
     // Issue order: K0, then pairs (K(i+1), V(i)).  Keys of tile j in K stage
     // j % 4, values in V stage j % 4.
-    const int pg0 = page_of(0), pg1 = page_of(1), pg2 = page_of(2), pg3 = page_of(3);
     fetch_k(0, pg0, 0);
     int issued = 0;  // pairs issued
     if (m > 0) { if (m > 1) fetch_k(1, pg1, 1); fetch_v(0, pg0, 0, ~0ull); ++issued; }
@@ -391,6 +430,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
     // K0 landed: behind it two groups per issued pair, less the key group of
     // a pair whose tile i+1 does not exist
     wait_groups<NLD>(2 * issued - (issued == m ? 1 : 0));
+    settle_row();  // Q and Z were issued before K0
     lds_barrier();
     f32x4 s[2];
     qk(0, s);
@@ -401,7 +441,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
     }
     int ks1 = 1, vs0 = 0, s3 = 3;  // K stage of t+1, V stage of t, stage of tile t+3
     int pv3 = pg3;                  // page of tile t+3 (values)
-    int pk4 = page_of(4);           // page of tile t+4 (keys)
+    int pk4 = pg4;                  // page of tile t+4 (keys)
     for (int t = 0; t < m; ++t) {
       // landed: K(t+1), V(t); in flight behind them: pairs t+1, t+2
       wait_groups<NLD>((t + 2 < m) + (t + 1 < m) + (t + 3 < m) + (t + 2 < m));
@@ -434,10 +474,11 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
   } else if (!DENSE && m > 0) {
     // Issue order: K0 K1 V0 K2 V1 | K3 V2 | K4 V3 | ...  Keys of tile j in K
     // stage j % 4, values in V stage j % 3.
-    const int ph0 = page_of(0), ph1 = page_of(1);
+    const int ph0 = pg0, ph1 = pg1;
     fetch_k(0, ph0, 0);
     if (m > 1) fetch_k(1, ph1, 1);
     wait_groups<NLD>(m > 1 ? 1 : 0);
+    settle_row();  // Q and Z were issued before K0
     lds_barrier();
     f32x4 s[2];
     qk(0, s);
@@ -447,7 +488,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
     debug_gates(0, w0.mask);
     fetch_v(0, ph0, 0, w0.mask);
     TileW w1 = {};
-    int ph2 = page_of(2), ph3 = page_of(3);
+    int ph2 = pg2, ph3 = pg3;
     if (m > 2) fetch_k(2, ph2, 2);
     if (m > 1) {
       wait_groups<NLD>(m > 2 ? 2 : 1);  // K1 landed; V0, K2 may fly
@@ -500,6 +541,11 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
     }
   }
 
+  if (m == 0) {
+    wait_vmcnt<0>();
+    settle_row();
+  }
+
   // L partials: the four lane groups of a row hold different keys.
   lsum += __shfl_xor(lsum, 16, 64);
   lsum += __shfl_xor(lsum, 32, 64);
@@ -521,11 +567,19 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
     const size_t slot = static_cast<size_t>(a.slot_offset) + p.split;
     const size_t prow = (slot * g.batch + ri.req) * g.heads + ri.head;
     float* dst = a.part_A + prow * D + 4 * grp;
+    const bool aligned = (reinterpret_cast<uintptr_t>(a.part_A) & 15) == 0;  // uniform
 #pragma unroll
-    for (int blk = 0; blk < NB; ++blk)
+    for (int blk = 0; blk < NB; ++blk) {
+      f32x4 v;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        dst[16 * blk + i] = acc[blk][i] + red[((rb * NB + blk) * 4 + i) * 64 + lane];
+      for (int i = 0; i < 4; ++i) v[i] = acc[blk][i] + red[((rb * NB + blk) * 4 + i) * 64 + lane];
+      if (aligned) {
+        *reinterpret_cast<f32x4*>(dst + 16 * blk) = v;
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dst[16 * blk + i] = v[i];
+      }
+    }
     if (grp == 0) a.part_L[prow] = lsum + redl[rb * 64 + lane];
   }
 }
