@@ -1,0 +1,358 @@
+"""Pins of the two-plane INT8 key oracle against facts other than itself (CPU).
+
+Each test names what fixes the expected value: a hand-computed fixture,
+exact rational arithmetic, a closed form, library softmax over the
+dequantized operands, or an invariant of the method.
+"""
+
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import q8_oracle as q8
+from oracle import bf16_bits_to_f64, combine
+from tests import _adapt
+from workloads import host_bits, make_cascade, make_custom
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+INF = float("inf")
+
+
+def _bits(x):
+    """BF16 bits of FP32-representable values that BF16 holds exactly."""
+    return (np.asarray(x, dtype=np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
+def _rand_bits(shape, seed, scale=1.0):
+    g = torch.Generator().manual_seed(seed)
+    t = (torch.randn(*shape, generator=g) * scale).to(torch.bfloat16)
+    return host_bits(t)
+
+
+# ------------------------------------------------------------------ Q1 -----
+@pytest.mark.parametrize("d", [1, 2, 4, 8, 64, 128])
+def test_hadamard_is_orthogonal_up_to_d(d):
+    """Closed form: H H^T = D I, entries +-1, first row and column all ones."""
+    h = q8.hadamard(d)
+    assert np.array_equal(np.abs(h), np.ones((d, d)))
+    assert np.array_equal(h @ h.T, d * np.eye(d))
+    assert np.all(h[0] == 1) and np.all(h[:, 0] == 1)
+
+
+def test_rotation_is_exact_rational_sum():
+    """Exact arithmetic: each rotated coordinate equals the rational sum of +-inputs."""
+    bits = _rand_bits((6, 128), seed=11)
+    rot = q8.rotate(bf16_bits_to_f64(bits))
+    h = q8.hadamard(128)
+    vals = bf16_bits_to_f64(bits)
+    for r in range(bits.shape[0]):
+        for i in (0, 1, 37, 127):
+            exact = sum(Fraction(float(vals[r, j])) * int(h[i, j]) for j in range(128))
+            assert Fraction(float(rot[r, i])) == exact
+
+
+def test_rotated_dot_product_is_d_times_original():
+    """Closed form: (Hq).(Hk) = D q.k."""
+    q = bf16_bits_to_f64(_rand_bits((3, 64), seed=1))
+    k = bf16_bits_to_f64(_rand_bits((5, 64), seed=2))
+    lhs = q8.rotate(q) @ q8.rotate(k).T
+    np.testing.assert_allclose(lhs, 64 * (q @ k.T), rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------------------------ Q2 -----
+def test_key_split_hand_example():
+    """Hand-computed fixture (Section 4, cache format; worked with H_4)."""
+    fx = json.load(open(os.path.join(GOLDEN, "q8_split_example.json")))
+    for key in fx["keys"]:
+        a, b, e = q8.split_keys(_bits(key["k"])[None, :])
+        assert np.array_equal(q8.rotate(np.array(key["k"])[None, :])[0], key["rotated"])
+        assert int(e[0]) == key["scale_bits"]
+        assert float(bf16_bits_to_f64(e)[0]) == key["scale"]
+        assert a[0].tolist() == key["a"]
+        assert b[0].tolist() == key["b"]
+
+
+def test_key_split_bounds_and_minimal_scale():
+    """Closed forms: |a| <= 127, |k'' - e(a + b/256)| <= e/256 (<= e/512 unless b
+    was clamped), and e is the smallest BF16 value with max|k''|/e <= 127."""
+    bits = _rand_bits((300, 128), seed=5, scale=3.0)
+    bits[7] = 0                                  # an all-zero key
+    bits[8] = _bits(np.where(np.arange(128) == 3, 100.0, 0.0))  # one spike
+    bits[9] = _bits(np.full(128, -0.5))          # constant key: rotated = one coordinate
+    a, b, e_bits = q8.split_keys(bits)
+    rot = q8.rotate(bf16_bits_to_f64(bits))
+    e = bf16_bits_to_f64(e_bits)
+    assert np.abs(a.astype(int)).max() <= 127
+    rec = q8.dequant(a, b, e)
+    err = np.abs(rec - rot)
+    assert np.all(err <= e[:, None] / 256 + 1e-300)
+    unclamped = b != 127
+    assert np.all(err[unclamped] <= e[:, None].repeat(128, 1)[unclamped] / 512 * (1 + 1e-12))
+    m = np.abs(rot).max(axis=1)
+    nz = m > 0
+    assert np.all(e[~nz] == 0) and np.all(a[~nz] == 0) and np.all(b[~nz] == 0)
+    assert np.all(m[nz] / e[nz] <= 127)
+    smaller = bf16_bits_to_f64((e_bits[nz] - 1).astype(np.uint16))   # next BF16 down
+    assert np.all(m[nz] / smaller > 127)
+    # the key's code depends on that key alone
+    a1, b1, e1 = q8.split_keys(bits[40:41])
+    assert np.array_equal(a1[0], a[40]) and np.array_equal(b1[0], b[40]) and e1[0] == e_bits[40]
+
+
+# ------------------------------------------------------------------ Q3 -----
+def test_query_split_hand_example():
+    """Hand-computed fixture: planes, scale and the refined score vs q.k = 1."""
+    fx = json.load(open(os.path.join(GOLDEN, "q8_split_example.json")))
+    qf = fx["query"]
+    qa, qb, eta = q8.split_queries(_bits(qf["q"])[None, :], qf["sm_scale"])
+    assert qa[0].tolist() == qf["qa"] and qb[0].tolist() == qf["qb"]
+    assert abs(float(eta[0]) - qf["eta_f64"]) <= 2.0 ** -24 * qf["eta_f64"]
+    ka, kb, ke = q8.split_keys(_bits(fx["keys"][0]["k"])[None, :])
+    coarse, refine = q8.coarse_and_refine(qa, qb, eta, ka, kb, bf16_bits_to_f64(ke))
+    s = coarse[0, 0] + refine[0, 0]
+    assert abs(s - qf["refined_score_vs_key0"]) < 1e-6
+    assert abs(s - qf["exact_score_vs_key0"]) < 1e-5
+
+
+def test_query_split_reconstruction():
+    """Closed form: q'' = f (qa + qb/256) within f/256 per coordinate, with
+    f = max|q''|/127 recovered from eta = log2(e) sm f / D."""
+    bits = _rand_bits((40, 64), seed=9)
+    bits[3] = 0
+    sm = 0.125
+    qa, qb, eta = q8.split_queries(bits, sm)
+    rot = q8.rotate(bf16_bits_to_f64(bits))
+    f = eta.astype(np.float64) * 64 / (math.log2(math.e) * sm)
+    rec = f[:, None] * (qa + qb / 256.0)
+    tol = np.abs(rot).max(axis=1, keepdims=True) / 127 / 256 * (1 + 1e-5) + 1e-6 * np.abs(rot)
+    assert np.all(np.abs(rec - rot) <= tol)
+    assert np.abs(qa.astype(int)).max() == 127
+    assert np.all(qa[3] == 0) and eta[3] == 0
+
+
+def test_refine_tau_follows_request_length():
+    """tau = kappa + ceil(log2 n) (the request's own length)."""
+    assert q8.refine_tau(1, 4.0) == 4.0
+    assert q8.refine_tau(2, 4.0) == 5.0
+    assert q8.refine_tau(8192, 4.0) == 17.0
+    assert q8.refine_tau(8193, 4.0) == 18.0
+    assert q8.refine_tau(100000, 0.5) == np.float32(17.5)
+
+
+# ------------------------------------------------------------- Q4/Q6 -------
+def test_scores_equal_dequantized_dot_products():
+    """Independent path: coarse = log2(e) sm (f(qa+qb/256)) . (e a) / D and
+    coarse + refine = the same with the full code e (a + b/256), up to the FP32
+    rounding of eta; both are close to the exact BF16 score."""
+    d, sm = 128, 1 / math.sqrt(128)
+    kb_ = _rand_bits((50, d), seed=21)
+    qb_ = _rand_bits((4, d), seed=22)
+    a, b, e_bits = q8.split_keys(kb_)
+    qa, qb, eta = q8.split_queries(qb_, sm)
+    e = bf16_bits_to_f64(e_bits)
+    coarse, refine = q8.coarse_and_refine(qa, qb, eta, a, b, e)
+    f = np.abs(q8.rotate(bf16_bits_to_f64(qb_))).max(axis=1) / 127
+    qdeq = f[:, None] * (qa + qb / 256.0)
+    scale = math.log2(math.e) * sm / d
+    want_coarse = scale * (qdeq @ (e[:, None] * a).T)
+    want_full = scale * (qdeq @ q8.dequant(a, b, e).T)
+    np.testing.assert_allclose(coarse, want_coarse, rtol=2 ** -23, atol=1e-12)
+    np.testing.assert_allclose(coarse + refine, want_full, rtol=2 ** -23, atol=1e-12)
+    exact = math.log2(math.e) * sm * (bf16_bits_to_f64(qb_) @ bf16_bits_to_f64(kb_).T)
+    assert np.abs(coarse + refine - exact).max() < 1e-3
+    # the refine term is what plane B adds: a strictly smaller correction
+    assert np.abs(coarse + refine - exact).max() < np.abs(coarse - exact).max() / 20
+
+
+def test_refine_term_closed_form_bound():
+    """|refine| <= eta e ||qa + qb/256||_1 / 2, since |b| <= 128 (a sign or
+    scale error in the refine term breaks it)."""
+    a, b, e_bits = q8.split_keys(_rand_bits((80, 64), seed=31, scale=2.0))
+    qa, qb, eta = q8.split_queries(_rand_bits((6, 64), seed=32), 0.125)
+    e = bf16_bits_to_f64(e_bits)
+    _, refine = q8.coarse_and_refine(qa, qb, eta, a, b, e)
+    bound = (eta.astype(np.float64)[:, None] * e[None, :]
+             * np.abs(qa + qb / 256.0).sum(axis=1)[:, None] / 2)
+    assert np.all(np.abs(refine) <= bound * (1 + 1e-12))
+    assert np.abs(refine).max() > 1e-3 * bound.max()   # not vacuous
+
+
+# ------------------------------------------------------------------ Q5 -----
+def _wl(seed=0, lens=(300, 513), heads=8, kv=2, d=64, spikes=6, sinks=2, paged=True):
+    return make_custom(batch=len(lens), heads=heads, kv_heads=kv, dim=d, lens=list(lens),
+                       paged=paged, spike_count=spikes, alpha_spike=3.0, n_sink=sinks,
+                       alpha_sink=6.0, seed=seed)
+
+
+def _q8_inputs(wl, kappa):
+    planes = q8.split_keys(host_bits(wl.k))
+    qa, qb, eta = q8.split_queries(host_bits(wl.q), wl.sm_scale)
+    lens = wl.flat.seq_lens_host
+    tau = np.array([q8.refine_tau(n, kappa) for n in lens], dtype=np.float32)
+    return planes, qa, qb, eta, tau
+
+
+def _run(wl, planes, qa, qb, eta, tau, z, T, splits=1, level=0, **kw):
+    lv = _adapt.level_args(wl.levels[level])
+    return q8.decode_level_q8(qa, qb, eta, planes, host_bits(wl.v), num_kv_heads=wl.num_kv_heads,
+                              page_size=wl.page_size, z=z, T=T, tau=tau, num_splits=splits,
+                              **lv, **kw)
+
+
+@pytest.mark.parametrize("T", [INF, 16.0, 6.0])
+@pytest.mark.parametrize("kappa", [-INF, 2.0, INF])
+def test_gate_invariants(T, kappa):
+    """refine implies live; kappa = +inf refines every live key; T = inf makes
+    every key live; the bits are the same for every row of a GQA group; every
+    counted key has x >= -T and every cut key x < -T."""
+    wl = _wl(seed=1)
+    planes, qa, qb, eta, tau = _q8_inputs(wl, kappa)
+    z = _adapt.estimate(_adapt.oracle_inputs(wl))
+    _, _, info = _run(wl, planes, qa, qb, eta, tau, z, T, want_scores=True)
+    group = wl.num_heads // wl.num_kv_heads
+    for (seq, g), (rows, xc, x, live, ref) in info.items():
+        assert not np.any(ref & ~live)
+        if math.isinf(kappa) and kappa > 0:
+            assert np.array_equal(ref, live)
+        if math.isinf(kappa) and kappa < 0:
+            assert not ref.any()
+        if math.isinf(T):
+            assert live.all()
+        assert np.all(live == live[0]) and np.all(ref == ref[0])   # one request: one group
+        assert len(rows) == group
+        if not math.isinf(T):
+            assert np.all(live == (xc >= -T).any(axis=0))
+            assert np.all((x < -T) | live)
+        assert np.array_equal(x != xc, ref & (x != xc))              # only refined keys move
+
+
+def test_gates_follow_request_not_batch():
+    """Cascade level with stacked rows of several requests: each request's
+    partials equal those of its rows scanned alone (gates do not depend on the
+    batch)."""
+    wl = make_cascade(requests=3, heads=4, kv_heads=1, dim=64, prefix_len=160, suffix_len=48,
+                      seed=4)
+    planes, qa, qb, eta, tau = _q8_inputs(wl, 1.0)
+    z = _adapt.estimate(_adapt.oracle_inputs(wl))
+    lv = _adapt.level_args(wl.levels[0])
+    full_a, full_l = _run(wl, planes, qa, qb, eta, tau, z, 8.0, splits=2)
+    for r in range(3):
+        one = dict(lv)
+        one["row_indptr"] = np.array([0, 1])
+        one["row_req"] = np.array([r])
+        pa, pl = q8.decode_level_q8(qa, qb, eta, planes, host_bits(wl.v),
+                                    num_kv_heads=1, page_size=wl.page_size, z=z, T=8.0, tau=tau,
+                                    num_splits=2, **one)
+        assert np.array_equal(pa[:, r], full_a[:, r]) and np.array_equal(pl[:, r], full_l[:, r])
+
+
+# ------------------------------------------------------------------ Q7 -----
+@pytest.mark.parametrize("d,paged", [(64, True), (128, True), (64, False)])
+def test_dense_full_refine_equals_library_softmax_on_codes(d, paged):
+    """Library routine: at T = inf with every key refined the output is softmax
+    attention over the dequantized rotated operands (torch SDPA in FP64), and it
+    stays close to softmax over the original BF16 operands."""
+    wl = _wl(seed=2, d=d, paged=paged, lens=(200, 77))
+    planes, qa, qb, eta, tau = _q8_inputs(wl, INF)
+    z = np.full((2, wl.num_heads), 3.25)
+    pa, pl = _run(wl, planes, qa, qb, eta, tau, z, INF, splits=3)
+    o, _ = combine(pa, pl)
+    oi = _adapt.oracle_inputs(wl)
+    group = wl.num_heads // wl.num_kv_heads
+    for r, n in enumerate(wl.flat.seq_lens_host):
+        for h in range(wl.num_heads):
+            g = h // group
+            a = q8._gather_raw(planes[0], r, g, n, oi["flat"]["block_table"], wl.page_size)
+            b = q8._gather_raw(planes[1], r, g, n, oi["flat"]["block_table"], wl.page_size)
+            e = bf16_bits_to_f64(q8._gather_raw(planes[2][..., None], r, g, n,
+                                                oi["flat"]["block_table"], wl.page_size)[:, 0])
+            kdeq = q8.dequant(a, b, e)
+            f = float(eta[r, h]) * d / (math.log2(math.e) * wl.sm_scale)
+            qdeq = f * (qa[r, h] + qb[r, h] / 256.0)
+            vals = bf16_bits_to_f64(q8._gather_raw(oi["v_bits"], r, g, n,
+                                                   oi["flat"]["block_table"], wl.page_size))
+            want = torch.nn.functional.scaled_dot_product_attention(
+                torch.from_numpy(qdeq)[None, None, None], torch.from_numpy(kdeq)[None, None],
+                torch.from_numpy(vals)[None, None], scale=wl.sm_scale / d)[0, 0, 0].numpy()
+            np.testing.assert_allclose(o[r, h], want, rtol=0, atol=1e-9 * np.abs(want).max() + 1e-12)
+            qo = bf16_bits_to_f64(oi["q_bits"][r, h])
+            ko = bf16_bits_to_f64(q8._gather_raw(oi["k_bits"], r, g, n,
+                                                 oi["flat"]["block_table"], wl.page_size))
+            plain = torch.nn.functional.scaled_dot_product_attention(
+                torch.from_numpy(qo)[None, None, None], torch.from_numpy(ko)[None, None],
+                torch.from_numpy(vals)[None, None], scale=wl.sm_scale)[0, 0, 0].numpy()
+            assert np.abs(o[r, h] - plain).max() < 2e-3 * max(1.0, np.abs(plain).max())
+
+
+@pytest.mark.parametrize("T,kappa", [(INF, 0.0), (12.0, 3.0), (5.0, -INF), (INF, INF)])
+def test_partials_add_over_splits(T, kappa):
+    """Additivity: the splits' partials add up to the one-split pair at any
+    depth and refine threshold (every decision is per key)."""
+    wl = _wl(seed=3, lens=(700, 130))
+    planes, qa, qb, eta, tau = _q8_inputs(wl, kappa)
+    z = _adapt.estimate(_adapt.oracle_inputs(wl))
+    a1, l1 = _run(wl, planes, qa, qb, eta, tau, z, T, splits=1)
+    a5, l5 = _run(wl, planes, qa, qb, eta, tau, z, T, splits=5)
+    np.testing.assert_allclose(a5.sum(axis=0), a1[0], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(l5.sum(axis=0), l1[0], rtol=1e-12, atol=1e-14)
+
+
+def test_huge_finite_depth_equals_dense():
+    """A depth above every |x| keeps every key live: same as T = inf."""
+    wl = _wl(seed=6)
+    planes, qa, qb, eta, tau = _q8_inputs(wl, 2.0)
+    z = _adapt.estimate(_adapt.oracle_inputs(wl))
+    ad, ld = _run(wl, planes, qa, qb, eta, tau, z, INF, splits=2)
+    ah, lh = _run(wl, planes, qa, qb, eta, tau, z, 1e30, splits=2)
+    assert np.array_equal(ad, ah) and np.array_equal(ld, lh)
+
+
+def test_imposed_mode_reproduces_own_decisions():
+    """Imposed decisions taken from FP32 copies of the oracle's own scores give
+    the own-mode partials wherever no score sits within FP32 rounding of -T or
+    -tau (here: none does)."""
+    wl = _wl(seed=7)
+    planes, qa, qb, eta, tau = _q8_inputs(wl, 2.0)
+    z = _adapt.estimate(_adapt.oracle_inputs(wl))
+    T = 9.0
+    pa, pl, info = _run(wl, planes, qa, qb, eta, tau, z, T, want_scores=True)
+    b_, h = wl.q.shape[:2]
+    n_max = max(wl.flat.seq_lens_host)
+    ixc = np.zeros((b_, h, n_max), dtype=np.float32)
+    ix = np.zeros((b_, h, n_max), dtype=np.float32)
+    for (seq, g), (rows, xc, x, live, ref) in info.items():
+        for k, (r, hh) in enumerate(rows):
+            ixc[r, hh, :xc.shape[1]] = xc[k]
+            ix[r, hh, :x.shape[1]] = x[k]
+        assert np.abs(np.abs(xc) - T).min() > 1e-4
+    pa2, pl2 = _run(wl, planes, qa, qb, eta, tau, z, T, imposed=(ixc, ix))
+    assert np.array_equal(pa, pa2) and np.array_equal(pl, pl2)
+
+
+# --------------------------------------------------------------- estimate -
+def test_estimate_on_coarse_scores_is_exact_lse_when_short():
+    """Closed form: for n <= 192 the estimate is log2 sum 2^coarse."""
+    wl = _wl(seed=8, lens=(150, 192))
+    planes, qa, qb, eta, _ = _q8_inputs(wl, 0.0)
+    oi = _adapt.oracle_inputs(wl)
+    z = q8.estimate_level_q8(qa, qb, eta, planes, num_kv_heads=wl.num_kv_heads,
+                             page_size=wl.page_size, seq_lens=oi["flat"]["seq_lens"],
+                             block_table=oi["flat"]["block_table"])
+    group = wl.num_heads // wl.num_kv_heads
+    for r, n in enumerate(wl.flat.seq_lens_host):
+        for h in range(wl.num_heads):
+            g = h // group
+            bt = oi["flat"]["block_table"]
+            a = q8._gather_raw(planes[0], r, g, n, bt, wl.page_size)
+            e = bf16_bits_to_f64(q8._gather_raw(planes[2][..., None], r, g, n, bt,
+                                                wl.page_size)[:, 0])
+            f = float(eta[r, h]) * 64 / (math.log2(math.e) * wl.sm_scale)
+            s = (math.log2(math.e) * wl.sm_scale / 64) * ((e[:, None] * a) @ (
+                f * (qa[r, h] + qb[r, h] / 256.0)))
+            want = float(np.logaddexp2.reduce(s))
+            assert abs(z[r, h] - want) < 1e-5
