@@ -1,7 +1,8 @@
 """FoldAttention decode hot path for MI355X (gfx950).
 
 The compute path is ``libfold.so`` (hand-written HIP kernels behind the C ABI
-of ``include/fold.h``); :mod:`paper_2609_33410_amd.fold` is its ctypes
+of ``include/fold.h`` and ``include/fold_q8.h``);
+:mod:`paper_2609_33410_amd.fold` is its ctypes
 binding.  PyTorch supplies device memory and streams only.
 """
 
@@ -16,13 +17,23 @@ from .fold import (  # noqa: F401
     LIB_PATH,
     FoldError,
     FoldLibraryMissing,
+    Q8Keys,
+    Q8Query,
     fold_combine,
     fold_decode,
     fold_decode_row_groups,
     fold_decode_rows_per_group,
     fold_decode_split,
+    fold_q8_decode_row_groups,
+    fold_q8_decode_rows_per_group,
+    fold_q8_decode_split,
+    fold_q8_ref_estimate,
+    fold_q8_split_query,
+    fold_q8_write_keys,
     fold_ref_estimate,
     kv_view,
     load_library,
+    q8_empty_keys,
+    q8_empty_query,
     q_view,
 )

@@ -18,7 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libfold.so")
 
-SOURCES = ["decode_split.hip", "decode_mfma.hip", "decode_stacked.hip", "ref_estimate.hip", "combine.hip", "fold_api.cpp"]
+SOURCES = ["decode_split.hip", "decode_mfma.hip", "decode_stacked.hip", "ref_estimate.hip", "combine.hip",
+           "decode_q8.hip", "q8_front.hip", "fold_api.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -1,0 +1,427 @@
+// Gated split-KV decode over a two-plane INT8 key cache (Section 4, "Cache
+// format", "Weight-gated reads", "Value product"; Algorithm 1 with BF16 values).
+//
+// Workgroup = (kv sequence, kv head, split, read group of 16*RB query rows);
+// four wave64s; wave w owns 16-key chunk 4t + w of each 64-key tile t of its
+// split, as in the BF16 scan.  Per chunk and 16-row block:
+//
+//   coarse   c_aa = A_keys . Qa^T and c_ab = A_keys . Qb^T with
+//            v_mfma_i32_16x16x64_i8 (keys on M, rows on N, channels on K;
+//            exact integer sums); xc = (eta_i e_j)(c_aa + c_ab/256) - Z_i in
+//            FP32.  Lane l loads 16 bytes of plane A of key l%16 per product
+//            and holds keys 4(l/16)+i of row l%16 afterwards.
+//   gates    per GQA group (the rows of one request): live = OR [xc >= -T],
+//            refine = live AND OR [xc >= -tau_r], ORed across the lanes that
+//            hold the group's rows; the unions over the read group are the
+//            chunk's 16-bit plane-B and value-row read masks.
+//   refine   plane B of refined keys only (other keys get an offset past the
+//            chunk's buffer resource, so no bytes move); c_ba, c_bb by the
+//            same product; x = xc + [refine] (eta_i e_j)(c_ba + c_bb/256)/256.
+//   values   value rows of live keys only; w = 2^x; a key counts for row i
+//            iff x >= -T; L adds every w.  The value product is the BF16
+//            scan's: channels on M, rows on N, the chunk's keys on K, the
+//            weight as bf16 hi + bf16 residual.
+//
+// Pipeline per wave, three chunks deep: plane A and scales of chunk t+2 are
+// requested, chunk t+1 is scored and its plane-B and value rows requested,
+// and chunk t is refined and multiplied.  Dense decode (T = inf) requests the
+// value rows together with plane A.
+#include "decode_common.h"
+
+namespace fold {
+namespace {
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// C += A . B on a 16x16 tile with K = 64 INT8 (v_mfma_i32_16x16x64_i8); lane l
+// holds 16 bytes of row l%16 of A and of column l%16 of B; C as the BF16 tiles.
+__device__ __forceinline__ i32x4 mfma_i8(u32x4 a, u32x4 b, i32x4 c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, a),
+                                               __builtin_bit_cast(i32x4, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t buf_load2(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+}
+
+// Where a 16-key chunk lives: its first key row in the cache's element
+// layout and its number of keys (0 past the sequence end or for a page id
+// outside [0, num_pages)).  Buffer resources are built from it at each use,
+// so a chunk in flight holds three scalar registers, not four resources.
+struct Q8Loc {
+  size_t row;
+  uint32_t nk;
+};
+
+__device__ __forceinline__ Q8Loc q8_loc(const Q8DecodeArgs& a, const ScanPlace& p, int c) {
+  const ScanGeometry& g = a.d.geo;
+  Q8Loc l{0, 0};
+  if (c < p.nchunks) {
+    const int key0 = c * kChunk;
+    bool ok = true;
+    if (g.page_size > 0) {
+      const int page = key0 / g.page_size;
+      const int phys = ld_uniform(g.block_table, static_cast<size_t>(p.seq) * g.max_pages + page);
+      ok = phys >= 0 && phys < g.num_pages;
+      l.row = (static_cast<size_t>(ok ? phys : 0) * g.hkv + p.kvh) * g.page_size +
+              (key0 - page * g.page_size);
+    } else {
+      l.row = (static_cast<size_t>(p.seq) * g.hkv + p.kvh) * g.max_seq_len + key0;
+    }
+    if (ok) l.nk = static_cast<uint32_t>(min(kChunk, p.n - key0));
+  }
+  return l;
+}
+
+template <int D, int RB>
+struct Q8Slot {  // one chunk between its plane-A request and its product
+  static constexpr int NKI = D / 64;
+  static constexpr int NK = D / 32;
+  Q8Loc loc;
+  u32x4 ka[NKI];
+  u32x4 kb[NKI];
+  u32x4 vv[NK];
+  uint32_t sc;     // BF16 scale of key l%16 (2-byte loads: any row alignment)
+  float xc[RB][4];
+  uint32_t ref;    // bit 4b+i: key 4(l/16)+i refined for the group of row block b
+  uint32_t vmask;  // value rows to read (wave-uniform)
+  uint32_t bmask;  // plane-B rows to read (wave-uniform)
+};
+
+template <int D, int RB, bool DENSE, bool DBG>
+struct Q8Scan {
+  static constexpr int NKI = D / 64;          // 16-byte plane loads per lane per chunk
+  static constexpr int NK = D / 32;           // 16-byte value loads per lane per chunk
+  static constexpr int NB = D / 16;           // 16-channel blocks of the value product
+  static constexpr int VSTRIDE = 2 * D + 16;  // bytes per key row of the LDS value tile
+  static constexpr int R = 16 * RB;
+  using Slot = Q8Slot<D, RB>;
+
+  const Q8DecodeArgs& a;
+  const ScanGeometry& g;
+  ScanPlace p;
+  int lane, n16, grp;
+  int gspan;     // lanes (within a 16-lane row) that share a GQA group, minus 1
+  bool cross_b;  // the GQA group spans both 16-row blocks
+  size_t gate_row;
+  unsigned char* vt;
+
+  u32x4 qa[RB][NKI], qb[RB][NKI];
+  float eta[RB], zr[RB], ntau[RB];
+  bool rok[RB];
+  size_t xrow[RB];
+  f32x4 acc[RB][NB];
+  float lsum[RB];
+
+  __device__ Q8Scan(const Q8DecodeArgs& a_) : a(a_), g(a_.d.geo) {}
+
+  __device__ __forceinline__ void load_a(Slot& s) const {
+    const rsrc_t ra = make_rsrc(a.keys.ka + s.loc.row * D, s.loc.nk * D);
+    const rsrc_t rs = make_rsrc(a.keys.ks + s.loc.row, s.loc.nk * 2);
+#pragma unroll
+    for (int c = 0; c < NKI; ++c) s.ka[c] = buf_load(ra, n16 * D + 64 * c + 16 * grp);
+    s.sc = buf_load2(rs, 2 * n16);
+  }
+
+  __device__ __forceinline__ void load_v(Slot& s, uint32_t mask) const {
+    const rsrc_t rv = make_rsrc(g.v + s.loc.row * D, s.loc.nk * D * 2);
+    // lane l, load i: the 16 bytes at 1024 i + 16 l of the chunk (key (1024 i + 16 l) / 2D)
+#pragma unroll
+    for (int i = 0; i < NK; ++i) {
+      const uint32_t off = 1024u * i + 16u * lane;
+      const uint32_t key = off / (2 * D);
+      s.vv[i] = buf_load(rv, DENSE || ((mask >> key) & 1u) ? off : kOutOfRange);
+    }
+  }
+
+  __device__ __forceinline__ void load_b(Slot& s) const {
+    const rsrc_t rb = make_rsrc(a.keys.kb + s.loc.row * D, s.loc.nk * D);
+    const bool want = (s.bmask >> n16) & 1u;
+#pragma unroll
+    for (int c = 0; c < NKI; ++c)
+      s.kb[c] = buf_load(rb, want ? n16 * D + 64 * c + 16 * grp : kOutOfRange);
+  }
+
+  // Scales of keys 4(l/16)+i, i < 4: key k's scale sits in lane k.
+  __device__ __forceinline__ void scales(const Slot& s, float (&e)[4]) const {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      e[i] = bf16_lo(static_cast<uint32_t>(__shfl(static_cast<int>(s.sc), 4 * grp + i, 64)));
+  }
+
+  // Coarse scores, group gates and read masks of chunk c (plane A in s.ka).
+  __device__ __forceinline__ void coarse(int c, Slot& s) const {
+    const int key0 = c * kChunk;
+    const int nk = c < p.nchunks ? min(kChunk, p.n - key0) : 0;
+    float e[4];
+    scales(s, e);
+    uint32_t lv = 0, rf = 0;
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      i32x4 caa = {0, 0, 0, 0}, cab = {0, 0, 0, 0};
+#pragma unroll
+      for (int c2 = 0; c2 < NKI; ++c2) {
+        caa = mfma_i8(s.ka[c2], qa[b][c2], caa);
+        cab = mfma_i8(s.ka[c2], qb[b][c2], cab);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = rok[b] && 4 * grp + i < nk;
+        const float t = static_cast<float>(caa[i]) + static_cast<float>(cab[i]) * (1.0f / 256.0f);
+        const float xc = __builtin_fmaf(eta[b] * e[i], t, -zr[b]);
+        s.xc[b][i] = xc;
+        if (ok && (DENSE || xc >= a.d.neg_T)) lv |= 1u << (4 * b + i);
+        if (ok && xc >= ntau[b]) rf |= 1u << (4 * b + i);
+        if (DBG && a.xc_out && ok) a.xc_out[xrow[b] * g.max_seq_len + key0 + 4 * grp + i] = xc;
+      }
+    }
+    // OR over the lanes holding the rows of one GQA group.
+    uint32_t both = lv | (rf << 16);
+#pragma unroll
+    for (int m = 1; m < 16; m <<= 1)
+      if (gspan & m) both |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(both), m, 64));
+    if (cross_b) both |= ((both >> 4) & 0x000F000Fu) | ((both & 0x000F000Fu) << 4);
+    both &= (both << 16) | 0xFFFFu;  // refine only live keys
+    s.ref = both >> 16;
+    // Unions over the read group: OR over each 16-lane row (row q holds keys
+    // 4q..4q+3), then one row value per readlane; the row blocks fold together.
+    const uint32_t u = group_or16(RB == 2 ? both | (both >> 4) : both);
+    uint32_t vmask = 0, bmask = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t r = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(u), 16 * q));
+      vmask |= (r & 0xFu) << (4 * q);
+      bmask |= ((r >> 16) & 0xFu) << (4 * q);
+    }
+    s.vmask = vmask;
+    s.bmask = bmask;
+    if (DBG) {
+      if (a.d.key_gate_out && lane < nk)
+        a.d.key_gate_out[gate_row * g.max_seq_len + key0 + lane] = (vmask >> lane) & 1u;
+      if (a.refine_gate_out && lane < nk)
+        a.refine_gate_out[gate_row * g.max_seq_len + key0 + lane] = (bmask >> lane) & 1u;
+      if (a.d.page_gate_out && lane == 0 && c < p.nchunks)
+        a.d.page_gate_out[gate_row * ((g.max_seq_len + kChunk - 1) / kChunk) + c] = vmask ? 1 : 0;
+    }
+  }
+
+  // Refined scores, weights, L and the value product of chunk c.
+  __device__ __forceinline__ void finish(int c, const Slot& s) {
+    const int key0 = c * kChunk;
+    const int nk = c < p.nchunks ? min(kChunk, p.n - key0) : 0;
+    float e[4];
+    scales(s, e);
+    u32x2 phi[RB], plo[RB];
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      i32x4 cba = {0, 0, 0, 0}, cbb = {0, 0, 0, 0};
+      if (s.bmask) {  // wave-uniform: some key of the chunk is refined
+#pragma unroll
+        for (int c2 = 0; c2 < NKI; ++c2) {
+          cba = mfma_i8(s.kb[c2], qa[b][c2], cba);
+          cbb = mfma_i8(s.kb[c2], qb[b][c2], cbb);
+        }
+      }
+      uint32_t hi[4], lo[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = rok[b] && 4 * grp + i < nk;
+        float x = s.xc[b][i];
+        if ((s.ref >> (4 * b + i)) & 1u) {
+          const float tb = static_cast<float>(cba[i]) + static_cast<float>(cbb[i]) * (1.0f / 256.0f);
+          x = x + (eta[b] * e[i]) * (tb * (1.0f / 256.0f));
+        }
+        const bool live = ok && (DENSE || x >= a.d.neg_T);
+        const float w = ok ? exp2_fast(x) : 0.0f;
+        lsum[b] += w;
+        const float pw = live ? w : 0.0f;
+        hi[i] = __float_as_uint(pw) & 0xffff0000u;
+        lo[i] = f32_to_bf16_rne(pw - __uint_as_float(hi[i]));
+        if (DBG && a.d.x_out && ok) a.d.x_out[xrow[b] * g.max_seq_len + key0 + 4 * grp + i] = x;
+      }
+      phi[b] = u32x2{(hi[0] >> 16) | hi[1], (hi[2] >> 16) | hi[3]};
+      plo[b] = u32x2{lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16)};
+    }
+    if (s.vmask == 0) return;  // wave-uniform: no live key in the chunk
+#pragma unroll
+    for (int i = 0; i < NK; ++i) {
+      const uint32_t off = 1024u * i + 16u * lane;
+      const uint32_t key = off / (2 * D);
+      *reinterpret_cast<u32x4*>(vt + key * VSTRIDE + (off - key * 2 * D)) = s.vv[i];
+    }
+    const unsigned char* col = vt + (4 * grp) * VSTRIDE + 2 * n16;
+#pragma unroll
+    for (int blk = 0; blk < NB; ++blk) {
+      const unsigned char* ep = col + 32 * blk;
+      const uint32_t v0 = *reinterpret_cast<const uint16_t*>(ep);
+      const uint32_t v1 = *reinterpret_cast<const uint16_t*>(ep + VSTRIDE);
+      const uint32_t v2 = *reinterpret_cast<const uint16_t*>(ep + 2 * VSTRIDE);
+      const uint32_t v3 = *reinterpret_cast<const uint16_t*>(ep + 3 * VSTRIDE);
+      const u32x2 va = {v0 | (v1 << 16), v2 | (v3 << 16)};
+#pragma unroll
+      for (int b = 0; b < RB; ++b) {
+        acc[b][blk] = mfma_16x16x16(va, phi[b], acc[b][blk]);
+        acc[b][blk] = mfma_16x16x16(va, plo[b], acc[b][blk]);
+      }
+    }
+  }
+};
+
+template <int D, int RB, bool DENSE, bool DBG>
+__global__ __launch_bounds__(kScanThreads) void decode_q8_kernel(const Q8DecodeArgs a) {
+  using S = Q8Scan<D, RB, DENSE, DBG>;
+  using Slot = typename S::Slot;
+  constexpr int NKI = S::NKI;
+  constexpr int R = S::R;
+  constexpr int kTileBytes = kScanWaves * 16 * S::VSTRIDE;
+  constexpr int kRedBytes = (R * D + RB * 64) * 4;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kTileBytes > kRedBytes ? kTileBytes : kRedBytes];
+
+  const ScanGeometry& g = a.d.geo;
+  S sc(a);
+  sc.p = scan_place(a.d);
+  if (sc.p.rg * R >= sc.p.nrows) return;  // uniform: this read group has no rows
+  sc.lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  sc.n16 = sc.lane & 15;
+  sc.grp = sc.lane >> 4;
+  sc.vt = smem + wave * 16 * S::VSTRIDE;
+  sc.gate_row = (static_cast<size_t>(sc.p.seq) * g.hkv + sc.p.kvh) * a.d.row_groups + sc.p.rg;
+  sc.gspan = (g.group < 16 ? g.group : 16) - 1;
+  sc.cross_b = RB == 2 && g.group > 16;
+
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+    const RowInfo ri = row_info(g, sc.p.seq, sc.p.kvh, sc.p.rg * R + 16 * b + sc.n16,
+                                sc.p.nrows, sc.p.req0);
+    sc.rok[b] = ri.ok;
+    const size_t row = static_cast<size_t>(ri.req) * g.heads + ri.head;
+    sc.xrow[b] = row;
+    sc.zr[b] = ri.ok ? a.d.z[row] : 0.0f;
+    sc.eta[b] = ri.ok ? a.eta[row] : 0.0f;
+    sc.ntau[b] = ri.ok ? -a.tau[ri.req] : 0.0f;
+#pragma unroll
+    for (int c = 0; c < NKI; ++c) {
+      sc.qa[b][c] = ri.ok ? *reinterpret_cast<const u32x4*>(a.qp + row * 2 * D + 64 * c + 16 * sc.grp)
+                          : u32x4{0, 0, 0, 0};
+      sc.qb[b][c] = ri.ok ? *reinterpret_cast<const u32x4*>(a.qp + row * 2 * D + D + 64 * c + 16 * sc.grp)
+                          : u32x4{0, 0, 0, 0};
+    }
+    sc.lsum[b] = 0.0f;
+#pragma unroll
+    for (int blk = 0; blk < S::NB; ++blk) sc.acc[b][blk] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  }
+
+  const int cstride = kScanWaves * a.d.num_splits;
+  const int c0 = kScanWaves * sc.p.split + wave;
+  const int m = sc.p.nchunks > c0 ? (sc.p.nchunks - c0 + cstride - 1) / cstride : 0;
+
+  if (m > 0) {
+    Slot s0, s1, s2;
+    auto request_a = [&](Slot& s, int k) {  // local chunk k: plane A, scales (+ values)
+      s.loc = q8_loc(a, sc.p, c0 + k * cstride);
+      sc.load_a(s);
+      if (DENSE) sc.load_v(s, 0xFFFFu);
+    };
+    auto score = [&](Slot& s, int k) {  // coarse pass, then the gated requests
+      sc.coarse(c0 + k * cstride, s);
+      sc.load_b(s);
+      if (!DENSE) sc.load_v(s, s.vmask);
+    };
+    // Slot X holds chunk t (requests issued), Y chunk t+1 (plane A issued).
+    auto step = [&](Slot& X, Slot& Y, Slot& Z, int t) {
+      if (t + 2 < m) request_a(Z, t + 2);
+      if (t + 1 < m) score(Y, t + 1);
+      sc.finish(c0 + t * cstride, X);
+      return t + 1 < m;
+    };
+    request_a(s0, 0);
+    if (m > 1) request_a(s1, 1);
+    score(s0, 0);
+    for (int t = 0; t < m; t += 3) {
+      if (!step(s0, s1, s2, t)) break;
+      if (!step(s1, s2, s0, t + 1)) break;
+      if (!step(s2, s0, s1, t + 2)) break;
+    }
+  }
+
+  // L partials: lanes of one row (l%16) hold different keys; add them.
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+    sc.lsum[b] += __shfl_xor(sc.lsum[b], 16, 64);
+    sc.lsum[b] += __shfl_xor(sc.lsum[b], 32, 64);
+  }
+
+  // Add the four waves in order through LDS (the value tiles are dead now).
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(smem);  // [RB][NB][4][64]
+  float* redl = red + RB * S::NB * 4 * 64;      // [RB][64]
+  for (int w = 0; w < kScanWaves; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int b = 0; b < RB; ++b) {
+#pragma unroll
+        for (int blk = 0; blk < S::NB; ++blk) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            float* d = red + ((b * S::NB + blk) * 4 + i) * 64 + sc.lane;
+            *d = (w == 0 ? 0.0f : *d) + sc.acc[b][blk][i];
+          }
+        }
+        if (sc.lane < 16) {
+          float* d = redl + b * 64 + sc.lane;
+          *d = (w == 0 ? 0.0f : *d) + sc.lsum[b];
+        }
+      }
+    }
+    __syncthreads();
+  }
+  const size_t slot_rows = (static_cast<size_t>(a.d.slot_offset) + sc.p.split) * g.batch * g.heads;
+  const int wl = threadIdx.x & 63;
+  const int wi = threadIdx.x >> 6;
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+    if (!sc.rok[b]) continue;
+    const size_t row = slot_rows + sc.xrow[b];
+#pragma unroll
+    for (int blk = 0; blk < S::NB; ++blk)
+      a.d.part_A[row * D + 16 * blk + 4 * (wl >> 4) + wi] = red[((b * S::NB + blk) * 4 + wi) * 64 + wl];
+    if (wi == 0 && wl < 16) a.d.part_L[row] = redl[b * 64 + wl];
+  }
+}
+
+template <int D, int RB, bool DENSE>
+hipError_t launch_q8_rb(const Q8DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
+  if (dbg)
+    hipLaunchKernelGGL((decode_q8_kernel<D, RB, DENSE, true>), dim3(blocks), dim3(kScanThreads), 0,
+                       stream, a);
+  else
+    hipLaunchKernelGGL((decode_q8_kernel<D, RB, DENSE, false>), dim3(blocks), dim3(kScanThreads), 0,
+                       stream, a);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_q8_d(const Q8DecodeArgs& a, unsigned blocks, hipStream_t stream) {
+  const bool dbg = a.d.x_out || a.d.key_gate_out || a.d.page_gate_out || a.xc_out ||
+                   a.refine_gate_out;
+  const int rb = a.d.rows_per_group / 16;
+  if (rb == 1) return a.d.dense ? launch_q8_rb<D, 1, true>(a, dbg, blocks, stream)
+                                : launch_q8_rb<D, 1, false>(a, dbg, blocks, stream);
+  if (rb == 2) return a.d.dense ? launch_q8_rb<D, 2, true>(a, dbg, blocks, stream)
+                                : launch_q8_rb<D, 2, false>(a, dbg, blocks, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_q8_decode(const Q8DecodeArgs& a, int head_dim, hipStream_t stream) {
+  const long long blocks = static_cast<long long>(a.d.geo.num_seqs) * a.d.geo.hkv *
+                           a.d.num_splits * a.d.row_groups;
+  if (blocks == 0) return hipSuccess;
+  if (head_dim == 128) return launch_q8_d<128>(a, static_cast<unsigned>(blocks), stream);
+  if (head_dim == 64) return launch_q8_d<64>(a, static_cast<unsigned>(blocks), stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace fold

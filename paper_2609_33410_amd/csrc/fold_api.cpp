@@ -1,5 +1,6 @@
-// Host side of the C ABI declared in include/fold.h: argument validation and
-// kernel launches.  Nothing here allocates, synchronises or keeps a pointer.
+// Host side of the C ABI declared in include/fold.h and include/fold_q8.h:
+// argument validation and kernel launches.  Nothing here allocates,
+// synchronises or keeps a pointer.
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -8,6 +9,7 @@
 #include <string>
 
 #include "fold.h"
+#include "fold_q8.h"
 #include "fold_internal.h"
 
 namespace {
@@ -33,21 +35,17 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 const float kLog2e = 1.4426950408889634f;
 
-// Checks shared by the calls that read the cache; fills the geometry.
-fold_status check_view(const fold_kv_view* kv, const fold_q_view* q, fold::ScanGeometry* g,
-                       bool need_v) {
-  if (!kv || !q) return fail(FOLD_E_INVAL, "kv view and q view are required");
-  if (!kv->k || (need_v && !kv->v) || !kv->seq_lens || !q->q)
-    return fail(FOLD_E_INVAL, "k%s, seq_lens and q pointers are required", need_v ? ", v" : "");
+// Size and layout checks of a view read by query rows [batch][num_heads];
+// fills the geometry.  Pointer checks are the caller's.
+fold_status check_layout(const fold_kv_view* kv, int32_t batch, int32_t num_heads,
+                         fold::ScanGeometry* g) {
   if (kv->head_dim != 64 && kv->head_dim != 128)
     return fail(FOLD_E_INVAL, "head_dim %d: must be 64 or 128", kv->head_dim);
-  if (kv->num_kv_heads < 1 || q->num_heads < 1 || q->num_heads % kv->num_kv_heads != 0)
+  if (kv->num_kv_heads < 1 || num_heads < 1 || num_heads % kv->num_kv_heads != 0)
     return fail(FOLD_E_INVAL, "num_heads %d must be a positive multiple of num_kv_heads %d",
-                q->num_heads, kv->num_kv_heads);
-  if (kv->num_seqs < 0 || q->batch < 0 || kv->max_seq_len < 0)
+                num_heads, kv->num_kv_heads);
+  if (kv->num_seqs < 0 || batch < 0 || kv->max_seq_len < 0)
     return fail(FOLD_E_INVAL, "negative size");
-  if (!aligned16(kv->k) || (need_v && !aligned16(kv->v)) || !aligned16(q->q))
-    return fail(FOLD_E_INVAL, "q, k and v must be 16-byte aligned");
   if (kv->block_table) {
     if (kv->page_size <= 0 || kv->page_size % fold::kChunk != 0)
       return fail(FOLD_E_INVAL, "page_size %d: must be a positive multiple of 16", kv->page_size);
@@ -58,9 +56,9 @@ fold_status check_view(const fold_kv_view* kv, const fold_q_view* q, fold::ScanG
     return fail(FOLD_E_INVAL, "row_indptr and row_req must both be set or both be NULL");
   if (kv->row_indptr && kv->max_reqs_per_seq < 1)
     return fail(FOLD_E_INVAL, "max_reqs_per_seq must be positive with CSR rows");
-  if (!kv->row_indptr && kv->num_seqs > q->batch)
+  if (!kv->row_indptr && kv->num_seqs > batch)
     return fail(FOLD_E_INVAL, "num_seqs %d exceeds batch %d (request s attends kv sequence s)",
-                kv->num_seqs, q->batch);
+                kv->num_seqs, batch);
   g->k = static_cast<const uint16_t*>(kv->k);
   g->v = static_cast<const uint16_t*>(kv->v);
   g->block_table = kv->block_table;
@@ -73,17 +71,69 @@ fold_status check_view(const fold_kv_view* kv, const fold_q_view* q, fold::ScanG
   g->max_pages = kv->block_table ? kv->max_pages_per_seq : 0;
   g->num_pages = kv->block_table ? kv->num_pages : 0;
   g->max_seq_len = kv->max_seq_len;
-  g->batch = q->batch;
-  g->heads = q->num_heads;
-  g->group = q->num_heads / kv->num_kv_heads;
+  g->batch = batch;
+  g->heads = num_heads;
+  g->group = num_heads / kv->num_kv_heads;
   return FOLD_OK;
 }
 
-int rows_per_seq(const fold_kv_view* kv, const fold_q_view* q) {
-  const int group = q->num_heads / kv->num_kv_heads;
+// Checks shared by the calls that read a BF16 cache; fills the geometry.
+fold_status check_view(const fold_kv_view* kv, const fold_q_view* q, fold::ScanGeometry* g,
+                       bool need_v) {
+  if (!kv || !q) return fail(FOLD_E_INVAL, "kv view and q view are required");
+  if (!kv->k || (need_v && !kv->v) || !kv->seq_lens || !q->q)
+    return fail(FOLD_E_INVAL, "k%s, seq_lens and q pointers are required", need_v ? ", v" : "");
+  if (!aligned16(kv->k) || (need_v && !aligned16(kv->v)) || !aligned16(q->q))
+    return fail(FOLD_E_INVAL, "q, k and v must be 16-byte aligned");
+  return check_layout(kv, q->batch, q->num_heads, g);
+}
+
+// Checks shared by the calls that read a two-plane key cache.
+fold_status check_q8_view(const fold_kv_view* kv, const fold_q8_keys* keys, const fold_q8_query* q,
+                          fold::ScanGeometry* g, bool need_v) {
+  if (!kv || !keys || !q) return fail(FOLD_E_INVAL, "kv view, keys and q are required");
+  if ((need_v && !kv->v) || !kv->seq_lens || !keys->plane_a || !keys->plane_b || !keys->scale ||
+      !q->planes || !q->eta)
+    return fail(FOLD_E_INVAL, "%splane_a, plane_b, scale, seq_lens, query planes and eta are "
+                "required", need_v ? "v, " : "");
+  if ((need_v && !aligned16(kv->v)) || !aligned16(keys->plane_a) || !aligned16(keys->plane_b) ||
+      !aligned16(keys->scale) || !aligned16(q->planes))
+    return fail(FOLD_E_INVAL, "v, planes and scales must be 16-byte aligned");
+  fold_status st = check_layout(kv, q->batch, q->num_heads, g);
+  if (st != FOLD_OK) return st;
+  const int G = g->group;
+  if (G > 32 || (G & (G - 1)) != 0)
+    return fail(FOLD_E_UNSUPPORTED, "GQA group %d: the two-plane scan needs 1, 2, 4, 8, 16 or 32", G);
+  return FOLD_OK;
+}
+
+int q8_rows_per_group(int rows) { return rows <= 16 ? 16 : 32; }
+
+int rows_per_seq_of(const fold_kv_view* kv, int num_heads) {
+  const int group = num_heads / kv->num_kv_heads;
   const long long reqs = kv->row_indptr ? kv->max_reqs_per_seq : 1;
   const long long rows = reqs * group;
   return rows > (1 << 30) ? (1 << 30) : static_cast<int>(rows);
+}
+
+int rows_per_seq(const fold_kv_view* kv, const fold_q_view* q) {
+  return rows_per_seq_of(kv, q->num_heads);
+}
+
+fold_status check_depth(float depth_T) {
+  if (isnan(depth_T) || depth_T < 0.0f)
+    return fail(FOLD_E_INVAL, "depth_T must be +INFINITY or a finite value >= 0");
+  return FOLD_OK;
+}
+
+fold_status check_est_params(const fold_est_params* params, fold_est_params* p) {
+  *p = {1, 63, 128, 8, 8};
+  if (params) *p = *params;
+  if (p->sink < 0 || p->recent < 0 || p->strata < 1 || p->trim_lo < 0 || p->trim_hi < 0 ||
+      p->trim_lo + p->trim_hi >= p->strata ||
+      static_cast<long long>(p->sink) + p->recent + p->strata > fold::kMaxEstSamples)
+    return fail(FOLD_E_INVAL, "estimator parameters out of range");
+  return FOLD_OK;
 }
 
 }  // namespace
@@ -128,12 +178,9 @@ fold_status fold_ref_estimate(const fold_kv_view* kv, const fold_q_view* q, floa
   if (!isfinite(sm_scale)) return fail(FOLD_E_INVAL, "sm_scale must be finite");
   if (a.geo.group > fold::kMaxEstRows)
     return fail(FOLD_E_UNSUPPORTED, "GQA group %d exceeds %d", a.geo.group, fold::kMaxEstRows);
-  fold_est_params p = {1, 63, 128, 8, 8};
-  if (params) p = *params;
-  if (p.sink < 0 || p.recent < 0 || p.strata < 1 || p.trim_lo < 0 || p.trim_hi < 0 ||
-      p.trim_lo + p.trim_hi >= p.strata ||
-      static_cast<long long>(p.sink) + p.recent + p.strata > fold::kMaxEstSamples)
-    return fail(FOLD_E_INVAL, "estimator parameters out of range");
+  fold_est_params p;
+  st = check_est_params(params, &p);
+  if (st != FOLD_OK) return st;
   a.q = static_cast<const uint16_t*>(q->q);
   a.z_out = z_out;
   a.score_scale = kLog2e * sm_scale;
@@ -157,8 +204,8 @@ fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, floa
   fold_status st = check_view(kv, q, &a.geo, true);
   if (st != FOLD_OK) return st;
   if (!z || !part_A || !part_L) return fail(FOLD_E_INVAL, "z, part_A and part_L are required");
-  if (isnan(depth_T) || depth_T < 0.0f)
-    return fail(FOLD_E_INVAL, "depth_T must be +INFINITY or a finite value >= 0");
+  st = check_depth(depth_T);
+  if (st != FOLD_OK) return st;
   if (!isfinite(sm_scale)) return fail(FOLD_E_INVAL, "sm_scale must be finite");
   if (num_splits < 1) return fail(FOLD_E_INVAL, "num_splits must be >= 1");
   if (slot_offset < 0 || static_cast<long long>(slot_offset) + num_splits > num_slots)
@@ -212,6 +259,154 @@ fold_status fold_combine(const float* part_A, const float* part_L, int32_t num_s
   a.out_bf16 = out_dtype == FOLD_DTYPE_BF16 ? 1 : 0;
   hipError_t e = fold::launch_combine(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(FOLD_E_HIP, "combine launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int32_t fold_q8_decode_rows_per_group(const fold_kv_view* kv, const fold_q8_query* q) {
+  if (!kv || !q) return -1;
+  fold::ScanGeometry g;
+  if (check_layout(kv, q->batch, q->num_heads, &g) != FOLD_OK) return -1;
+  return q8_rows_per_group(rows_per_seq_of(kv, q->num_heads));
+}
+
+int32_t fold_q8_decode_row_groups(const fold_kv_view* kv, const fold_q8_query* q) {
+  if (!kv || !q) return -1;
+  fold::ScanGeometry g;
+  if (check_layout(kv, q->batch, q->num_heads, &g) != FOLD_OK) return -1;
+  const int rows = rows_per_seq_of(kv, q->num_heads);
+  const int gr = q8_rows_per_group(rows);
+  return (rows + gr - 1) / gr;
+}
+
+fold_status fold_q8_write_keys(const fold_kv_view* kv, const void* k_src, const int32_t* tok_seq,
+                               const int32_t* tok_pos, int32_t n_tok, int8_t* plane_a,
+                               int8_t* plane_b, uint16_t* scale, void* stream) {
+  if (!kv) return fail(FOLD_E_INVAL, "kv view is required");
+  if (n_tok < 0) return fail(FOLD_E_INVAL, "n_tok must be >= 0");
+  fold::Q8WriteArgs a;
+  fold_status st = check_layout(kv, kv->num_seqs, kv->num_kv_heads, &a.geo);
+  if (st != FOLD_OK) return st;
+  if (n_tok > 0 && (!k_src || !tok_seq || !tok_pos || !plane_a || !plane_b || !scale))
+    return fail(FOLD_E_INVAL, "k_src, tok_seq, tok_pos, plane_a, plane_b and scale are required");
+  if (static_cast<long long>(n_tok) * kv->num_kv_heads > 0x1fffffffLL)
+    return fail(FOLD_E_INVAL, "grid too large");
+  a.k_src = static_cast<const uint16_t*>(k_src);
+  a.tok_seq = tok_seq;
+  a.tok_pos = tok_pos;
+  a.n_tok = n_tok;
+  a.ka = plane_a;
+  a.kb = plane_b;
+  a.ks = scale;
+  hipError_t e = fold::launch_q8_write(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "q8 write launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_q8_split_query(const fold_q_view* q, int32_t head_dim, float sm_scale,
+                                const int32_t* req_lens, float kappa, int8_t* planes_out,
+                                float* eta_out, float* tau_out, void* stream) {
+  if (!q) return fail(FOLD_E_INVAL, "q view is required");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(FOLD_E_INVAL, "head_dim %d: must be 64 or 128", head_dim);
+  if (q->batch < 0 || q->num_heads < 1) return fail(FOLD_E_INVAL, "batch >= 0, num_heads >= 1");
+  const long long rows = static_cast<long long>(q->batch) * q->num_heads;
+  if (rows > 0x1fffffffLL) return fail(FOLD_E_INVAL, "grid too large");
+  if (rows > 0 && (!q->q || !planes_out || !eta_out))
+    return fail(FOLD_E_INVAL, "q, planes_out and eta_out are required");
+  if ((req_lens == nullptr) != (tau_out == nullptr))
+    return fail(FOLD_E_INVAL, "req_lens and tau_out must both be set or both be NULL");
+  if (!isfinite(sm_scale)) return fail(FOLD_E_INVAL, "sm_scale must be finite");
+  if (isnan(kappa)) return fail(FOLD_E_INVAL, "kappa must not be NaN");
+  fold::Q8SplitArgs a;
+  a.q = static_cast<const uint16_t*>(q->q);
+  a.qp = planes_out;
+  a.eta = eta_out;
+  a.rows = static_cast<int>(rows);
+  a.sm_scale = sm_scale;
+  a.req_lens = req_lens;
+  a.tau = tau_out;
+  a.batch = q->batch;
+  a.kappa = kappa;
+  hipError_t e = fold::launch_q8_split(a, head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "q8 split launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_q8_ref_estimate(const fold_kv_view* kv, const fold_q8_keys* keys,
+                                 const fold_q8_query* q, const fold_est_params* params,
+                                 float* z_out, void* stream) {
+  fold::Q8EstimateArgs a;
+  fold_status st = check_q8_view(kv, keys, q, &a.e.geo, false);
+  if (st != FOLD_OK) return st;
+  if (!z_out) return fail(FOLD_E_INVAL, "z_out is required");
+  if (kv->row_indptr) return fail(FOLD_E_INVAL, "the estimate needs a per-request view (no CSR rows)");
+  if (a.e.geo.group > fold::kMaxEstRows)
+    return fail(FOLD_E_UNSUPPORTED, "GQA group %d exceeds %d", a.e.geo.group, fold::kMaxEstRows);
+  fold_est_params p;
+  st = check_est_params(params, &p);
+  if (st != FOLD_OK) return st;
+  if (static_cast<long long>(q->batch) * kv->num_kv_heads > 0x7fffffffLL)
+    return fail(FOLD_E_INVAL, "grid too large");
+  a.e.q = nullptr;
+  a.e.z_out = z_out;
+  a.e.score_scale = 0.0f;
+  a.e.sink = p.sink;
+  a.e.recent = p.recent;
+  a.e.strata = p.strata;
+  a.e.trim_lo = p.trim_lo;
+  a.e.trim_hi = p.trim_hi;
+  a.keys = {keys->plane_a, keys->plane_b, keys->scale};
+  a.qp = q->planes;
+  a.eta = q->eta;
+  hipError_t e = fold::launch_q8_estimate(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "q8 estimate launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* keys,
+                                 const fold_q8_query* q, const float* z, float depth_T,
+                                 int32_t num_splits, int32_t slot_offset, int32_t num_slots,
+                                 float* part_A, float* part_L, const fold_q8_debug* dbg,
+                                 void* stream) {
+  fold::Q8DecodeArgs a;
+  fold_status st = check_q8_view(kv, keys, q, &a.d.geo, true);
+  if (st != FOLD_OK) return st;
+  if (!q->tau) return fail(FOLD_E_INVAL, "tau is required");
+  if (!z || !part_A || !part_L) return fail(FOLD_E_INVAL, "z, part_A and part_L are required");
+  st = check_depth(depth_T);
+  if (st != FOLD_OK) return st;
+  if (num_splits < 1) return fail(FOLD_E_INVAL, "num_splits must be >= 1");
+  if (slot_offset < 0 || static_cast<long long>(slot_offset) + num_splits > num_slots)
+    return fail(FOLD_E_INVAL, "slots [%d, %d) exceed num_slots %d", slot_offset,
+                slot_offset + num_splits, num_slots);
+  const int rows = rows_per_seq_of(kv, q->num_heads);
+  const int gr = q8_rows_per_group(rows);
+  const int groups = (rows + gr - 1) / gr;
+  const long long blocks = static_cast<long long>(kv->num_seqs) * kv->num_kv_heads * num_splits * groups;
+  if (blocks > 0x7fffffffLL) return fail(FOLD_E_INVAL, "grid too large");
+  a.d.q = nullptr;
+  a.d.z = z;
+  a.d.part_A = part_A;
+  a.d.part_L = part_L;
+  a.d.x_out = dbg ? dbg->x_out : nullptr;
+  a.d.key_gate_out = dbg ? dbg->key_gate_out : nullptr;
+  a.d.page_gate_out = dbg ? dbg->page_gate_out : nullptr;
+  a.d.score_scale = 0.0f;
+  a.d.dense = isinf(depth_T) ? 1 : 0;
+  a.d.neg_T = a.d.dense ? 0.0f : -depth_T;
+  a.d.num_splits = num_splits;
+  a.d.slot_offset = slot_offset;
+  a.d.rows_per_seq = rows;
+  a.d.rows_per_group = gr;
+  a.d.row_groups = groups;
+  a.keys = {keys->plane_a, keys->plane_b, keys->scale};
+  a.qp = q->planes;
+  a.eta = q->eta;
+  a.tau = q->tau;
+  a.xc_out = dbg ? dbg->xc_out : nullptr;
+  a.refine_gate_out = dbg ? dbg->refine_gate_out : nullptr;
+  hipError_t e = fold::launch_q8_decode(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "q8 decode launch: %s", hipGetErrorString(e));
   return ok();
 }
 

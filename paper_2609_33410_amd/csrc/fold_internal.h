@@ -70,6 +70,55 @@ struct CombineArgs {
   int out_bf16;
 };
 
+// Two-plane INT8 key cache (Section 4, "Cache format"): the planes use the
+// element layout of a BF16 key cache with one byte per element; the BF16
+// scales one element per key.
+struct Q8Keys {
+  const int8_t* ka;
+  const int8_t* kb;
+  const uint16_t* ks;
+};
+
+struct Q8DecodeArgs {
+  DecodeArgs d;           // d.geo.k and d.q are not read; d.x_out holds the refined x
+  Q8Keys keys;
+  const int8_t* qp;       // [batch][heads][2][D]: qa then qb
+  const float* eta;       // [batch][heads]
+  const float* tau;       // [batch] refine thresholds
+  float* xc_out;          // coarse x (debug)
+  uint8_t* refine_gate_out;
+};
+
+struct Q8WriteArgs {
+  ScanGeometry geo;       // layout of the destination cache (geo.k, geo.v unused)
+  const uint16_t* k_src;  // [n_tok][hkv][D] bf16
+  const int32_t* tok_seq;
+  const int32_t* tok_pos;
+  int n_tok;
+  int8_t* ka;
+  int8_t* kb;
+  uint16_t* ks;
+};
+
+struct Q8SplitArgs {
+  const uint16_t* q;      // [rows][D] bf16
+  int8_t* qp;             // [rows][2][D]
+  float* eta;             // [rows]
+  int rows;
+  float sm_scale;
+  const int32_t* req_lens;  // [batch] or NULL
+  float* tau;               // [batch] or NULL
+  int batch;
+  float kappa;
+};
+
+struct Q8EstimateArgs {
+  EstimateArgs e;         // e.geo.k and e.q are not read
+  Q8Keys keys;
+  const int8_t* qp;
+  const float* eta;
+};
+
 // Keys a kv sequence of this view can hold: max_seq_len, and for a paged view
 // also max_pages * page_size.  Device-supplied lengths are clamped to it.
 __host__ __device__ inline int view_capacity(const ScanGeometry& g) {
@@ -84,6 +133,10 @@ __host__ __device__ inline int view_capacity(const ScanGeometry& g) {
 hipError_t launch_decode(const DecodeArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_estimate(const EstimateArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
+hipError_t launch_q8_decode(const Q8DecodeArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_q8_write(const Q8WriteArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_q8_split(const Q8SplitArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_q8_estimate(const Q8EstimateArgs& a, int head_dim, hipStream_t stream);
 
 // Rows per read group the decode kernel is instantiated for, given the rows
 // that attend one (kv sequence, kv head).

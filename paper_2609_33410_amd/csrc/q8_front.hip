@@ -1,0 +1,173 @@
+// Front of a two-plane INT8 key cache (Section 4, "Cache format"): the key
+// writer and the per-step query split.
+//
+// Both rotate a D-vector by the Sylvester Hadamard matrix H_D (entries +-1;
+// the paper's orthonormal rotation is H_D / sqrt(D), and its 1/D on a dot
+// product is folded into the query scale) and split the result into two INT8
+// planes under one scale:
+//   key   k'' = e (a + b/256), e = the smallest BF16 value >= max|k''| / 127
+//         (rounded up: plane A never saturates); a key whose scale would fall
+//         below 2^-126 is stored as zero;
+//   query q'' = f (qa + qb/256), f = max|q''| / 127, with the base-2 score
+//         scale eta = log2(e) sm_scale f / D rounded once to FP32;
+//   a = rint(x / s), b = rint(256 (x / s - a)) clamped to [-128, 127].
+// One wave64 handles one vector; lane l holds elements 64 i + l.  The
+// transform is a radix-2 butterfly in FP64: every partial sum of +-BF16
+// inputs is exact while the inputs of one vector span at most 38 binades, so
+// the codes do not depend on the order of the butterflies.  Division, rint and
+// the rounded-up scale are exact IEEE FP64 operations.
+#include "fold_device.h"
+#include "fold_internal.h"
+
+namespace fold {
+namespace {
+
+constexpr int kFrontThreads = 256;
+constexpr int kWavesPerBlock = kFrontThreads / 64;
+constexpr double kLog2e = 0x1.71547652b82fep+0;
+
+template <int D>
+__device__ __forceinline__ void hadamard_wave(double (&x)[D / 64], int lane) {
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) {
+#pragma unroll
+    for (int i = 0; i < D / 64; ++i) {
+      const double o = __shfl_xor(x[i], s, 64);
+      x[i] = (lane & s) ? o - x[i] : x[i] + o;
+    }
+  }
+  if constexpr (D == 128) {
+    const double u = x[0], v = x[1];
+    x[0] = u + v;
+    x[1] = u - v;
+  }
+}
+
+template <int D>
+__device__ __forceinline__ double wave_absmax_f64(const double (&x)[D / 64]) {
+  double m = 0.0;
+#pragma unroll
+  for (int i = 0; i < D / 64; ++i) m = fmax(m, fabs(x[i]));
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) m = fmax(m, __shfl_xor(m, s, 64));
+  return m;
+}
+
+// Smallest value with 8 significant bits (a BF16 significand) >= t, t > 0 normal.
+__device__ __forceinline__ double ceil_to_bf16(double t) {
+  constexpr unsigned long long kLow = (1ull << 45) - 1;
+  const unsigned long long u = static_cast<unsigned long long>(__double_as_longlong(t));
+  return __longlong_as_double(static_cast<long long>((u + kLow) & ~kLow));
+}
+
+__device__ __forceinline__ void split_value(double x, double s, int8_t* a, int8_t* b) {
+  if (s > 0.0) {
+    const double y = x / s;
+    const double ai = rint(y);
+    const double bi = fmin(fmax(rint(256.0 * (y - ai)), -128.0), 127.0);
+    *a = static_cast<int8_t>(ai);
+    *b = static_cast<int8_t>(bi);
+  } else {
+    *a = 0;
+    *b = 0;
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kFrontThreads) void q8_write_kernel(const Q8WriteArgs a) {
+  const ScanGeometry& g = a.geo;
+  const int lane = threadIdx.x & 63;
+  const long long item = static_cast<long long>(blockIdx.x) * kWavesPerBlock +
+                         __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (item >= static_cast<long long>(a.n_tok) * g.hkv) return;  // uniform per wave
+  const int tok = static_cast<int>(item / g.hkv);
+  const int kvh = static_cast<int>(item % g.hkv);
+  const int seq = ld_uniform(a.tok_seq, tok);
+  const int pos = ld_uniform(a.tok_pos, tok);
+  if (seq < 0 || seq >= g.num_seqs || pos < 0 || pos >= view_capacity(g)) return;
+  size_t row;
+  if (g.page_size > 0) {
+    const int phys = ld_uniform(a.geo.block_table,
+                                static_cast<size_t>(seq) * g.max_pages + pos / g.page_size);
+    if (phys < 0 || phys >= g.num_pages) return;
+    row = (static_cast<size_t>(phys) * g.hkv + kvh) * g.page_size + pos % g.page_size;
+  } else {
+    row = (static_cast<size_t>(seq) * g.hkv + kvh) * g.max_seq_len + pos;
+  }
+  const uint16_t* src = a.k_src + (static_cast<size_t>(tok) * g.hkv + kvh) * D;
+  double x[D / 64];
+#pragma unroll
+  for (int i = 0; i < D / 64; ++i) x[i] = static_cast<double>(bf16_lo(src[64 * i + lane]));
+  hadamard_wave<D>(x, lane);
+  const double m = wave_absmax_f64<D>(x);
+  const double e = m >= 127.0 * 0x1p-126 ? ceil_to_bf16(m / 127.0) : 0.0;
+#pragma unroll
+  for (int i = 0; i < D / 64; ++i) {
+    int8_t qa, qb;
+    split_value(x[i], e, &qa, &qb);
+    a.ka[row * D + 64 * i + lane] = qa;
+    a.kb[row * D + 64 * i + lane] = qb;
+  }
+  if (lane == 0) a.ks[row] = static_cast<uint16_t>(__float_as_uint(static_cast<float>(e)) >> 16);
+}
+
+template <int D>
+__global__ __launch_bounds__(kFrontThreads) void q8_split_kernel(const Q8SplitArgs a) {
+  const int lane = threadIdx.x & 63;
+  if (blockIdx.x == 0 && a.tau) {
+    for (int r = threadIdx.x; r < a.batch; r += kFrontThreads) {
+      const int n = a.req_lens[r];
+      const int c = n > 1 ? 32 - __builtin_clz(static_cast<unsigned>(n - 1)) : 0;
+      a.tau[r] = a.kappa + static_cast<float>(c);
+    }
+  }
+  const long long row = static_cast<long long>(blockIdx.x) * kWavesPerBlock +
+                        __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (row >= a.rows) return;  // uniform per wave
+  const uint16_t* src = a.q + row * D;
+  double x[D / 64];
+#pragma unroll
+  for (int i = 0; i < D / 64; ++i) x[i] = static_cast<double>(bf16_lo(src[64 * i + lane]));
+  hadamard_wave<D>(x, lane);
+  const double f = wave_absmax_f64<D>(x) / 127.0;
+  int8_t* dst = a.qp + row * 2 * D;
+#pragma unroll
+  for (int i = 0; i < D / 64; ++i) {
+    int8_t qa, qb;
+    split_value(x[i], f, &qa, &qb);
+    dst[64 * i + lane] = qa;
+    dst[D + 64 * i + lane] = qb;
+  }
+  if (lane == 0)
+    a.eta[row] = static_cast<float>(((kLog2e * static_cast<double>(a.sm_scale)) * f) / D);
+}
+
+}  // namespace
+
+hipError_t launch_q8_write(const Q8WriteArgs& a, int head_dim, hipStream_t stream) {
+  const long long items = static_cast<long long>(a.n_tok) * a.geo.hkv;
+  if (items == 0) return hipSuccess;
+  const unsigned blocks = static_cast<unsigned>((items + kWavesPerBlock - 1) / kWavesPerBlock);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(q8_write_kernel<128>, dim3(blocks), dim3(kFrontThreads), 0, stream, a);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL(q8_write_kernel<64>, dim3(blocks), dim3(kFrontThreads), 0, stream, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_q8_split(const Q8SplitArgs& a, int head_dim, hipStream_t stream) {
+  const long long waves = a.rows > 0 ? a.rows : 1;  // block 0 also writes tau
+  if (a.rows == 0 && !a.tau) return hipSuccess;
+  const unsigned blocks = static_cast<unsigned>((waves + kWavesPerBlock - 1) / kWavesPerBlock);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(q8_split_kernel<128>, dim3(blocks), dim3(kFrontThreads), 0, stream, a);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL(q8_split_kernel<64>, dim3(blocks), dim3(kFrontThreads), 0, stream, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace fold

@@ -11,6 +11,10 @@
 // after removing the trim_hi largest and the trim_lo smallest centre scores
 // (ranking by score equals ranking by weight because 2^x is monotone).
 //
+// Over a two-plane INT8 key cache the samples are scored with the scan's own
+// coarse logits, eta_i e_j (a_j . qa_i + a_j . qb_i / 256), from plane A and
+// the scales (v_mfma_i32_16x16x64_i8, the same operand layout).
+//
 // Latency, not bandwidth, bounds this kernel (48 KiB per (request, kv head) at
 // D = 128).  Scores come from the matrix cores, 16 samples x 16 rows per
 // v_mfma_f32_16x16x32_bf16 (the decode scan's layout); every lane issues the
@@ -26,9 +30,15 @@ namespace {
 
 constexpr int kThreads = 256;
 
-template <int D>
-__global__ __launch_bounds__(kThreads) void estimate_kernel(const EstimateArgs a) {
-  constexpr int NK = D / 32;            // 16-byte key loads per lane per sample tile
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// BF16 keys (Q8 = false): scores from the BF16 cache.  Two-plane INT8 keys
+// (Q8 = true): the kernel's coarse logits eta_i e_j (a_j . qa_i + a_j . qb_i / 256)
+// from plane A and the scales (Section 3 estimates from coarse logits).
+template <int D, bool Q8>
+__global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs qa8) {
+  const EstimateArgs& a = qa8.e;
+  constexpr int NK = Q8 ? D / 64 : D / 32;  // 16-byte key loads per lane per sample tile
   constexpr int kTilesPerPass = 4;      // sample tiles per wave whose loads fly together
   constexpr int kScanWavesEst = kThreads / 64;
   const ScanGeometry& g = a.geo;
@@ -58,14 +68,25 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const EstimateArgs a
   // of query row l%16 (rows past the group are zero).
   const int n16 = lane & 15;
   const int grp = lane >> 4;
-  u32x4 qb[NK];
+  // Q8: the same lanes hold 16 bytes of qa (and of qb) per product instead.
+  u32x4 qb[NK], qb2[NK];
+  float eta_r = 0.0f;
 #pragma unroll
   for (int c = 0; c < NK; ++c) {
     qb[c] = u32x4{0, 0, 0, 0};
+    qb2[c] = u32x4{0, 0, 0, 0};
     if (n16 < G) {
       const size_t row = static_cast<size_t>(req) * g.heads + kvh * G + n16;
-      qb[c] = *reinterpret_cast<const u32x4*>(a.q + row * D + 32 * c + 8 * grp);
+      if constexpr (Q8) {
+        qb[c] = *reinterpret_cast<const u32x4*>(qa8.qp + row * 2 * D + 64 * c + 16 * grp);
+        qb2[c] = *reinterpret_cast<const u32x4*>(qa8.qp + row * 2 * D + D + 64 * c + 16 * grp);
+      } else {
+        qb[c] = *reinterpret_cast<const u32x4*>(a.q + row * D + 32 * c + 8 * grp);
+      }
     }
+  }
+  if constexpr (Q8) {
+    if (n16 < G) eta_r = qa8.eta[static_cast<size_t>(req) * g.heads + kvh * G + n16];
   }
 
   for (int t = threadIdx.x; t < m; t += kThreads) {
@@ -105,36 +126,65 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const EstimateArgs a
                     ? g.block_table[static_cast<size_t>(req) * g.max_pages + jb[u] / g.page_size]
                     : 0;
     u32x4 kv[kTilesPerPass][NK];
+    float ks[kTilesPerPass];  // Q8: the scale of this lane's sample
 #pragma unroll
     for (int u = 0; u < kTilesPerPass; ++u) {
       const int t = 16 * (tau0 + kScanWavesEst * u) + n16;
       const int j = jb[u];
-      size_t off;
+      size_t krow;  // key row in the cache's element layout
       bool ok = t < m;
       if (g.page_size > 0) {
         ok = ok && phys[u] >= 0 && phys[u] < g.num_pages;
-        off = ((static_cast<size_t>(ok ? phys[u] : 0) * g.hkv + kvh) * g.page_size +
-               (j % g.page_size)) * D;
+        krow = (static_cast<size_t>(ok ? phys[u] : 0) * g.hkv + kvh) * g.page_size +
+               (j % g.page_size);
       } else {
-        off = ((static_cast<size_t>(req) * g.hkv + kvh) * g.max_seq_len + j) * D;
+        krow = (static_cast<size_t>(req) * g.hkv + kvh) * g.max_seq_len + j;
       }
+      if (!ok) krow = 0;
 #pragma unroll
       for (int c = 0; c < NK; ++c) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(g.k + (ok ? off : 0) + 32 * c + 8 * grp);
+        u32x4 v;
+        if constexpr (Q8)
+          v = *reinterpret_cast<const u32x4*>(qa8.keys.ka + krow * D + 64 * c + 16 * grp);
+        else
+          v = *reinterpret_cast<const u32x4*>(g.k + krow * D + 32 * c + 8 * grp);
         kv[u][c] = ok ? v : u32x4{0, 0, 0, 0};
       }
+      ks[u] = 0.0f;
+      if constexpr (Q8) ks[u] = ok ? bf16_lo(qa8.keys.ks[krow]) : 0.0f;
     }
 #pragma unroll
     for (int u = 0; u < kTilesPerPass; ++u) {
       const int tau = tau0 + kScanWavesEst * u;
       if (tau >= ntiles) break;  // uniform
-      f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
+      float sv[4];
+      if constexpr (Q8) {
+        i32x4 caa = {0, 0, 0, 0}, cab = {0, 0, 0, 0};
 #pragma unroll
-      for (int c = 0; c < NK; ++c) s = mfma_16x16x32(kv[u][c], qb[c], s);
+        for (int c = 0; c < NK; ++c) {
+          caa = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, kv[u][c]),
+                                                     __builtin_bit_cast(i32x4, qb[c]), caa, 0, 0, 0);
+          cab = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, kv[u][c]),
+                                                     __builtin_bit_cast(i32x4, qb2[c]), cab, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          // the scale of sample 4(l/16)+i sits in lane 4(l/16)+i
+          const float e = __shfl(ks[u], 4 * grp + i, 64);
+          const float t = static_cast<float>(caa[i]) + static_cast<float>(cab[i]) * (1.0f / 256.0f);
+          sv[i] = (eta_r * e) * t;
+        }
+      } else {
+        f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int c = 0; c < NK; ++c) s = mfma_16x16x32(kv[u][c], qb[c], s);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sv[i] = s[i] * a.score_scale;
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int t = 16 * tau + 4 * grp + i;
-        if (n16 < G && t < m) sc[n16][t] = s[i] * a.score_scale;
+        if (n16 < G && t < m) sc[n16][t] = sv[i];
       }
     }
   }
@@ -234,20 +284,31 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const EstimateArgs a
   }
 }
 
-}  // namespace
-
-hipError_t launch_estimate(const EstimateArgs& a, int head_dim, hipStream_t stream) {
-  const long long blocks = static_cast<long long>(a.geo.batch) * a.geo.hkv;
+template <bool Q8>
+hipError_t launch_est(const Q8EstimateArgs& a, int head_dim, hipStream_t stream) {
+  const long long blocks = static_cast<long long>(a.e.geo.batch) * a.e.geo.hkv;
   if (blocks == 0) return hipSuccess;
   if (head_dim == 128)
-    hipLaunchKernelGGL(estimate_kernel<128>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0,
-                       stream, a);
+    hipLaunchKernelGGL((estimate_kernel<128, Q8>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(kThreads), 0, stream, a);
   else if (head_dim == 64)
-    hipLaunchKernelGGL(estimate_kernel<64>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0,
-                       stream, a);
+    hipLaunchKernelGGL((estimate_kernel<64, Q8>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(kThreads), 0, stream, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_estimate(const EstimateArgs& a, int head_dim, hipStream_t stream) {
+  Q8EstimateArgs q{};
+  q.e = a;
+  return launch_est<false>(q, head_dim, stream);
+}
+
+hipError_t launch_q8_estimate(const Q8EstimateArgs& a, int head_dim, hipStream_t stream) {
+  return launch_est<true>(a, head_dim, stream);
 }
 
 }  // namespace fold

@@ -1,4 +1,5 @@
-"""ctypes binding of ``libfold.so`` (the C ABI in ``include/fold.h``).
+"""ctypes binding of ``libfold.so`` (the C ABI in ``include/fold.h`` and
+``include/fold_q8.h``).
 
 Argument marshalling only: torch tensors supply device memory and
 ``torch.cuda.current_stream()`` supplies the HIP stream; every step of the
@@ -31,6 +32,12 @@ EXPORTED = (
     "fold_ref_estimate",
     "fold_decode_split",
     "fold_combine",
+    "fold_q8_write_keys",
+    "fold_q8_split_query",
+    "fold_q8_ref_estimate",
+    "fold_q8_decode_rows_per_group",
+    "fold_q8_decode_row_groups",
+    "fold_q8_decode_split",
 )
 
 
@@ -77,6 +84,22 @@ class fold_debug(ctypes.Structure):
                 ("page_gate_out", ctypes.c_void_p)]
 
 
+class fold_q8_keys(ctypes.Structure):
+    _fields_ = [("plane_a", ctypes.c_void_p), ("plane_b", ctypes.c_void_p),
+                ("scale", ctypes.c_void_p)]
+
+
+class fold_q8_query(ctypes.Structure):
+    _fields_ = [("planes", ctypes.c_void_p), ("eta", ctypes.c_void_p), ("tau", ctypes.c_void_p),
+                ("batch", ctypes.c_int32), ("num_heads", ctypes.c_int32)]
+
+
+class fold_q8_debug(ctypes.Structure):
+    _fields_ = [("x_out", ctypes.c_void_p), ("xc_out", ctypes.c_void_p),
+                ("key_gate_out", ctypes.c_void_p), ("page_gate_out", ctypes.c_void_p),
+                ("refine_gate_out", ctypes.c_void_p)]
+
+
 _lib = None
 
 
@@ -113,6 +136,26 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.fold_combine.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                  ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.fold_q8_write_keys.restype = ctypes.c_int
+    lib.fold_q8_write_keys.argtypes = [P(fold_kv_view), ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.fold_q8_split_query.restype = ctypes.c_int
+    lib.fold_q8_split_query.argtypes = [P(fold_q_view), ctypes.c_int32, ctypes.c_float,
+                                        ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.fold_q8_ref_estimate.restype = ctypes.c_int
+    lib.fold_q8_ref_estimate.argtypes = [P(fold_kv_view), P(fold_q8_keys), P(fold_q8_query),
+                                         P(fold_est_params), ctypes.c_void_p, ctypes.c_void_p]
+    for name in ("fold_q8_decode_rows_per_group", "fold_q8_decode_row_groups"):
+        fn = getattr(lib, name)
+        fn.restype = ctypes.c_int32
+        fn.argtypes = [P(fold_kv_view), P(fold_q8_query)]
+    lib.fold_q8_decode_split.restype = ctypes.c_int
+    lib.fold_q8_decode_split.argtypes = [P(fold_kv_view), P(fold_q8_keys), P(fold_q8_query),
+                                         ctypes.c_void_p, ctypes.c_float, ctypes.c_int32,
+                                         ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                         ctypes.c_void_p, P(fold_q8_debug), ctypes.c_void_p]
     _lib = lib
     return lib
 
@@ -157,17 +200,22 @@ class Q:
 def kv_view(k: torch.Tensor, v: Optional[torch.Tensor], seq_lens: torch.Tensor, *,
             num_kv_heads: int, max_seq_len: int, block_table: Optional[torch.Tensor] = None,
             row_indptr: Optional[torch.Tensor] = None, row_req: Optional[torch.Tensor] = None,
-            max_reqs_per_seq: int = 1) -> KV:
+            max_reqs_per_seq: int = 1, k_is_layout_only: bool = False) -> KV:
     """Describe one scan level.  Paged: ``k, v [num_pages, Hkv, P, D]`` with
     ``block_table [num_seqs, max_pages]``; contiguous: ``k, v [num_seqs, Hkv,
-    max_seq_len, D]``."""
-    _need(k, "k", torch.bfloat16)
+    max_seq_len, D]``.  With ``k_is_layout_only`` (two-plane key caches), ``k``
+    is a key plane that gives the shape only and the view's key pointer is
+    NULL."""
+    if k_is_layout_only:
+        _need(k, "plane", torch.int8)
+    else:
+        _need(k, "k", torch.bfloat16)
     if v is not None:
         _need(v, "v", torch.bfloat16)
     _need(seq_lens, "seq_lens", torch.int32)
     d = int(k.shape[-1])
     s = fold_kv_view()
-    s.k, s.v = _ptr(k), _ptr(v)
+    s.k, s.v = (None if k_is_layout_only else _ptr(k)), _ptr(v)
     s.seq_lens = _ptr(seq_lens)
     s.num_seqs = int(seq_lens.shape[0])
     s.num_kv_heads = num_kv_heads
@@ -287,3 +335,124 @@ def fold_decode(levels, q: torch.Tensor, z: torch.Tensor, depth_T: float, splits
 def depth_value(T) -> float:
     """``None`` / ``inf`` -> +INFINITY (dense decode); otherwise float(T)."""
     return math.inf if T is None else float(T)
+
+
+# ------------------------------------------------- two-plane INT8 key cache --
+@dataclass
+class Q8Keys:
+    """The planes and scales of a two-plane key cache (kept alive here).
+
+    ``plane_a, plane_b`` int8 and ``scale`` int16 (BF16 bits) in the element
+    layout of the BF16 key cache they replace."""
+    plane_a: torch.Tensor
+    plane_b: torch.Tensor
+    scale: torch.Tensor
+
+    def view(self) -> fold_q8_keys:
+        return fold_q8_keys(_ptr(self.plane_a), _ptr(self.plane_b), _ptr(self.scale))
+
+
+@dataclass
+class Q8Query:
+    """Query codes ``planes [B, H, 2, D]`` int8, ``eta [B, H]`` and ``tau [B]`` fp32."""
+    planes: torch.Tensor
+    eta: torch.Tensor
+    tau: Optional[torch.Tensor]
+
+    def view(self) -> fold_q8_query:
+        return fold_q8_query(_ptr(self.planes), _ptr(self.eta), _ptr(self.tau),
+                             int(self.planes.shape[0]), int(self.planes.shape[1]))
+
+
+def q8_empty_keys(k_like: torch.Tensor) -> Q8Keys:
+    """Uninitialised planes and scales shaped like a BF16 key cache."""
+    return Q8Keys(torch.empty(k_like.shape, dtype=torch.int8, device=k_like.device),
+                  torch.empty(k_like.shape, dtype=torch.int8, device=k_like.device),
+                  torch.empty(k_like.shape[:-1], dtype=torch.int16, device=k_like.device))
+
+
+def fold_q8_write_keys(kv: KV, k_src: torch.Tensor, tok_seq: torch.Tensor, tok_pos: torch.Tensor,
+                       keys: Q8Keys, stream=None) -> None:
+    _need(k_src, "k_src", torch.bfloat16)
+    _need(tok_seq, "tok_seq", torch.int32)
+    _need(tok_pos, "tok_pos", torch.int32)
+    for t, nm, dt in ((keys.plane_a, "plane_a", torch.int8), (keys.plane_b, "plane_b", torch.int8),
+                      (keys.scale, "scale", torch.int16)):
+        _need(t, nm, dt)
+    _check(load_library().fold_q8_write_keys(
+        ctypes.byref(kv.view), _ptr(k_src), _ptr(tok_seq), _ptr(tok_pos), int(tok_seq.shape[0]),
+        _ptr(keys.plane_a), _ptr(keys.plane_b), _ptr(keys.scale), _stream(stream)))
+
+
+def fold_q8_split_query(q: torch.Tensor, sm_scale: float, out: Q8Query,
+                        req_lens: Optional[torch.Tensor] = None, kappa: float = 0.0,
+                        stream=None) -> Q8Query:
+    qv = q_view(q)
+    _need(out.planes, "planes", torch.int8)
+    _need(out.eta, "eta", torch.float32)
+    if req_lens is not None:
+        _need(req_lens, "req_lens", torch.int32)
+        _need(out.tau, "tau", torch.float32)
+    _check(load_library().fold_q8_split_query(
+        ctypes.byref(qv.view), int(q.shape[-1]), sm_scale, _ptr(req_lens), kappa,
+        _ptr(out.planes), _ptr(out.eta), None if req_lens is None else _ptr(out.tau),
+        _stream(stream)))
+    return out
+
+
+def q8_empty_query(q: torch.Tensor) -> Q8Query:
+    b, h, d = q.shape
+    return Q8Query(torch.empty(b, h, 2, d, dtype=torch.int8, device=q.device),
+                   torch.empty(b, h, dtype=torch.float32, device=q.device),
+                   torch.empty(b, dtype=torch.float32, device=q.device))
+
+
+def fold_q8_ref_estimate(kv: KV, keys: Q8Keys, q: Q8Query, z_out: torch.Tensor, params=None,
+                         stream=None) -> torch.Tensor:
+    _need(z_out, "z_out", torch.float32)
+    p = None
+    if params is not None:
+        p = fold_est_params(params["sink"], params["recent"], params["strata"],
+                            params["trim_lo"], params["trim_hi"])
+    kk, qq = keys.view(), q.view()
+    _check(load_library().fold_q8_ref_estimate(
+        ctypes.byref(kv.view), ctypes.byref(kk), ctypes.byref(qq),
+        None if p is None else ctypes.byref(p), _ptr(z_out), _stream(stream)))
+    return z_out
+
+
+def fold_q8_decode_rows_per_group(kv: KV, q: Q8Query) -> int:
+    qq = q.view()
+    return load_library().fold_q8_decode_rows_per_group(ctypes.byref(kv.view), ctypes.byref(qq))
+
+
+def fold_q8_decode_row_groups(kv: KV, q: Q8Query) -> int:
+    qq = q.view()
+    return load_library().fold_q8_decode_row_groups(ctypes.byref(kv.view), ctypes.byref(qq))
+
+
+def fold_q8_decode_split(kv: KV, keys: Q8Keys, q: Q8Query, z: torch.Tensor, depth_T: float,
+                         num_splits: int, slot_offset: int, part_A: torch.Tensor,
+                         part_L: torch.Tensor, x_out: Optional[torch.Tensor] = None,
+                         xc_out: Optional[torch.Tensor] = None,
+                         key_gate_out: Optional[torch.Tensor] = None,
+                         page_gate_out: Optional[torch.Tensor] = None,
+                         refine_gate_out: Optional[torch.Tensor] = None, stream=None) -> None:
+    _need(z, "z", torch.float32)
+    _need(part_A, "part_A", torch.float32)
+    _need(part_L, "part_L", torch.float32)
+    outs = ((x_out, "x_out", torch.float32), (xc_out, "xc_out", torch.float32),
+            (key_gate_out, "key_gate_out", torch.uint8),
+            (page_gate_out, "page_gate_out", torch.uint8),
+            (refine_gate_out, "refine_gate_out", torch.uint8))
+    dbg = None
+    if any(t is not None for t, _, _ in outs):
+        for t, nm, dt in outs:
+            if t is not None:
+                _need(t, nm, dt)
+        dbg = fold_q8_debug(*(_ptr(t) for t, _, _ in outs))
+    kk, qq = keys.view(), q.view()
+    _check(load_library().fold_q8_decode_split(
+        ctypes.byref(kv.view), ctypes.byref(kk), ctypes.byref(qq), _ptr(z), depth_T, num_splits,
+        slot_offset, int(part_A.shape[0]), _ptr(part_A), _ptr(part_L),
+        None if dbg is None else ctypes.byref(dbg), _stream(stream)))

@@ -23,14 +23,18 @@ def lib():
 
 
 def _declared():
-    src = open(os.path.join(ROOT, "include", "fold.h")).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(fold_[a-z0-9_]+)\s*\(", src)))
+    names = set()
+    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if h.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", h)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b(fold_[a-z0-9_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_every_declared_symbol_is_exported(lib):
     names = _declared()
-    assert len(names) >= 8
+    assert len(names) >= 14 and "fold_q8_decode_split" in names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(F.EXPORTED)
@@ -146,3 +150,81 @@ def test_binding_raises_when_library_missing(tmp_path):
             fmod.load_library(str(tmp_path / "libfold.so"))
     finally:
         fmod._lib = saved
+
+
+# ------------------------------------------------- two-plane INT8 key cache --
+def _q8(kv_heads=2, heads=8, **over):
+    from paper_2609_33410_amd.fold import fold_q8_keys, fold_q8_query
+    keys = fold_q8_keys(FAKE, FAKE, FAKE)
+    q = fold_q8_query(FAKE, FAKE, FAKE, 2, heads)
+    for k, v in over.items():
+        setattr(keys if k in ("plane_a", "plane_b", "scale") else q, k, v)
+    return keys, q
+
+
+def _q8_decode(lib, kv, keys, q, T=math.inf, splits=1, z=FAKE):
+    return lib.fold_q8_decode_split(ctypes.byref(kv), ctypes.byref(keys), ctypes.byref(q), z, T,
+                                    splits, 0, splits, FAKE, FAKE, None, None)
+
+
+@pytest.mark.parametrize("over,kvo,want", [
+    ({"plane_b": None}, {}, F.FOLD_E_INVAL),
+    ({"scale": FAKE + 2}, {}, F.FOLD_E_INVAL),
+    ({"planes": FAKE + 4}, {}, F.FOLD_E_INVAL),
+    ({"tau": None}, {}, F.FOLD_E_INVAL),
+    ({"eta": None}, {}, F.FOLD_E_INVAL),
+    ({}, {"v": None}, F.FOLD_E_INVAL),
+    ({"num_heads": 6}, {}, F.FOLD_E_UNSUPPORTED),     # GQA group 3
+    ({"num_heads": 128}, {}, F.FOLD_E_UNSUPPORTED),   # GQA group 64
+])
+def test_q8_decode_rejects_bad_args(lib, over, kvo, want):
+    keys, q = _q8(**over)
+    kv = _kv(**kvo)
+    kv.k = None                     # the two-plane calls never read the BF16 key pointer
+    assert _q8_decode(lib, kv, keys, q) == want
+    assert len(lib.fold_last_error()) > 0
+
+
+def test_q8_decode_rejects_bad_depth_and_split(lib):
+    keys, q = _q8()
+    assert _q8_decode(lib, _kv(), keys, q, T=float("nan")) == F.FOLD_E_INVAL
+    assert _q8_decode(lib, _kv(), keys, q, splits=0) == F.FOLD_E_INVAL
+    assert _q8_decode(lib, _kv(), keys, q, z=None) == F.FOLD_E_INVAL
+
+
+def test_q8_front_rejects_bad_args(lib):
+    kv = _kv()
+    # writer: a token list without planes; negative count
+    assert lib.fold_q8_write_keys(ctypes.byref(kv), FAKE, FAKE, FAKE, 4, None, FAKE, FAKE,
+                                  None) == F.FOLD_E_INVAL
+    assert lib.fold_q8_write_keys(ctypes.byref(kv), FAKE, FAKE, FAKE, -1, FAKE, FAKE, FAKE,
+                                  None) == F.FOLD_E_INVAL
+    assert lib.fold_q8_write_keys(ctypes.byref(_kv(page_size=8)), FAKE, FAKE, FAKE, 4, FAKE,
+                                  FAKE, FAKE, None) == F.FOLD_E_INVAL
+    # an empty token list is a valid no-op
+    assert lib.fold_q8_write_keys(ctypes.byref(kv), None, None, None, 0, None, None, None,
+                                  None) == F.FOLD_OK
+    q = _q()
+    split = lib.fold_q8_split_query
+    assert split(ctypes.byref(q), 96, 0.1, None, 0.0, FAKE, FAKE, None, None) == F.FOLD_E_INVAL
+    assert split(ctypes.byref(q), 128, 0.1, FAKE, 0.0, FAKE, FAKE, None, None) == F.FOLD_E_INVAL
+    assert split(ctypes.byref(q), 128, 0.1, FAKE, float("nan"), FAKE, FAKE, FAKE,
+                 None) == F.FOLD_E_INVAL
+    assert split(ctypes.byref(q), 128, float("inf"), None, 0.0, FAKE, FAKE, None,
+                 None) == F.FOLD_E_INVAL
+    keys, q8 = _q8()
+    csr = _kv(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=4)
+    assert lib.fold_q8_ref_estimate(ctypes.byref(csr), ctypes.byref(keys), ctypes.byref(q8), None,
+                                    FAKE, None) == F.FOLD_E_INVAL
+
+
+def test_q8_row_group_queries(lib):
+    keys, q = _q8()
+    kv = _kv()
+    assert lib.fold_q8_decode_rows_per_group(ctypes.byref(kv), ctypes.byref(q)) == 16
+    assert lib.fold_q8_decode_row_groups(ctypes.byref(kv), ctypes.byref(q)) == 1
+    # 64 requests x 8 heads stacked on one kv sequence: groups of 32 rows (whole GQA groups)
+    csr = _kv(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=64, num_kv_heads=1)
+    assert lib.fold_q8_decode_rows_per_group(ctypes.byref(csr), ctypes.byref(q)) == 32
+    assert lib.fold_q8_decode_row_groups(ctypes.byref(csr), ctypes.byref(q)) == 16
+    assert lib.fold_q8_decode_row_groups(ctypes.byref(_kv(head_dim=5)), ctypes.byref(q)) == -1
