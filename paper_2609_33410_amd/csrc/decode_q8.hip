@@ -22,10 +22,11 @@
 //            scan's: channels on M, rows on N, the chunk's keys on K, the
 //            weight as bf16 hi + bf16 residual.
 //
-// Pipeline per wave, three chunks deep: plane A and scales of chunk t+2 are
-// requested, chunk t+1 is scored and its plane-B and value rows requested,
-// and chunk t is refined and multiplied.  Dense decode (T = inf) requests the
-// value rows together with plane A.
+// Pipeline per wave: while chunk t is refined and multiplied, chunk t+1 has
+// been scored and its plane-B and value rows requested, and plane A of the
+// next chunks is in flight in a ring of four (at a finite depth chunks t+2 ..
+// t+5; in dense decode, where every value row is requested with plane A,
+// chunks t+1 .. t+3).
 #include "decode_common.h"
 
 namespace fold {
@@ -53,15 +54,22 @@ struct Q8Loc {
   uint32_t nk;
 };
 
-__device__ __forceinline__ Q8Loc q8_loc(const Q8DecodeArgs& a, const ScanPlace& p, int c) {
-  const ScanGeometry& g = a.d.geo;
+// Page of 16-key chunk c: pshift = log2(page_size / 16) when that is a power
+// of two (a shift), else -1 (a division).
+__device__ __forceinline__ int chunk_page_of(const ScanGeometry& g, int c, int pshift) {
+  return pshift >= 0 ? c >> pshift : (c * kChunk) / g.page_size;
+}
+
+// Where chunk c lives, given its block-table entry phys (ignored for a
+// contiguous view).
+__device__ __forceinline__ Q8Loc q8_loc(const ScanGeometry& g, const ScanPlace& p, int c,
+                                        int phys, int pshift) {
   Q8Loc l{0, 0};
   if (c < p.nchunks) {
     const int key0 = c * kChunk;
     bool ok = true;
     if (g.page_size > 0) {
-      const int page = key0 / g.page_size;
-      const int phys = ld_uniform(g.block_table, static_cast<size_t>(p.seq) * g.max_pages + page);
+      const int page = chunk_page_of(g, c, pshift);
       ok = phys >= 0 && phys < g.num_pages;
       l.row = (static_cast<size_t>(ok ? phys : 0) * g.hkv + p.kvh) * g.page_size +
               (key0 - page * g.page_size);
@@ -73,15 +81,21 @@ __device__ __forceinline__ Q8Loc q8_loc(const Q8DecodeArgs& a, const ScanPlace& 
   return l;
 }
 
-template <int D, int RB>
-struct Q8Slot {  // one chunk between its plane-A request and its product
-  static constexpr int NKI = D / 64;
-  static constexpr int NK = D / 32;
+template <int D, bool DENSE>
+struct Q8AStage {
   Q8Loc loc;
-  u32x4 ka[NKI];
-  u32x4 kb[NKI];
-  u32x4 vv[NK];
-  uint32_t sc;     // BF16 scale of key l%16 (2-byte loads: any row alignment)
+  u32x4 ka[D / 64];
+  uint32_t sc;                    // BF16 scale of key 4(l/16) + l%4 (2-byte loads: any row alignment)
+  u32x4 vv[DENSE ? D / 32 : 1];
+};
+
+// A chunk from its coarse pass to its product.
+template <int D, int RB, bool DENSE>
+struct Q8BStage {
+  Q8Loc loc;
+  uint32_t sc;
+  u32x4 kb[D / 64];
+  u32x4 vv[DENSE ? 1 : D / 32];
   float xc[RB][4];
   uint32_t ref;    // bit 4b+i: key 4(l/16)+i refined for the group of row block b
   uint32_t vmask;  // value rows to read (wave-uniform)
@@ -95,7 +109,9 @@ struct Q8Scan {
   static constexpr int NB = D / 16;           // 16-channel blocks of the value product
   static constexpr int VSTRIDE = 2 * D + 16;  // bytes per key row of the LDS value tile
   static constexpr int R = 16 * RB;
-  using Slot = Q8Slot<D, RB>;
+  static constexpr int NA = 4;                 // plane-A ring depth (chunks)
+  using AS = Q8AStage<D, DENSE>;
+  using BS = Q8BStage<D, RB, DENSE>;
 
   const Q8DecodeArgs& a;
   const ScanGeometry& g;
@@ -115,54 +131,68 @@ struct Q8Scan {
 
   __device__ Q8Scan(const Q8DecodeArgs& a_) : a(a_), g(a_.d.geo) {}
 
-  __device__ __forceinline__ void load_a(Slot& s) const {
+  // Plane A and the scales (dense decode: and every value row) of a chunk.
+  __device__ __forceinline__ void load_a(AS& s) const {
     const rsrc_t ra = make_rsrc(a.keys.ka + s.loc.row * D, s.loc.nk * D);
     const rsrc_t rs = make_rsrc(a.keys.ks + s.loc.row, s.loc.nk * 2);
 #pragma unroll
     for (int c = 0; c < NKI; ++c) s.ka[c] = buf_load(ra, n16 * D + 64 * c + 16 * grp);
-    s.sc = buf_load2(rs, 2 * n16);
+    s.sc = buf_load2(rs, 2 * (4 * grp + (lane & 3)));
+    if constexpr (DENSE) load_v(s.loc, 0xFFFFu, s.vv);
   }
 
-  __device__ __forceinline__ void load_v(Slot& s, uint32_t mask) const {
-    const rsrc_t rv = make_rsrc(g.v + s.loc.row * D, s.loc.nk * D * 2);
+  __device__ __forceinline__ void load_v(const Q8Loc& loc, uint32_t mask, u32x4 (&vv)[NK]) const {
+    const rsrc_t rv = make_rsrc(g.v + loc.row * D, loc.nk * D * 2);
     // lane l, load i: the 16 bytes at 1024 i + 16 l of the chunk (key (1024 i + 16 l) / 2D)
 #pragma unroll
     for (int i = 0; i < NK; ++i) {
       const uint32_t off = 1024u * i + 16u * lane;
       const uint32_t key = off / (2 * D);
-      s.vv[i] = buf_load(rv, DENSE || ((mask >> key) & 1u) ? off : kOutOfRange);
+      vv[i] = buf_load(rv, DENSE || ((mask >> key) & 1u) ? off : kOutOfRange);
     }
   }
 
-  __device__ __forceinline__ void load_b(Slot& s) const {
-    const rsrc_t rb = make_rsrc(a.keys.kb + s.loc.row * D, s.loc.nk * D);
-    const bool want = (s.bmask >> n16) & 1u;
+  // The gated requests of a scored chunk: plane B of refined keys (and, at a
+  // finite depth, value rows of live keys).
+  __device__ __forceinline__ void load_bv(BS& s) const {
+    if (s.bmask) {  // wave-uniform: no request at all when no key is refined
+      const rsrc_t rb = make_rsrc(a.keys.kb + s.loc.row * D, s.loc.nk * D);
+      const bool want = (s.bmask >> n16) & 1u;
 #pragma unroll
-    for (int c = 0; c < NKI; ++c)
-      s.kb[c] = buf_load(rb, want ? n16 * D + 64 * c + 16 * grp : kOutOfRange);
+      for (int c = 0; c < NKI; ++c)
+        s.kb[c] = buf_load(rb, want ? n16 * D + 64 * c + 16 * grp : kOutOfRange);
+    }
+    if constexpr (!DENSE) {
+      if (s.vmask) load_v(s.loc, s.vmask, s.vv);
+    }
   }
 
-  // Scales of keys 4(l/16)+i, i < 4: key k's scale sits in lane k.
-  __device__ __forceinline__ void scales(const Slot& s, float (&e)[4]) const {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      e[i] = bf16_lo(static_cast<uint32_t>(__shfl(static_cast<int>(s.sc), 4 * grp + i, 64)));
+  // Scales of keys 4(l/16)+i, i < 4: lane l loaded key 4(l/16) + l%4, so key
+  // 4(l/16)+i sits in lane i of the lane's own quad (DPP quad broadcast).
+  __device__ __forceinline__ void scales(uint32_t sc16, float (&e)[4]) const {
+    const int v = static_cast<int>(sc16);
+    e[0] = bf16_lo(static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, v, 0x00, 0xF, 0xF, false)));
+    e[1] = bf16_lo(static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, v, 0x55, 0xF, 0xF, false)));
+    e[2] = bf16_lo(static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, v, 0xAA, 0xF, 0xF, false)));
+    e[3] = bf16_lo(static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, v, 0xFF, 0xF, 0xF, false)));
   }
 
-  // Coarse scores, group gates and read masks of chunk c (plane A in s.ka).
-  __device__ __forceinline__ void coarse(int c, Slot& s) const {
+  // Coarse scores, group gates and read masks of chunk c (plane A in in.ka).
+  __device__ __forceinline__ void coarse(int c, const AS& in, BS& s) const {
     const int key0 = c * kChunk;
     const int nk = c < p.nchunks ? min(kChunk, p.n - key0) : 0;
+    s.loc = in.loc;
+    s.sc = in.sc;
     float e[4];
-    scales(s, e);
+    scales(in.sc, e);
     uint32_t lv = 0, rf = 0;
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
       i32x4 caa = {0, 0, 0, 0}, cab = {0, 0, 0, 0};
 #pragma unroll
       for (int c2 = 0; c2 < NKI; ++c2) {
-        caa = mfma_i8(s.ka[c2], qa[b][c2], caa);
-        cab = mfma_i8(s.ka[c2], qb[b][c2], cab);
+        caa = mfma_i8(in.ka[c2], qa[b][c2], caa);
+        cab = mfma_i8(in.ka[c2], qb[b][c2], cab);
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -175,11 +205,13 @@ struct Q8Scan {
         if (DBG && a.xc_out && ok) a.xc_out[xrow[b] * g.max_seq_len + key0 + 4 * grp + i] = xc;
       }
     }
-    // OR over the lanes holding the rows of one GQA group.
+    // OR over the lanes holding the rows of one GQA group: aligned groups of
+    // 2, 4, 8 or 16 lanes (quad swaps, then half-row and row mirrors).
     uint32_t both = lv | (rf << 16);
-#pragma unroll
-    for (int m = 1; m < 16; m <<= 1)
-      if (gspan & m) both |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(both), m, 64));
+    if (gspan >= 1) both |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(both), 0xB1, 0xF, 0xF, false));
+    if (gspan >= 3) both |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(both), 0x4E, 0xF, 0xF, false));
+    if (gspan >= 7) both |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(both), 0x141, 0xF, 0xF, false));
+    if (gspan >= 15) both |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(both), 0x140, 0xF, 0xF, false));
     if (cross_b) both |= ((both >> 4) & 0x000F000Fu) | ((both & 0x000F000Fu) << 4);
     both &= (both << 16) | 0xFFFFu;  // refine only live keys
     s.ref = both >> 16;
@@ -206,11 +238,11 @@ struct Q8Scan {
   }
 
   // Refined scores, weights, L and the value product of chunk c.
-  __device__ __forceinline__ void finish(int c, const Slot& s) {
+  __device__ __forceinline__ void finish(int c, const BS& s, const u32x4 (&vv)[NK]) {
     const int key0 = c * kChunk;
     const int nk = c < p.nchunks ? min(kChunk, p.n - key0) : 0;
     float e[4];
-    scales(s, e);
+    scales(s.sc, e);
     u32x2 phi[RB], plo[RB];
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
@@ -222,7 +254,8 @@ struct Q8Scan {
           cbb = mfma_i8(s.kb[c2], qb[b][c2], cbb);
         }
       }
-      uint32_t hi[4], lo[4];
+      uint32_t hi[4];
+      float res[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const bool ok = rok[b] && 4 * grp + i < nk;
@@ -236,18 +269,18 @@ struct Q8Scan {
         lsum[b] += w;
         const float pw = live ? w : 0.0f;
         hi[i] = __float_as_uint(pw) & 0xffff0000u;
-        lo[i] = f32_to_bf16_rne(pw - __uint_as_float(hi[i]));
+        res[i] = pw - __uint_as_float(hi[i]);
         if (DBG && a.d.x_out && ok) a.d.x_out[xrow[b] * g.max_seq_len + key0 + 4 * grp + i] = x;
       }
       phi[b] = u32x2{(hi[0] >> 16) | hi[1], (hi[2] >> 16) | hi[3]};
-      plo[b] = u32x2{lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16)};
+      plo[b] = u32x2{pack_bf16_rne(res[0], res[1]), pack_bf16_rne(res[2], res[3])};
     }
     if (s.vmask == 0) return;  // wave-uniform: no live key in the chunk
 #pragma unroll
     for (int i = 0; i < NK; ++i) {
       const uint32_t off = 1024u * i + 16u * lane;
       const uint32_t key = off / (2 * D);
-      *reinterpret_cast<u32x4*>(vt + key * VSTRIDE + (off - key * 2 * D)) = s.vv[i];
+      *reinterpret_cast<u32x4*>(vt + key * VSTRIDE + (off - key * 2 * D)) = vv[i];
     }
     const unsigned char* col = vt + (4 * grp) * VSTRIDE + 2 * n16;
 #pragma unroll
@@ -270,7 +303,6 @@ struct Q8Scan {
 template <int D, int RB, bool DENSE, bool DBG>
 __global__ __launch_bounds__(kScanThreads) void decode_q8_kernel(const Q8DecodeArgs a) {
   using S = Q8Scan<D, RB, DENSE, DBG>;
-  using Slot = typename S::Slot;
   constexpr int NKI = S::NKI;
   constexpr int R = S::R;
   constexpr int kTileBytes = kScanWaves * 16 * S::VSTRIDE;
@@ -312,36 +344,65 @@ __global__ __launch_bounds__(kScanThreads) void decode_q8_kernel(const Q8DecodeA
     for (int blk = 0; blk < S::NB; ++blk) sc.acc[b][blk] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   }
 
+  int pshift = -1;
+  if (g.page_size > 0) {
+    const int cpp = g.page_size / kChunk;
+    if ((cpp & (cpp - 1)) == 0) pshift = __builtin_ctz(static_cast<unsigned>(cpp));
+  }
   const int cstride = kScanWaves * a.d.num_splits;
   const int c0 = kScanWaves * sc.p.split + wave;
   const int m = sc.p.nchunks > c0 ? (sc.p.nchunks - c0 + cstride - 1) / cstride : 0;
 
   if (m > 0) {
-    Slot s0, s1, s2;
-    auto request_a = [&](Slot& s, int k) {  // local chunk k: plane A, scales (+ values)
-      s.loc = q8_loc(a, sc.p, c0 + k * cstride);
+    // Chunk k's plane A lives in A[k % NA] from its request to its coarse pass
+    // (dense: to its product); its gated requests and coarse scores in
+    // B[k % 2] until its product.
+    constexpr int NA = S::NA;
+    typename S::AS A[NA];
+    typename S::BS B[2];
+    // Block-table entries of this wave's chunks c0 + k cstride, 64 local
+    // chunks at a time: lane j holds local chunk pt_base + j.  One vector load
+    // per window (one window covers a split of up to 64 chunks per wave), read
+    // with v_readlane, instead of a scalar load and its wait per chunk.
+    int pt = 0, pt_base = -64;
+    auto page_window = [&](int base) {
+      pt_base = base;
+      const int c = c0 + (base + sc.lane) * cstride;
+      pt = g.page_size > 0 && c < sc.p.nchunks
+               ? g.block_table[static_cast<size_t>(sc.p.seq) * g.max_pages +
+                               chunk_page_of(g, c, pshift)]
+               : 0;
+    };
+    auto request_a = [&](typename S::AS& s, int k) {
+      if (k >= pt_base + 64) page_window(k & ~63);  // uniform
+      const int phys = __builtin_amdgcn_readlane(pt, k - pt_base);
+      s.loc = q8_loc(g, sc.p, c0 + k * cstride, phys, pshift);
       sc.load_a(s);
-      if (DENSE) sc.load_v(s, 0xFFFFu);
     };
-    auto score = [&](Slot& s, int k) {  // coarse pass, then the gated requests
-      sc.coarse(c0 + k * cstride, s);
-      sc.load_b(s);
-      if (!DENSE) sc.load_v(s, s.vmask);
-    };
-    // Slot X holds chunk t (requests issued), Y chunk t+1 (plane A issued).
-    auto step = [&](Slot& X, Slot& Y, Slot& Z, int t) {
-      if (t + 2 < m) request_a(Z, t + 2);
-      if (t + 1 < m) score(Y, t + 1);
-      sc.finish(c0 + t * cstride, X);
-      return t + 1 < m;
-    };
-    request_a(s0, 0);
-    if (m > 1) request_a(s1, 1);
-    score(s0, 0);
-    for (int t = 0; t < m; t += 3) {
-      if (!step(s0, s1, s2, t)) break;
-      if (!step(s1, s2, s0, t + 1)) break;
-      if (!step(s2, s0, s1, t + 2)) break;
+#pragma unroll
+    for (int k = 0; k < NA; ++k)
+      if (k < m) request_a(A[k], k);
+    sc.coarse(c0, A[0], B[0]);
+    if (!DENSE && NA < m) request_a(A[0], NA);
+    sc.load_bv(B[0]);
+    for (int t = 0; t < m; t += NA) {
+#pragma unroll
+      for (int u = 0; u < NA; ++u) {
+        const int k = t + u;
+        if (k >= m) break;  // uniform
+        const int u1 = (u + 1) % NA;
+        if (k + 1 < m) {
+          sc.coarse(c0 + (k + 1) * cstride, A[u1], B[(u + 1) & 1]);
+          if (!DENSE && k + 1 + NA < m) request_a(A[u1], k + 1 + NA);
+          sc.load_bv(B[(u + 1) & 1]);
+        }
+        if constexpr (DENSE) {
+          sc.finish(c0 + k * cstride, B[u & 1], A[u].vv);
+          if (k + NA < m) request_a(A[u], k + NA);
+        } else {
+          sc.finish(c0 + k * cstride, B[u & 1], B[u & 1].vv);
+        }
+      }
     }
   }
 
