@@ -10,8 +10,10 @@ cache (4 MB L2 per XCD, 256 MB MALL) holds any of the step's data and no dirty
 line is left to drain during the step; each step is bracketed by HIP events on
 the stream the kernels are launched on.
 
-Prints ONE JSON line (rank 0).  ``--all`` adds one JSON line per workload and
-depth on stderr (used for the design notes' tables).
+Prints ONE JSON line (rank 0).  The line also carries the same workload over
+a two-plane INT8 key cache (``q8_keys``; Section 4, cache format).  ``--all``
+adds one JSON line per workload and depth on stderr (used for the design
+notes' tables).
 """
 
 from __future__ import annotations
@@ -39,6 +41,7 @@ def parse():
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--all", action="store_true", help="also time workloads 1-5 (stderr)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-q8", action="store_true", help="skip the two-plane INT8 key leg")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--splits", type=int, default=None, help="override the split count")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -100,6 +103,171 @@ class Path:
             read += int(kg.sum().item())
             total += sum(lv.seq_lens_host) * self.wl.num_kv_heads * rg
         return read / max(total, 1)
+
+
+class Q8Path:
+    """The same workload over a two-plane INT8 key cache (values stay BF16).
+
+    The cache is written once by the cache writer (untimed set-up, as a
+    prompt would be); a step is the query split, the reference estimate from
+    coarse logits, every level's gated scan and the combine."""
+
+    def __init__(self, wl, F, torch, kappa=0.0):
+        self.wl, self.F, self.torch, self.kappa = wl, F, torch, kappa
+        dev = wl.q.device
+        n_pool, hkv, rows, d = wl.k.shape
+        pool = F.kv_view(wl.k, None, torch.full((n_pool,), rows, dtype=torch.int32, device=dev),
+                         num_kv_heads=hkv, max_seq_len=rows)
+        self.keys = F.q8_empty_keys(wl.k)
+        tok_seq = torch.arange(n_pool, dtype=torch.int32, device=dev).repeat_interleave(rows)
+        tok_pos = torch.arange(rows, dtype=torch.int32, device=dev).repeat(n_pool)
+        k_src = wl.k.permute(0, 2, 1, 3).reshape(n_pool * rows, hkv, d).contiguous()
+        F.fold_q8_write_keys(pool, k_src, tok_seq, tok_pos, self.keys)
+        del k_src, tok_seq, tok_pos
+        # one appended token per request (the per-step append), for timing
+        self.app_kv = F.kv_view(self.keys.plane_a, None, wl.flat.seq_lens,
+                                num_kv_heads=hkv, max_seq_len=wl.flat.max_seq_len,
+                                block_table=wl.flat.block_table, k_is_layout_only=True)
+        b = wl.batch
+        self.app_seq = torch.arange(b, dtype=torch.int32, device=dev)
+        self.app_pos = (wl.flat.seq_lens - 1).to(torch.int32).contiguous()
+        self.app_src = torch.randn(b, hkv, d, device=dev).to(torch.bfloat16)
+        self.levels = [F.kv_view(self.keys.plane_a, wl.v, lv.seq_lens,
+                                 num_kv_heads=wl.num_kv_heads, max_seq_len=lv.max_seq_len,
+                                 block_table=lv.block_table, row_indptr=lv.row_indptr,
+                                 row_req=lv.row_req, max_reqs_per_seq=lv.max_reqs_per_seq,
+                                 k_is_layout_only=True) for lv in wl.levels]
+        self.flat = self.app_kv
+        self.qq = F.q8_empty_query(wl.q)
+        bq, h, d = wl.q.shape
+        self.splits = list(wl.level_splits)
+        total = sum(self.splits)
+        self.z = torch.empty(bq, h, dtype=torch.float32, device=dev)
+        self.part_A = torch.empty(total, bq, h, d, dtype=torch.float32, device=dev)
+        self.part_L = torch.empty(total, bq, h, dtype=torch.float32, device=dev)
+        self.out = torch.empty(bq, h, d, dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
+
+    def split(self, stream):
+        self.F.fold_q8_split_query(self.wl.q, self.wl.sm_scale, self.qq,
+                                   req_lens=self.wl.flat.seq_lens, kappa=self.kappa,
+                                   stream=stream)
+
+    def append(self, stream):
+        self.F.fold_q8_write_keys(self.app_kv, self.app_src, self.app_seq, self.app_pos,
+                                  self.keys, stream=stream)
+
+    def estimate(self, stream):
+        self.F.fold_q8_ref_estimate(self.flat, self.keys, self.qq, self.z, stream=stream)
+
+    def decode(self, T, stream):
+        off = 0
+        for kv, s in zip(self.levels, self.splits):
+            self.F.fold_q8_decode_split(kv, self.keys, self.qq, self.z, T, s, off, self.part_A,
+                                        self.part_L, stream=stream)
+            off += s
+
+    def combine(self, stream):
+        self.F.fold_combine(self.part_A, self.part_L, self.out, stream=stream)
+
+    def read_counts(self, T):
+        """(value rows, plane-B rows, read-group key rows) the scan reads at
+        depth T, from its own read-bit exports (untimed)."""
+        torch, F = self.torch, self.F
+        dev = self.wl.q.device
+        nv = nb = total = 0
+        off = 0
+        for lv, kv, s in zip(self.wl.levels, self.levels, self.splits):
+            rg = F.fold_q8_decode_row_groups(kv, self.qq)
+            kg = torch.zeros(lv.num_seqs, self.wl.num_kv_heads, rg, lv.max_seq_len,
+                             dtype=torch.uint8, device=dev)
+            bg = torch.zeros_like(kg)
+            F.fold_q8_decode_split(kv, self.keys, self.qq, self.z, T, s, off, self.part_A,
+                                   self.part_L, key_gate_out=kg, refine_gate_out=bg)
+            off += s
+            nv += int(kg.sum().item())
+            nb += int(bg.sum().item())
+            total += sum(lv.seq_lens_host) * self.wl.num_kv_heads * rg
+        return nv, nb, total
+
+
+def q8_bytes(wl, nv, nb):
+    """Algorithmic bytes of one two-plane scan (all levels): plane A and the
+    scale of every key, plane B of the nb refined rows, the nv value rows,
+    the query codes, eta, tau, references, block-table entries and partials."""
+    d = wl.head_dim
+    b, h, _ = wl.q.shape
+    keys = sum(sum(lv.seq_lens_host) for lv in wl.levels) * wl.num_kv_heads
+    total = keys * (d + 2) + nb * d + nv * 2 * d
+    total += 2 * b * h * d + 4 * b * h + 4 * b + 4 * b * h
+    if wl.page_size:
+        total += 4 * sum(sum((n + wl.page_size - 1) // wl.page_size for n in lv.seq_lens_host)
+                         for lv in wl.levels)
+    total += 4 * sum(wl.level_splits) * b * h * (d + 1)
+    return total, keys
+
+
+def time_q8(qp, T, steps, warmup, flush, torch):
+    """Median per-kernel and per-step durations (ms) of the two-plane step."""
+    stream = torch.cuda.current_stream()
+    res = {"split": [], "est": [], "dec": [], "comb": [], "step": [], "append": []}
+    for it in range(warmup + steps):
+        evict_caches(flush)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        ev[0].record(stream)
+        qp.split(stream)
+        ev[1].record(stream)
+        qp.estimate(stream)
+        ev[2].record(stream)
+        qp.decode(T, stream)
+        ev[3].record(stream)
+        qp.combine(stream)
+        ev[4].record(stream)
+        qp.append(stream)
+        ev[5].record(stream)
+        if it >= warmup:
+            ev[5].synchronize()
+            res["split"].append(ev[0].elapsed_time(ev[1]))
+            res["est"].append(ev[1].elapsed_time(ev[2]))
+            res["dec"].append(ev[2].elapsed_time(ev[3]))
+            res["comb"].append(ev[3].elapsed_time(ev[4]))
+            res["step"].append(ev[0].elapsed_time(ev[4]))
+            res["append"].append(ev[4].elapsed_time(ev[5]))
+    return {k: statistics.median(v) for k, v in res.items()}
+
+
+def q8_leg(wl, F, torch, flush, steps, warmup, name=None):
+    """Timings of the two-plane key path on the benchmark workload."""
+    qp = Q8Path(wl, F, torch)
+    stream = torch.cuda.current_stream()
+    qp.split(stream)
+    qp.estimate(stream)
+    out = {"kappa": qp.kappa, "cache": "two INT8 key planes + BF16 scale per key; BF16 values",
+           "step": "query split + estimate (coarse logits) + split scan + combine; the "
+                   "one-token append is timed apart"}
+    for T in (math.inf, 16.0):
+        nv, nb, total = qp.read_counts(T)
+        med = time_q8(qp, T, steps, warmup, flush, torch)
+        nbytes, keys = q8_bytes(wl, nv, nb)
+        key = "T=inf" if math.isinf(T) else f"T={T:g}"
+        out[key] = {"us_per_call": round(med["step"] * 1e3, 2),
+                    "decode_us": round(med["dec"] * 1e3, 2),
+                    "decode_bytes": int(nbytes),
+                    "decode_gbps": round(nbytes / (med["dec"] * 1e-3) / 1e9, 1),
+                    "bytes_per_key": round(nbytes / keys, 1),
+                    "value_read_fraction": round(nv / max(total, 1), 5),
+                    "refined_fraction": round(nb / max(total, 1), 5),
+                    "breakdown_us": {k: round(v * 1e3, 2) for k, v in med.items()}}
+        if math.isinf(T):
+            ach = nbytes / (med["dec"] * 1e-3) / 1e9
+            traffic = None if name is None else counter_traffic(name + " [two-plane keys]")[0]
+            out["roofline"] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
+                               "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
+                               "traffic": None if traffic is None else int(traffic),
+                               "kernel": "decode_q8_kernel (dense)"}
+    del qp
+    torch.cuda.empty_cache()
+    return out
 
 
 def kv_bytes(wl, lam):
@@ -331,6 +499,9 @@ def main():
         "keys_per_s": round(dense["keys"] / (step_ms * 1e-3), 1),
         "wall_s": round(wall, 2),
     }
+    if not args.no_q8:
+        line["q8_keys"] = q8_leg(wl, F, torch, flush, args.steps, args.warmup,
+                                 name=CONFIG_NAMES[args.config])
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(line), flush=True)
@@ -358,6 +529,11 @@ def main():
                        "decode_gbps": round(v["bytes"] / (v["med"]["dec"] * 1e-3) / 1e9, 1),
                        "value_read_fraction": round(v["lam"], 5),
                        "keys_per_s": round(v["keys"] / (v["med"]["step"] * 1e-3), 1)}
+                print(json.dumps(rec), file=sys.stderr, flush=True)
+            if not args.no_q8:
+                rec = {"workload": CONFIG_NAMES[i],
+                       "q8_keys": q8_leg(wl_i, F, torch, flush, args.steps, args.warmup,
+                                         name=CONFIG_NAMES[i])}
                 print(json.dumps(rec), file=sys.stderr, flush=True)
             del wl_i
             torch.cuda.empty_cache()
