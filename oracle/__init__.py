@@ -25,6 +25,8 @@ from .fold_oracle import (  # noqa: F401
     lse_and_cert,
     read_gates,
     row_diagnostics,
+    running_mean,
     scores,
     split_of_key,
+    value_mean,
 )

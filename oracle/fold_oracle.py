@@ -122,6 +122,24 @@ def split_of_key(n: int, num_splits: int) -> np.ndarray:
     return (np.arange(n) // TILE) % num_splits
 
 
+# --------------------------------------------------------- cut-key model ---
+def value_mean(v_bits: np.ndarray, seq: int, g: int, n: int, block_table, page_size: int
+               ) -> np.ndarray:
+    """Mean value row of keys 0..n-1 of (seq, g), FP64 (0 for an empty row).
+
+    The request's running mean of Section 4 ("Depth as a dial"): the value
+    model that stands in for every cut key."""
+    d = v_bits.shape[-1]
+    if n == 0:
+        return np.zeros(d)
+    return gather(v_bits, seq, g, n, block_table, page_size).mean(axis=0)
+
+
+def running_mean(prev: np.ndarray, count: int, v_new: np.ndarray) -> np.ndarray:
+    """Mean of count + 1 rows from the mean of the first count and the new row."""
+    return prev + (np.asarray(v_new, dtype=np.float64) - prev) / (count + 1)
+
+
 # ------------------------------------------------------------ level driver -
 def _rows_of(seq: int, g: int, group: int, row_indptr, row_req) -> List[Tuple[int, int]]:
     """(request, head) pairs of the query rows that attend kv seq ``seq``, head ``g``."""
@@ -136,21 +154,24 @@ def decode_level(q_bits, k_bits, v_bits, *, num_kv_heads: int, page_size: int,
                  sm_scale: float, seq_lens: Sequence[int], block_table=None,
                  row_indptr=None, row_req=None, z: np.ndarray, T: float, num_splits: int,
                  imposed_x: Optional[np.ndarray] = None,
-                 chunks: Optional[Iterable[Tuple[int, int]]] = None
-                 ) -> Tuple[np.ndarray, np.ndarray]:
+                 chunks: Optional[Iterable[Tuple[int, int]]] = None,
+                 with_cut: bool = False):
     """Split partials of one scan level (steps O1-O6).
 
     Returns ``part_A [S, B, H, D]`` and ``part_L [S, B, H]`` (FP64); rows the
     level does not cover stay zero.  ``imposed_x`` ``[B, H, max_len]`` FP32,
     if given, replaces the FP64 live decisions by the FP32 rule applied to
     those values.  ``chunks`` restricts the work to the listed
-    ``(kv seq, kv head)`` pairs.
+    ``(kv seq, kv head)`` pairs.  With ``with_cut`` a third array
+    ``part_Lcut [S, B, H]`` holds the cut keys' summed weights (the mass the
+    value model of Section 4 attaches to its virtual row).
     """
     q = bf16_bits_to_f64(q_bits)
     b, h, d = q.shape
     group = h // num_kv_heads
     part_a = np.zeros((num_splits, b, h, d))
     part_l = np.zeros((num_splits, b, h))
+    part_c = np.zeros((num_splits, b, h))
     if chunks is None:
         chunks = [(s, g) for s in range(len(seq_lens)) for g in range(num_kv_heads)]
     for seq, g in chunks:
@@ -176,17 +197,37 @@ def decode_level(q_bits, k_bits, v_bits, *, num_kv_heads: int, page_size: int,
             a, l = fold(x[:, m], live[:, m], vals[m])
             part_a[sp, ri, hi] = a
             part_l[sp, ri, hi] = l
+            part_c[sp, ri, hi] = (np.exp2(x[:, m]) * ~live[:, m]).sum(axis=-1)
+    if with_cut:
+        return part_a, part_l, part_c
     return part_a, part_l
 
 
 # ---------------------------------------------------------------- O7 -------
-def combine(part_a: np.ndarray, part_l: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
-    """Sum the slots in increasing order and take the quotient ``A / L``."""
+def combine(part_a: np.ndarray, part_l: np.ndarray, part_lcut: Optional[np.ndarray] = None,
+            mean: Optional[np.ndarray] = None, num_kv_heads: int = 1
+            ) -> Tuple[np.ndarray, np.ndarray]:
+    """Sum the slots in increasing order and take the quotient ``A / L``.
+
+    With the cut-key value model (``part_lcut [S, B, H]`` and the request
+    means ``mean [B, Hkv, D]``), the cut keys of every slot add their summed
+    weight times the mean of the row's request and kv head to *A*: a virtual
+    row whose weight is the cut mass (Section 4, "Depth as a dial").  The
+    term is linear in the cut mass, so adding it per slot or after the slot
+    sum is the same value."""
     a = np.zeros(part_a.shape[1:])
     l = np.zeros(part_l.shape[1:])
     for s in range(part_a.shape[0]):
         a = a + part_a[s]
         l = l + part_l[s]
+    if part_lcut is not None:
+        c = np.zeros(part_lcut.shape[1:])
+        for s in range(part_lcut.shape[0]):
+            c = c + part_lcut[s]
+        b_, h = c.shape
+        group = h // num_kv_heads
+        mu = np.asarray(mean, dtype=np.float64)[:, np.arange(h) // group, :]  # [B, H, D]
+        a = a + c[..., None] * mu
     with np.errstate(invalid="ignore", divide="ignore"):
         o = a / l[..., None]
     return o, l

@@ -186,7 +186,7 @@ def decode_level_q8(qa, qb, eta, planes, v_bits, *, num_kv_heads: int, page_size
                     z: np.ndarray, T: float, tau: np.ndarray, num_splits: int,
                     imposed: Optional[Tuple[np.ndarray, np.ndarray]] = None,
                     chunks: Optional[Iterable[Tuple[int, int]]] = None,
-                    want_scores: bool = False):
+                    want_scores: bool = False, with_cut: bool = False):
     """Split partials of one level over a two-plane key cache.
 
     ``qa, qb`` [B, H, D] int8 and ``eta`` [B, H] FP32 are the query codes;
@@ -195,7 +195,8 @@ def decode_level_q8(qa, qb, eta, planes, v_bits, *, num_kv_heads: int, page_size
     threshold.  ``imposed = (xc_f32, x_f32)`` [B, H, max_len] replaces the
     FP64 decisions by FP32 decisions on those values: the group bits from the
     coarse scores, each row's own cut from the refined score.
-    Returns ``part_A [S, B, H, D]``, ``part_L [S, B, H]`` and, with
+    Returns ``part_A [S, B, H, D]``, ``part_L [S, B, H]``, with ``with_cut``
+    also ``part_Lcut [S, B, H]`` (the cut keys' summed weights) and, with
     ``want_scores``, a dict ``(seq, g) -> (rows, xc, x, live, refine)``.
     """
     pa_, pb_, pe_ = planes
@@ -203,6 +204,7 @@ def decode_level_q8(qa, qb, eta, planes, v_bits, *, num_kv_heads: int, page_size
     group = h // num_kv_heads
     part_a = np.zeros((num_splits, b_, h, d))
     part_l = np.zeros((num_splits, b_, h))
+    part_c = np.zeros((num_splits, b_, h))
     info = {}
     if chunks is None:
         chunks = [(s, g) for s in range(len(seq_lens)) for g in range(num_kv_heads)]
@@ -242,11 +244,13 @@ def decode_level_q8(qa, qb, eta, planes, v_bits, *, num_kv_heads: int, page_size
                 continue
             part_a[sp, ri, hi] = (w[:, m] * counts[:, m]) @ vals[m]
             part_l[sp, ri, hi] = w[:, m].sum(axis=1)
+            part_c[sp, ri, hi] = (w[:, m] * ~counts[:, m]).sum(axis=1)
         if want_scores:
             info[(seq, g)] = (list(zip(ri.tolist(), hi.tolist())), xc, x, live, ref)
+    out = (part_a, part_l) + ((part_c,) if with_cut else ())
     if want_scores:
-        return part_a, part_l, info
-    return part_a, part_l
+        return out + (info,)
+    return out
 
 
 def _gather_raw(arr: np.ndarray, seq: int, g: int, n: int, block_table, page_size: int):
