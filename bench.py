@@ -191,6 +191,62 @@ class Q8Path:
         return nv, nb, total
 
 
+def model_leg(path, wl, F, torch, flush, steps, warmup):
+    """The cut-key value model on the benchmark workload at T=16: scan time with
+    the cut masses written, and the output error against the dense output
+    (exact softmax up to FP32 rounding) without and with the model."""
+    dev = wl.q.device
+    b, h, d = wl.q.shape
+    fl = wl.flat
+    kv = F.kv_view(wl.k, wl.v, fl.seq_lens, num_kv_heads=wl.num_kv_heads,
+                   max_seq_len=fl.max_seq_len, block_table=fl.block_table)
+    mean = torch.empty(fl.num_seqs, wl.num_kv_heads, d, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    path.estimate(stream)
+    F.fold_value_mean(kv, mean)
+    part_C = torch.empty_like(path.part_L)
+
+    def decode_cut(stream):
+        off = 0
+        for kvl, s in zip(path.levels, path.splits):
+            F.fold_decode_split(kvl, path.qv, wl.sm_scale, path.z, 16.0, s, off, path.part_A,
+                                path.part_L, part_Lcut=part_C, stream=stream)
+            off += s
+
+    ts = []
+    for it in range(warmup + steps):
+        evict_caches(flush)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        decode_cut(stream)
+        e1.record(stream)
+        if it >= warmup:
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+    dense = torch.empty(b, h, d, dtype=torch.float32, device=dev)
+    path.decode(math.inf, stream)
+    F.fold_combine(path.part_A, path.part_L, dense, stream=stream)
+    plain = torch.empty_like(dense)
+    path.decode(16.0, stream)
+    F.fold_combine(path.part_A, path.part_L, plain, stream=stream)
+    model = torch.empty_like(dense)
+    decode_cut(stream)
+    F.fold_combine(path.part_A, path.part_L, model, part_Lcut=part_C, mean=mean, stream=stream)
+    torch.cuda.synchronize()
+    scale = dense.abs().amax(dim=-1).clamp_min(1e-30)
+
+    def err(o):
+        return float(((o - dense).abs().amax(dim=-1) / scale).max())
+
+    def l2(o):
+        return float((o - dense).norm() / dense.norm())
+
+    return {"T": 16.0, "model": "request mean (cut keys carry their request's mean value row)",
+            "decode_us_with_cut_masses": round(statistics.median(ts) * 1e3, 2),
+            "max_row_err_vs_dense": {"no_model": err(plain), "request_mean": err(model)},
+            "rel_l2_vs_dense": {"no_model": l2(plain), "request_mean": l2(model)}}
+
+
 def q8_bytes(wl, nv, nb):
     """Algorithmic bytes of one two-plane scan (all levels): plane A and the
     scale of every key, plane B of the nb refined rows, the nv value rows,
@@ -499,6 +555,8 @@ def main():
         "keys_per_s": round(dense["keys"] / (step_ms * 1e-3), 1),
         "wall_s": round(wall, 2),
     }
+    line["value_model"] = model_leg(Path(wl, F, torch), wl, F, torch, flush, args.steps,
+                                    args.warmup)
     if not args.no_q8:
         line["q8_keys"] = q8_leg(wl, F, torch, flush, args.steps, args.warmup,
                                  name=CONFIG_NAMES[args.config])

@@ -40,7 +40,7 @@
 extern "C" {
 #endif
 
-#define FOLD_ABI_VERSION 1
+#define FOLD_ABI_VERSION 2
 
 typedef enum fold_status {
   FOLD_OK = 0,
@@ -126,6 +126,25 @@ typedef struct fold_debug {
   uint8_t* page_gate_out;
 } fold_debug;
 
+/* Cut-key value model (Section 4, "Depth as a dial"): at a finite depth the
+ * keys cut from row i's A are modelled by the mean value row of row i's
+ * request and kv head.  Their summed weight, the cut mass (an extra output
+ * of the scans, one FP32 per slot and row), multiplies that mean in
+ * fold_combine: a virtual row whose weight is the cut mass.  The term is
+ * linear in the cut mass, so it is the same added per slot or after the slot
+ * sum, and pairs stay additive.
+ *   part_Lcut [num_slots][num_rows] fp32: the scans' cut masses
+ *   mean      [batch][num_kv_heads][head_dim] fp32: request means
+ *             (fold_value_mean, fold_value_mean_append)
+ *   rows are [batch][num_heads]; row r * num_heads + h uses
+ *   mean[r][h / (num_heads / num_kv_heads)]. */
+typedef struct fold_value_model {
+  const float* part_Lcut;
+  const float* mean;
+  int32_t num_heads;
+  int32_t num_kv_heads;
+} fold_value_model;
+
 /* FOLD_ABI_VERSION of the built library. */
 int fold_abi_version(void);
 
@@ -169,12 +188,16 @@ fold_status fold_ref_estimate(const fold_kv_view* kv, const fold_q_view* q, floa
  *   z        [batch][num_heads] fp32, the declared references
  *   depth_T  +INFINITY for dense decode, else a finite T >= 0 (NaN or negative
  *            is FOLD_E_INVAL); a key is live for row i iff x_ij >= -T
+ *   part_Lcut [num_slots][batch][num_heads] fp32 or NULL: the cut mass of
+ *            each written slot and row (the summed weights of keys with
+ *            x_ij < -T; 0 at T = inf), for the cut-key value model
  *   dbg      NULL, or the optional exports above
  */
 fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
                               const float* z, float depth_T, int32_t num_splits,
                               int32_t slot_offset, int32_t num_slots, float* part_A,
-                              float* part_L, const fold_debug* dbg, void* stream);
+                              float* part_L, float* part_Lcut, const fold_debug* dbg,
+                              void* stream);
 
 /*
  * fold_combine - additive combine (Algorithm 1, last step; Section 4): for
@@ -186,10 +209,36 @@ fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, floa
  *   lse_out [num_rows] fp32 or NULL: base-2 log-sum-exp Z + log2(sum L)
  *   cert_out [num_rows] u8 or NULL: range certificate of Section 3,
  *            bit0 sum L < 2^-1, bit1 sum L > 2^100, bit2 a non-finite output
+ *   model    NULL, or the cut-key value model: o = (sum A + (sum Lcut) mean) / sum L
+ *            (num_rows must equal batch * num_heads of the model's rows)
  */
 fold_status fold_combine(const float* part_A, const float* part_L, int32_t num_slots,
                          int32_t num_rows, int32_t head_dim, const float* z, void* out,
-                         fold_dtype out_dtype, float* lse_out, uint8_t* cert_out, void* stream);
+                         fold_dtype out_dtype, float* lse_out, uint8_t* cert_out,
+                         const fold_value_model* model, void* stream);
+
+/*
+ * fold_value_mean - request mean value rows (the running mean of Section 4's
+ * value model): mean_out[s][g] = mean of value rows 0..n_s-1 of kv sequence
+ * s, head g (0 for an empty sequence), FP32 sums in a fixed order.
+ *   kv        per-request view (kv->v read; kv->k not read; no CSR rows)
+ *   mean_out  [num_seqs][num_kv_heads][head_dim] fp32
+ */
+fold_status fold_value_mean(const fold_kv_view* kv, float* mean_out, void* stream);
+
+/*
+ * fold_value_mean_append - running update of the request means for appended
+ * tokens: mean[s][g] += (v - mean[s][g]) / (pos + 1) for a token of kv
+ * sequence s at position pos (its new length is pos + 1).
+ *   kv        layout of the means (num_seqs, num_kv_heads, head_dim)
+ *   v_src     [n_tok][num_kv_heads][head_dim] bf16, the tokens' value rows
+ *   tok_seq, tok_pos [n_tok] int32; a token with an unknown sequence or a
+ *             negative position is skipped.  At most one token per sequence
+ *             per call (two would race).
+ */
+fold_status fold_value_mean_append(const fold_kv_view* kv, const void* v_src,
+                                   const int32_t* tok_seq, const int32_t* tok_pos,
+                                   int32_t n_tok, float* mean, void* stream);
 
 #ifdef __cplusplus
 }

@@ -143,13 +143,14 @@ int32_t fold_q8_decode_row_groups(const fold_kv_view* kv, const fold_q8_query* q
  *   q        query codes, eta and tau (fold_q8_split_query)
  *   z        [batch][num_heads] fp32 references
  *   depth_T  +INFINITY (dense) or a finite T >= 0
+ *   part_Lcut NULL, or the cut masses for the value model (fold_decode_split)
  *   dbg      NULL, or the optional exports above
  */
 fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* keys,
                                  const fold_q8_query* q, const float* z, float depth_T,
                                  int32_t num_splits, int32_t slot_offset, int32_t num_slots,
-                                 float* part_A, float* part_L, const fold_q8_debug* dbg,
-                                 void* stream);
+                                 float* part_A, float* part_L, float* part_Lcut,
+                                 const fold_q8_debug* dbg, void* stream);
 
 #ifdef __cplusplus
 }

@@ -31,6 +31,8 @@ from .fold import (  # noqa: F401
     fold_q8_split_query,
     fold_q8_write_keys,
     fold_ref_estimate,
+    fold_value_mean,
+    fold_value_mean_append,
     kv_view,
     load_library,
     q8_empty_keys,

@@ -4,7 +4,10 @@
 // One workgroup of head_dim threads per query row.  Thread d adds the slots'
 // A[d] in increasing slot order; every thread forms the same L sum in the same
 // order.  o = A / L with no maximum and no rescale.  Optional outputs: the
-// base-2 log-sum-exp Z + log2 L and the certificate bits.
+// base-2 log-sum-exp Z + log2 L and the certificate bits.  With the cut-key
+// value model (Section 4, depth paragraph) the slots' cut masses, summed in
+// slot order, multiply the request's mean value row and join A: a virtual row
+// standing in for every cut key.
 #include "fold_device.h"
 #include "fold_internal.h"
 
@@ -38,6 +41,13 @@ __global__ __launch_bounds__(128) void combine_kernel(const CombineArgs a) {
     const size_t sr = static_cast<size_t>(s) * a.num_rows + row;
     acc += a.part_A[sr * D + d];
     l += a.part_L[sr];
+  }
+  if (a.part_Lcut) {
+    float c = 0.0f;
+    for (int t = 0; t < a.num_slots; ++t) c += a.part_Lcut[static_cast<size_t>(t) * a.num_rows + row];
+    const int req = row / a.heads;
+    const int kvh = (row - req * a.heads) / (a.heads / a.hkv);
+    acc = __builtin_fmaf(c, a.mean[(static_cast<size_t>(req) * a.hkv + kvh) * D + d], acc);
   }
   const float o = acc / l;
   const size_t oi = static_cast<size_t>(row) * D + d;

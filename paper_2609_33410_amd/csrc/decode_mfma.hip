@@ -56,6 +56,7 @@ struct MfmaScan {
   size_t xrow[RB];
   f32x4 acc[RB][NB];
   float lsum[RB];
+  float lcut[RB];  // weights of cut keys (finite depth)
 
   __device__ MfmaScan(const DecodeArgs& a_) : a(a_), g(a_.geo) {}
 
@@ -96,6 +97,7 @@ struct MfmaScan {
         const bool live = ok && (DENSE || x >= a.neg_T);
         const float w = ok ? exp2_fast(x) : 0.0f;
         lsum[b] += w;
+        if (!DENSE) lcut[b] += live ? 0.0f : w;
         const float pw = live ? w : 0.0f;
         hi[i] = __float_as_uint(pw) & 0xffff0000u;
         lo[i] = f32_to_bf16_rne(pw - __uint_as_float(hi[i]));
@@ -180,6 +182,7 @@ __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeA
       sc.qb[b][c] = ri.ok ? *reinterpret_cast<const u32x4*>(a.q + row * D + 32 * c + 8 * sc.grp)
                           : u32x4{0, 0, 0, 0};
     sc.lsum[b] = 0.0f;
+    sc.lcut[b] = 0.0f;
 #pragma unroll
     for (int blk = 0; blk < S::NB; ++blk) sc.acc[b][blk] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   }
@@ -252,6 +255,10 @@ __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeA
   for (int b = 0; b < RB; ++b) {
     sc.lsum[b] += __shfl_xor(sc.lsum[b], 16, 64);
     sc.lsum[b] += __shfl_xor(sc.lsum[b], 32, 64);
+    if (!DENSE) {
+      sc.lcut[b] += __shfl_xor(sc.lcut[b], 16, 64);
+      sc.lcut[b] += __shfl_xor(sc.lcut[b], 32, 64);
+    }
   }
 
   // Add the four waves in order through LDS (the value tiles are dead now),
@@ -270,8 +277,11 @@ __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeA
             float* r = red + ((b * S::NB + blk) * 4 + i) * 64 + sc.lane;
             *r = (w == 0 ? 0.0f : *r) + sc.acc[b][blk][i];
           }
-        float* rl = redl + b * 64 + sc.lane;
-        *rl = (w == 0 ? 0.0f : *rl) + sc.lsum[b];
+        // lanes 0-15 add the row's L, lanes 16-31 its cut mass
+        if (sc.lane < 32) {
+          float* d = redl + b * 64 + sc.lane;
+          *d = (w == 0 ? 0.0f : *d) + (sc.lane < 16 ? sc.lsum[b] : sc.lcut[b]);
+        }
       }
     }
     __syncthreads();
@@ -293,6 +303,7 @@ __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeA
     for (int blk = 0; blk < S::NB; ++blk)
       a.part_A[row * D + 16 * blk + 4 * (wl >> 4) + wi] = red[((b * S::NB + blk) * 4 + wi) * 64 + wl];
     if (wi == 0 && wl < 16) a.part_L[row] = redl[b * 64 + wl];
+    if (a.part_Lcut && wi == 1 && wl < 16) a.part_Lcut[row] = redl[b * 64 + 16 + wl];
   }
 }
 

@@ -128,6 +128,7 @@ struct Q8Scan {
   size_t xrow[RB];
   f32x4 acc[RB][NB];
   float lsum[RB];
+  float lcut[RB];  // weights of cut keys (finite depth)
 
   __device__ Q8Scan(const Q8DecodeArgs& a_) : a(a_), g(a_.d.geo) {}
 
@@ -267,6 +268,7 @@ struct Q8Scan {
         const bool live = ok && (DENSE || x >= a.d.neg_T);
         const float w = ok ? exp2_fast(x) : 0.0f;
         lsum[b] += w;
+        if (!DENSE) lcut[b] += live ? 0.0f : w;
         const float pw = live ? w : 0.0f;
         hi[i] = __float_as_uint(pw) & 0xffff0000u;
         res[i] = pw - __uint_as_float(hi[i]);
@@ -340,6 +342,7 @@ __global__ __launch_bounds__(kScanThreads) void decode_q8_kernel(const Q8DecodeA
                           : u32x4{0, 0, 0, 0};
     }
     sc.lsum[b] = 0.0f;
+    sc.lcut[b] = 0.0f;
 #pragma unroll
     for (int blk = 0; blk < S::NB; ++blk) sc.acc[b][blk] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   }
@@ -411,6 +414,10 @@ __global__ __launch_bounds__(kScanThreads) void decode_q8_kernel(const Q8DecodeA
   for (int b = 0; b < RB; ++b) {
     sc.lsum[b] += __shfl_xor(sc.lsum[b], 16, 64);
     sc.lsum[b] += __shfl_xor(sc.lsum[b], 32, 64);
+    if (!DENSE) {
+      sc.lcut[b] += __shfl_xor(sc.lcut[b], 16, 64);
+      sc.lcut[b] += __shfl_xor(sc.lcut[b], 32, 64);
+    }
   }
 
   // Add the four waves in order through LDS (the value tiles are dead now).
@@ -429,9 +436,10 @@ __global__ __launch_bounds__(kScanThreads) void decode_q8_kernel(const Q8DecodeA
             *d = (w == 0 ? 0.0f : *d) + sc.acc[b][blk][i];
           }
         }
-        if (sc.lane < 16) {
+        // lanes 0-15 add the row's L, lanes 16-31 its cut mass
+        if (sc.lane < 32) {
           float* d = redl + b * 64 + sc.lane;
-          *d = (w == 0 ? 0.0f : *d) + sc.lsum[b];
+          *d = (w == 0 ? 0.0f : *d) + (sc.lane < 16 ? sc.lsum[b] : sc.lcut[b]);
         }
       }
     }
@@ -448,6 +456,7 @@ __global__ __launch_bounds__(kScanThreads) void decode_q8_kernel(const Q8DecodeA
     for (int blk = 0; blk < S::NB; ++blk)
       a.d.part_A[row * D + 16 * blk + 4 * (wl >> 4) + wi] = red[((b * S::NB + blk) * 4 + wi) * 64 + wl];
     if (wi == 0 && wl < 16) a.d.part_L[row] = redl[b * 64 + wl];
+    if (a.d.part_Lcut && wi == 1 && wl < 16) a.d.part_Lcut[row] = redl[b * 64 + 16 + wl];
   }
 }
 

@@ -48,6 +48,7 @@ struct Scan {
   size_t xrow[GR];  // query row index req * heads + head (debug export)
   float acc[GR][8];
   float lsum[GR];
+  float lcut[GR];  // weights of cut keys (finite depth)
 
   __device__ Scan(const DecodeArgs& a_) : a(a_), g(a_.geo) {}
 
@@ -78,6 +79,7 @@ struct Scan {
         const bool live = ok && (DENSE || x >= a.neg_T);
         const float w = ok ? exp2_fast(x) : 0.0f;
         lsum[r] += w;
+        if (!DENSE) lcut[r] += live ? 0.0f : w;
         p[i][r] = live ? w : 0.0f;
         anyl[i] = anyl[i] || live;
         if (DBG && a.x_out && ok && part == 0) a.x_out[xrow[r] * g.max_seq_len + j] = x;
@@ -152,6 +154,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs
     sc.zr[r] = ri.ok ? a.z[row] : 0.0f;
     sc.xrow[r] = row;
     sc.lsum[r] = 0.0f;
+    sc.lcut[r] = 0.0f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) sc.acc[r][e] = 0.0f;
   }
@@ -226,6 +229,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs
 #pragma unroll
     for (int r = 0; r < GR; ++r) {
       sc.lsum[r] += __shfl_xor(sc.lsum[r], off, 64);
+      if (!DENSE) sc.lcut[r] += __shfl_xor(sc.lcut[r], off, 64);
 #pragma unroll
       for (int e = 0; e < 8; ++e) sc.acc[r][e] += __shfl_xor(sc.acc[r][e], off, 64);
     }
@@ -233,6 +237,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs
 
   __shared__ float red_a[kWaves][GR][D];
   __shared__ float red_l[kWaves][GR];
+  __shared__ float red_c[kWaves][GR];
   if (sc.kslot == 0) {
 #pragma unroll
     for (int r = 0; r < GR; ++r)
@@ -241,7 +246,10 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs
   }
   if (sc.lane == 0) {
 #pragma unroll
-    for (int r = 0; r < GR; ++r) red_l[wave][r] = sc.lsum[r];
+    for (int r = 0; r < GR; ++r) {
+      red_l[wave][r] = sc.lsum[r];
+      red_c[wave][r] = sc.lcut[r];
+    }
   }
   __syncthreads();
 
@@ -261,6 +269,12 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs
 #pragma unroll
       for (int w = 1; w < kWaves; ++w) l += red_l[w][r];
       a.part_L[row] = l;
+      if (a.part_Lcut) {
+        float c = red_c[0][r];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) c += red_c[w][r];
+        a.part_Lcut[row] = c;
+      }
     }
   }
 }

@@ -293,6 +293,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   float lsum = 0.0f;
+  float lcut = 0.0f;  // weights of cut keys (finite depth)
 
   // S^T of this wave's two 16-key subtiles of the tile in K stage kst.  K
   // operand: lane l reads chunk 4 cc + l/16 of key 32 kh + 16 st + l%16.
@@ -336,6 +337,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
         const bool live = ok && (DENSE || x >= a.neg_T);
         const float w = FULL ? exp2_fast(x) : (ok ? exp2_fast(x) : 0.0f);
         lsum += w;
+        if (!DENSE) lcut += live ? 0.0f : w;
         const float pw = (FULL && DENSE) ? w : (live ? w : 0.0f);
         hb[st][i] = __float_as_uint(pw) & 0xffff0000u;
         lf[st][i] = pw - __uint_as_float(hb[st][i]);
@@ -540,18 +542,22 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
   // L partials: the four lane groups of a row hold different keys.
   lsum += __shfl_xor(lsum, 16, 64);
   lsum += __shfl_xor(lsum, 32, 64);
+  if (!DENSE) {
+    lcut += __shfl_xor(lcut, 16, 64);
+    lcut += __shfl_xor(lcut, 32, 64);
+  }
 
   // Key half 1 hands its partials to key half 0 through LDS (the tiles are dead).
   wait_vmcnt<0>();
   __syncthreads();
   float* red = reinterpret_cast<float*>(smem);  // [4 row blocks][NB][4][64]
-  float* redl = red + 4 * NB * 4 * 64;          // [4][64]
+  float* redl = red + 4 * NB * 4 * 64;          // [4][64]: L (lanes 0-15), cut mass (16-31)
   if (kh == 1) {
 #pragma unroll
     for (int blk = 0; blk < NB; ++blk)
 #pragma unroll
       for (int i = 0; i < 4; ++i) red[((rb * NB + blk) * 4 + i) * 64 + lane] = acc[blk][i];
-    redl[rb * 64 + lane] = lsum;
+    redl[rb * 64 + lane] = lane < 16 ? lsum : lcut;
   }
   __syncthreads();
   if (kh == 0 && ri.ok) {
@@ -572,6 +578,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
       }
     }
     if (grp == 0) a.part_L[prow] = lsum + redl[rb * 64 + lane];
+    if (grp == 1 && a.part_Lcut) a.part_Lcut[prow] = lcut + redl[rb * 64 + lane];
   }
 }
 

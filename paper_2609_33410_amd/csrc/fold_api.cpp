@@ -199,7 +199,8 @@ fold_status fold_ref_estimate(const fold_kv_view* kv, const fold_q_view* q, floa
 fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
                               const float* z, float depth_T, int32_t num_splits,
                               int32_t slot_offset, int32_t num_slots, float* part_A,
-                              float* part_L, const fold_debug* dbg, void* stream) {
+                              float* part_L, float* part_Lcut, const fold_debug* dbg,
+                              void* stream) {
   fold::DecodeArgs a;
   fold_status st = check_view(kv, q, &a.geo, true);
   if (st != FOLD_OK) return st;
@@ -220,6 +221,7 @@ fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, floa
   a.z = z;
   a.part_A = part_A;
   a.part_L = part_L;
+  a.part_Lcut = part_Lcut;
   a.x_out = dbg ? dbg->x_out : nullptr;
   a.key_gate_out = dbg ? dbg->key_gate_out : nullptr;
   a.page_gate_out = dbg ? dbg->page_gate_out : nullptr;
@@ -238,7 +240,8 @@ fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, floa
 
 fold_status fold_combine(const float* part_A, const float* part_L, int32_t num_slots,
                          int32_t num_rows, int32_t head_dim, const float* z, void* out,
-                         fold_dtype out_dtype, float* lse_out, uint8_t* cert_out, void* stream) {
+                         fold_dtype out_dtype, float* lse_out, uint8_t* cert_out,
+                         const fold_value_model* model, void* stream) {
   if (!part_A || !part_L || !out) return fail(FOLD_E_INVAL, "part_A, part_L and out are required");
   if (num_slots < 1 || num_rows < 0) return fail(FOLD_E_INVAL, "num_slots >= 1, num_rows >= 0");
   if (head_dim != 64 && head_dim != 128)
@@ -247,6 +250,21 @@ fold_status fold_combine(const float* part_A, const float* part_L, int32_t num_s
     return fail(FOLD_E_INVAL, "unknown out_dtype");
   if (lse_out && !z) return fail(FOLD_E_INVAL, "lse_out needs z");
   fold::CombineArgs a;
+  a.part_Lcut = nullptr;
+  a.mean = nullptr;
+  a.heads = a.hkv = 1;
+  if (model) {
+    if (!model->part_Lcut || !model->mean)
+      return fail(FOLD_E_INVAL, "the value model needs part_Lcut and mean");
+    if (model->num_kv_heads < 1 || model->num_heads < 1 ||
+        model->num_heads % model->num_kv_heads != 0 || num_rows % model->num_heads != 0)
+      return fail(FOLD_E_INVAL, "value model: num_heads %d must be a multiple of num_kv_heads %d "
+                  "and divide num_rows %d", model->num_heads, model->num_kv_heads, num_rows);
+    a.part_Lcut = model->part_Lcut;
+    a.mean = model->mean;
+    a.heads = model->num_heads;
+    a.hkv = model->num_kv_heads;
+  }
   a.part_A = part_A;
   a.part_L = part_L;
   a.z = z;
@@ -259,6 +277,42 @@ fold_status fold_combine(const float* part_A, const float* part_L, int32_t num_s
   a.out_bf16 = out_dtype == FOLD_DTYPE_BF16 ? 1 : 0;
   hipError_t e = fold::launch_combine(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(FOLD_E_HIP, "combine launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_value_mean(const fold_kv_view* kv, float* mean_out, void* stream) {
+  if (!kv) return fail(FOLD_E_INVAL, "kv view is required");
+  fold::MeanArgs a{};
+  fold_status st = check_layout(kv, kv->num_seqs, kv->num_kv_heads, &a.geo);
+  if (st != FOLD_OK) return st;
+  if (kv->row_indptr) return fail(FOLD_E_INVAL, "the means need a per-request view (no CSR rows)");
+  if (kv->num_seqs > 0 && (!kv->v || !kv->seq_lens || !mean_out))
+    return fail(FOLD_E_INVAL, "v, seq_lens and mean_out are required");
+  a.mean = mean_out;
+  hipError_t e = fold::launch_value_mean(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "value mean launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_value_mean_append(const fold_kv_view* kv, const void* v_src,
+                                   const int32_t* tok_seq, const int32_t* tok_pos,
+                                   int32_t n_tok, float* mean, void* stream) {
+  if (!kv) return fail(FOLD_E_INVAL, "kv view is required");
+  if (n_tok < 0) return fail(FOLD_E_INVAL, "n_tok must be >= 0");
+  fold::MeanArgs a{};
+  fold_status st = check_layout(kv, kv->num_seqs, kv->num_kv_heads, &a.geo);
+  if (st != FOLD_OK) return st;
+  if (n_tok > 0 && (!v_src || !tok_seq || !tok_pos || !mean))
+    return fail(FOLD_E_INVAL, "v_src, tok_seq, tok_pos and mean are required");
+  if (static_cast<long long>(n_tok) * kv->num_kv_heads > 0x1fffffffLL)
+    return fail(FOLD_E_INVAL, "grid too large");
+  a.mean = mean;
+  a.v_src = static_cast<const uint16_t*>(v_src);
+  a.tok_seq = tok_seq;
+  a.tok_pos = tok_pos;
+  a.n_tok = n_tok;
+  hipError_t e = fold::launch_value_mean_append(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "value mean append launch: %s", hipGetErrorString(e));
   return ok();
 }
 
@@ -366,8 +420,8 @@ fold_status fold_q8_ref_estimate(const fold_kv_view* kv, const fold_q8_keys* key
 fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* keys,
                                  const fold_q8_query* q, const float* z, float depth_T,
                                  int32_t num_splits, int32_t slot_offset, int32_t num_slots,
-                                 float* part_A, float* part_L, const fold_q8_debug* dbg,
-                                 void* stream) {
+                                 float* part_A, float* part_L, float* part_Lcut,
+                                 const fold_q8_debug* dbg, void* stream) {
   fold::Q8DecodeArgs a;
   fold_status st = check_q8_view(kv, keys, q, &a.d.geo, true);
   if (st != FOLD_OK) return st;
@@ -388,6 +442,7 @@ fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* key
   a.d.z = z;
   a.d.part_A = part_A;
   a.d.part_L = part_L;
+  a.d.part_Lcut = part_Lcut;
   a.d.x_out = dbg ? dbg->x_out : nullptr;
   a.d.key_gate_out = dbg ? dbg->key_gate_out : nullptr;
   a.d.page_gate_out = dbg ? dbg->page_gate_out : nullptr;

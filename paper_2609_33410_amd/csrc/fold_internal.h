@@ -36,6 +36,7 @@ struct DecodeArgs {
   const float* z;
   float* part_A;
   float* part_L;
+  float* part_Lcut;   // cut keys' summed weights per slot and row, or NULL
   float* x_out;
   uint8_t* key_gate_out;
   uint8_t* page_gate_out;
@@ -60,6 +61,9 @@ struct EstimateArgs {
 struct CombineArgs {
   const float* part_A;
   const float* part_L;
+  const float* part_Lcut;  // value model: cut masses per slot and row, or NULL
+  const float* mean;       // value model: [batch][hkv][D] request means
+  int heads, hkv;          // value model: rows are [batch][heads]
   const float* z;
   void* out;
   float* lse_out;
@@ -68,6 +72,16 @@ struct CombineArgs {
   int num_rows;
   int head_dim;
   int out_bf16;
+};
+
+// Request mean value rows (the cut-key value model).
+struct MeanArgs {
+  ScanGeometry geo;       // per-request view (geo.k unused)
+  float* mean;            // [num_seqs][hkv][D]
+  const uint16_t* v_src;  // append: [n_tok][hkv][D] bf16
+  const int32_t* tok_seq;
+  const int32_t* tok_pos;
+  int n_tok;
 };
 
 // Two-plane INT8 key cache (Section 4, "Cache format"): the planes use the
@@ -134,6 +148,8 @@ hipError_t launch_decode(const DecodeArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_estimate(const EstimateArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_q8_decode(const Q8DecodeArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_value_mean(const MeanArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_value_mean_append(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_write(const Q8WriteArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_split(const Q8SplitArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_estimate(const Q8EstimateArgs& a, int head_dim, hipStream_t stream);

@@ -32,6 +32,8 @@ EXPORTED = (
     "fold_ref_estimate",
     "fold_decode_split",
     "fold_combine",
+    "fold_value_mean",
+    "fold_value_mean_append",
     "fold_q8_write_keys",
     "fold_q8_split_query",
     "fold_q8_ref_estimate",
@@ -84,6 +86,11 @@ class fold_debug(ctypes.Structure):
                 ("page_gate_out", ctypes.c_void_p)]
 
 
+class fold_value_model(ctypes.Structure):
+    _fields_ = [("part_Lcut", ctypes.c_void_p), ("mean", ctypes.c_void_p),
+                ("num_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32)]
+
+
 class fold_q8_keys(ctypes.Structure):
     _fields_ = [("plane_a", ctypes.c_void_p), ("plane_b", ctypes.c_void_p),
                 ("scale", ctypes.c_void_p)]
@@ -131,11 +138,19 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.fold_decode_split.argtypes = [P(fold_kv_view), P(fold_q_view), ctypes.c_float,
                                       ctypes.c_void_p, ctypes.c_float, ctypes.c_int32,
                                       ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                                      ctypes.c_void_p, P(fold_debug), ctypes.c_void_p]
+                                      ctypes.c_void_p, ctypes.c_void_p, P(fold_debug),
+                                      ctypes.c_void_p]
     lib.fold_combine.restype = ctypes.c_int
     lib.fold_combine.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                  ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
-                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+                                 ctypes.c_void_p, ctypes.c_void_p, P(fold_value_model),
+                                 ctypes.c_void_p]
+    lib.fold_value_mean.restype = ctypes.c_int
+    lib.fold_value_mean.argtypes = [P(fold_kv_view), ctypes.c_void_p, ctypes.c_void_p]
+    lib.fold_value_mean_append.restype = ctypes.c_int
+    lib.fold_value_mean_append.argtypes = [P(fold_kv_view), ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                           ctypes.c_void_p]
     lib.fold_q8_write_keys.restype = ctypes.c_int
     lib.fold_q8_write_keys.argtypes = [P(fold_kv_view), ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
@@ -155,7 +170,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.fold_q8_decode_split.argtypes = [P(fold_kv_view), P(fold_q8_keys), P(fold_q8_query),
                                          ctypes.c_void_p, ctypes.c_float, ctypes.c_int32,
                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                                         ctypes.c_void_p, P(fold_q8_debug), ctypes.c_void_p]
+                                         ctypes.c_void_p, ctypes.c_void_p, P(fold_q8_debug),
+                                         ctypes.c_void_p]
     _lib = lib
     return lib
 
@@ -268,10 +284,13 @@ def fold_decode_split(kv: KV, q: Q, sm_scale: float, z: torch.Tensor, depth_T: f
                       num_splits: int, slot_offset: int, part_A: torch.Tensor,
                       part_L: torch.Tensor, x_out: Optional[torch.Tensor] = None,
                       key_gate_out: Optional[torch.Tensor] = None,
-                      page_gate_out: Optional[torch.Tensor] = None, stream=None) -> None:
+                      page_gate_out: Optional[torch.Tensor] = None,
+                      part_Lcut: Optional[torch.Tensor] = None, stream=None) -> None:
     _need(z, "z", torch.float32)
     _need(part_A, "part_A", torch.float32)
     _need(part_L, "part_L", torch.float32)
+    if part_Lcut is not None:
+        _need(part_Lcut, "part_Lcut", torch.float32)
     dbg = None
     if x_out is not None or key_gate_out is not None or page_gate_out is not None:
         for t, nm, dt in ((x_out, "x_out", torch.float32), (key_gate_out, "key_gate_out", torch.uint8),
@@ -281,15 +300,26 @@ def fold_decode_split(kv: KV, q: Q, sm_scale: float, z: torch.Tensor, depth_T: f
         dbg = fold_debug(_ptr(x_out), _ptr(key_gate_out), _ptr(page_gate_out))
     _check(load_library().fold_decode_split(
         ctypes.byref(kv.view), ctypes.byref(q.view), sm_scale, _ptr(z), depth_T, num_splits,
-        slot_offset, int(part_A.shape[0]), _ptr(part_A), _ptr(part_L),
+        slot_offset, int(part_A.shape[0]), _ptr(part_A), _ptr(part_L), _ptr(part_Lcut),
         None if dbg is None else ctypes.byref(dbg), _stream(stream)))
 
 
 def fold_combine(part_A: torch.Tensor, part_L: torch.Tensor, out: torch.Tensor,
                  z: Optional[torch.Tensor] = None, lse_out: Optional[torch.Tensor] = None,
-                 cert_out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+                 cert_out: Optional[torch.Tensor] = None,
+                 part_Lcut: Optional[torch.Tensor] = None, mean: Optional[torch.Tensor] = None,
+                 num_kv_heads: Optional[int] = None, stream=None) -> torch.Tensor:
+    """Slot-order combine; with ``part_Lcut`` and ``mean`` ([B, Hkv, D]) the
+    cut-key value model adds the cut masses times the request means."""
     _need(part_A, "part_A", torch.float32)
     _need(part_L, "part_L", torch.float32)
+    model = None
+    if part_Lcut is not None or mean is not None:
+        _need(part_Lcut, "part_Lcut", torch.float32)
+        _need(mean, "mean", torch.float32)
+        heads = int(part_A.shape[-2])
+        model = fold_value_model(_ptr(part_Lcut), _ptr(mean), heads,
+                                 int(num_kv_heads if num_kv_heads is not None else mean.shape[1]))
     if out.dtype == torch.float32:
         odt = FOLD_DTYPE_F32
     elif out.dtype == torch.bfloat16:
@@ -303,32 +333,56 @@ def fold_combine(part_A: torch.Tensor, part_L: torch.Tensor, out: torch.Tensor,
     rows = part_A[0].numel() // d if num_slots else 0
     _check(load_library().fold_combine(_ptr(part_A), _ptr(part_L), num_slots, rows, d, _ptr(z),
                                        _ptr(out), odt, _ptr(lse_out), _ptr(cert_out),
+                                       None if model is None else ctypes.byref(model),
                                        _stream(stream)))
     return out
 
 
+def fold_value_mean(kv: KV, mean_out: torch.Tensor, stream=None) -> torch.Tensor:
+    """Request mean value rows ``[num_seqs, Hkv, D]`` of a per-request view."""
+    _need(mean_out, "mean_out", torch.float32)
+    _check(load_library().fold_value_mean(ctypes.byref(kv.view), _ptr(mean_out), _stream(stream)))
+    return mean_out
+
+
+def fold_value_mean_append(kv: KV, v_src: torch.Tensor, tok_seq: torch.Tensor,
+                           tok_pos: torch.Tensor, mean: torch.Tensor, stream=None) -> None:
+    """Running update of the request means for appended tokens (one per sequence)."""
+    _need(v_src, "v_src", torch.bfloat16)
+    _need(tok_seq, "tok_seq", torch.int32)
+    _need(tok_pos, "tok_pos", torch.int32)
+    _need(mean, "mean", torch.float32)
+    _check(load_library().fold_value_mean_append(
+        ctypes.byref(kv.view), _ptr(v_src), _ptr(tok_seq), _ptr(tok_pos), int(tok_seq.shape[0]),
+        _ptr(mean), _stream(stream)))
+
+
 def fold_decode(levels, q: torch.Tensor, z: torch.Tensor, depth_T: float, splits,
                 sm_scale: float, out_dtype=torch.float32, lse: bool = False, cert: bool = False,
-                stream=None):
+                value_mean: Optional[torch.Tensor] = None, stream=None):
     """Every level's split scan into one slot array, then the combine.
 
-    ``levels`` is a list of ``KV`` views; ``splits`` their split counts.  Returns
-    ``(out, part_A, part_L, lse_out, cert_out)``.
+    ``levels`` is a list of ``KV`` views; ``splits`` their split counts;
+    ``value_mean`` ([B, Hkv, D], from ``fold_value_mean``) turns on the cut-key
+    value model.  Returns ``(out, part_A, part_L, lse_out, cert_out)``.
     """
     b, h, d = q.shape
     qv = q_view(q)
     total = sum(splits)
     part_A = torch.empty(total, b, h, d, dtype=torch.float32, device=q.device)
     part_L = torch.empty(total, b, h, dtype=torch.float32, device=q.device)
+    part_C = (torch.empty(total, b, h, dtype=torch.float32, device=q.device)
+              if value_mean is not None else None)
     off = 0
     for kv, s in zip(levels, splits):
-        fold_decode_split(kv, qv, sm_scale, z, depth_T, s, off, part_A, part_L, stream=stream)
+        fold_decode_split(kv, qv, sm_scale, z, depth_T, s, off, part_A, part_L,
+                          part_Lcut=part_C, stream=stream)
         off += s
     out = torch.empty(b, h, d, dtype=out_dtype, device=q.device)
     lse_out = torch.empty(b, h, dtype=torch.float32, device=q.device) if lse else None
     cert_out = torch.empty(b, h, dtype=torch.uint8, device=q.device) if cert else None
     fold_combine(part_A, part_L, out, z=z if lse else None, lse_out=lse_out, cert_out=cert_out,
-                 stream=stream)
+                 part_Lcut=part_C, mean=value_mean, stream=stream)
     return out, part_A, part_L, lse_out, cert_out
 
 
@@ -437,10 +491,13 @@ def fold_q8_decode_split(kv: KV, keys: Q8Keys, q: Q8Query, z: torch.Tensor, dept
                          xc_out: Optional[torch.Tensor] = None,
                          key_gate_out: Optional[torch.Tensor] = None,
                          page_gate_out: Optional[torch.Tensor] = None,
-                         refine_gate_out: Optional[torch.Tensor] = None, stream=None) -> None:
+                         refine_gate_out: Optional[torch.Tensor] = None,
+                         part_Lcut: Optional[torch.Tensor] = None, stream=None) -> None:
     _need(z, "z", torch.float32)
     _need(part_A, "part_A", torch.float32)
     _need(part_L, "part_L", torch.float32)
+    if part_Lcut is not None:
+        _need(part_Lcut, "part_Lcut", torch.float32)
     outs = ((x_out, "x_out", torch.float32), (xc_out, "xc_out", torch.float32),
             (key_gate_out, "key_gate_out", torch.uint8),
             (page_gate_out, "page_gate_out", torch.uint8),
@@ -454,5 +511,5 @@ def fold_q8_decode_split(kv: KV, keys: Q8Keys, q: Q8Query, z: torch.Tensor, dept
     kk, qq = keys.view(), q.view()
     _check(load_library().fold_q8_decode_split(
         ctypes.byref(kv.view), ctypes.byref(kk), ctypes.byref(qq), _ptr(z), depth_T, num_splits,
-        slot_offset, int(part_A.shape[0]), _ptr(part_A), _ptr(part_L),
+        slot_offset, int(part_A.shape[0]), _ptr(part_A), _ptr(part_L), _ptr(part_Lcut),
         None if dbg is None else ctypes.byref(dbg), _stream(stream)))

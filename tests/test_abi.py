@@ -41,7 +41,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.fold_abi_version() == 1
+    assert lib.fold_abi_version() == 2
     for code, word in ((0, b"FOLD_OK"), (1, b"FOLD_E_INVAL"), (2, b"FOLD_E_UNSUPPORTED"),
                        (3, b"FOLD_E_HIP")):
         assert lib.fold_status_string(code).startswith(word)
@@ -72,7 +72,7 @@ def _q(**over):
 
 def _decode(lib, kv, q, T=math.inf, splits=1, slot_offset=0, num_slots=1, z=FAKE):
     return lib.fold_decode_split(ctypes.byref(kv), ctypes.byref(q), 0.125, z, T, splits,
-                                 slot_offset, num_slots, FAKE, FAKE, None, None)
+                                 slot_offset, num_slots, FAKE, FAKE, None, None, None)
 
 
 @pytest.mark.parametrize("case", [
@@ -113,10 +113,28 @@ def test_estimate_rejects_csr_view_and_bad_params(lib):
 
 
 def test_combine_rejects_bad_args(lib):
-    assert lib.fold_combine(FAKE, FAKE, 0, 4, 128, None, FAKE, 0, None, None, None) == F.FOLD_E_INVAL
-    assert lib.fold_combine(FAKE, FAKE, 2, 4, 80, None, FAKE, 0, None, None, None) == F.FOLD_E_INVAL
-    assert lib.fold_combine(FAKE, FAKE, 2, 4, 128, None, FAKE, 7, None, None, None) == F.FOLD_E_INVAL
-    assert lib.fold_combine(FAKE, FAKE, 2, 4, 128, None, FAKE, 0, FAKE, None, None) == F.FOLD_E_INVAL
+    c = lib.fold_combine
+    assert c(FAKE, FAKE, 0, 4, 128, None, FAKE, 0, None, None, None, None) == F.FOLD_E_INVAL
+    assert c(FAKE, FAKE, 2, 4, 80, None, FAKE, 0, None, None, None, None) == F.FOLD_E_INVAL
+    assert c(FAKE, FAKE, 2, 4, 128, None, FAKE, 7, None, None, None, None) == F.FOLD_E_INVAL
+    assert c(FAKE, FAKE, 2, 4, 128, None, FAKE, 0, FAKE, None, None, None) == F.FOLD_E_INVAL
+    from paper_2609_33410_amd.fold import fold_value_model
+    bad = (fold_value_model(None, FAKE, 8, 2), fold_value_model(FAKE, FAKE, 8, 3),
+           fold_value_model(FAKE, FAKE, 6, 2))  # no masses; 8 % 3; 4 rows % 6
+    for m in bad:
+        assert c(FAKE, FAKE, 2, 4, 128, None, FAKE, 0, None, None, ctypes.byref(m),
+                 None) == F.FOLD_E_INVAL
+
+
+def test_value_mean_rejects_bad_args(lib):
+    kv = _kv(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=2)
+    assert lib.fold_value_mean(ctypes.byref(kv), FAKE, None) == F.FOLD_E_INVAL
+    assert lib.fold_value_mean(ctypes.byref(_kv(v=None)), FAKE, None) == F.FOLD_E_INVAL
+    assert lib.fold_value_mean(ctypes.byref(_kv()), None, None) == F.FOLD_E_INVAL
+    ap = lib.fold_value_mean_append
+    assert ap(ctypes.byref(_kv()), FAKE, FAKE, FAKE, -1, FAKE, None) == F.FOLD_E_INVAL
+    assert ap(ctypes.byref(_kv()), None, FAKE, FAKE, 3, FAKE, None) == F.FOLD_E_INVAL
+    assert ap(ctypes.byref(_kv()), None, None, None, 0, None, None) == F.FOLD_OK
 
 
 def test_row_group_queries(lib):
@@ -164,7 +182,7 @@ def _q8(kv_heads=2, heads=8, **over):
 
 def _q8_decode(lib, kv, keys, q, T=math.inf, splits=1, z=FAKE):
     return lib.fold_q8_decode_split(ctypes.byref(kv), ctypes.byref(keys), ctypes.byref(q), z, T,
-                                    splits, 0, splits, FAKE, FAKE, None, None)
+                                    splits, 0, splits, FAKE, FAKE, None, None, None)
 
 
 @pytest.mark.parametrize("over,kvo,want", [
