@@ -138,6 +138,71 @@ def dequant(a: np.ndarray, b: np.ndarray, scale: np.ndarray) -> np.ndarray:
                                                              + b.astype(np.float64) / 256.0)
 
 
+# ---------------------------------------------------------------- V1/V2 ----
+# 8-bit values (Section 4, "Cache format"): two E4M3 planes under a power-of-
+# two scale 2^e for the whole cache.  E4M3 here is the OCP "E4M3FN" format:
+# sign, 4 exponent bits (bias 7), 3 mantissa bits, subnormals m 2^-9, largest
+# finite 448, codes S.1111.111 are NaN and no infinity exists.
+E4M3_MAX = 448.0
+
+
+def e4m3_table() -> np.ndarray:
+    """Value of each of the 256 codes (NaN for the two NaN codes)."""
+    out = np.zeros(256)
+    for c in range(256):
+        sgn = -1.0 if c & 0x80 else 1.0
+        ex, m = (c >> 3) & 15, c & 7
+        if ex == 15 and m == 7:
+            out[c] = np.nan
+        elif ex == 0:
+            out[c] = sgn * m * 2.0 ** -9
+        else:
+            out[c] = sgn * (1 + m / 8) * 2.0 ** (ex - 7)
+    return out
+
+
+_E4M3 = e4m3_table()
+_POS_CODES = np.arange(0x7F)                      # 0 .. 0x7E: the finite non-negative codes
+_POS_VALS = _E4M3[_POS_CODES]
+
+
+def e4m3_encode(x: np.ndarray) -> np.ndarray:
+    """Codes of x rounded to the nearest E4M3 value, ties to the even code
+    (the one whose mantissa LSB is 0); magnitudes above 448 saturate to 448.
+    Nearest-value search over the code table (FP64)."""
+    x = np.asarray(x, dtype=np.float64)
+    a = np.minimum(np.abs(x), E4M3_MAX)
+    i = np.clip(np.searchsorted(_POS_VALS, a), 1, len(_POS_VALS) - 1)
+    lo, hi = _POS_VALS[i - 1], _POS_VALS[i]
+    pick_hi = (a - lo > hi - a) | ((a - lo == hi - a) & (_POS_CODES[i] % 2 == 0))
+    code = np.where(pick_hi, _POS_CODES[i], _POS_CODES[i - 1])
+    code = np.where(a == 0, 0, code)
+    neg = (x < 0) & (code != 0)
+    return (code | (neg.astype(np.int64) << 7)).astype(np.uint8)
+
+
+def e4m3_decode(codes: np.ndarray) -> np.ndarray:
+    return _E4M3[np.asarray(codes, dtype=np.int64)]
+
+
+def split_values(v_bits: np.ndarray, scale_exp: int):
+    """Value planes of BF16 value rows: y = v 2^-e, p = E4M3(y),
+    r = E4M3(16 (y - p)); the value stands for 2^e (p + r/16)."""
+    y = bf16_bits_to_f64(v_bits) * 2.0 ** -scale_exp
+    p = e4m3_encode(y)
+    r = e4m3_encode(16.0 * (y - e4m3_decode(p)))
+    return p, r
+
+
+def dequant_values(p: np.ndarray, r: np.ndarray, scale_exp: int, refined=True) -> np.ndarray:
+    """2^e (p + [refined] r / 16), FP64."""
+    v = e4m3_decode(p)
+    if refined is not False:
+        v = v + np.where(np.asarray(refined)[..., None] if np.ndim(refined) else refined,
+                         e4m3_decode(r) / 16.0, 0.0)
+    return v * 2.0 ** scale_exp
+
+
 # ---------------------------------------------------------------- Q4/Q6 ----
 def coarse_and_refine(qa, qb, eta, a, b, e):
     """``(coarse, refine)`` score terms [rows, keys], FP64, before the reference.
@@ -186,7 +251,9 @@ def decode_level_q8(qa, qb, eta, planes, v_bits, *, num_kv_heads: int, page_size
                     z: np.ndarray, T: float, tau: np.ndarray, num_splits: int,
                     imposed: Optional[Tuple[np.ndarray, np.ndarray]] = None,
                     chunks: Optional[Iterable[Tuple[int, int]]] = None,
-                    want_scores: bool = False, with_cut: bool = False):
+                    want_scores: bool = False, with_cut: bool = False,
+                    values8: Optional[Tuple[np.ndarray, np.ndarray, int]] = None,
+                    tau_v: Optional[np.ndarray] = None):
     """Split partials of one level over a two-plane key cache.
 
     ``qa, qb`` [B, H, D] int8 and ``eta`` [B, H] FP32 are the query codes;
@@ -198,6 +265,11 @@ def decode_level_q8(qa, qb, eta, planes, v_bits, *, num_kv_heads: int, page_size
     Returns ``part_A [S, B, H, D]``, ``part_L [S, B, H]``, with ``with_cut``
     also ``part_Lcut [S, B, H]`` (the cut keys' summed weights) and, with
     ``want_scores``, a dict ``(seq, g) -> (rows, xc, x, live, refine)``.
+
+    ``values8 = (p, r, e)`` replaces the BF16 values by two E4M3 planes: key j
+    contributes 2^e (p_j + [refine_v_j] r_j / 16), where refine_v_j = live_j
+    AND OR over the GQA group of [xc_ij >= -tau_v] (``tau_v`` [B], Algorithm
+    1's third verdict bit; imposed mode applies it in FP32 to the given xc).
     """
     pa_, pb_, pe_ = planes
     b_, h, d = qa.shape
@@ -221,7 +293,11 @@ def decode_level_q8(qa, qb, eta, planes, v_bits, *, num_kv_heads: int, page_size
         bb = _gather_raw(pb_, seq, g, n, block_table, page_size)
         e = bf16_bits_to_f64(_gather_raw(pe_[..., None], seq, g, n, block_table,
                                          page_size)[:, 0])
-        vals = gather(v_bits, seq, g, n, block_table, page_size)
+        if values8 is None:
+            vals = gather(v_bits, seq, g, n, block_table, page_size)
+        else:
+            vp = _gather_raw(values8[0], seq, g, n, block_table, page_size)
+            vr = _gather_raw(values8[1], seq, g, n, block_table, page_size)
         coarse, refine = coarse_and_refine(qa[ri, hi], qb[ri, hi], eta[ri, hi], a, bb, e)
         xc = coarse - np.asarray(z, dtype=np.float64)[ri, hi][:, None]
         tau_rows = np.asarray(tau)[ri]
@@ -237,12 +313,23 @@ def decode_level_q8(qa, qb, eta, planes, v_bits, *, num_kv_heads: int, page_size
             counts = (np.ones(x.shape, dtype=bool) if math.isinf(T)
                       else np.asarray(ix, dtype=np.float32) >= np.float32(-T))
         w = np.exp2(x)
+        if values8 is not None:
+            tv = np.asarray(tau_v)[ri]
+            xsrc = xc if imposed is None else imposed[0][ri, hi, :n]
+            _, ref_v = gate_bits(xsrc, blocks, T, tv, f32=imposed is not None)
+            # per row its group's bit; one value row per key for every row of
+            # a group, so rows of different groups may see different values
+            v_rows = [dequant_values(vp, vr, values8[2], ref_v[k]) for k in range(len(ri))]
         owner = split_of_key(n, num_splits)
         for sp in range(num_splits):
             m = owner == sp
             if not m.any():
                 continue
-            part_a[sp, ri, hi] = (w[:, m] * counts[:, m]) @ vals[m]
+            if values8 is None:
+                part_a[sp, ri, hi] = (w[:, m] * counts[:, m]) @ vals[m]
+            else:
+                part_a[sp, ri, hi] = np.stack([(w[k, m] * counts[k, m]) @ v_rows[k][m]
+                                               for k in range(len(ri))])
             part_l[sp, ri, hi] = w[:, m].sum(axis=1)
             part_c[sp, ri, hi] = (w[:, m] * ~counts[:, m]).sum(axis=1)
         if want_scores:
@@ -297,6 +384,7 @@ def estimate_level_q8(qa, qb, eta, planes, *, num_kv_heads, page_size, seq_lens,
     return z
 
 
-__all__ = ["LOG2E_F64", "TILE", "bf16_ceil", "coarse_and_refine", "decode_level_q8", "dequant",
+__all__ = ["E4M3_MAX", "LOG2E_F64", "TILE", "bf16_ceil", "coarse_and_refine", "decode_level_q8",
+           "dequant", "dequant_values", "e4m3_decode", "e4m3_encode", "e4m3_table", "split_values",
            "estimate_level_q8", "gate_bits", "hadamard", "q8_read_gates", "refine_tau",
            "rotate", "split_keys", "split_queries"]

@@ -356,3 +356,91 @@ def test_estimate_on_coarse_scores_is_exact_lse_when_short():
                 f * (qa[r, h] + qb[r, h] / 256.0)))
             want = float(np.logaddexp2.reduce(s))
             assert abs(z[r, h] - want) < 1e-5
+
+
+# ------------------------------------------------------ 8-bit values -------
+def test_e4m3_table_matches_torch():
+    """Library routine: torch's float8_e4m3fn decoding of all 256 codes."""
+    ref = torch.arange(256, dtype=torch.uint8).view(torch.float8_e4m3fn).double().numpy()
+    ours = q8.e4m3_table()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(ours), nan)
+    assert np.array_equal(ours[~nan], ref[~nan])
+
+
+def test_e4m3_encode_matches_torch_rounding():
+    """Library routine: torch's round-to-nearest-even cast to float8_e4m3fn on
+    random magnitudes, every code's value and every midpoint (ties); beyond
+    448 the writer saturates (reading) where torch gives NaN."""
+    g = torch.Generator().manual_seed(0)
+    x = torch.cat([torch.randn(20000, generator=g) * s for s in (1e-3, 0.1, 3.0, 60.0)])
+    vals = torch.from_numpy(q8.e4m3_table()[:0x7F]).float()
+    mids = (vals[1:] + vals[:-1]) / 2
+    x = torch.cat([x, vals, -vals, mids, -mids]).double()
+    x = x[x.abs() <= 448]
+    want = x.float().to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    got = q8.e4m3_encode(x.numpy())
+    neg_zero = (want == 0x80) & (got == 0)   # -0 encodes as +0 here
+    assert np.array_equal(got[~neg_zero], want[~neg_zero])
+    assert q8.e4m3_encode(np.array([449.0, 1e9, -500.0])).tolist() == [0x7E, 0x7E, 0xFE]
+
+
+def test_two_value_planes_are_lossless():
+    """Brute force over every finite BF16 value: 2^e (p + r/16) gives it back
+    exactly when |v 2^-e| <= 448 (and at least 2^-6, the normal E4M3 range)."""
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    v = bf16_bits_to_f64(bits)
+    for e in (-3, 0, 4):
+        y = v * 2.0 ** -e
+        ok = np.isfinite(v) & (np.abs(y) <= 448) & (np.abs(y) >= 2.0 ** -6)
+        p, r = q8.split_values(bits[ok], e)
+        assert np.array_equal(q8.dequant_values(p, r, e), v[ok])
+        # plane 1 alone is within half an E4M3 step (relative 2^-4)
+        err = np.abs(q8.dequant_values(p, r, e, refined=False) - v[ok])
+        assert np.all(err <= np.abs(v[ok]) * 2.0 ** -4 + 1e-300)
+
+
+@pytest.mark.parametrize("T", [INF, 8.0])
+def test_value_planes_fully_refined_equal_bf16_values(T):
+    """With every live key's second value plane read (kappa_v = +inf), the
+    8-bit-value decode equals the BF16-value decode (the planes are exact
+    here); with none read, it differs by at most plane 1's rounding."""
+    wl = _wl(seed=9)
+    planes, qa, qb, eta, tau = _q8_inputs(wl, 0.0)
+    z = _adapt.estimate(_adapt.oracle_inputs(wl))
+    vb = host_bits(wl.v)
+    vmax = float(np.abs(bf16_bits_to_f64(vb)).max())
+    e = int(np.ceil(np.log2(vmax / 448.0)))
+    p, r = q8.split_values(vb, e)
+    lv = _adapt.level_args(wl.levels[0])
+    args = dict(num_kv_heads=wl.num_kv_heads, page_size=wl.page_size, z=z, T=T, tau=tau,
+                num_splits=2, **lv)
+    a0, l0 = q8.decode_level_q8(qa, qb, eta, planes, vb, **args)
+    tinf = np.full_like(tau, np.inf)
+    a1, l1 = q8.decode_level_q8(qa, qb, eta, planes, vb, values8=(p, r, e), tau_v=tinf, **args)
+    small = (np.abs(bf16_bits_to_f64(vb)) < 2.0 ** (e - 6)).any()
+    if not small:
+        assert np.array_equal(a0, a1)
+    np.testing.assert_allclose(a1, a0, rtol=1e-12, atol=1e-12 * np.abs(a0).max())
+    assert np.array_equal(l0, l1)
+    a2, _ = q8.decode_level_q8(qa, qb, eta, planes, vb, values8=(p, r, e),
+                               tau_v=np.full_like(tau, -np.inf), **args)
+    o0, _ = combine(a0, l0)
+    o2, _ = combine(a2, l0)
+    assert np.abs(o2 - o0).max() <= 2.0 ** -4 * vmax * 1.01
+    assert np.abs(o2 - o0).max() > 0
+
+
+def test_refine_v_gate_invariants():
+    """refine_v implies live; it follows the coarse scores per GQA group."""
+    wl = _wl(seed=10)
+    planes, qa, qb, eta, tau = _q8_inputs(wl, 0.0)
+    z = _adapt.estimate(_adapt.oracle_inputs(wl))
+    _, _, info = _run(wl, planes, qa, qb, eta, tau, z, 8.0, want_scores=True)
+    group = wl.num_heads // wl.num_kv_heads
+    for (seq, g), (rows, xc, x, live, ref) in info.items():
+        tv = np.full(len(rows), 3.0)
+        lv_, rv = q8.gate_bits(xc, np.repeat(np.arange(len(rows) // group), group), 8.0, tv)
+        assert np.array_equal(lv_, live)
+        assert not np.any(rv & ~live)
+        assert np.array_equal(rv[0], live[0] & (xc >= -3.0).any(axis=0))
