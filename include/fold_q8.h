@@ -64,20 +64,39 @@ typedef struct fold_q8_query {
   const float* tau;      /* [batch]; read by fold_q8_decode_split only */
   int32_t batch;
   int32_t num_heads;
+  const float* tau_v;    /* [batch] refine-V thresholds; read with 8-bit values only */
 } fold_q8_query;
+
+/* 8-bit values (Section 4, "Cache format"): two E4M3 planes under one
+ * power-of-two scale 2^scale_exp for the cache.  E4M3 is the OCP E4M3FN
+ * format (bias 7, largest finite 448).  Value row v is stored as
+ * p = E4M3(v 2^-e) and r = E4M3(16 (v 2^-e - p)), both rounded to nearest
+ * even and saturating at 448, and stands for 2^e (p + r/16); for BF16 values
+ * with 2^-6 <= |v 2^-e| <= 448 that is v exactly.  Layout: the element layout
+ * of the BF16 value cache, one byte per element, 16-byte aligned.  The scan
+ * reads p for live keys and r only for keys whose refine-V verdict is set:
+ * refine_v_j = live_j AND OR over the GQA group of [xc_ij >= -tau_v_r]
+ * (Algorithm 1's third verdict bit), tau_v_r = kappa_v + ceil(log2 n_r). */
+typedef struct fold_v8_values {
+  const uint8_t* plane_p;
+  const uint8_t* plane_r;
+  int32_t scale_exp;
+} fold_v8_values;
 
 /* Optional exports of exactly the values the scan compared (not timed); the
  * shapes and the read-group numbering are those of fold_debug.
  * x_out, xc_out [batch][num_heads][max_seq_len] fp32: refined and coarse x.
  * key_gate_out / page_gate_out: value rows / 16-key pages read.
  * refine_gate_out [num_seqs][num_kv_heads][row_groups][max_seq_len] u8:
- *   plane-B rows read. */
+ *   plane-B rows read.  refine_v_gate_out, same shape: second value plane
+ *   rows read (8-bit values). */
 typedef struct fold_q8_debug {
   float* x_out;
   float* xc_out;
   uint8_t* key_gate_out;
   uint8_t* page_gate_out;
   uint8_t* refine_gate_out;
+  uint8_t* refine_v_gate_out;
 } fold_q8_debug;
 
 /*
@@ -111,10 +130,26 @@ fold_status fold_q8_write_keys(const fold_kv_view* kv, const void* k_src, const 
  *   kappa      any value but NaN; +INFINITY refines every live key,
  *              -INFINITY none.  0 refines the keys whose coarse weight
  *              2^xc is at least 2^-ceil(log2 n_r), about their mean share.
+ *   kappa_v, tau_v_out: the same for the second value plane of 8-bit values
+ *              (tau_v_out may be NULL; written only with req_lens).
  */
 fold_status fold_q8_split_query(const fold_q_view* q, int32_t head_dim, float sm_scale,
-                                const int32_t* req_lens, float kappa, int8_t* planes_out,
-                                float* eta_out, float* tau_out, void* stream);
+                                const int32_t* req_lens, float kappa, float kappa_v,
+                                int8_t* planes_out, float* eta_out, float* tau_out,
+                                float* tau_v_out, void* stream);
+
+/*
+ * fold_v8_write_values - writer of 8-bit values (Section 4, "Cache format"):
+ * the two E4M3 planes of n_tok BF16 value rows, stored like
+ * fold_q8_write_keys stores key codes (same token list, view and skipping).
+ *   v_src      [n_tok][num_kv_heads][head_dim] bf16
+ *   scale_exp  e of the cache's scale 2^e (choose e >= log2(max|v| / 448))
+ *   plane_p, plane_r: the value planes written
+ */
+fold_status fold_v8_write_values(const fold_kv_view* kv, const void* v_src,
+                                 const int32_t* tok_seq, const int32_t* tok_pos, int32_t n_tok,
+                                 int32_t scale_exp, uint8_t* plane_p, uint8_t* plane_r,
+                                 void* stream);
 
 /*
  * fold_q8_ref_estimate - fold_ref_estimate on the coarse logits
@@ -143,14 +178,17 @@ int32_t fold_q8_decode_row_groups(const fold_kv_view* kv, const fold_q8_query* q
  *   q        query codes, eta and tau (fold_q8_split_query)
  *   z        [batch][num_heads] fp32 references
  *   depth_T  +INFINITY (dense) or a finite T >= 0
+ *   values   NULL (BF16 values from kv->v), or 8-bit values (then q->tau_v
+ *            is required and kv->v is not read)
  *   part_Lcut NULL, or the cut masses for the value model (fold_decode_split)
  *   dbg      NULL, or the optional exports above
  */
 fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* keys,
-                                 const fold_q8_query* q, const float* z, float depth_T,
-                                 int32_t num_splits, int32_t slot_offset, int32_t num_slots,
-                                 float* part_A, float* part_L, float* part_Lcut,
-                                 const fold_q8_debug* dbg, void* stream);
+                                 const fold_q8_query* q, const fold_v8_values* values,
+                                 const float* z, float depth_T, int32_t num_splits,
+                                 int32_t slot_offset, int32_t num_slots, float* part_A,
+                                 float* part_L, float* part_Lcut, const fold_q8_debug* dbg,
+                                 void* stream);
 
 #ifdef __cplusplus
 }

@@ -19,6 +19,7 @@ from .fold import (  # noqa: F401
     FoldLibraryMissing,
     Q8Keys,
     Q8Query,
+    V8Values,
     fold_combine,
     fold_decode,
     fold_decode_row_groups,
@@ -32,10 +33,12 @@ from .fold import (  # noqa: F401
     fold_q8_write_keys,
     fold_ref_estimate,
     fold_value_mean,
+    fold_v8_write_values,
     fold_value_mean_append,
     kv_view,
     load_library,
     q8_empty_keys,
     q8_empty_query,
+    v8_empty_values,
     q_view,
 )

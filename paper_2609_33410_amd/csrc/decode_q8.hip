@@ -21,6 +21,13 @@
 //            iff x >= -T; L adds every w.  The value product is the BF16
 //            scan's: channels on M, rows on N, the chunk's keys on K, the
 //            weight as bf16 hi + bf16 residual.
+//   8-bit    (values as two E4M3 planes under a scale 2^e for the cache)
+//            the first plane is read for live keys and the second only for
+//            keys whose refine-V verdict (coarse score >= -tau_v, ORed per GQA
+//            group) is set; both widen exactly to BF16 (v_cvt_scalef32_pk_bf16_
+//            fp8, scale 1 and 1/16) and enter two value products, the second
+//            with weights kept only where the row's own group set the verdict.
+//            A is multiplied by 2^e when written.
 //
 // Pipeline per wave: while chunk t is refined and multiplied, chunk t+1 has
 // been scored and its plane-B and value rows requested, and plane A of the
@@ -81,37 +88,44 @@ __device__ __forceinline__ Q8Loc q8_loc(const ScanGeometry& g, const ScanPlace& 
   return l;
 }
 
-template <int D, bool DENSE>
+// 16-byte value loads per lane and chunk: BF16 rows, or one E4M3 plane.
+template <int D, bool V8>
+constexpr int kValueLoads = V8 ? D / 64 : D / 32;
+
+template <int D, bool DENSE, bool V8>
 struct Q8AStage {
   Q8Loc loc;
   u32x4 ka[D / 64];
   uint32_t sc;                    // BF16 scale of key 4(l/16) + l%4 (2-byte loads: any row alignment)
-  u32x4 vv[DENSE ? D / 32 : 1];
+  u32x4 vv[DENSE ? kValueLoads<D, V8> : 1];
 };
 
 // A chunk from its coarse pass to its product.
-template <int D, int RB, bool DENSE>
+template <int D, int RB, bool DENSE, bool V8>
 struct Q8BStage {
   Q8Loc loc;
   uint32_t sc;
   u32x4 kb[D / 64];
-  u32x4 vv[DENSE ? 1 : D / 32];
+  u32x4 vv[DENSE ? 1 : kValueLoads<D, V8>];
+  u32x4 vr[V8 ? D / 64 : 1];  // second value plane (8-bit values)
   float xc[RB][4];
-  uint32_t ref;    // bit 4b+i: key 4(l/16)+i refined for the group of row block b
-  uint32_t vmask;  // value rows to read (wave-uniform)
-  uint32_t bmask;  // plane-B rows to read (wave-uniform)
+  uint32_t ref;     // bit 4b+i: key 4(l/16)+i refined for the group of row block b
+  uint32_t refv;    // the same for the second value plane (8-bit values)
+  uint32_t vmask;   // value rows to read (wave-uniform)
+  uint32_t bmask;   // plane-B rows to read (wave-uniform)
+  uint32_t rvmask;  // second-value-plane rows to read (wave-uniform)
 };
 
-template <int D, int RB, bool DENSE, bool DBG>
+template <int D, int RB, bool DENSE, bool DBG, bool V8>
 struct Q8Scan {
   static constexpr int NKI = D / 64;          // 16-byte plane loads per lane per chunk
-  static constexpr int NK = D / 32;           // 16-byte value loads per lane per chunk
+  static constexpr int NK = kValueLoads<D, V8>;  // 16-byte value loads per lane per chunk
   static constexpr int NB = D / 16;           // 16-channel blocks of the value product
   static constexpr int VSTRIDE = 2 * D + 16;  // bytes per key row of the LDS value tile
   static constexpr int R = 16 * RB;
   static constexpr int NA = 4;                 // plane-A ring depth (chunks)
-  using AS = Q8AStage<D, DENSE>;
-  using BS = Q8BStage<D, RB, DENSE>;
+  using AS = Q8AStage<D, DENSE, V8>;
+  using BS = Q8BStage<D, RB, DENSE, V8>;
 
   const Q8DecodeArgs& a;
   const ScanGeometry& g;
@@ -123,7 +137,7 @@ struct Q8Scan {
   unsigned char* vt;
 
   u32x4 qa[RB][NKI], qb[RB][NKI];
-  float eta[RB], zr[RB], ntau[RB];
+  float eta[RB], zr[RB], ntau[RB], ntau_v[RB];
   bool rok[RB];
   size_t xrow[RB];
   f32x4 acc[RB][NB];
@@ -142,14 +156,28 @@ struct Q8Scan {
     if constexpr (DENSE) load_v(s.loc, 0xFFFFu, s.vv);
   }
 
+  // BF16 value rows, or the first E4M3 plane (8-bit values), of the chunk's
+  // keys in mask.
   __device__ __forceinline__ void load_v(const Q8Loc& loc, uint32_t mask, u32x4 (&vv)[NK]) const {
-    const rsrc_t rv = make_rsrc(g.v + loc.row * D, loc.nk * D * 2);
-    // lane l, load i: the 16 bytes at 1024 i + 16 l of the chunk (key (1024 i + 16 l) / 2D)
+    constexpr uint32_t kRowBytes = V8 ? D : 2 * D;
+    const rsrc_t rv = V8 ? make_rsrc(a.vp + loc.row * D, loc.nk * D)
+                         : make_rsrc(g.v + loc.row * D, loc.nk * D * 2);
+    // lane l, load i: the 16 bytes at 1024 i + 16 l of the chunk (key (1024 i + 16 l) / row bytes)
 #pragma unroll
     for (int i = 0; i < NK; ++i) {
       const uint32_t off = 1024u * i + 16u * lane;
-      const uint32_t key = off / (2 * D);
+      const uint32_t key = off / kRowBytes;
       vv[i] = buf_load(rv, DENSE || ((mask >> key) & 1u) ? off : kOutOfRange);
+    }
+  }
+
+  // Second E4M3 value plane of the chunk's keys in mask.
+  __device__ __forceinline__ void load_vr(const Q8Loc& loc, uint32_t mask, u32x4 (&vr)[D / 64]) const {
+    const rsrc_t rr = make_rsrc(a.vr + loc.row * D, loc.nk * D);
+#pragma unroll
+    for (int i = 0; i < D / 64; ++i) {
+      const uint32_t off = 1024u * i + 16u * lane;
+      vr[i] = buf_load(rr, ((mask >> (off / D)) & 1u) ? off : kOutOfRange);
     }
   }
 
@@ -165,6 +193,9 @@ struct Q8Scan {
     }
     if constexpr (!DENSE) {
       if (s.vmask) load_v(s.loc, s.vmask, s.vv);
+    }
+    if constexpr (V8) {
+      if (s.rvmask) load_vr(s.loc, s.rvmask, s.vr);
     }
   }
 
@@ -186,7 +217,7 @@ struct Q8Scan {
     s.sc = in.sc;
     float e[4];
     scales(in.sc, e);
-    uint32_t lv = 0, rf = 0;
+    uint32_t lv = 0, rf = 0, rv = 0;
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
       i32x4 caa = {0, 0, 0, 0}, cab = {0, 0, 0, 0};
@@ -203,87 +234,80 @@ struct Q8Scan {
         s.xc[b][i] = xc;
         if (ok && (DENSE || xc >= a.d.neg_T)) lv |= 1u << (4 * b + i);
         if (ok && xc >= ntau[b]) rf |= 1u << (4 * b + i);
+        if (V8 && ok && xc >= ntau_v[b]) rv |= 1u << (4 * b + i);
         if (DBG && a.xc_out && ok) a.xc_out[xrow[b] * g.max_seq_len + key0 + 4 * grp + i] = xc;
       }
     }
     // OR over the lanes holding the rows of one GQA group: aligned groups of
     // 2, 4, 8 or 16 lanes (quad swaps, then half-row and row mirrors).
-    uint32_t both = lv | (rf << 16);
+    uint32_t both = lv | (rv << 8) | (rf << 16);
     if (gspan >= 1) both |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(both), 0xB1, 0xF, 0xF, false));
     if (gspan >= 3) both |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(both), 0x4E, 0xF, 0xF, false));
     if (gspan >= 7) both |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(both), 0x141, 0xF, 0xF, false));
     if (gspan >= 15) both |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(both), 0x140, 0xF, 0xF, false));
     if (cross_b) both |= ((both >> 4) & 0x000F000Fu) | ((both & 0x000F000Fu) << 4);
-    both &= (both << 16) | 0xFFFFu;  // refine only live keys
+    both &= ((both & 0xFFu) << 16) | ((both & 0xFFu) << 8) | 0xFFu;  // refine only live keys
     s.ref = both >> 16;
+    s.refv = (both >> 8) & 0xFFu;
     // Unions over the read group: OR over each 16-lane row (row q holds keys
     // 4q..4q+3), then one row value per readlane; the row blocks fold together.
     const uint32_t u = group_or16(RB == 2 ? both | (both >> 4) : both);
-    uint32_t vmask = 0, bmask = 0;
+    uint32_t vmask = 0, bmask = 0, rvmask = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const uint32_t r = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(u), 16 * q));
       vmask |= (r & 0xFu) << (4 * q);
+      rvmask |= ((r >> 8) & 0xFu) << (4 * q);
       bmask |= ((r >> 16) & 0xFu) << (4 * q);
     }
     s.vmask = vmask;
     s.bmask = bmask;
+    s.rvmask = V8 ? rvmask : 0u;
     if (DBG) {
       if (a.d.key_gate_out && lane < nk)
         a.d.key_gate_out[gate_row * g.max_seq_len + key0 + lane] = (vmask >> lane) & 1u;
       if (a.refine_gate_out && lane < nk)
         a.refine_gate_out[gate_row * g.max_seq_len + key0 + lane] = (bmask >> lane) & 1u;
+      if (V8 && a.refine_v_gate_out && lane < nk)
+        a.refine_v_gate_out[gate_row * g.max_seq_len + key0 + lane] = (rvmask >> lane) & 1u;
       if (a.d.page_gate_out && lane == 0 && c < p.nchunks)
         a.d.page_gate_out[gate_row * ((g.max_seq_len + kChunk - 1) / kChunk) + c] = vmask ? 1 : 0;
     }
   }
 
-  // Refined scores, weights, L and the value product of chunk c.
-  __device__ __forceinline__ void finish(int c, const BS& s, const u32x4 (&vv)[NK]) {
-    const int key0 = c * kChunk;
-    const int nk = c < p.nchunks ? min(kChunk, p.n - key0) : 0;
-    float e[4];
-    scales(s.sc, e);
-    u32x2 phi[RB], plo[RB];
+  // The value tile of a chunk in LDS: [16 keys][VSTRIDE] BF16 rows.  8-bit
+  // values are widened exactly by v_cvt_scalef32_pk_bf16_fp8 (2 codes per
+  // instruction), the second plane with scale 1/16.
+  __device__ __forceinline__ void stage(const u32x4 (&vv)[NK], float scale) const {
+    if constexpr (V8) {
 #pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      i32x4 cba = {0, 0, 0, 0}, cbb = {0, 0, 0, 0};
-      if (s.bmask) {  // wave-uniform: some key of the chunk is refined
+      for (int i = 0; i < NK; ++i) {
+        const uint32_t off = 1024u * i + 16u * lane;  // 16 codes of key off / D
+        const uint32_t key = off / D;
+        uint32_t w[8];
 #pragma unroll
-        for (int c2 = 0; c2 < NKI; ++c2) {
-          cba = mfma_i8(s.kb[c2], qa[b][c2], cba);
-          cbb = mfma_i8(s.kb[c2], qb[b][c2], cbb);
+        for (int j = 0; j < 4; ++j) {
+          w[2 * j] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(
+                                                      static_cast<int>(vv[i][j]), scale, false));
+          w[2 * j + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(
+                                                          static_cast<int>(vv[i][j]), scale, true));
         }
+        unsigned char* dst = vt + key * VSTRIDE + 2 * (off - key * D);
+        *reinterpret_cast<u32x4*>(dst) = u32x4{w[0], w[1], w[2], w[3]};
+        *reinterpret_cast<u32x4*>(dst + 16) = u32x4{w[4], w[5], w[6], w[7]};
       }
-      uint32_t hi[4];
-      float res[4];
+    } else {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bool ok = rok[b] && 4 * grp + i < nk;
-        float x = s.xc[b][i];
-        if ((s.ref >> (4 * b + i)) & 1u) {
-          const float tb = static_cast<float>(cba[i]) + static_cast<float>(cbb[i]) * (1.0f / 256.0f);
-          x = x + (eta[b] * e[i]) * (tb * (1.0f / 256.0f));
-        }
-        const bool live = ok && (DENSE || x >= a.d.neg_T);
-        const float w = ok ? exp2_fast(x) : 0.0f;
-        lsum[b] += w;
-        if (!DENSE) lcut[b] += live ? 0.0f : w;
-        const float pw = live ? w : 0.0f;
-        hi[i] = __float_as_uint(pw) & 0xffff0000u;
-        res[i] = pw - __uint_as_float(hi[i]);
-        if (DBG && a.d.x_out && ok) a.d.x_out[xrow[b] * g.max_seq_len + key0 + 4 * grp + i] = x;
+      for (int i = 0; i < NK; ++i) {
+        const uint32_t off = 1024u * i + 16u * lane;
+        const uint32_t key = off / (2 * D);
+        *reinterpret_cast<u32x4*>(vt + key * VSTRIDE + (off - key * 2 * D)) = vv[i];
       }
-      phi[b] = u32x2{(hi[0] >> 16) | hi[1], (hi[2] >> 16) | hi[3]};
-      plo[b] = u32x2{pack_bf16_rne(res[0], res[1]), pack_bf16_rne(res[2], res[3])};
     }
-    if (s.vmask == 0) return;  // wave-uniform: no live key in the chunk
-#pragma unroll
-    for (int i = 0; i < NK; ++i) {
-      const uint32_t off = 1024u * i + 16u * lane;
-      const uint32_t key = off / (2 * D);
-      *reinterpret_cast<u32x4*>(vt + key * VSTRIDE + (off - key * 2 * D)) = vv[i];
-    }
+  }
+
+  // acc += V^T P^T over the staged tile (hi and residual weights).
+  __device__ __forceinline__ void product(const u32x2 (&phi)[RB], const u32x2 (&plo)[RB]) {
     const unsigned char* col = vt + (4 * grp) * VSTRIDE + 2 * n16;
 #pragma unroll
     for (int blk = 0; blk < NB; ++blk) {
@@ -300,11 +324,69 @@ struct Q8Scan {
       }
     }
   }
+
+  // Refined scores, weights, L and the value product of chunk c.
+  __device__ __forceinline__ void finish(int c, const BS& s, const u32x4 (&vv)[NK]) {
+    const int key0 = c * kChunk;
+    const int nk = c < p.nchunks ? min(kChunk, p.n - key0) : 0;
+    float e[4];
+    scales(s.sc, e);
+    u32x2 phi[RB], plo[RB], phi2[RB], plo2[RB];
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      i32x4 cba = {0, 0, 0, 0}, cbb = {0, 0, 0, 0};
+      if (s.bmask) {  // wave-uniform: some key of the chunk is refined
+#pragma unroll
+        for (int c2 = 0; c2 < NKI; ++c2) {
+          cba = mfma_i8(s.kb[c2], qa[b][c2], cba);
+          cbb = mfma_i8(s.kb[c2], qb[b][c2], cbb);
+        }
+      }
+      uint32_t hi[4], hi2[4];
+      float res[4], res2[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = rok[b] && 4 * grp + i < nk;
+        float x = s.xc[b][i];
+        if ((s.ref >> (4 * b + i)) & 1u) {
+          const float tb = static_cast<float>(cba[i]) + static_cast<float>(cbb[i]) * (1.0f / 256.0f);
+          x = x + (eta[b] * e[i]) * (tb * (1.0f / 256.0f));
+        }
+        const bool live = ok && (DENSE || x >= a.d.neg_T);
+        const float w = ok ? exp2_fast(x) : 0.0f;
+        lsum[b] += w;
+        if (!DENSE) lcut[b] += live ? 0.0f : w;
+        const float pw = live ? w : 0.0f;
+        hi[i] = __float_as_uint(pw) & 0xffff0000u;
+        res[i] = pw - __uint_as_float(hi[i]);
+        // the second value plane counts only where this row's group read it
+        const bool rv = V8 && ((s.refv >> (4 * b + i)) & 1u);
+        hi2[i] = rv ? hi[i] : 0u;
+        res2[i] = rv ? res[i] : 0.0f;
+        if (DBG && a.d.x_out && ok) a.d.x_out[xrow[b] * g.max_seq_len + key0 + 4 * grp + i] = x;
+      }
+      phi[b] = u32x2{(hi[0] >> 16) | hi[1], (hi[2] >> 16) | hi[3]};
+      plo[b] = u32x2{pack_bf16_rne(res[0], res[1]), pack_bf16_rne(res[2], res[3])};
+      phi2[b] = u32x2{(hi2[0] >> 16) | hi2[1], (hi2[2] >> 16) | hi2[3]};
+      plo2[b] = u32x2{pack_bf16_rne(res2[0], res2[1]), pack_bf16_rne(res2[2], res2[3])};
+    }
+    if (s.vmask == 0) return;  // wave-uniform: no live key in the chunk
+    stage(vv, 1.0f);
+    product(phi, plo);
+    if constexpr (V8) {
+      // second plane (r / 16) of the keys some group of the read group refined;
+      // the tile is wave-private and its reads above precede these writes
+      if (s.rvmask) {
+        stage(s.vr, 0.0625f);
+        product(phi2, plo2);
+      }
+    }
+  }
 };
 
-template <int D, int RB, bool DENSE, bool DBG>
+template <int D, int RB, bool DENSE, bool DBG, bool V8>
 __global__ __launch_bounds__(kScanThreads) void decode_q8_kernel(const Q8DecodeArgs a) {
-  using S = Q8Scan<D, RB, DENSE, DBG>;
+  using S = Q8Scan<D, RB, DENSE, DBG, V8>;
   constexpr int NKI = S::NKI;
   constexpr int R = S::R;
   constexpr int kTileBytes = kScanWaves * 16 * S::VSTRIDE;
@@ -334,6 +416,7 @@ __global__ __launch_bounds__(kScanThreads) void decode_q8_kernel(const Q8DecodeA
     sc.zr[b] = ri.ok ? a.d.z[row] : 0.0f;
     sc.eta[b] = ri.ok ? a.eta[row] : 0.0f;
     sc.ntau[b] = ri.ok ? -a.tau[ri.req] : 0.0f;
+    sc.ntau_v[b] = V8 && ri.ok ? -a.tau_v[ri.req] : 0.0f;
 #pragma unroll
     for (int c = 0; c < NKI; ++c) {
       sc.qa[b][c] = ri.ok ? *reinterpret_cast<const u32x4*>(a.qp + row * 2 * D + 64 * c + 16 * sc.grp)
@@ -453,33 +536,42 @@ __global__ __launch_bounds__(kScanThreads) void decode_q8_kernel(const Q8DecodeA
     if (!sc.rok[b]) continue;
     const size_t row = slot_rows + sc.xrow[b];
 #pragma unroll
-    for (int blk = 0; blk < S::NB; ++blk)
-      a.d.part_A[row * D + 16 * blk + 4 * (wl >> 4) + wi] = red[((b * S::NB + blk) * 4 + wi) * 64 + wl];
+    for (int blk = 0; blk < S::NB; ++blk) {
+      const float v = red[((b * S::NB + blk) * 4 + wi) * 64 + wl];
+      a.d.part_A[row * D + 16 * blk + 4 * (wl >> 4) + wi] = V8 ? v * a.v_scale : v;  // 2^e: exact
+    }
     if (wi == 0 && wl < 16) a.d.part_L[row] = redl[b * 64 + wl];
     if (a.d.part_Lcut && wi == 1 && wl < 16) a.d.part_Lcut[row] = redl[b * 64 + 16 + wl];
   }
 }
 
-template <int D, int RB, bool DENSE>
+template <int D, int RB, bool DENSE, bool V8>
 hipError_t launch_q8_rb(const Q8DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
   if (dbg)
-    hipLaunchKernelGGL((decode_q8_kernel<D, RB, DENSE, true>), dim3(blocks), dim3(kScanThreads), 0,
-                       stream, a);
+    hipLaunchKernelGGL((decode_q8_kernel<D, RB, DENSE, true, V8>), dim3(blocks), dim3(kScanThreads),
+                       0, stream, a);
   else
-    hipLaunchKernelGGL((decode_q8_kernel<D, RB, DENSE, false>), dim3(blocks), dim3(kScanThreads), 0,
-                       stream, a);
+    hipLaunchKernelGGL((decode_q8_kernel<D, RB, DENSE, false, V8>), dim3(blocks), dim3(kScanThreads),
+                       0, stream, a);
   return hipGetLastError();
+}
+
+template <int D, int RB, bool V8>
+hipError_t launch_q8_v(const Q8DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
+  return a.d.dense ? launch_q8_rb<D, RB, true, V8>(a, dbg, blocks, stream)
+                   : launch_q8_rb<D, RB, false, V8>(a, dbg, blocks, stream);
 }
 
 template <int D>
 hipError_t launch_q8_d(const Q8DecodeArgs& a, unsigned blocks, hipStream_t stream) {
   const bool dbg = a.d.x_out || a.d.key_gate_out || a.d.page_gate_out || a.xc_out ||
-                   a.refine_gate_out;
+                   a.refine_gate_out || a.refine_v_gate_out;
   const int rb = a.d.rows_per_group / 16;
-  if (rb == 1) return a.d.dense ? launch_q8_rb<D, 1, true>(a, dbg, blocks, stream)
-                                : launch_q8_rb<D, 1, false>(a, dbg, blocks, stream);
-  if (rb == 2) return a.d.dense ? launch_q8_rb<D, 2, true>(a, dbg, blocks, stream)
-                                : launch_q8_rb<D, 2, false>(a, dbg, blocks, stream);
+  const bool v8 = a.vp != nullptr;
+  if (rb == 1) return v8 ? launch_q8_v<D, 1, true>(a, dbg, blocks, stream)
+                         : launch_q8_v<D, 1, false>(a, dbg, blocks, stream);
+  if (rb == 2) return v8 ? launch_q8_v<D, 2, true>(a, dbg, blocks, stream)
+                         : launch_q8_v<D, 2, false>(a, dbg, blocks, stream);
   return hipErrorInvalidValue;
 }
 

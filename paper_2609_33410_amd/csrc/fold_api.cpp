@@ -356,9 +356,37 @@ fold_status fold_q8_write_keys(const fold_kv_view* kv, const void* k_src, const 
   return ok();
 }
 
+fold_status fold_v8_write_values(const fold_kv_view* kv, const void* v_src,
+                                 const int32_t* tok_seq, const int32_t* tok_pos, int32_t n_tok,
+                                 int32_t scale_exp, uint8_t* plane_p, uint8_t* plane_r,
+                                 void* stream) {
+  if (!kv) return fail(FOLD_E_INVAL, "kv view is required");
+  if (n_tok < 0) return fail(FOLD_E_INVAL, "n_tok must be >= 0");
+  if (scale_exp < -100 || scale_exp > 100)
+    return fail(FOLD_E_INVAL, "scale_exp %d out of range", scale_exp);
+  fold::V8WriteArgs a;
+  fold_status st = check_layout(kv, kv->num_seqs, kv->num_kv_heads, &a.geo);
+  if (st != FOLD_OK) return st;
+  if (n_tok > 0 && (!v_src || !tok_seq || !tok_pos || !plane_p || !plane_r))
+    return fail(FOLD_E_INVAL, "v_src, tok_seq, tok_pos, plane_p and plane_r are required");
+  if (static_cast<long long>(n_tok) * kv->num_kv_heads > 0x1fffffffLL)
+    return fail(FOLD_E_INVAL, "grid too large");
+  a.v_src = static_cast<const uint16_t*>(v_src);
+  a.tok_seq = tok_seq;
+  a.tok_pos = tok_pos;
+  a.n_tok = n_tok;
+  a.scale_exp = scale_exp;
+  a.vp = plane_p;
+  a.vr = plane_r;
+  hipError_t e = fold::launch_v8_write(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "v8 write launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 fold_status fold_q8_split_query(const fold_q_view* q, int32_t head_dim, float sm_scale,
-                                const int32_t* req_lens, float kappa, int8_t* planes_out,
-                                float* eta_out, float* tau_out, void* stream) {
+                                const int32_t* req_lens, float kappa, float kappa_v,
+                                int8_t* planes_out, float* eta_out, float* tau_out,
+                                float* tau_v_out, void* stream) {
   if (!q) return fail(FOLD_E_INVAL, "q view is required");
   if (head_dim != 64 && head_dim != 128)
     return fail(FOLD_E_INVAL, "head_dim %d: must be 64 or 128", head_dim);
@@ -370,7 +398,8 @@ fold_status fold_q8_split_query(const fold_q_view* q, int32_t head_dim, float sm
   if ((req_lens == nullptr) != (tau_out == nullptr))
     return fail(FOLD_E_INVAL, "req_lens and tau_out must both be set or both be NULL");
   if (!isfinite(sm_scale)) return fail(FOLD_E_INVAL, "sm_scale must be finite");
-  if (isnan(kappa)) return fail(FOLD_E_INVAL, "kappa must not be NaN");
+  if (isnan(kappa) || isnan(kappa_v)) return fail(FOLD_E_INVAL, "kappa and kappa_v must not be NaN");
+  if (tau_v_out && !req_lens) return fail(FOLD_E_INVAL, "tau_v_out needs req_lens");
   fold::Q8SplitArgs a;
   a.q = static_cast<const uint16_t*>(q->q);
   a.qp = planes_out;
@@ -379,8 +408,10 @@ fold_status fold_q8_split_query(const fold_q_view* q, int32_t head_dim, float sm
   a.sm_scale = sm_scale;
   a.req_lens = req_lens;
   a.tau = tau_out;
+  a.tau_v = tau_v_out;
   a.batch = q->batch;
   a.kappa = kappa;
+  a.kappa_v = kappa_v;
   hipError_t e = fold::launch_q8_split(a, head_dim, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(FOLD_E_HIP, "q8 split launch: %s", hipGetErrorString(e));
   return ok();
@@ -418,14 +449,31 @@ fold_status fold_q8_ref_estimate(const fold_kv_view* kv, const fold_q8_keys* key
 }
 
 fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* keys,
-                                 const fold_q8_query* q, const float* z, float depth_T,
-                                 int32_t num_splits, int32_t slot_offset, int32_t num_slots,
-                                 float* part_A, float* part_L, float* part_Lcut,
-                                 const fold_q8_debug* dbg, void* stream) {
+                                 const fold_q8_query* q, const fold_v8_values* values,
+                                 const float* z, float depth_T, int32_t num_splits,
+                                 int32_t slot_offset, int32_t num_slots, float* part_A,
+                                 float* part_L, float* part_Lcut, const fold_q8_debug* dbg,
+                                 void* stream) {
   fold::Q8DecodeArgs a;
-  fold_status st = check_q8_view(kv, keys, q, &a.d.geo, true);
+  fold_status st = check_q8_view(kv, keys, q, &a.d.geo, values == nullptr);
   if (st != FOLD_OK) return st;
   if (!q->tau) return fail(FOLD_E_INVAL, "tau is required");
+  a.vp = nullptr;
+  a.vr = nullptr;
+  a.v_scale = 1.0f;
+  a.tau_v = nullptr;
+  if (values) {
+    if (!values->plane_p || !values->plane_r || !q->tau_v)
+      return fail(FOLD_E_INVAL, "8-bit values need plane_p, plane_r and q->tau_v");
+    if (!aligned16(values->plane_p) || !aligned16(values->plane_r))
+      return fail(FOLD_E_INVAL, "value planes must be 16-byte aligned");
+    if (values->scale_exp < -100 || values->scale_exp > 100)
+      return fail(FOLD_E_INVAL, "scale_exp %d out of range", values->scale_exp);
+    a.vp = values->plane_p;
+    a.vr = values->plane_r;
+    a.v_scale = ldexpf(1.0f, values->scale_exp);
+    a.tau_v = q->tau_v;
+  }
   if (!z || !part_A || !part_L) return fail(FOLD_E_INVAL, "z, part_A and part_L are required");
   st = check_depth(depth_T);
   if (st != FOLD_OK) return st;
@@ -460,6 +508,7 @@ fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* key
   a.tau = q->tau;
   a.xc_out = dbg ? dbg->xc_out : nullptr;
   a.refine_gate_out = dbg ? dbg->refine_gate_out : nullptr;
+  a.refine_v_gate_out = dbg ? dbg->refine_v_gate_out : nullptr;
   hipError_t e = fold::launch_q8_decode(a, kv->head_dim, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(FOLD_E_HIP, "q8 decode launch: %s", hipGetErrorString(e));
   return ok();

@@ -101,6 +101,12 @@ struct Q8DecodeArgs {
   const float* tau;       // [batch] refine thresholds
   float* xc_out;          // coarse x (debug)
   uint8_t* refine_gate_out;
+  // 8-bit values (NULL vp: BF16 values from d.geo.v)
+  const uint8_t* vp;      // plane 1, one byte per element
+  const uint8_t* vr;      // plane 2 (residual x 16)
+  float v_scale;          // 2^scale_exp
+  const float* tau_v;     // [batch] refine-V thresholds
+  uint8_t* refine_v_gate_out;
 };
 
 struct Q8WriteArgs {
@@ -114,6 +120,17 @@ struct Q8WriteArgs {
   uint16_t* ks;
 };
 
+struct V8WriteArgs {
+  ScanGeometry geo;       // layout of the destination cache
+  const uint16_t* v_src;  // [n_tok][hkv][D] bf16
+  const int32_t* tok_seq;
+  const int32_t* tok_pos;
+  int n_tok;
+  int scale_exp;          // values are stored as 2^scale_exp (p + r/16)
+  uint8_t* vp;
+  uint8_t* vr;
+};
+
 struct Q8SplitArgs {
   const uint16_t* q;      // [rows][D] bf16
   int8_t* qp;             // [rows][2][D]
@@ -121,9 +138,11 @@ struct Q8SplitArgs {
   int rows;
   float sm_scale;
   const int32_t* req_lens;  // [batch] or NULL
-  float* tau;               // [batch] or NULL
+  float* tau;               // [batch] or NULL: refine-K thresholds
+  float* tau_v;             // [batch] or NULL: refine-V thresholds
   int batch;
   float kappa;
+  float kappa_v;
 };
 
 struct Q8EstimateArgs {
@@ -152,6 +171,7 @@ hipError_t launch_value_mean(const MeanArgs& a, int head_dim, hipStream_t stream
 hipError_t launch_value_mean_append(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_write(const Q8WriteArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_split(const Q8SplitArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_v8_write(const V8WriteArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_estimate(const Q8EstimateArgs& a, int head_dim, hipStream_t stream);
 
 // Rows per read group the decode kernel is instantiated for, given the rows

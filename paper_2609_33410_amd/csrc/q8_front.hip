@@ -1,5 +1,5 @@
 // Front of a two-plane INT8 key cache (Section 4, "Cache format"): the key
-// writer and the per-step query split.
+// writer, the per-step query split and the writer of 8-bit values.
 //
 // Both rotate a D-vector by the Sylvester Hadamard matrix H_D (entries +-1;
 // the paper's orthonormal rotation is H_D / sqrt(D), and its 1/D on a dot
@@ -119,6 +119,7 @@ __global__ __launch_bounds__(kFrontThreads) void q8_split_kernel(const Q8SplitAr
       const int n = a.req_lens[r];
       const int c = n > 1 ? 32 - __builtin_clz(static_cast<unsigned>(n - 1)) : 0;
       a.tau[r] = a.kappa + static_cast<float>(c);
+      if (a.tau_v) a.tau_v[r] = a.kappa_v + static_cast<float>(c);
     }
   }
   const long long row = static_cast<long long>(blockIdx.x) * kWavesPerBlock +
@@ -142,7 +143,80 @@ __global__ __launch_bounds__(kFrontThreads) void q8_split_kernel(const Q8SplitAr
     a.eta[row] = static_cast<float>(((kLog2e * static_cast<double>(a.sm_scale)) * f) / D);
 }
 
+// E4M3 (OCP E4M3FN: bias 7, subnormals m 2^-9, largest finite 448) code of
+// y rounded to nearest even; magnitudes of 448 and above saturate to 448.  The
+// mantissa is rounded with rintf on an exactly scaled copy, so the tie goes
+// to the even code.  *val receives the code's value.
+__device__ __forceinline__ uint32_t e4m3_rne_sat(float y, float* val) {
+  const uint32_t sign = (__float_as_uint(y) >> 24) & 0x80u;
+  const float a = fabsf(y);
+  const float sg = sign ? -1.0f : 1.0f;
+  if (!(a < 448.0f)) {
+    *val = sg * 448.0f;
+    return sign | 0x7Eu;
+  }
+  if (a < 0x1p-6f) {  // subnormal steps of 2^-9; 8 steps is the code of 2^-6
+    const float q = rintf(a * 512.0f);
+    *val = sg * q * 0x1p-9f;
+    return q == 0.0f ? 0u : sign | static_cast<uint32_t>(q);
+  }
+  int e = ilogbf(a);
+  float q = rintf(ldexpf(a, 3 - e));  // in [8, 16]
+  if (q == 16.0f) {
+    q = 8.0f;
+    e += 1;
+  }
+  *val = sg * ldexpf(q, e - 3);
+  return sign | static_cast<uint32_t>((e + 7) << 3) | static_cast<uint32_t>(q - 8.0f);
+}
+
+template <int D>
+__global__ __launch_bounds__(kFrontThreads) void v8_write_kernel(const V8WriteArgs a) {
+  const ScanGeometry& g = a.geo;
+  const int lane = threadIdx.x & 63;
+  const long long item = static_cast<long long>(blockIdx.x) * kWavesPerBlock +
+                         __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (item >= static_cast<long long>(a.n_tok) * g.hkv) return;  // uniform per wave
+  const int tok = static_cast<int>(item / g.hkv);
+  const int kvh = static_cast<int>(item % g.hkv);
+  const int seq = ld_uniform(a.tok_seq, tok);
+  const int pos = ld_uniform(a.tok_pos, tok);
+  if (seq < 0 || seq >= g.num_seqs || pos < 0 || pos >= view_capacity(g)) return;
+  size_t row;
+  if (g.page_size > 0) {
+    const int phys = ld_uniform(a.geo.block_table,
+                                static_cast<size_t>(seq) * g.max_pages + pos / g.page_size);
+    if (phys < 0 || phys >= g.num_pages) return;
+    row = (static_cast<size_t>(phys) * g.hkv + kvh) * g.page_size + pos % g.page_size;
+  } else {
+    row = (static_cast<size_t>(seq) * g.hkv + kvh) * g.max_seq_len + pos;
+  }
+  const uint16_t* src = a.v_src + (static_cast<size_t>(tok) * g.hkv + kvh) * D;
+#pragma unroll
+  for (int i = 0; i < D / 64; ++i) {
+    const float y = ldexpf(bf16_lo(src[64 * i + lane]), -a.scale_exp);  // exact
+    float pv, rv;
+    const uint32_t p = e4m3_rne_sat(y, &pv);
+    const uint32_t r = e4m3_rne_sat(16.0f * (y - pv), &rv);  // y - pv and the x16 are exact
+    a.vp[row * D + 64 * i + lane] = static_cast<uint8_t>(p);
+    a.vr[row * D + 64 * i + lane] = static_cast<uint8_t>(r);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_v8_write(const V8WriteArgs& a, int head_dim, hipStream_t stream) {
+  const long long items = static_cast<long long>(a.n_tok) * a.geo.hkv;
+  if (items == 0) return hipSuccess;
+  const unsigned blocks = static_cast<unsigned>((items + kWavesPerBlock - 1) / kWavesPerBlock);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(v8_write_kernel<128>, dim3(blocks), dim3(kFrontThreads), 0, stream, a);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL(v8_write_kernel<64>, dim3(blocks), dim3(kFrontThreads), 0, stream, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
 
 hipError_t launch_q8_write(const Q8WriteArgs& a, int head_dim, hipStream_t stream) {
   const long long items = static_cast<long long>(a.n_tok) * a.geo.hkv;

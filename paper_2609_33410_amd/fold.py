@@ -35,6 +35,7 @@ EXPORTED = (
     "fold_value_mean",
     "fold_value_mean_append",
     "fold_q8_write_keys",
+    "fold_v8_write_values",
     "fold_q8_split_query",
     "fold_q8_ref_estimate",
     "fold_q8_decode_rows_per_group",
@@ -98,13 +99,19 @@ class fold_q8_keys(ctypes.Structure):
 
 class fold_q8_query(ctypes.Structure):
     _fields_ = [("planes", ctypes.c_void_p), ("eta", ctypes.c_void_p), ("tau", ctypes.c_void_p),
-                ("batch", ctypes.c_int32), ("num_heads", ctypes.c_int32)]
+                ("batch", ctypes.c_int32), ("num_heads", ctypes.c_int32),
+                ("tau_v", ctypes.c_void_p)]
+
+
+class fold_v8_values(ctypes.Structure):
+    _fields_ = [("plane_p", ctypes.c_void_p), ("plane_r", ctypes.c_void_p),
+                ("scale_exp", ctypes.c_int32)]
 
 
 class fold_q8_debug(ctypes.Structure):
     _fields_ = [("x_out", ctypes.c_void_p), ("xc_out", ctypes.c_void_p),
                 ("key_gate_out", ctypes.c_void_p), ("page_gate_out", ctypes.c_void_p),
-                ("refine_gate_out", ctypes.c_void_p)]
+                ("refine_gate_out", ctypes.c_void_p), ("refine_v_gate_out", ctypes.c_void_p)]
 
 
 _lib = None
@@ -157,8 +164,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.fold_q8_split_query.restype = ctypes.c_int
     lib.fold_q8_split_query.argtypes = [P(fold_q_view), ctypes.c_int32, ctypes.c_float,
-                                        ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p,
-                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+                                        ctypes.c_void_p, ctypes.c_float, ctypes.c_float,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p]
+    lib.fold_v8_write_values.restype = ctypes.c_int
+    lib.fold_v8_write_values.argtypes = [P(fold_kv_view), ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.fold_q8_ref_estimate.restype = ctypes.c_int
     lib.fold_q8_ref_estimate.argtypes = [P(fold_kv_view), P(fold_q8_keys), P(fold_q8_query),
                                          P(fold_est_params), ctypes.c_void_p, ctypes.c_void_p]
@@ -168,6 +180,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         fn.argtypes = [P(fold_kv_view), P(fold_q8_query)]
     lib.fold_q8_decode_split.restype = ctypes.c_int
     lib.fold_q8_decode_split.argtypes = [P(fold_kv_view), P(fold_q8_keys), P(fold_q8_query),
+                                         P(fold_v8_values),
                                          ctypes.c_void_p, ctypes.c_float, ctypes.c_int32,
                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_void_p, P(fold_q8_debug),
@@ -408,14 +421,47 @@ class Q8Keys:
 
 @dataclass
 class Q8Query:
-    """Query codes ``planes [B, H, 2, D]`` int8, ``eta [B, H]`` and ``tau [B]`` fp32."""
+    """Query codes ``planes [B, H, 2, D]`` int8, ``eta [B, H]``, ``tau [B]`` and
+    (8-bit values) ``tau_v [B]`` fp32."""
     planes: torch.Tensor
     eta: torch.Tensor
     tau: Optional[torch.Tensor]
+    tau_v: Optional[torch.Tensor] = None
 
     def view(self) -> fold_q8_query:
         return fold_q8_query(_ptr(self.planes), _ptr(self.eta), _ptr(self.tau),
-                             int(self.planes.shape[0]), int(self.planes.shape[1]))
+                             int(self.planes.shape[0]), int(self.planes.shape[1]),
+                             _ptr(self.tau_v))
+
+
+@dataclass
+class V8Values:
+    """8-bit values: E4M3 planes ``plane_p, plane_r`` (uint8, the BF16 value
+    cache's element layout) under the scale ``2 ** scale_exp``."""
+    plane_p: torch.Tensor
+    plane_r: torch.Tensor
+    scale_exp: int
+
+    def view(self) -> fold_v8_values:
+        return fold_v8_values(_ptr(self.plane_p), _ptr(self.plane_r), int(self.scale_exp))
+
+
+def v8_empty_values(v_like: torch.Tensor, scale_exp: int) -> V8Values:
+    return V8Values(torch.empty(v_like.shape, dtype=torch.uint8, device=v_like.device),
+                    torch.empty(v_like.shape, dtype=torch.uint8, device=v_like.device),
+                    scale_exp)
+
+
+def fold_v8_write_values(kv: KV, v_src: torch.Tensor, tok_seq: torch.Tensor,
+                         tok_pos: torch.Tensor, values: V8Values, stream=None) -> None:
+    _need(v_src, "v_src", torch.bfloat16)
+    _need(tok_seq, "tok_seq", torch.int32)
+    _need(tok_pos, "tok_pos", torch.int32)
+    _need(values.plane_p, "plane_p", torch.uint8)
+    _need(values.plane_r, "plane_r", torch.uint8)
+    _check(load_library().fold_v8_write_values(
+        ctypes.byref(kv.view), _ptr(v_src), _ptr(tok_seq), _ptr(tok_pos), int(tok_seq.shape[0]),
+        int(values.scale_exp), _ptr(values.plane_p), _ptr(values.plane_r), _stream(stream)))
 
 
 def q8_empty_keys(k_like: torch.Tensor) -> Q8Keys:
@@ -440,17 +486,19 @@ def fold_q8_write_keys(kv: KV, k_src: torch.Tensor, tok_seq: torch.Tensor, tok_p
 
 def fold_q8_split_query(q: torch.Tensor, sm_scale: float, out: Q8Query,
                         req_lens: Optional[torch.Tensor] = None, kappa: float = 0.0,
-                        stream=None) -> Q8Query:
+                        kappa_v: float = 0.0, stream=None) -> Q8Query:
     qv = q_view(q)
     _need(out.planes, "planes", torch.int8)
     _need(out.eta, "eta", torch.float32)
     if req_lens is not None:
         _need(req_lens, "req_lens", torch.int32)
         _need(out.tau, "tau", torch.float32)
+    if req_lens is not None and out.tau_v is not None:
+        _need(out.tau_v, "tau_v", torch.float32)
     _check(load_library().fold_q8_split_query(
-        ctypes.byref(qv.view), int(q.shape[-1]), sm_scale, _ptr(req_lens), kappa,
+        ctypes.byref(qv.view), int(q.shape[-1]), sm_scale, _ptr(req_lens), kappa, kappa_v,
         _ptr(out.planes), _ptr(out.eta), None if req_lens is None else _ptr(out.tau),
-        _stream(stream)))
+        None if req_lens is None else _ptr(out.tau_v), _stream(stream)))
     return out
 
 
@@ -458,6 +506,7 @@ def q8_empty_query(q: torch.Tensor) -> Q8Query:
     b, h, d = q.shape
     return Q8Query(torch.empty(b, h, 2, d, dtype=torch.int8, device=q.device),
                    torch.empty(b, h, dtype=torch.float32, device=q.device),
+                   torch.empty(b, dtype=torch.float32, device=q.device),
                    torch.empty(b, dtype=torch.float32, device=q.device))
 
 
@@ -492,7 +541,9 @@ def fold_q8_decode_split(kv: KV, keys: Q8Keys, q: Q8Query, z: torch.Tensor, dept
                          key_gate_out: Optional[torch.Tensor] = None,
                          page_gate_out: Optional[torch.Tensor] = None,
                          refine_gate_out: Optional[torch.Tensor] = None,
-                         part_Lcut: Optional[torch.Tensor] = None, stream=None) -> None:
+                         part_Lcut: Optional[torch.Tensor] = None,
+                         values: Optional[V8Values] = None,
+                         refine_v_gate_out: Optional[torch.Tensor] = None, stream=None) -> None:
     _need(z, "z", torch.float32)
     _need(part_A, "part_A", torch.float32)
     _need(part_L, "part_L", torch.float32)
@@ -501,7 +552,8 @@ def fold_q8_decode_split(kv: KV, keys: Q8Keys, q: Q8Query, z: torch.Tensor, dept
     outs = ((x_out, "x_out", torch.float32), (xc_out, "xc_out", torch.float32),
             (key_gate_out, "key_gate_out", torch.uint8),
             (page_gate_out, "page_gate_out", torch.uint8),
-            (refine_gate_out, "refine_gate_out", torch.uint8))
+            (refine_gate_out, "refine_gate_out", torch.uint8),
+            (refine_v_gate_out, "refine_v_gate_out", torch.uint8))
     dbg = None
     if any(t is not None for t, _, _ in outs):
         for t, nm, dt in outs:
@@ -509,7 +561,9 @@ def fold_q8_decode_split(kv: KV, keys: Q8Keys, q: Q8Query, z: torch.Tensor, dept
                 _need(t, nm, dt)
         dbg = fold_q8_debug(*(_ptr(t) for t, _, _ in outs))
     kk, qq = keys.view(), q.view()
+    vals = None if values is None else values.view()
     _check(load_library().fold_q8_decode_split(
-        ctypes.byref(kv.view), ctypes.byref(kk), ctypes.byref(qq), _ptr(z), depth_T, num_splits,
+        ctypes.byref(kv.view), ctypes.byref(kk), ctypes.byref(qq),
+        None if vals is None else ctypes.byref(vals), _ptr(z), depth_T, num_splits,
         slot_offset, int(part_A.shape[0]), _ptr(part_A), _ptr(part_L), _ptr(part_Lcut),
         None if dbg is None else ctypes.byref(dbg), _stream(stream)))

@@ -174,15 +174,15 @@ def test_binding_raises_when_library_missing(tmp_path):
 def _q8(kv_heads=2, heads=8, **over):
     from paper_2609_33410_amd.fold import fold_q8_keys, fold_q8_query
     keys = fold_q8_keys(FAKE, FAKE, FAKE)
-    q = fold_q8_query(FAKE, FAKE, FAKE, 2, heads)
+    q = fold_q8_query(FAKE, FAKE, FAKE, 2, heads, FAKE)
     for k, v in over.items():
         setattr(keys if k in ("plane_a", "plane_b", "scale") else q, k, v)
     return keys, q
 
 
 def _q8_decode(lib, kv, keys, q, T=math.inf, splits=1, z=FAKE):
-    return lib.fold_q8_decode_split(ctypes.byref(kv), ctypes.byref(keys), ctypes.byref(q), z, T,
-                                    splits, 0, splits, FAKE, FAKE, None, None, None)
+    return lib.fold_q8_decode_split(ctypes.byref(kv), ctypes.byref(keys), ctypes.byref(q), None,
+                                    z, T, splits, 0, splits, FAKE, FAKE, None, None, None)
 
 
 @pytest.mark.parametrize("over,kvo,want", [
@@ -224,12 +224,34 @@ def test_q8_front_rejects_bad_args(lib):
                                   None) == F.FOLD_OK
     q = _q()
     split = lib.fold_q8_split_query
-    assert split(ctypes.byref(q), 96, 0.1, None, 0.0, FAKE, FAKE, None, None) == F.FOLD_E_INVAL
-    assert split(ctypes.byref(q), 128, 0.1, FAKE, 0.0, FAKE, FAKE, None, None) == F.FOLD_E_INVAL
-    assert split(ctypes.byref(q), 128, 0.1, FAKE, float("nan"), FAKE, FAKE, FAKE,
+    assert split(ctypes.byref(q), 96, 0.1, None, 0.0, 0.0, FAKE, FAKE, None, None,
                  None) == F.FOLD_E_INVAL
-    assert split(ctypes.byref(q), 128, float("inf"), None, 0.0, FAKE, FAKE, None,
+    assert split(ctypes.byref(q), 128, 0.1, FAKE, 0.0, 0.0, FAKE, FAKE, None, None,
                  None) == F.FOLD_E_INVAL
+    assert split(ctypes.byref(q), 128, 0.1, FAKE, float("nan"), 0.0, FAKE, FAKE, FAKE, None,
+                 None) == F.FOLD_E_INVAL
+    assert split(ctypes.byref(q), 128, 0.1, FAKE, 0.0, float("nan"), FAKE, FAKE, FAKE, None,
+                 None) == F.FOLD_E_INVAL
+    assert split(ctypes.byref(q), 128, 0.1, None, 0.0, 0.0, FAKE, FAKE, None, FAKE,
+                 None) == F.FOLD_E_INVAL   # tau_v without lengths
+    assert split(ctypes.byref(q), 128, float("inf"), None, 0.0, 0.0, FAKE, FAKE, None, None,
+                 None) == F.FOLD_E_INVAL
+    from paper_2609_33410_amd.fold import fold_v8_values
+    keys8, q88 = _q8(tau_v=None)
+    v8 = fold_v8_values(FAKE, FAKE, 0)
+    kvv = _kv()
+    assert lib.fold_q8_decode_split(ctypes.byref(kvv), ctypes.byref(keys8), ctypes.byref(q88),
+                                    ctypes.byref(v8), FAKE, math.inf, 1, 0, 1, FAKE, FAKE, None,
+                                    None, None) == F.FOLD_E_INVAL   # no tau_v
+    keys8, q88 = _q8()
+    v8 = fold_v8_values(FAKE + 1, FAKE, 0)
+    assert lib.fold_q8_decode_split(ctypes.byref(kvv), ctypes.byref(keys8), ctypes.byref(q88),
+                                    ctypes.byref(v8), FAKE, math.inf, 1, 0, 1, FAKE, FAKE, None,
+                                    None, None) == F.FOLD_E_INVAL   # misaligned plane
+    assert lib.fold_v8_write_values(ctypes.byref(kvv), FAKE, FAKE, FAKE, 2, 500, FAKE, FAKE,
+                                    None) == F.FOLD_E_INVAL   # scale exponent
+    assert lib.fold_v8_write_values(ctypes.byref(kvv), FAKE, FAKE, FAKE, 2, 0, None, FAKE,
+                                    None) == F.FOLD_E_INVAL
     keys, q8 = _q8()
     csr = _kv(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=4)
     assert lib.fold_q8_ref_estimate(ctypes.byref(csr), ctypes.byref(keys), ctypes.byref(q8), None,
