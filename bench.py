@@ -41,7 +41,8 @@ def parse():
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--all", action="store_true", help="also time workloads 1-5 (stderr)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--no-q8", action="store_true", help="skip the two-plane INT8 key leg")
+    ap.add_argument("--no-q8", action="store_true",
+                    help="skip the two-plane INT8 key legs (BF16 and 8-bit values)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--splits", type=int, default=None, help="override the split count")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -106,14 +107,16 @@ class Path:
 
 
 class Q8Path:
-    """The same workload over a two-plane INT8 key cache (values stay BF16).
+    """The same workload over a two-plane INT8 key cache, with BF16 values or
+    (``values8``) two E4M3 value planes.
 
-    The cache is written once by the cache writer (untimed set-up, as a
+    The cache is written once by the cache writers (untimed set-up, as a
     prompt would be); a step is the query split, the reference estimate from
     coarse logits, every level's gated scan and the combine."""
 
-    def __init__(self, wl, F, torch, kappa=0.0):
+    def __init__(self, wl, F, torch, kappa=-4.0, values8=False, kappa_v=-4.0):
         self.wl, self.F, self.torch, self.kappa = wl, F, torch, kappa
+        self.kappa_v = kappa_v
         dev = wl.q.device
         n_pool, hkv, rows, d = wl.k.shape
         pool = F.kv_view(wl.k, None, torch.full((n_pool,), rows, dtype=torch.int32, device=dev),
@@ -123,7 +126,16 @@ class Q8Path:
         tok_pos = torch.arange(rows, dtype=torch.int32, device=dev).repeat(n_pool)
         k_src = wl.k.permute(0, 2, 1, 3).reshape(n_pool * rows, hkv, d).contiguous()
         F.fold_q8_write_keys(pool, k_src, tok_seq, tok_pos, self.keys)
-        del k_src, tok_seq, tok_pos
+        del k_src
+        self.vals = None
+        if values8:
+            vmax = float(wl.v.float().abs().max())
+            e = int(math.ceil(math.log2(vmax / 448.0))) if vmax > 0 else 0
+            self.vals = F.v8_empty_values(wl.v, e)
+            v_src = wl.v.permute(0, 2, 1, 3).reshape(n_pool * rows, hkv, d).contiguous()
+            F.fold_v8_write_values(pool, v_src, tok_seq, tok_pos, self.vals)
+            del v_src
+        del tok_seq, tok_pos
         # one appended token per request (the per-step append), for timing
         self.app_kv = F.kv_view(self.keys.plane_a, None, wl.flat.seq_lens,
                                 num_kv_heads=hkv, max_seq_len=wl.flat.max_seq_len,
@@ -132,6 +144,7 @@ class Q8Path:
         self.app_seq = torch.arange(b, dtype=torch.int32, device=dev)
         self.app_pos = (wl.flat.seq_lens - 1).to(torch.int32).contiguous()
         self.app_src = torch.randn(b, hkv, d, device=dev).to(torch.bfloat16)
+        self.app_vsrc = torch.randn(b, hkv, d, device=dev).to(torch.bfloat16)
         self.levels = [F.kv_view(self.keys.plane_a, wl.v, lv.seq_lens,
                                  num_kv_heads=wl.num_kv_heads, max_seq_len=lv.max_seq_len,
                                  block_table=lv.block_table, row_indptr=lv.row_indptr,
@@ -151,11 +164,14 @@ class Q8Path:
     def split(self, stream):
         self.F.fold_q8_split_query(self.wl.q, self.wl.sm_scale, self.qq,
                                    req_lens=self.wl.flat.seq_lens, kappa=self.kappa,
-                                   stream=stream)
+                                   kappa_v=self.kappa_v, stream=stream)
 
     def append(self, stream):
         self.F.fold_q8_write_keys(self.app_kv, self.app_src, self.app_seq, self.app_pos,
                                   self.keys, stream=stream)
+        if self.vals is not None:
+            self.F.fold_v8_write_values(self.app_kv, self.app_vsrc, self.app_seq, self.app_pos,
+                                        self.vals, stream=stream)
 
     def estimate(self, stream):
         self.F.fold_q8_ref_estimate(self.flat, self.keys, self.qq, self.z, stream=stream)
@@ -164,31 +180,38 @@ class Q8Path:
         off = 0
         for kv, s in zip(self.levels, self.splits):
             self.F.fold_q8_decode_split(kv, self.keys, self.qq, self.z, T, s, off, self.part_A,
-                                        self.part_L, stream=stream)
+                                        self.part_L, values=self.vals, stream=stream)
             off += s
 
     def combine(self, stream):
         self.F.fold_combine(self.part_A, self.part_L, self.out, stream=stream)
 
     def read_counts(self, T):
-        """(value rows, plane-B rows, read-group key rows) the scan reads at
-        depth T, from its own read-bit exports (untimed)."""
+        """(value rows, plane-B rows, read-group key rows, second-value-plane
+        rows) the scan reads at depth T, from its own read-bit exports
+        (untimed)."""
         torch, F = self.torch, self.F
         dev = self.wl.q.device
-        nv = nb = total = 0
+        nv = nb = total = nr = 0
         off = 0
         for lv, kv, s in zip(self.wl.levels, self.levels, self.splits):
             rg = F.fold_q8_decode_row_groups(kv, self.qq)
             kg = torch.zeros(lv.num_seqs, self.wl.num_kv_heads, rg, lv.max_seq_len,
                              dtype=torch.uint8, device=dev)
             bg = torch.zeros_like(kg)
+            ex = {}
+            if self.vals is not None:
+                ex["refine_v_gate_out"] = torch.zeros_like(kg)
             F.fold_q8_decode_split(kv, self.keys, self.qq, self.z, T, s, off, self.part_A,
-                                   self.part_L, key_gate_out=kg, refine_gate_out=bg)
+                                   self.part_L, key_gate_out=kg, refine_gate_out=bg,
+                                   values=self.vals, **ex)
             off += s
             nv += int(kg.sum().item())
             nb += int(bg.sum().item())
+            if ex:
+                nr += int(ex["refine_v_gate_out"].sum().item())
             total += sum(lv.seq_lens_host) * self.wl.num_kv_heads * rg
-        return nv, nb, total
+        return nv, nb, total, nr
 
 
 def model_leg(path, wl, F, torch, flush, steps, warmup):
@@ -247,14 +270,16 @@ def model_leg(path, wl, F, torch, flush, steps, warmup):
             "rel_l2_vs_dense": {"no_model": l2(plain), "request_mean": l2(model)}}
 
 
-def q8_bytes(wl, nv, nb):
+def q8_bytes(wl, nv, nb, nr=None):
     """Algorithmic bytes of one two-plane scan (all levels): plane A and the
-    scale of every key, plane B of the nb refined rows, the nv value rows,
-    the query codes, eta, tau, references, block-table entries and partials."""
+    scale of every key, plane B of the nb refined rows, the nv value rows
+    (BF16, or with ``nr`` the first E4M3 plane of nv rows and the second of
+    nr), the query codes, eta, tau, references, block-table entries and
+    partials."""
     d = wl.head_dim
     b, h, _ = wl.q.shape
     keys = sum(sum(lv.seq_lens_host) for lv in wl.levels) * wl.num_kv_heads
-    total = keys * (d + 2) + nb * d + nv * 2 * d
+    total = keys * (d + 2) + nb * d + (nv * 2 * d if nr is None else (nv + nr) * d)
     total += 2 * b * h * d + 4 * b * h + 4 * b + 4 * b * h
     if wl.page_size:
         total += 4 * sum(sum((n + wl.page_size - 1) // wl.page_size for n in lv.seq_lens_host)
@@ -292,19 +317,25 @@ def time_q8(qp, T, steps, warmup, flush, torch):
     return {k: statistics.median(v) for k, v in res.items()}
 
 
-def q8_leg(wl, F, torch, flush, steps, warmup, name=None):
-    """Timings of the two-plane key path on the benchmark workload."""
-    qp = Q8Path(wl, F, torch)
+def q8_leg(wl, F, torch, flush, steps, warmup, name=None, values8=False):
+    """Timings of the two-plane key path (with ``values8``, also 8-bit values)
+    on the benchmark workload."""
+    qp = Q8Path(wl, F, torch, values8=values8)
     stream = torch.cuda.current_stream()
     qp.split(stream)
     qp.estimate(stream)
-    out = {"kappa": qp.kappa, "cache": "two INT8 key planes + BF16 scale per key; BF16 values",
+    out = {"kappa": qp.kappa,
+           "cache": "two INT8 key planes + BF16 scale per key; " +
+                    ("two E4M3 value planes, scale 2^%d" % qp.vals.scale_exp if values8
+                     else "BF16 values"),
            "step": "query split + estimate (coarse logits) + split scan + combine; the "
                    "one-token append is timed apart"}
+    if values8:
+        out["kappa_v"] = qp.kappa_v
     for T in (math.inf, 16.0):
-        nv, nb, total = qp.read_counts(T)
+        nv, nb, total, nr = qp.read_counts(T)
         med = time_q8(qp, T, steps, warmup, flush, torch)
-        nbytes, keys = q8_bytes(wl, nv, nb)
+        nbytes, keys = q8_bytes(wl, nv, nb, nr if values8 else None)
         key = "T=inf" if math.isinf(T) else f"T={T:g}"
         out[key] = {"us_per_call": round(med["step"] * 1e3, 2),
                     "decode_us": round(med["dec"] * 1e3, 2),
@@ -314,13 +345,17 @@ def q8_leg(wl, F, torch, flush, steps, warmup, name=None):
                     "value_read_fraction": round(nv / max(total, 1), 5),
                     "refined_fraction": round(nb / max(total, 1), 5),
                     "breakdown_us": {k: round(v * 1e3, 2) for k, v in med.items()}}
+        if values8:
+            out[key]["refined_v_fraction"] = round(nr / max(total, 1), 5)
         if math.isinf(T):
             ach = nbytes / (med["dec"] * 1e-3) / 1e9
-            traffic = None if name is None else counter_traffic(name + " [two-plane keys]")[0]
+            tag = " [8-bit values]" if values8 else " [two-plane keys]"
+            traffic = None if name is None else counter_traffic(name + tag)[0]
             out["roofline"] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
                                "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
                                "traffic": None if traffic is None else int(traffic),
-                               "kernel": "decode_q8_kernel (dense)"}
+                               "kernel": "decode_q8_kernel (dense%s)"
+                                         % (", 8-bit values" if values8 else "")}
     del qp
     torch.cuda.empty_cache()
     return out
@@ -560,6 +595,8 @@ def main():
     if not args.no_q8:
         line["q8_keys"] = q8_leg(wl, F, torch, flush, args.steps, args.warmup,
                                  name=CONFIG_NAMES[args.config])
+        line["v8_values"] = q8_leg(wl, F, torch, flush, args.steps, args.warmup,
+                                   name=CONFIG_NAMES[args.config], values8=True)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(line), flush=True)
@@ -591,7 +628,9 @@ def main():
             if not args.no_q8:
                 rec = {"workload": CONFIG_NAMES[i],
                        "q8_keys": q8_leg(wl_i, F, torch, flush, args.steps, args.warmup,
-                                         name=CONFIG_NAMES[i])}
+                                         name=CONFIG_NAMES[i]),
+                       "v8_values": q8_leg(wl_i, F, torch, flush, args.steps, args.warmup,
+                                           name=CONFIG_NAMES[i], values8=True)}
                 print(json.dumps(rec), file=sys.stderr, flush=True)
             del wl_i
             torch.cuda.empty_cache()

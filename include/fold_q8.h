@@ -129,7 +129,8 @@ fold_status fold_q8_write_keys(const fold_kv_view* kv, const void* k_src, const 
  *              Both NULL: no thresholds are written.
  *   kappa      any value but NaN; +INFINITY refines every live key,
  *              -INFINITY none.  0 refines the keys whose coarse weight
- *              2^xc is at least 2^-ceil(log2 n_r), about their mean share.
+ *              2^xc is at least 2^-ceil(log2 n_r), about their mean share;
+ *              -4 (16 times that share) is the Python binding's default.
  *   kappa_v, tau_v_out: the same for the second value plane of 8-bit values
  *              (tau_v_out may be NULL; written only with req_lens).
  */

@@ -485,8 +485,8 @@ def fold_q8_write_keys(kv: KV, k_src: torch.Tensor, tok_seq: torch.Tensor, tok_p
 
 
 def fold_q8_split_query(q: torch.Tensor, sm_scale: float, out: Q8Query,
-                        req_lens: Optional[torch.Tensor] = None, kappa: float = 0.0,
-                        kappa_v: float = 0.0, stream=None) -> Q8Query:
+                        req_lens: Optional[torch.Tensor] = None, kappa: float = -4.0,
+                        kappa_v: float = -4.0, stream=None) -> Q8Query:
     qv = q_view(q)
     _need(out.planes, "planes", torch.int8)
     _need(out.eta, "eta", torch.float32)
