@@ -9,10 +9,13 @@ gating. Both the CPU oracle and the HIP path read the tensors it produces.
 
 from .synth import (  # noqa: F401
     CONFIG_NAMES,
+    DraftWorkload,
     KVView,
     Workload,
     host_bits,
     make_cascade,
     make_config,
+    chain_parents,
     make_custom,
+    make_drafts,
 )

@@ -332,3 +332,59 @@ def make_custom(*, batch: int, heads: int, kv_heads: int, dim: int, lens: List[i
                      alpha_spike=alpha_spike, n_sink=n_sink, alpha_sink=alpha_sink, seed=seed,
                      device=device, level_splits=[splits], depths=[INF, 16.0],
                      keep_logical=keep_logical)
+
+
+@dataclass
+class DraftWorkload:
+    """Draft columns over a paged cache: request r holds ``committed[r]``
+    committed keys followed by its ``m_r`` draft tokens' keys (in column
+    order); ``q`` holds one query column per draft token; ``parent[c]`` is
+    the parent column relative to the request's first column (-1: the
+    committed cache); ``spare_pages [C][pages_per_col]`` are free pages of
+    the pool reserved for each column."""
+    wl: Workload                  # the cache (its q is unused), seq_lens = committed + m
+    q: torch.Tensor               # [C, H, D] bf16
+    col_indptr: torch.Tensor      # [B + 1] int32
+    parent: torch.Tensor          # [C] int32
+    spare_pages: torch.Tensor     # [C, pages_per_col] int32
+    committed: List[int]
+
+    @property
+    def num_cols(self) -> int:
+        return int(self.q.shape[0])
+
+
+def chain_parents(m: int) -> List[int]:
+    return [-1] + list(range(m - 1))
+
+
+def make_drafts(*, committed: List[int], parents: List[List[int]], heads: int, kv_heads: int,
+                dim: int, page_size: int = 16, spike_count: int = 0, n_sink: int = 0,
+                seed: int = 0, device: str = "cpu") -> DraftWorkload:
+    """A paged cache with draft tokens appended, one query column per draft,
+    and spare pages for each column (``ceil(max m / page_size)`` each)."""
+    lens = [c + len(p) for c, p in zip(committed, parents)]
+    wl = _generate(name="drafts", batch=len(lens), heads=heads, kv_heads=kv_heads, dim=dim,
+                   lens=lens, paged=True, page_size=page_size,
+                   spike_count=lambda m: min(spike_count, max(0, m - n_sink)),
+                   alpha_spike=3.0, n_sink=n_sink, alpha_sink=6.0, seed=seed, device=device,
+                   level_splits=[1], depths=[INF, 16.0], keep_logical=True)
+    dev = torch.device(device)
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed + 7919)
+    cols = sum(len(p) for p in parents)
+    q = _bf16(torch.randn(max(cols, 1), heads, dim, generator=g, device=dev))[:cols]
+    indptr = [0]
+    for p in parents:
+        indptr.append(indptr[-1] + len(p))
+    ppc = max(1, (max((len(p) for p in parents), default=1) + page_size - 1) // page_size)
+    n_pool = wl.k.shape[0]
+    extra = cols * ppc
+    pad = torch.zeros((extra,) + tuple(wl.k.shape[1:]), dtype=wl.k.dtype, device=dev)
+    wl.k = torch.cat([wl.k, pad]).contiguous()
+    wl.v = torch.cat([wl.v, pad]).contiguous()
+    spare = (n_pool + torch.arange(extra, dtype=torch.int32, device=dev)).view(cols, ppc)
+    flat_par = [x for p in parents for x in p]
+    return DraftWorkload(wl, q, torch.tensor(indptr, dtype=torch.int32, device=dev),
+                         torch.tensor(flat_par, dtype=torch.int32, device=dev), spare,
+                         list(committed))
