@@ -240,6 +240,43 @@ fold_status fold_value_mean_append(const fold_kv_view* kv, const void* v_src,
                                    const int32_t* tok_seq, const int32_t* tok_pos,
                                    int32_t n_tok, float* mean, void* stream);
 
+/*
+ * fold_append_kv - cache append (Section 4, "Weight-gated reads": the front
+ * appends each step's new token): token t's key and value rows are stored at
+ * position tok_pos[t] of kv sequence tok_seq[t].
+ *   kv       layout of the destination cache (block table, page size, sizes;
+ *            kv->k, kv->v, seq_lens and the row lists are not read)
+ *   k_src, v_src [n_tok][num_kv_heads][head_dim] bf16, 16-byte aligned
+ *   tok_seq, tok_pos [n_tok] int32 (device).  A token whose sequence or
+ *            position the view cannot address, or whose page id is outside
+ *            [0, num_pages), is skipped.
+ *   k_cache, v_cache  the arrays written, in the view's element layout
+ *            (16-byte aligned); either may be NULL (that side is not written)
+ * Two tokens with the same destination race.  The caller extends seq_lens.
+ */
+fold_status fold_append_kv(const fold_kv_view* kv, const void* k_src, const void* v_src,
+                           const int32_t* tok_seq, const int32_t* tok_pos, int32_t n_tok,
+                           void* k_cache, void* v_cache, void* stream);
+
+/*
+ * fold_cert_update - references of the certificate's rerun (Section 3,
+ * certificate paragraph: a row outside the window is decoded again with Z
+ * set to its base-2 log-sum-exp).  For every row with nonzero cert bits
+ * (fold_combine's cert_out): z = lse where lse is finite; z - 64 where
+ * lse = -inf (sum L was 0); z + 64 where lse = +inf; a NaN lse keeps z.
+ *   cert [num_rows] u8, lse [num_rows] fp32 (fold_combine's outputs, the
+ *            latter computed with the same z)
+ *   z        [num_rows] fp32, updated in place
+ *   reruns   [num_rows] int32 or NULL: incremented for flagged rows
+ *   count_out [1] int32 (device): the number of flagged rows
+ * One workgroup.  The caller reads count_out (a synchronisation of its own)
+ * and, if it is nonzero, decodes and combines again with the updated z;
+ * rows that were not flagged keep their z and reproduce their output bit
+ * for bit.
+ */
+fold_status fold_cert_update(const uint8_t* cert, const float* lse, float* z, int32_t num_rows,
+                             int32_t* reruns, int32_t* count_out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,7 +1,7 @@
 """FoldAttention decode hot path for MI355X (gfx950).
 
 The compute path is ``libfold.so`` (hand-written HIP kernels behind the C ABI
-of ``include/fold.h`` and ``include/fold_q8.h``);
+of ``include/fold.h``, ``include/fold_q8.h`` and ``include/fold_draft.h``);
 :mod:`paper_2609_33410_amd.fold` is its ctypes
 binding.  PyTorch supplies device memory and streams only.
 """
@@ -19,9 +19,14 @@ from .fold import (  # noqa: F401
     FoldLibraryMissing,
     Q8Keys,
     Q8Query,
+    DraftViews,
     V8Values,
+    fold_append_kv,
+    fold_cert_update,
+    fold_certified_decode,
     fold_combine,
     fold_decode,
+    fold_draft_views,
     fold_decode_row_groups,
     fold_decode_rows_per_group,
     fold_decode_split,

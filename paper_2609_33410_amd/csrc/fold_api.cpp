@@ -6,10 +6,13 @@
 #include <stdio.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <string>
+#include <vector>
 
 #include "fold.h"
 #include "fold_q8.h"
+#include "fold_draft.h"
 #include "fold_internal.h"
 
 namespace {
@@ -511,6 +514,150 @@ fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* key
   a.refine_v_gate_out = dbg ? dbg->refine_v_gate_out : nullptr;
   hipError_t e = fold::launch_q8_decode(a, kv->head_dim, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(FOLD_E_HIP, "q8 decode launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_append_kv(const fold_kv_view* kv, const void* k_src, const void* v_src,
+                           const int32_t* tok_seq, const int32_t* tok_pos, int32_t n_tok,
+                           void* k_cache, void* v_cache, void* stream) {
+  if (!kv) return fail(FOLD_E_INVAL, "kv view is required");
+  if (n_tok < 0) return fail(FOLD_E_INVAL, "n_tok must be >= 0");
+  fold::AppendArgs a;
+  fold_status st = check_layout(kv, kv->num_seqs, kv->num_kv_heads, &a.geo);
+  if (st != FOLD_OK) return st;
+  if (n_tok > 0) {
+    if (!tok_seq || !tok_pos) return fail(FOLD_E_INVAL, "tok_seq and tok_pos are required");
+    if ((k_cache && !k_src) || (v_cache && !v_src))
+      return fail(FOLD_E_INVAL, "a written cache needs its source rows");
+    if ((k_cache && (!aligned16(k_cache) || !aligned16(k_src))) ||
+        (v_cache && (!aligned16(v_cache) || !aligned16(v_src))))
+      return fail(FOLD_E_INVAL, "caches and source rows must be 16-byte aligned");
+  }
+  if (static_cast<long long>(n_tok) * kv->num_kv_heads > 0x1fffffffLL)
+    return fail(FOLD_E_INVAL, "grid too large");
+  a.k_src = static_cast<const uint8_t*>(k_src);
+  a.v_src = static_cast<const uint8_t*>(v_src);
+  a.k_dst = static_cast<uint8_t*>(k_cache);
+  a.v_dst = static_cast<uint8_t*>(v_cache);
+  a.tok_seq = tok_seq;
+  a.tok_pos = tok_pos;
+  a.n_tok = (k_cache || v_cache) ? n_tok : 0;
+  a.row_bytes = 2 * kv->head_dim;
+  hipError_t e = fold::launch_append_rows(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "append launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_cert_update(const uint8_t* cert, const float* lse, float* z, int32_t num_rows,
+                             int32_t* reruns, int32_t* count_out, void* stream) {
+  if (num_rows < 0) return fail(FOLD_E_INVAL, "num_rows must be >= 0");
+  if (!count_out) return fail(FOLD_E_INVAL, "count_out is required");
+  if (num_rows > 0 && (!cert || !lse || !z))
+    return fail(FOLD_E_INVAL, "cert, lse and z are required");
+  fold::CertArgs a{cert, lse, z, reruns, count_out, num_rows};
+  hipError_t e = fold::launch_cert_update(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "certificate update launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_draft_plan(int32_t num_seqs, const int32_t* seq_lens, const int32_t* col_indptr,
+                            const int32_t* parent, int32_t page_size, int32_t pages_per_col,
+                            int32_t* committed_lens, int32_t* col_req, int32_t* col_lens,
+                            int32_t* anc_lens, int32_t* anc_pos) {
+  if (num_seqs < 0) return fail(FOLD_E_INVAL, "num_seqs must be >= 0");
+  if (page_size < 1 || pages_per_col < 1)
+    return fail(FOLD_E_INVAL, "page_size and pages_per_col must be positive");
+  if (static_cast<long long>(page_size) * pages_per_col > (1 << 20))
+    return fail(FOLD_E_INVAL, "pages_per_col * page_size too large");
+  if (!col_indptr || (num_seqs > 0 && (!seq_lens || !committed_lens)))
+    return fail(FOLD_E_INVAL, "seq_lens, col_indptr and committed_lens are required");
+  if (col_indptr[0] != 0) return fail(FOLD_E_INVAL, "col_indptr[0] must be 0");
+  for (int r = 0; r < num_seqs; ++r) {
+    const int m = col_indptr[r + 1] - col_indptr[r];
+    if (m < 0) return fail(FOLD_E_INVAL, "col_indptr decreases at request %d", r);
+    if (seq_lens[r] < m)
+      return fail(FOLD_E_INVAL, "request %d holds %d keys but has %d drafts", r, seq_lens[r], m);
+  }
+  const int cols = num_seqs > 0 ? col_indptr[num_seqs] : 0;
+  if (cols > 0 && (!parent || !col_req || !col_lens || !anc_lens || !anc_pos))
+    return fail(FOLD_E_INVAL, "parent, col_req, col_lens, anc_lens and anc_pos are required");
+  const int cap = page_size * pages_per_col;
+  for (int r = 0; r < num_seqs; ++r) {
+    const int c0 = col_indptr[r];
+    const int m = col_indptr[r + 1] - c0;
+    for (int c = 0; c < m; ++c) {
+      const int p = parent[c0 + c];
+      if (p < -1 || p >= c)
+        return fail(FOLD_E_INVAL, "parent[%d] = %d: must be in [-1, %d)", c0 + c, p, c);
+    }
+    for (int c = 0; c < m; ++c) {  // parents precede their children: every walk ends
+      int depth = 0;
+      for (int t = c; t >= 0; t = parent[c0 + t]) ++depth;
+      if (depth > cap)
+        return fail(FOLD_E_INVAL, "column %d has %d ancestors: more than the %d spare slots",
+                    c0 + c, depth, cap);
+    }
+  }
+  // every check passed: write the plan
+  std::vector<int> path;
+  for (int r = 0; r < num_seqs; ++r) {
+    const int c0 = col_indptr[r];
+    const int m = col_indptr[r + 1] - c0;
+    const int n0 = seq_lens[r] - m;
+    committed_lens[r] = n0;
+    for (int c = 0; c < m; ++c) {
+      path.clear();
+      for (int t = c; t >= 0; t = parent[c0 + t]) path.push_back(t);
+      std::sort(path.begin(), path.end());
+      const int col = c0 + c;
+      col_req[col] = r;
+      col_lens[col] = n0;
+      anc_lens[col] = static_cast<int32_t>(path.size());
+      int32_t* out = anc_pos + static_cast<size_t>(col) * cap;
+      for (int i = 0; i < cap; ++i)
+        out[i] = i < static_cast<int>(path.size()) ? n0 + path[i] : -1;
+    }
+  }
+  return ok();
+}
+
+fold_status fold_draft_gather(const fold_kv_view* kv, const int32_t* col_req,
+                              const int32_t* anc_lens, const int32_t* anc_pos,
+                              const int32_t* spare_pages, int32_t num_cols,
+                              int32_t pages_per_col, int32_t row_bytes, const void* src,
+                              void* dst, int32_t* col_block_table, void* stream) {
+  if (!kv) return fail(FOLD_E_INVAL, "kv view is required");
+  if (num_cols < 0) return fail(FOLD_E_INVAL, "num_cols must be >= 0");
+  fold::DraftGatherArgs a;
+  fold_status st = check_layout(kv, kv->num_seqs, kv->num_kv_heads, &a.geo);
+  if (st != FOLD_OK) return st;
+  if (!kv->block_table) return fail(FOLD_E_INVAL, "drafts need a paged view");
+  if (pages_per_col < 1) return fail(FOLD_E_INVAL, "pages_per_col must be positive");
+  if (static_cast<long long>(pages_per_col) * kv->page_size > (1 << 20))
+    return fail(FOLD_E_INVAL, "pages_per_col * page_size too large");
+  if (row_bytes < 1 || row_bytes > 4096)
+    return fail(FOLD_E_INVAL, "row_bytes %d: must be in [1, 4096]", row_bytes);
+  if ((src == nullptr) != (dst == nullptr))
+    return fail(FOLD_E_INVAL, "src and dst must both be set or both be NULL");
+  if (num_cols > 0 && (!col_req || !anc_lens || !anc_pos || !spare_pages))
+    return fail(FOLD_E_INVAL, "col_req, anc_lens, anc_pos and spare_pages are required");
+  const uintptr_t align = (row_bytes % 16 == 0) ? 16 : (row_bytes % 2 == 0 ? 2 : 1);
+  if (src && ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) % align))
+    return fail(FOLD_E_INVAL, "src and dst must be %zu-byte aligned", static_cast<size_t>(align));
+  if (static_cast<long long>(num_cols) * kv->num_kv_heads > 0x1fffffffLL)
+    return fail(FOLD_E_INVAL, "grid too large");
+  a.col_req = col_req;
+  a.anc_lens = anc_lens;
+  a.anc_pos = anc_pos;
+  a.spare_pages = spare_pages;
+  a.col_block_table = col_block_table;
+  a.src = static_cast<const uint8_t*>(src);
+  a.dst = static_cast<uint8_t*>(dst);
+  a.num_cols = (src || col_block_table) ? num_cols : 0;
+  a.pages_per_col = pages_per_col;
+  a.row_bytes = row_bytes;
+  hipError_t e = fold::launch_draft_gather(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "draft gather launch: %s", hipGetErrorString(e));
   return ok();
 }
 

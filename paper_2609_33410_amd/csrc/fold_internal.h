@@ -131,6 +131,41 @@ struct V8WriteArgs {
   uint8_t* vr;
 };
 
+struct AppendArgs {
+  ScanGeometry geo;       // layout of the destination cache (geo.k, geo.v unused)
+  const uint8_t* k_src;   // [n_tok][hkv][row_bytes]
+  const uint8_t* v_src;
+  uint8_t* k_dst;         // cache arrays written (either may be null)
+  uint8_t* v_dst;
+  const int32_t* tok_seq;
+  const int32_t* tok_pos;
+  int n_tok;
+  int row_bytes;          // bytes of one (token, kv head) row
+};
+
+struct CertArgs {
+  const uint8_t* cert;    // [n] certificate bits of the last decode
+  const float* lse;       // [n] base-2 log-sum-exp of the last decode
+  float* z;               // [n] references, updated in place for flagged rows
+  int32_t* reruns;        // [n] or null: incremented for flagged rows
+  int32_t* count;         // [1] number of flagged rows
+  int n;
+};
+
+struct DraftGatherArgs {
+  ScanGeometry geo;       // the requests' paged view (source layout; pool size)
+  const int32_t* col_req;      // [num_cols] request of each column
+  const int32_t* anc_lens;     // [num_cols]
+  const int32_t* anc_pos;      // [num_cols][pages_per_col * page_size] positions
+  const int32_t* spare_pages;  // [num_cols][pages_per_col]
+  int32_t* col_block_table;    // [num_cols][max_pages] or null
+  const uint8_t* src;          // pool array read (may alias dst), or null
+  uint8_t* dst;
+  int num_cols;
+  int pages_per_col;
+  int row_bytes;
+};
+
 struct Q8SplitArgs {
   const uint16_t* q;      // [rows][D] bf16
   int8_t* qp;             // [rows][2][D]
@@ -173,6 +208,9 @@ hipError_t launch_q8_write(const Q8WriteArgs& a, int head_dim, hipStream_t strea
 hipError_t launch_q8_split(const Q8SplitArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_v8_write(const V8WriteArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_estimate(const Q8EstimateArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_append_rows(const AppendArgs& a, hipStream_t stream);
+hipError_t launch_cert_update(const CertArgs& a, hipStream_t stream);
+hipError_t launch_draft_gather(const DraftGatherArgs& a, hipStream_t stream);
 
 // Rows per read group the decode kernel is instantiated for, given the rows
 // that attend one (kv sequence, kv head).

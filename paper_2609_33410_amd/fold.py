@@ -1,5 +1,5 @@
-"""ctypes binding of ``libfold.so`` (the C ABI in ``include/fold.h`` and
-``include/fold_q8.h``).
+"""ctypes binding of ``libfold.so`` (the C ABI in ``include/fold.h``,
+``include/fold_q8.h`` and ``include/fold_draft.h``).
 
 Argument marshalling only: torch tensors supply device memory and
 ``torch.cuda.current_stream()`` supplies the HIP stream; every step of the
@@ -41,6 +41,10 @@ EXPORTED = (
     "fold_q8_decode_rows_per_group",
     "fold_q8_decode_row_groups",
     "fold_q8_decode_split",
+    "fold_append_kv",
+    "fold_cert_update",
+    "fold_draft_plan",
+    "fold_draft_gather",
 )
 
 
@@ -185,6 +189,16 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_void_p, P(fold_q8_debug),
                                          ctypes.c_void_p]
+    V = ctypes.c_void_p
+    I32 = ctypes.c_int32
+    lib.fold_append_kv.restype = ctypes.c_int
+    lib.fold_append_kv.argtypes = [P(fold_kv_view), V, V, V, V, I32, V, V, V]
+    lib.fold_cert_update.restype = ctypes.c_int
+    lib.fold_cert_update.argtypes = [V, V, V, I32, V, V, V]
+    lib.fold_draft_plan.restype = ctypes.c_int
+    lib.fold_draft_plan.argtypes = [I32, V, V, V, I32, I32, V, V, V, V, V]
+    lib.fold_draft_gather.restype = ctypes.c_int
+    lib.fold_draft_gather.argtypes = [P(fold_kv_view), V, V, V, V, I32, I32, I32, V, V, V, V]
     _lib = lib
     return lib
 
@@ -397,6 +411,139 @@ def fold_decode(levels, q: torch.Tensor, z: torch.Tensor, depth_T: float, splits
     fold_combine(part_A, part_L, out, z=z if lse else None, lse_out=lse_out, cert_out=cert_out,
                  part_Lcut=part_C, mean=value_mean, stream=stream)
     return out, part_A, part_L, lse_out, cert_out
+
+
+def fold_append_kv(kv: KV, k_src: Optional[torch.Tensor], v_src: Optional[torch.Tensor],
+                   tok_seq: torch.Tensor, tok_pos: torch.Tensor, k_cache: Optional[torch.Tensor],
+                   v_cache: Optional[torch.Tensor], stream=None) -> None:
+    """Store token rows ``[n_tok, Hkv, D]`` bf16 at (``tok_seq``, ``tok_pos``)
+    of the caches laid out as ``kv`` (either cache may be None)."""
+    for t, nm in ((k_src, "k_src"), (v_src, "v_src"), (k_cache, "k_cache"), (v_cache, "v_cache")):
+        if t is not None:
+            _need(t, nm, torch.bfloat16)
+    _need(tok_seq, "tok_seq", torch.int32)
+    _need(tok_pos, "tok_pos", torch.int32)
+    _check(load_library().fold_append_kv(
+        ctypes.byref(kv.view), _ptr(k_src), _ptr(v_src), _ptr(tok_seq), _ptr(tok_pos),
+        int(tok_seq.shape[0]), _ptr(k_cache), _ptr(v_cache), _stream(stream)))
+
+
+def fold_cert_update(cert: torch.Tensor, lse: torch.Tensor, z: torch.Tensor,
+                     count: torch.Tensor, reruns: Optional[torch.Tensor] = None,
+                     stream=None) -> None:
+    """New references of the certificate's flagged rows, in place in ``z``;
+    ``count`` (int32, one element) receives how many rows were flagged."""
+    _need(cert, "cert", torch.uint8)
+    _need(lse, "lse", torch.float32)
+    _need(z, "z", torch.float32)
+    _need(count, "count", torch.int32)
+    if reruns is not None:
+        _need(reruns, "reruns", torch.int32)
+    _check(load_library().fold_cert_update(_ptr(cert), _ptr(lse), _ptr(z), int(z.numel()),
+                                           _ptr(reruns), _ptr(count), _stream(stream)))
+
+
+def fold_certified_decode(levels, q: torch.Tensor, z: torch.Tensor, depth_T: float, splits,
+                          sm_scale: float, max_reruns: int = 8, out_dtype=torch.float32,
+                          value_mean: Optional[torch.Tensor] = None, stream=None):
+    """``fold_decode`` under the range certificate: rows outside the window are
+    decoded again with their new references, at most ``max_reruns`` times
+    (each rerun reads a flag count back to the host).  Returns
+    ``(out, z_final, reruns [B, H] int32, cert [B, H] u8)``; ``z`` is not
+    modified."""
+    z = z.clone()
+    reruns = torch.zeros(z.shape, dtype=torch.int32, device=z.device)
+    count = torch.zeros(1, dtype=torch.int32, device=z.device)
+    out, _, _, lse, cert = fold_decode(levels, q, z, depth_T, splits, sm_scale, out_dtype,
+                                       lse=True, cert=True, value_mean=value_mean, stream=stream)
+    for _ in range(max_reruns):
+        fold_cert_update(cert, lse, z, count, reruns, stream=stream)
+        if int(count.item()) == 0:
+            break
+        out, _, _, lse, cert = fold_decode(levels, q, z, depth_T, splits, sm_scale, out_dtype,
+                                           lse=True, cert=True, value_mean=value_mean,
+                                           stream=stream)
+    return out, z, reruns, cert
+
+
+# ---------------------------------------------------------------- drafts ----
+@dataclass
+class DraftViews:
+    """The two levels and the estimate view of draft columns (include/fold_draft.h)."""
+    committed: KV          # requests' pages, committed lengths, columns stacked as CSR rows
+    ancestors: KV          # one kv sequence per column: its ancestors' keys
+    estimate: KV           # per-column view of the committed keys
+    num_cols: int
+    keep: tuple
+
+
+def _host_i32(x) -> torch.Tensor:
+    return torch.as_tensor(x, dtype=torch.int32).contiguous().cpu()
+
+
+def fold_draft_views(k: torch.Tensor, v: Optional[torch.Tensor], block_table: torch.Tensor,
+                     seq_lens, col_indptr, parent, spare_pages: torch.Tensor, *,
+                     num_kv_heads: int, extra=(), layout: Optional[torch.Tensor] = None,
+                     stream=None) -> DraftViews:
+    """Plan draft columns on the host (``seq_lens``, ``col_indptr`` and
+    ``parent`` are host sequences), copy each column's ancestor rows of
+    ``k``, ``v`` and every ``(array, row_bytes)`` of ``extra`` into its spare
+    pages, and return the views.  ``layout`` (a key plane) replaces ``k`` as
+    the views' shape for a two-plane cache; then ``k`` may be None."""
+    lib = load_library()
+    shape_src = layout if layout is not None else k
+    dev = shape_src.device
+    n_pool, hkv, page, d = shape_src.shape
+    sl = _host_i32(seq_lens)
+    ind = _host_i32(col_indptr)
+    par = _host_i32(parent)
+    b = int(sl.shape[0])
+    cols = int(ind[-1]) if b else 0
+    ppc = int(spare_pages.shape[1])
+    cap = ppc * page
+    committed = torch.empty(b, dtype=torch.int32)
+    col_req = torch.empty(cols, dtype=torch.int32)
+    col_lens = torch.empty(cols, dtype=torch.int32)
+    anc_lens = torch.empty(cols, dtype=torch.int32)
+    anc_pos = torch.empty(cols, cap, dtype=torch.int32)
+    _check(lib.fold_draft_plan(b, _ptr(sl), _ptr(ind), _ptr(par), page, ppc, _ptr(committed),
+                               _ptr(col_req), _ptr(col_lens), _ptr(anc_lens), _ptr(anc_pos)))
+    committed_d, col_req_d, col_lens_d = committed.to(dev), col_req.to(dev), col_lens.to(dev)
+    anc_lens_d, anc_pos_d, ind_d = anc_lens.to(dev), anc_pos.to(dev), ind.to(dev)
+    _need(spare_pages, "spare_pages", torch.int32)
+    _need(block_table, "block_table", torch.int32)
+    max_len = int(sl.max()) if b else 0
+    req_view = kv_view(shape_src, None, sl.to(dev), num_kv_heads=num_kv_heads,
+                       max_seq_len=max_len, block_table=block_table,
+                       k_is_layout_only=layout is not None)
+    col_bt = torch.empty(cols, block_table.shape[1], dtype=torch.int32, device=dev)
+    arrays = [(a, 2 * d) for a in (k, v) if a is not None] + list(extra)
+    first = True
+    for arr, row_bytes in arrays:
+        _check(lib.fold_draft_gather(ctypes.byref(req_view.view), _ptr(col_req_d), _ptr(anc_lens_d),
+                                     _ptr(anc_pos_d), _ptr(spare_pages), cols, ppc, int(row_bytes),
+                                     _ptr(arr), _ptr(arr), _ptr(col_bt) if first else None,
+                                     _stream(stream)))
+        first = False
+    if first:
+        _check(lib.fold_draft_gather(ctypes.byref(req_view.view), _ptr(col_req_d), _ptr(anc_lens_d),
+                                     _ptr(anc_pos_d), _ptr(spare_pages), cols, ppc, 2 * d, None,
+                                     None, _ptr(col_bt), _stream(stream)))
+    lay = layout is not None
+    kk = layout if lay else k
+    row_req = torch.arange(cols, dtype=torch.int32, device=dev)
+    max_m = int((ind[1:] - ind[:-1]).max()) if b else 1
+    max_committed = int(committed.max()) if b else 0
+    committed_kv = kv_view(kk, v, committed_d, num_kv_heads=num_kv_heads,
+                           max_seq_len=max_committed, block_table=block_table, row_indptr=ind_d,
+                           row_req=row_req, max_reqs_per_seq=max(1, max_m), k_is_layout_only=lay)
+    anc_kv = kv_view(kk, v, anc_lens_d, num_kv_heads=num_kv_heads, max_seq_len=cap,
+                     block_table=spare_pages, k_is_layout_only=lay)
+    est_kv = kv_view(kk, None, col_lens_d, num_kv_heads=num_kv_heads, max_seq_len=max_committed,
+                     block_table=col_bt, k_is_layout_only=lay)
+    return DraftViews(committed_kv, anc_kv, est_kv, cols,
+                      (committed_d, col_req_d, col_lens_d, anc_lens_d, anc_pos_d, ind_d, col_bt,
+                       row_req, req_view))
 
 
 def depth_value(T) -> float:

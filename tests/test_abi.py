@@ -268,3 +268,97 @@ def test_q8_row_group_queries(lib):
     assert lib.fold_q8_decode_rows_per_group(ctypes.byref(csr), ctypes.byref(q)) == 32
     assert lib.fold_q8_decode_row_groups(ctypes.byref(csr), ctypes.byref(q)) == 16
     assert lib.fold_q8_decode_row_groups(ctypes.byref(_kv(head_dim=5)), ctypes.byref(q)) == -1
+
+
+# ------------------------------------------------------------- the step ----
+def _i32(xs):
+    import torch
+    return torch.tensor(xs, dtype=torch.int32)
+
+
+def test_append_and_cert_reject_bad_args(lib):
+    kv = _kv()
+    V = ctypes.c_void_p
+    # a written cache needs its sources; tokens need their lists
+    assert lib.fold_append_kv(ctypes.byref(kv), None, None, V(FAKE), V(FAKE), 3, V(FAKE), None,
+                              None) == F.FOLD_E_INVAL
+    assert lib.fold_append_kv(ctypes.byref(kv), V(FAKE), V(FAKE), None, V(FAKE), 3, V(FAKE),
+                              V(FAKE), None) == F.FOLD_E_INVAL
+    assert lib.fold_append_kv(ctypes.byref(kv), V(FAKE + 4), V(FAKE), V(FAKE), V(FAKE), 3,
+                              V(FAKE), V(FAKE), None) == F.FOLD_E_INVAL      # misaligned
+    assert lib.fold_append_kv(ctypes.byref(_kv(head_dim=96)), V(FAKE), V(FAKE), V(FAKE), V(FAKE),
+                              3, V(FAKE), V(FAKE), None) == F.FOLD_E_INVAL
+    assert lib.fold_append_kv(ctypes.byref(kv), V(FAKE), V(FAKE), V(FAKE), V(FAKE), -1,
+                              V(FAKE), V(FAKE), None) == F.FOLD_E_INVAL
+    assert lib.fold_cert_update(V(FAKE), V(FAKE), V(FAKE), 4, None, None, None) == F.FOLD_E_INVAL
+    assert lib.fold_cert_update(None, V(FAKE), V(FAKE), 4, None, V(FAKE), None) == F.FOLD_E_INVAL
+    assert lib.fold_cert_update(V(FAKE), V(FAKE), V(FAKE), -1, None, V(FAKE),
+                                None) == F.FOLD_E_INVAL
+
+
+def _plan(lib, seq_lens, indptr, parent, page=16, ppc=1):
+    import torch
+    b = len(seq_lens)
+    cols = indptr[-1]
+    out = [torch.full((b,), -7, dtype=torch.int32)] + \
+          [torch.full((cols,), -7, dtype=torch.int32) for _ in range(3)] + \
+          [torch.full((cols, page * ppc), -7, dtype=torch.int32)]
+    sl, ind, par = _i32(seq_lens), _i32(indptr), _i32(parent if parent else [0])
+    st = lib.fold_draft_plan(b, sl.data_ptr(), ind.data_ptr(), par.data_ptr(), page, ppc,
+                             *[t.data_ptr() for t in out])
+    return st, out
+
+
+def test_draft_plan_matches_the_oracle_visible_sets(lib):
+    """The host plan's ancestor positions are the draft part of the oracle's
+    visible set for every column of a chain and two trees."""
+    from oracle import step_oracle as st_oracle
+    parents = [[-1, 0, 1, 2], [-1, 0, 0, 1, 2, 2, 3, -1], [-1]]
+    seq_lens = [40, 100, 3]
+    indptr = [0, 4, 12, 13]
+    st, (committed, col_req, col_lens, anc_lens, anc_pos) = _plan(
+        lib, seq_lens, indptr, [p for ps in parents for p in ps])
+    assert st == F.FOLD_OK
+    assert committed.tolist() == [36, 92, 2]
+    for r, ps in enumerate(parents):
+        n, m = seq_lens[r], len(ps)
+        for c in range(m):
+            col = indptr[r] + c
+            vis = st_oracle.draft_visible(n, m, ps, c)
+            anc = vis[vis >= n - m].tolist()
+            assert col_req[col] == r and col_lens[col] == n - m
+            assert anc_lens[col] == len(anc)
+            assert anc_pos[col, :len(anc)].tolist() == anc
+            assert (anc_pos[col, len(anc):] == -1).all()
+
+
+@pytest.mark.parametrize("seq_lens, indptr, parent", [
+    ([10, 10], [1, 2, 3], [-1, -1, -1]),        # col_indptr[0] != 0
+    ([10, 10], [0, 2, 1], [-1, 0]),             # decreasing
+    ([1, 10], [0, 2, 3], [-1, 0, -1]),          # more drafts than keys
+    ([10], [0, 3], [-1, 2, 0]),                 # parent not before its child
+    ([10], [0, 2], [-1, -2]),                   # parent below -1
+    ([40], [0, 17], [-1] + list(range(16))),    # 17 ancestors, 16 spare slots
+])
+def test_draft_plan_rejects_bad_trees(lib, seq_lens, indptr, parent):
+    st, outs = _plan(lib, seq_lens, indptr, parent)
+    assert st == F.FOLD_E_INVAL
+    assert all((t == -7).all() for t in outs)  # nothing written
+
+
+def test_draft_gather_rejects_bad_args(lib):
+    V = ctypes.c_void_p
+    kv = _kv()
+    args = [V(FAKE)] * 4
+    assert lib.fold_draft_gather(ctypes.byref(_kv(block_table=None)), *args, 2, 1, 256, V(FAKE),
+                                 V(FAKE), None, None) == F.FOLD_E_INVAL      # contiguous view
+    assert lib.fold_draft_gather(ctypes.byref(kv), *args, 2, 0, 256, V(FAKE), V(FAKE), None,
+                                 None) == F.FOLD_E_INVAL                    # pages_per_col
+    assert lib.fold_draft_gather(ctypes.byref(kv), *args, 2, 1, 0, V(FAKE), V(FAKE), None,
+                                 None) == F.FOLD_E_INVAL                    # row_bytes
+    assert lib.fold_draft_gather(ctypes.byref(kv), *args, 2, 1, 256, V(FAKE), None, None,
+                                 None) == F.FOLD_E_INVAL                    # src without dst
+    assert lib.fold_draft_gather(ctypes.byref(kv), *args, 2, 1, 256, V(FAKE + 2), V(FAKE), None,
+                                 None) == F.FOLD_E_INVAL                    # misaligned rows
+    assert lib.fold_draft_gather(ctypes.byref(kv), None, V(FAKE), V(FAKE), V(FAKE), 2, 1, 256,
+                                 V(FAKE), V(FAKE), None, None) == F.FOLD_E_INVAL
