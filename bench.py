@@ -377,6 +377,98 @@ def kv_bytes(wl, lam):
     return total, keys
 
 
+class DraftPath:
+    """Draft verification: ``requests`` requests of ``committed`` keys with a
+    chain of ``m`` drafts each, one query column per draft (Llama-3-8B GQA
+    heads).  A step is the per-column estimate, the committed level (every
+    committed key read once for all of a request's columns), the ancestor
+    level and the combine; the plan and the row gather run once (they
+    belong to the append).  The baseline decodes every column as a request
+    of its own (its committed keys plus its chain), reading the committed
+    keys once per column."""
+
+    def __init__(self, F, torch, requests=32, committed=4096, m=4, splits=4):
+        from workloads import chain_parents, make_drafts
+        self.F, self.torch = F, torch
+        dw = make_drafts(committed=[committed] * requests, parents=[chain_parents(m)] * requests,
+                         heads=32, kv_heads=8, dim=128, spike_count=committed // 100, n_sink=4,
+                         seed=1, device="cuda")
+        self.dw, wl = dw, dw.wl
+        fl = wl.flat
+        self.dv = F.fold_draft_views(wl.k, wl.v, fl.block_table, fl.seq_lens_host,
+                                     dw.col_indptr.cpu().tolist(), dw.parent.cpu().tolist(),
+                                     dw.spare_pages, num_kv_heads=8)
+        c = dw.num_cols
+        self.splits = [splits, 1]
+        self.z = torch.empty(c, 32, dtype=torch.float32, device="cuda")
+        self.pa = torch.empty(splits + 1, c, 32, 128, dtype=torch.float32, device="cuda")
+        self.pl = torch.empty(splits + 1, c, 32, dtype=torch.float32, device="cuda")
+        self.out = torch.empty(c, 32, 128, dtype=torch.float32, device="cuda")
+        self.qv = F.q_view(dw.q)
+        # baseline: column c of a chain is its request truncated at n0 + c + 1 keys
+        col_req = self.dv.keep[1]
+        lens = torch.tensor([committed + (i % m) + 1 for i in range(c)], dtype=torch.int32,
+                            device="cuda")
+        self.base_kv = F.kv_view(wl.k, wl.v, lens, num_kv_heads=8, max_seq_len=committed + m,
+                                 block_table=fl.block_table.index_select(0, col_req.long()))
+        self.base_pa = torch.empty(splits, c, 32, 128, dtype=torch.float32, device="cuda")
+        self.base_pl = torch.empty(splits, c, 32, dtype=torch.float32, device="cuda")
+        self.base_z = torch.empty(c, 32, dtype=torch.float32, device="cuda")
+        self.keys = requests * committed * 8
+        torch.cuda.synchronize()
+
+    def step(self, T, stream):
+        F = self.F
+        F.fold_ref_estimate(self.dv.estimate, self.qv, self.dw.wl.sm_scale, self.z, stream=stream)
+        F.fold_decode_split(self.dv.committed, self.qv, self.dw.wl.sm_scale, self.z, T,
+                            self.splits[0], 0, self.pa, self.pl, stream=stream)
+        F.fold_decode_split(self.dv.ancestors, self.qv, self.dw.wl.sm_scale, self.z, T, 1,
+                            self.splits[0], self.pa, self.pl, stream=stream)
+        F.fold_combine(self.pa, self.pl, self.out, stream=stream)
+
+    def baseline(self, T, stream):
+        F = self.F
+        F.fold_ref_estimate(self.base_kv, self.qv, self.dw.wl.sm_scale, self.base_z,
+                            stream=stream)
+        F.fold_decode_split(self.base_kv, self.qv, self.dw.wl.sm_scale, self.base_z, T,
+                            self.splits[0], 0, self.base_pa, self.base_pl, stream=stream)
+        F.fold_combine(self.base_pa, self.base_pl, self.out, stream=stream)
+
+
+def drafts_leg(F, torch, flush, steps, warmup):
+    """Draft verification timings (chains of 2 and 4 drafts, 32 requests of
+    4096 committed keys)."""
+    out = {"workload": "32 requests x 4096 committed keys, GQA 32/8, D=128, chains of drafts",
+           "step": "estimate + committed level + ancestor level + combine",
+           "baseline": "every column decoded as its own request (estimate + scan + combine)"}
+    stream = torch.cuda.current_stream()
+    for m in (2, 4):
+        dp = DraftPath(F, torch, m=m)
+        rec = {}
+        for T in (math.inf, 16.0):
+            times = {"drafts": [], "per_column": []}
+            for it in range(warmup + steps):
+                for name, fn in (("drafts", dp.step), ("per_column", dp.baseline)):
+                    evict_caches(flush)
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    fn(T, stream)
+                    e1.record(stream)
+                    if it >= warmup:
+                        e1.synchronize()
+                        times[name].append(e0.elapsed_time(e1))
+            med = {k: statistics.median(v) for k, v in times.items()}
+            rec["T=inf" if math.isinf(T) else f"T={T:g}"] = {
+                "drafts_us": round(med["drafts"] * 1e3, 2),
+                "per_column_us": round(med["per_column"] * 1e3, 2),
+                "speedup": round(med["per_column"] / med["drafts"], 3)}
+        out[f"chain{m}"] = rec
+        del dp
+        torch.cuda.empty_cache()
+    return out
+
+
 def evict_caches(flush):
     """Read (not write) a 1 GiB buffer: every cache line of the step's data is
     evicted, and no dirty line is left to be written back during the step."""
@@ -597,6 +689,8 @@ def main():
                                  name=CONFIG_NAMES[args.config])
         line["v8_values"] = q8_leg(wl, F, torch, flush, args.steps, args.warmup,
                                    name=CONFIG_NAMES[args.config], values8=True)
+    if args.all:
+        line["drafts"] = drafts_leg(F, torch, flush, args.steps, args.warmup)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(line), flush=True)

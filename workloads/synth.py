@@ -361,8 +361,9 @@ def chain_parents(m: int) -> List[int]:
 def make_drafts(*, committed: List[int], parents: List[List[int]], heads: int, kv_heads: int,
                 dim: int, page_size: int = 16, spike_count: int = 0, n_sink: int = 0,
                 seed: int = 0, device: str = "cpu") -> DraftWorkload:
-    """A paged cache with draft tokens appended, one query column per draft,
-    and spare pages for each column (``ceil(max m / page_size)`` each)."""
+    """A paged cache with draft tokens appended, one query column per draft
+    (its request's query row plus N(0, 1/9) noise), and spare pages for each
+    column (``ceil(max m / page_size)`` each)."""
     lens = [c + len(p) for c, p in zip(committed, parents)]
     wl = _generate(name="drafts", batch=len(lens), heads=heads, kv_heads=kv_heads, dim=dim,
                    lens=lens, paged=True, page_size=page_size,
@@ -373,7 +374,12 @@ def make_drafts(*, committed: List[int], parents: List[List[int]], heads: int, k
     g = torch.Generator(device=dev)
     g.manual_seed(seed + 7919)
     cols = sum(len(p) for p in parents)
-    q = _bf16(torch.randn(max(cols, 1), heads, dim, generator=g, device=dev))[:cols]
+    # a column's query is its request's query plus noise of a third of its
+    # scale: consecutive tokens' queries share the request's spike direction
+    base = torch.cat([wl.q[r:r + 1].float().expand(len(p), -1, -1)
+                      for r, p in enumerate(parents)]) if cols else wl.q[:0].float()
+    noise = torch.randn(max(cols, 1), heads, dim, generator=g, device=dev)[:cols]
+    q = _bf16(base + noise / 3.0)
     indptr = [0]
     for p in parents:
         indptr.append(indptr[-1] + len(p))
