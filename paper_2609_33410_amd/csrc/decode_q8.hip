@@ -40,6 +40,7 @@ namespace fold {
 namespace {
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 // C += A . B on a 16x16 tile with K = 64 INT8 (v_mfma_i32_16x16x64_i8); lane l
 // holds 16 bytes of row l%16 of A and of column l%16 of B; C as the BF16 tiles.
@@ -104,7 +105,7 @@ struct Q8AStage {
 template <int D, int RB, bool DENSE, bool V8>
 struct Q8BStage {
   Q8Loc loc;
-  uint32_t sc;
+  float e[4];       // BF16 scales of keys 4(l/16)+i
   u32x4 kb[D / 64];
   u32x4 vv[DENSE ? 1 : kValueLoads<D, V8>];
   u32x4 vr[V8 ? D / 64 : 1];  // second value plane (8-bit values)
@@ -214,8 +215,7 @@ struct Q8Scan {
     const int key0 = c * kChunk;
     const int nk = c < p.nchunks ? min(kChunk, p.n - key0) : 0;
     s.loc = in.loc;
-    s.sc = in.sc;
-    float e[4];
+    float (&e)[4] = s.e;
     scales(in.sc, e);
     uint32_t lv = 0, rf = 0, rv = 0;
 #pragma unroll
@@ -306,17 +306,16 @@ struct Q8Scan {
     }
   }
 
-  // acc += V^T P^T over the staged tile (hi and residual weights).
+  // acc += V^T P^T over the staged tile (hi and residual weights).  The V^T
+  // operand is one transposing LDS read per 16 channels: lane 4i + a of each
+  // 16-lane group points at channels 16 blk + 4a .. +4 of key 4(l/16) + i, and
+  // lane l receives channel 16 blk + l%16 of those four keys.
   __device__ __forceinline__ void product(const u32x2 (&phi)[RB], const u32x2 (&plo)[RB]) {
-    const unsigned char* col = vt + (4 * grp) * VSTRIDE + 2 * n16;
+    const unsigned char* src = vt + (4 * grp + (n16 >> 2)) * VSTRIDE + 8 * (n16 & 3);
 #pragma unroll
     for (int blk = 0; blk < NB; ++blk) {
-      const unsigned char* ep = col + 32 * blk;
-      const uint32_t v0 = *reinterpret_cast<const uint16_t*>(ep);
-      const uint32_t v1 = *reinterpret_cast<const uint16_t*>(ep + VSTRIDE);
-      const uint32_t v2 = *reinterpret_cast<const uint16_t*>(ep + 2 * VSTRIDE);
-      const uint32_t v3 = *reinterpret_cast<const uint16_t*>(ep + 3 * VSTRIDE);
-      const u32x2 va = {v0 | (v1 << 16), v2 | (v3 << 16)};
+      const u32x2 va = __builtin_bit_cast(
+          u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(src + 32 * blk)));
 #pragma unroll
       for (int b = 0; b < RB; ++b) {
         acc[b][blk] = mfma_16x16x16(va, phi[b], acc[b][blk]);
@@ -329,9 +328,8 @@ struct Q8Scan {
   __device__ __forceinline__ void finish(int c, const BS& s, const u32x4 (&vv)[NK]) {
     const int key0 = c * kChunk;
     const int nk = c < p.nchunks ? min(kChunk, p.n - key0) : 0;
-    float e[4];
-    scales(s.sc, e);
-    u32x2 phi[RB], plo[RB], phi2[RB], plo2[RB];
+    const float (&e)[4] = s.e;
+    u32x2 phi[RB], plo[RB];
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
       i32x4 cba = {0, 0, 0, 0}, cbb = {0, 0, 0, 0};
@@ -342,8 +340,8 @@ struct Q8Scan {
           cbb = mfma_i8(s.kb[c2], qb[b][c2], cbb);
         }
       }
-      uint32_t hi[4], hi2[4];
-      float res[4], res2[4];
+      uint32_t hi[4];
+      float res[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const bool ok = rok[b] && 4 * grp + i < nk;
@@ -359,16 +357,10 @@ struct Q8Scan {
         const float pw = live ? w : 0.0f;
         hi[i] = __float_as_uint(pw) & 0xffff0000u;
         res[i] = pw - __uint_as_float(hi[i]);
-        // the second value plane counts only where this row's group read it
-        const bool rv = V8 && ((s.refv >> (4 * b + i)) & 1u);
-        hi2[i] = rv ? hi[i] : 0u;
-        res2[i] = rv ? res[i] : 0.0f;
         if (DBG && a.d.x_out && ok) a.d.x_out[xrow[b] * g.max_seq_len + key0 + 4 * grp + i] = x;
       }
       phi[b] = u32x2{(hi[0] >> 16) | hi[1], (hi[2] >> 16) | hi[3]};
       plo[b] = u32x2{pack_bf16_rne(res[0], res[1]), pack_bf16_rne(res[2], res[3])};
-      phi2[b] = u32x2{(hi2[0] >> 16) | hi2[1], (hi2[2] >> 16) | hi2[3]};
-      plo2[b] = u32x2{pack_bf16_rne(res2[0], res2[1]), pack_bf16_rne(res2[2], res2[3])};
     }
     if (s.vmask == 0) return;  // wave-uniform: no live key in the chunk
     stage(vv, 1.0f);
@@ -377,6 +369,17 @@ struct Q8Scan {
       // second plane (r / 16) of the keys some group of the read group refined;
       // the tile is wave-private and its reads above precede these writes
       if (s.rvmask) {
+        // the second plane counts only where this row's own group read it:
+        // keep the 16-bit weight halves of keys 4(l/16)+i with refv bit 4b+i
+        u32x2 phi2[RB], plo2[RB];
+#pragma unroll
+        for (int b = 0; b < RB; ++b) {
+          const uint32_t rv = s.refv >> (4 * b);
+          const u32x2 m = {((rv & 1u) ? 0x0000FFFFu : 0u) | ((rv & 2u) ? 0xFFFF0000u : 0u),
+                           ((rv & 4u) ? 0x0000FFFFu : 0u) | ((rv & 8u) ? 0xFFFF0000u : 0u)};
+          phi2[b] = u32x2{phi[b].x & m.x, phi[b].y & m.y};
+          plo2[b] = u32x2{plo[b].x & m.x, plo[b].y & m.y};
+        }
         stage(s.vr, 0.0625f);
         product(phi2, plo2);
       }

@@ -17,11 +17,12 @@
 //
 // Latency, not bandwidth, bounds this kernel (48 KiB per (request, kv head) at
 // D = 128).  Scores come from the matrix cores, 16 samples x 16 rows per
-// v_mfma_f32_16x16x32_bf16 (the decode scan's layout); every lane issues the
-// block-table reads of all its samples at once and then all their key loads,
-// so scoring costs two memory round trips.  The trim sorts the centre scores
-// with a bitonic network across the wave; wave reductions use DPP and
-// v_readlane.  Every sum has a fixed order, so the result is deterministic.
+// v_mfma_f32_16x16x32_bf16 (the decode scan's layout); every lane computes its
+// samples' key indices, issues their block-table reads at once and then all
+// their key loads, so scoring costs two memory round trips (the query load
+// overlaps the first).  The trim sorts the centre scores with a bitonic
+// network across the wave whose exchanges are DPP moves within rows of 16
+// lanes; wave reductions use DPP and v_readlane.  Every sum has a fixed order, so the result is deterministic.
 #include "fold_device.h"
 #include "fold_internal.h"
 
@@ -35,6 +36,95 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 // BF16 keys (Q8 = false): scores from the BF16 cache.  Two-plane INT8 keys
 // (Q8 = true): the kernel's coarse logits eta_i e_j (a_j . qa_i + a_j . qb_i / 256)
 // from plane A and the scales (Section 3 estimates from coarse logits).
+// Lane-xor exchange: the partner lane's value.  XOR 1, 2, 3, 7 and 15 are one
+// DPP move (quad permutations, row half-mirror, row mirror), 4 and 8 two;
+// partners in another row of 16 lanes go through the LDS crossbar.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+
+template <int L>
+__device__ __forceinline__ float lane_xor(float v) {
+  if constexpr (L == 1) return dpp_f<0xB1>(v);
+  else if constexpr (L == 2) return dpp_f<0x4E>(v);
+  else if constexpr (L == 3) return dpp_f<0x1B>(v);
+  else if constexpr (L == 4) return dpp_f<0x1B>(dpp_f<0x141>(v));
+  else if constexpr (L == 7) return dpp_f<0x141>(v);
+  else if constexpr (L == 8) return dpp_f<0x141>(dpp_f<0x140>(v));
+  else if constexpr (L == 15) return dpp_f<0x140>(v);
+  else return __shfl_xor(v, L, 64);
+}
+
+__device__ __forceinline__ void sort_pair(float& v0, float& v1) {
+  const float lo = fminf(v0, v1), hi = fmaxf(v0, v1);
+  v0 = lo;
+  v1 = hi;
+}
+
+// One compare-exchange stage of the sorting network on elements e = 2 lane + u:
+// element e meets e ^ (2L + 1) (FLIP: the mirror image within a block) or
+// e ^ 2L; the lower element keeps the minimum.
+template <int L, bool FLIP>
+__device__ __forceinline__ void net_stage(float& v0, float& v1, int lane) {
+  const float p0 = lane_xor<L>(v0), p1 = lane_xor<L>(v1);
+  const float a0 = FLIP ? p1 : p0;
+  const float a1 = FLIP ? p0 : p1;
+  constexpr int hb = FLIP ? (L + 1) / 2 : L;  // highest bit where lane and partner differ
+  const bool keep_min = (lane & hb) == 0;
+  v0 = keep_min ? fminf(v0, a0) : fmaxf(v0, a0);
+  v1 = keep_min ? fminf(v1, a1) : fmaxf(v1, a1);
+}
+
+// Ascending sort of 128 values held two per lane (element 2 lane + u): a
+// bitonic network in its mirror form, so that every comparator keeps the
+// minimum at the lower index and each block merge starts with a flip.
+__device__ __forceinline__ void sort128(float& v0, float& v1, int lane) {
+  sort_pair(v0, v1);
+  net_stage<1, true>(v0, v1, lane);
+  sort_pair(v0, v1);
+  net_stage<3, true>(v0, v1, lane);
+  net_stage<1, false>(v0, v1, lane);
+  sort_pair(v0, v1);
+  net_stage<7, true>(v0, v1, lane);
+  net_stage<2, false>(v0, v1, lane);
+  net_stage<1, false>(v0, v1, lane);
+  sort_pair(v0, v1);
+  net_stage<15, true>(v0, v1, lane);
+  net_stage<4, false>(v0, v1, lane);
+  net_stage<2, false>(v0, v1, lane);
+  net_stage<1, false>(v0, v1, lane);
+  sort_pair(v0, v1);
+  net_stage<31, true>(v0, v1, lane);
+  net_stage<8, false>(v0, v1, lane);
+  net_stage<4, false>(v0, v1, lane);
+  net_stage<2, false>(v0, v1, lane);
+  net_stage<1, false>(v0, v1, lane);
+  sort_pair(v0, v1);
+  net_stage<63, true>(v0, v1, lane);
+  net_stage<16, false>(v0, v1, lane);
+  net_stage<8, false>(v0, v1, lane);
+  net_stage<4, false>(v0, v1, lane);
+  net_stage<2, false>(v0, v1, lane);
+  net_stage<1, false>(v0, v1, lane);
+  sort_pair(v0, v1);
+}
+
+// Key index of sample t of a row of n keys (the sink, the recent keys, then
+// the stratum centres; every key when the row is short).
+__device__ __forceinline__ int sample_index(int t, int n, bool stratified, int sink, int recent,
+                                            int strata, long long rmid) {
+  if (!stratified || t < sink) return t;
+  if (t < sink + recent) return n - recent + (t - sink);
+  // floor(b r / strata) in double: b r < 2^53 is exact, and a quotient that is
+  // not an integer sits at least 1/strata above its floor, far more than the
+  // division's rounding error.
+  const int b = t - sink - recent;
+  const int lo = sink + static_cast<int>(floor(static_cast<double>(b) * rmid / strata));
+  const int hi = sink + static_cast<int>(floor(static_cast<double>(b + 1) * rmid / strata));
+  return (lo + hi - 1) / 2;
+}
+
 template <int D, bool Q8>
 __global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs qa8) {
   const EstimateArgs& a = qa8.e;
@@ -49,7 +139,6 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs
   const int G = g.group;
 
   __shared__ float sc[kMaxEstRows][kMaxEstSamples];
-  __shared__ int sidx[kMaxEstSamples];
 
   int n = 0;
   if (req < g.num_seqs) n = clamp_len(ld_uniform(g.seq_lens, req), view_capacity(g));
@@ -89,27 +178,6 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs
     if (n16 < G) eta_r = qa8.eta[static_cast<size_t>(req) * g.heads + kvh * G + n16];
   }
 
-  for (int t = threadIdx.x; t < m; t += kThreads) {
-    int j;
-    if (!stratified) {
-      j = t;
-    } else if (t < a.sink) {
-      j = t;
-    } else if (t < a.sink + a.recent) {
-      j = n - a.recent + (t - a.sink);
-    } else {
-      // floor(b r / strata) in double: b r < 2^53 is exact, and a quotient that
-      // is not an integer sits at least 1/strata above its floor, far more than
-      // the division's rounding error.
-      const int b = t - a.sink - a.recent;
-      const int lo = a.sink + static_cast<int>(floor(static_cast<double>(b) * rmid / a.strata));
-      const int hi = a.sink + static_cast<int>(floor(static_cast<double>(b + 1) * rmid / a.strata));
-      j = (lo + hi - 1) / 2;
-    }
-    sidx[t] = j;
-  }
-  __syncthreads();
-
   // Tiles of 16 samples; wave w scores tiles w, w+4, ...; lane l loads sample l%16.
   const int ntiles = (m + 15) / 16;
   for (int tau0 = wave; tau0 < ntiles; tau0 += kScanWavesEst * kTilesPerPass) {
@@ -117,7 +185,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs
 #pragma unroll
     for (int u = 0; u < kTilesPerPass; ++u) {
       const int t = 16 * (tau0 + kScanWavesEst * u) + n16;
-      jb[u] = sidx[t < m ? t : m - 1];
+      jb[u] = sample_index(t < m ? t : m - 1, n, stratified, a.sink, a.recent, a.strata, rmid);
     }
     int phys[kTilesPerPass];
 #pragma unroll
@@ -213,29 +281,13 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs
       const float* cs = &sc[r][a.sink + a.recent];
       float kept = 0.0f;
       if (a.strata <= 128) {
-        // Bitonic sort of the (at most 128) centre scores across the wave, two
-        // per lane (element e = 2 * lane + u), padded with +inf; sorted
-        // positions [trim_lo, strata - trim_hi) are kept.  A fixed network:
-        // the kept multiset, hence the sum, does not depend on tie order.
+        // Sort the (at most 128) centre scores across the wave, two per lane
+        // (element e = 2 * lane + u), padded with +inf; sorted positions
+        // [trim_lo, strata - trim_hi) are kept.  A fixed network: the kept
+        // multiset, hence the sum, does not depend on tie order.
         float v0 = 2 * lane < a.strata ? cs[2 * lane] : INFINITY;
         float v1 = 2 * lane + 1 < a.strata ? cs[2 * lane + 1] : INFINITY;
-        for (int k = 2; k <= 128; k <<= 1) {
-          for (int j = k >> 1; j >= 1; j >>= 1) {
-            const bool asc = ((2 * lane) & k) == 0;  // both elements of a lane share it
-            if (j == 1) {
-              const float lo = fminf(v0, v1), hi = fmaxf(v0, v1);
-              v0 = asc ? lo : hi;
-              v1 = asc ? hi : lo;
-            } else {
-              const int d = j >> 1;  // partner lane = lane ^ d
-              const float p0 = __shfl_xor(v0, d, 64);
-              const float p1 = __shfl_xor(v1, d, 64);
-              const bool keep_min = ((lane & d) == 0) == asc;
-              v0 = keep_min ? fminf(v0, p0) : fmaxf(v0, p0);
-              v1 = keep_min ? fminf(v1, p1) : fmaxf(v1, p1);
-            }
-          }
-        }
+        sort128(v0, v1, lane);
         const int hi_pos = a.strata - a.trim_hi;
         const int e0 = 2 * lane, e1 = 2 * lane + 1;
         if (e0 >= a.trim_lo && e0 < hi_pos) kept += exp2_fast(v0 - mx);
