@@ -50,7 +50,7 @@ __device__ __forceinline__ i32x4 mfma_i8(u32x4 a, u32x4 b, i32x4 c) {
 }
 
 __device__ __forceinline__ uint32_t buf_load2(rsrc_t r, uint32_t off) {
-  return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+  return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, kStreamPolicy);
 }
 
 // Where a 16-key chunk lives: its first key row in the cache's element
