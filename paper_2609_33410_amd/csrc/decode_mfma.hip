@@ -42,12 +42,6 @@ struct MfmaScan {
   static constexpr int NB = D / 16;           // 16-channel blocks of the value product
   static constexpr int VSTRIDE = 2 * D + 16;  // bytes per key row of the LDS value tile
   static constexpr int R = 16 * RB;           // rows per read group
-  // Key loads stream non-temporally in the dense scan.  The gated scan keeps
-  // the default policy for keys: its key-only stream measured 12 % slower
-  // with the non-temporal bit (51.6 against 57.9 us on the Llama-3-8B-shaped
-  // workload at T = 16), while the dense stream of keys and values is 11 %
-  // faster with it.
-  static constexpr int kKeyPolicy = DENSE ? kStreamPolicy : 0;
 
   const DecodeArgs& a;
   const ScanGeometry& g;
@@ -66,10 +60,27 @@ struct MfmaScan {
 
   __device__ MfmaScan(const DecodeArgs& a_) : a(a_), g(a_.geo) {}
 
+  // Keys load as whole lines: lane l, load c takes the 16 bytes at
+  // 1024 c + 16 l of the chunk (key (1024 c + 16 l) / 2D).  kstage() turns
+  // them into the QK A operand through the wave's LDS tile.
   __device__ __forceinline__ void kload(rsrc_t r, u32x4 (&kv)[NK]) const {
-    // lane l: key l%16, channels 32c + 8(l/16) .. +8  (the QK A operand)
 #pragma unroll
-    for (int c = 0; c < NK; ++c) kv[c] = buf_load<kKeyPolicy>(r, n16 * (2 * D) + 64 * c + 16 * grp);
+    for (int c = 0; c < NK; ++c) kv[c] = buf_load(r, 1024u * c + 16u * lane);
+  }
+
+  // The QK A operand (lane l: key l%16, channels 32c + 8(l/16) .. +8) from a
+  // chunk loaded by kload(), through the wave's tile (rows padded to VSTRIDE
+  // bytes, so the 16 rows of one read fall in distinct banks).
+  __device__ __forceinline__ void kstage(const u32x4 (&kv)[NK], u32x4 (&ka)[NK]) const {
+#pragma unroll
+    for (int c = 0; c < NK; ++c) {
+      const uint32_t off = 1024u * c + 16u * lane;
+      const uint32_t key = off / (2 * D);
+      *reinterpret_cast<u32x4*>(vt + key * VSTRIDE + (off - key * 2 * D)) = kv[c];
+    }
+#pragma unroll
+    for (int c = 0; c < NK; ++c)
+      ka[c] = *reinterpret_cast<const u32x4*>(vt + n16 * VSTRIDE + 64 * c + 16 * grp);
   }
 
   __device__ __forceinline__ void vload(rsrc_t r, uint32_t mask, u32x4 (&vv)[NK]) const {
@@ -89,11 +100,13 @@ struct MfmaScan {
     const int key0 = c * kChunk;
     const int nk = c < p.nchunks ? min(kChunk, p.n - key0) : 0;
     uint64_t any[4] = {0, 0, 0, 0};
+    u32x4 ka[NK];
+    kstage(kv, ka);
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
       f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int c2 = 0; c2 < NK; ++c2) s = mfma_qk(kv[c2], qb[b][c2], s);
+      for (int c2 = 0; c2 < NK; ++c2) s = mfma_qk(ka[c2], qb[b][c2], s);
       uint32_t hi[4], lo[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -337,7 +350,11 @@ hipError_t launch_mfma_d(const DecodeArgs& a, unsigned blocks, hipStream_t strea
 
 }  // namespace
 
+hipError_t launch_decode_packed(const DecodeArgs& a, int head_dim, hipStream_t stream);
+
 hipError_t launch_decode_mfma(const DecodeArgs& a, int head_dim, hipStream_t stream) {
+  // at most eight rows per kv sequence: several chunks per score pass
+  if (a.rows_per_seq <= 8) return launch_decode_packed(a, head_dim, stream);
   const long long blocks = static_cast<long long>(a.geo.num_seqs) * a.geo.hkv * a.num_splits *
                            a.row_groups;
   if (blocks == 0) return hipSuccess;
