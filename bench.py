@@ -289,7 +289,8 @@ def q8_bytes(wl, nv, nb, nr=None):
 
 
 def time_q8(qp, T, steps, warmup, flush, torch):
-    """Median per-kernel and per-step durations (ms) of the two-plane step."""
+    """Median per-kernel and per-step durations (ms) of the two-plane step
+    (the step timed on its own, as in time_variant)."""
     stream = torch.cuda.current_stream()
     res = {"split": [], "est": [], "dec": [], "comb": [], "step": [], "append": []}
     for it in range(warmup + steps):
@@ -312,8 +313,20 @@ def time_q8(qp, T, steps, warmup, flush, torch):
             res["est"].append(ev[1].elapsed_time(ev[2]))
             res["dec"].append(ev[2].elapsed_time(ev[3]))
             res["comb"].append(ev[3].elapsed_time(ev[4]))
-            res["step"].append(ev[0].elapsed_time(ev[4]))
             res["append"].append(ev[4].elapsed_time(ev[5]))
+    for it in range(warmup + steps):
+        evict_caches(flush)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        qp.split(stream)
+        qp.estimate(stream)
+        qp.decode(T, stream)
+        qp.combine(stream)
+        e1.record(stream)
+        if it >= warmup:
+            e1.synchronize()
+            res["step"].append(e0.elapsed_time(e1))
     return {k: statistics.median(v) for k, v in res.items()}
 
 
@@ -477,9 +490,15 @@ def evict_caches(flush):
 
 def time_variant(path, T, steps, warmup, flush, torch):
     """Median per-kernel and per-step durations (ms) with a cache eviction
-    before every step; events are recorded on the launch stream."""
+    before every step; events are recorded on the launch stream.
+
+    The step is timed on its own, with events only before and after it: an
+    event recorded between two kernels adds a queue marker that lengthens the
+    step (by about 3.5 us each on MI355X).  The per-kernel breakdown comes
+    from separate steps with events between the kernels; its parts add up to
+    more than the step."""
     stream = torch.cuda.current_stream()
-    res = {"est": [], "dec": [], "comb": [], "step": []}
+    res = {"est": [], "dec": [], "comb": [], "step": [], "step_with_markers": []}
     for it in range(warmup + steps):
         evict_caches(flush)
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
@@ -495,7 +514,19 @@ def time_variant(path, T, steps, warmup, flush, torch):
             res["est"].append(ev[0].elapsed_time(ev[1]))
             res["dec"].append(ev[1].elapsed_time(ev[2]))
             res["comb"].append(ev[2].elapsed_time(ev[3]))
-            res["step"].append(ev[0].elapsed_time(ev[3]))
+            res["step_with_markers"].append(ev[0].elapsed_time(ev[3]))
+    for it in range(warmup + steps):
+        evict_caches(flush)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        path.estimate(stream)
+        path.decode(T, stream)
+        path.combine(stream)
+        e1.record(stream)
+        if it >= warmup:
+            e1.synchronize()
+            res["step"].append(e0.elapsed_time(e1))
     torch.cuda.synchronize()
     return {k: statistics.median(v) for k, v in res.items()}, res
 
@@ -661,8 +692,10 @@ def main():
                    "head_dim": wl.head_dim, "keys_per_request": wl.flat.seq_lens_host[0],
                    "page_size": wl.page_size, "splits": wl.level_splits,
                    "step": "estimate + split scan + combine at T=inf, launched on one stream",
-                   "timing": "median over steps of HIP events around the step on its stream; "
-                             "a 1 GiB read before each step evicts all caches"},
+                   "timing": "median over steps of HIP events around the step on its stream "
+                             "(no event inside the step); a 1 GiB read before each step evicts "
+                             "all caches; the breakdown comes from separate steps with events "
+                             "between the kernels"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": None if traffic is None else int(traffic),
