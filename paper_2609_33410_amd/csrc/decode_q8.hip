@@ -34,60 +34,10 @@
 // next chunks is in flight in a ring of four (at a finite depth chunks t+2 ..
 // t+5; in dense decode, where every value row is requested with plane A,
 // chunks t+1 .. t+3).
-#include "decode_common.h"
+#include "q8_common.h"
 
 namespace fold {
 namespace {
-
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-
-// C += A . B on a 16x16 tile with K = 64 INT8 (v_mfma_i32_16x16x64_i8); lane l
-// holds 16 bytes of row l%16 of A and of column l%16 of B; C as the BF16 tiles.
-__device__ __forceinline__ i32x4 mfma_i8(u32x4 a, u32x4 b, i32x4 c) {
-  return __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, a),
-                                               __builtin_bit_cast(i32x4, b), c, 0, 0, 0);
-}
-
-__device__ __forceinline__ uint32_t buf_load2(rsrc_t r, uint32_t off) {
-  return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, kStreamPolicy);
-}
-
-// Where a 16-key chunk lives: its first key row in the cache's element
-// layout and its number of keys (0 past the sequence end or for a page id
-// outside [0, num_pages)).  Buffer resources are built from it at each use,
-// so a chunk in flight holds three scalar registers, not four resources.
-struct Q8Loc {
-  size_t row;
-  uint32_t nk;
-};
-
-// Page of 16-key chunk c: pshift = log2(page_size / 16) when that is a power
-// of two (a shift), else -1 (a division).
-__device__ __forceinline__ int chunk_page_of(const ScanGeometry& g, int c, int pshift) {
-  return pshift >= 0 ? c >> pshift : (c * kChunk) / g.page_size;
-}
-
-// Where chunk c lives, given its block-table entry phys (ignored for a
-// contiguous view).
-__device__ __forceinline__ Q8Loc q8_loc(const ScanGeometry& g, const ScanPlace& p, int c,
-                                        int phys, int pshift) {
-  Q8Loc l{0, 0};
-  if (c < p.nchunks) {
-    const int key0 = c * kChunk;
-    bool ok = true;
-    if (g.page_size > 0) {
-      const int page = chunk_page_of(g, c, pshift);
-      ok = phys >= 0 && phys < g.num_pages;
-      l.row = (static_cast<size_t>(ok ? phys : 0) * g.hkv + p.kvh) * g.page_size +
-              (key0 - page * g.page_size);
-    } else {
-      l.row = (static_cast<size_t>(p.seq) * g.hkv + p.kvh) * g.max_seq_len + key0;
-    }
-    if (ok) l.nk = static_cast<uint32_t>(min(kChunk, p.n - key0));
-  }
-  return l;
-}
 
 // 16-byte value loads per lane and chunk: BF16 rows, or one E4M3 plane.
 template <int D, bool V8>
@@ -580,7 +530,11 @@ hipError_t launch_q8_d(const Q8DecodeArgs& a, unsigned blocks, hipStream_t strea
 
 }  // namespace
 
+hipError_t launch_q8_decode_packed(const Q8DecodeArgs& a, int head_dim, hipStream_t stream);
+
 hipError_t launch_q8_decode(const Q8DecodeArgs& a, int head_dim, hipStream_t stream) {
+  // gated scans of at most eight rows per kv sequence: several chunks per pass
+  if (!a.d.dense && a.d.rows_per_seq <= 8) return launch_q8_decode_packed(a, head_dim, stream);
   const long long blocks = static_cast<long long>(a.d.geo.num_seqs) * a.d.geo.hkv *
                            a.d.num_splits * a.d.row_groups;
   if (blocks == 0) return hipSuccess;
