@@ -482,6 +482,19 @@ def drafts_leg(F, torch, flush, steps, warmup):
     return out
 
 
+def progress(msg):
+    """One line on stderr as each leg ends (long runs under a profiler stay
+    visibly alive)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def scan_kernel_name(wl):
+    """The scan kernel the library launches for a single-level workload."""
+    if wl.group == 1:
+        return "decode_split_kernel"
+    return "decode_packed_kernel" if wl.group <= 8 else "decode_mfma_kernel"
+
+
 def evict_caches(flush):
     """Read (not write) a 1 GiB buffer: every cache line of the step's data is
     evicted, and no dirty line is left to be written back during the step."""
@@ -645,6 +658,7 @@ def run_workload(i, args, torch, F, make_config, flush, steps, warmup, splits=No
         graph_ms = time_graph(path, T, steps, warmup, flush, torch)
         nbytes, keys = kv_bytes(wl, lam)
         out[T] = {"med": med, "graph": graph_ms, "lam": lam, "bytes": nbytes, "keys": keys}
+        progress(f"workload {i} T={T:g}: step {med['step'] * 1e3:.1f} us")
     return wl, out
 
 
@@ -699,7 +713,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": None if traffic is None else int(traffic),
-                     "kernel": "decode_mfma_kernel" if wl.group > 1 else "decode_split_kernel",
+                     "kernel": scan_kernel_name(wl),
                      "algorithmic_bytes_per_launch": int(dense["bytes"]),
                      "avg_launch_us": round(dec_ms * 1e3, 2),
                      "launch_timing": "HIP events around the eager launch on its stream"},
@@ -717,13 +731,17 @@ def main():
     }
     line["value_model"] = model_leg(Path(wl, F, torch), wl, F, torch, flush, args.steps,
                                     args.warmup)
+    progress("value model leg done")
     if not args.no_q8:
         line["q8_keys"] = q8_leg(wl, F, torch, flush, args.steps, args.warmup,
                                  name=CONFIG_NAMES[args.config])
+        progress("two-plane key leg done")
         line["v8_values"] = q8_leg(wl, F, torch, flush, args.steps, args.warmup,
                                    name=CONFIG_NAMES[args.config], values8=True)
+        progress("8-bit value leg done")
     if args.all:
         line["drafts"] = drafts_leg(F, torch, flush, args.steps, args.warmup)
+        progress("draft leg done")
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(line), flush=True)

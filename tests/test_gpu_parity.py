@@ -202,6 +202,18 @@ def test_stacked_rows_cascade(d, requests, prefix, splits, shallow):
         _full_parity(wl, T)
 
 
+@pytest.mark.parametrize("heads,kv_heads,requests", [(4, 2, 2), (8, 2, 2), (4, 1, 2), (2, 1, 3)])
+def test_small_stacked_groups(heads, kv_heads, requests):
+    """Prefix levels of 4 to 8 stacked rows: the GQA groups (of 2 or 4 rows) of
+    two or three requests share the row lanes of one packed chunk, so their
+    verdicts, read bits and sums must stay apart."""
+    wl = make_cascade(requests=requests, heads=heads, kv_heads=kv_heads, dim=128,
+                      prefix_len=720, suffix_len=48, splits=(3, 1),
+                      seed=heads + kv_heads + requests, device="cuda")
+    for T in (INF, 16.0, 6.0):
+        _full_parity(wl, T)
+
+
 def test_stacked_rows_two_kv_heads():
     """Eight heads on two kv heads with 24 requests: 96 stacked rows per (prefix, kv head)."""
     wl = make_cascade(requests=24, heads=8, kv_heads=2, dim=128, prefix_len=784, suffix_len=32,

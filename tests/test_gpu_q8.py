@@ -280,6 +280,18 @@ def test_q8_cascade_stacked_rows(requests, prefix, splits):
         _full_parity(wl, T)
 
 
+@pytest.mark.parametrize("heads,kv_heads,requests", [(4, 2, 2), (8, 2, 2), (2, 1, 3)])
+def test_q8_small_stacked_groups(heads, kv_heads, requests):
+    """Prefix levels of 4 to 8 stacked rows: two or three requests' GQA groups
+    share the row lanes of one packed chunk; the refine and value verdicts are
+    per group, the read bits per read group."""
+    wl = make_cascade(requests=requests, heads=heads, kv_heads=kv_heads, dim=128,
+                      prefix_len=720, suffix_len=48, splits=(3, 1),
+                      seed=heads + kv_heads + requests, device="cuda")
+    for T in (INF, 16.0, 6.0):
+        _full_parity(wl, T)
+
+
 # ------------------------------------------------------- invariants ---------
 @pytest.mark.parametrize("T", [INF, 16.0])
 def test_q8_debug_exports_do_not_change_results(T):
