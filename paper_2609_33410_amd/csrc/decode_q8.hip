@@ -533,8 +533,8 @@ hipError_t launch_q8_d(const Q8DecodeArgs& a, unsigned blocks, hipStream_t strea
 hipError_t launch_q8_decode_packed(const Q8DecodeArgs& a, int head_dim, hipStream_t stream);
 
 hipError_t launch_q8_decode(const Q8DecodeArgs& a, int head_dim, hipStream_t stream) {
-  // gated scans of at most eight rows per kv sequence: several chunks per pass
-  if (!a.d.dense && a.d.rows_per_seq <= 8) return launch_q8_decode_packed(a, head_dim, stream);
+  // at most eight rows per kv sequence: several chunks per pass
+  if (a.d.rows_per_seq <= 8) return launch_q8_decode_packed(a, head_dim, stream);
   const long long blocks = static_cast<long long>(a.d.geo.num_seqs) * a.d.geo.hkv *
                            a.d.num_splits * a.d.row_groups;
   if (blocks == 0) return hipSuccess;

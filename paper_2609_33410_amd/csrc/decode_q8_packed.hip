@@ -1,5 +1,5 @@
-// Gated split-KV decode over a two-plane INT8 key cache for read groups of at
-// most eight query rows (Section 4, "Cache format", "Weight-gated reads",
+// Split-KV decode over a two-plane INT8 key cache for read groups of at most
+// eight query rows, at any depth (Section 4, "Cache format", "Weight-gated reads",
 // "Value product", "Depth as a dial"; Algorithm 1 with BF16 or 8-bit values).
 //
 // The arithmetic is the two-plane scan's (decode_q8.hip): coarse scores from
@@ -50,7 +50,7 @@ constexpr int kDppRowShl = 0x100;   // row_shl:n = 0x100 + n (lane i reads lane 
 constexpr int kDppRowShr = 0x110;   // row_shr:n = 0x110 + n (lane i reads lane i - n)
 constexpr int kDppIdentity = 0xE4;  // quad_perm [0, 1, 2, 3]
 
-template <int D, int PK, bool DBG, bool V8>
+template <int D, int PK, bool DENSE, bool DBG, bool V8>
 struct Q8Packed {
   static constexpr int NKI = D / 64;               // plane loads per lane per chunk
   static constexpr int NKV = V8 ? D / 64 : D / 32;  // value loads per lane per chunk
@@ -111,6 +111,18 @@ struct Q8Packed {
     }
   }
 
+  // Dense decode: every value row of a step's chunks (or the first E4M3
+  // plane), requested together with its plane A.
+  __device__ __forceinline__ void issue_v(const Q8Loc (&loc)[PK], u32x4 (&V)[PK][NKV]) const {
+#pragma unroll
+    for (int q = 0; q < PK; ++q) {
+      const rsrc_t rv = V8 ? make_rsrc(a.vp + loc[q].row * D, loc[q].nk * D)
+                           : make_rsrc(g.v + loc[q].row * D, loc[q].nk * D * 2);
+#pragma unroll
+      for (int i = 0; i < NKV; ++i) V[q][i] = buf_load(rv, 1024u * i + 16u * lane);
+    }
+  }
+
   // Plane-B rows of refined keys and value rows of live keys (and, 8-bit
   // values, second-plane rows of refine-V keys) of the scored step.
   __device__ __forceinline__ void issue_bv(const Q8Loc (&loc)[PK], u32x4 (&B)[PK][NKI],
@@ -125,7 +137,7 @@ struct Q8Packed {
           B[q][i] = buf_load(rb, ((bm[q] >> (off / D)) & 1u) ? off : kOutOfRange);
         }
       }
-      if (vm[q]) {
+      if (!DENSE && vm[q]) {  // dense decode: requested with plane A
         constexpr uint32_t kRowBytes = V8 ? D : 2 * D;
         const rsrc_t rv = V8 ? make_rsrc(a.vp + loc[q].row * D, loc[q].nk * D)
                              : make_rsrc(g.v + loc[q].row * D, loc[q].nk * D * 2);
@@ -206,7 +218,7 @@ struct Q8Packed {
       const float x = __builtin_fmaf(etap * e[i], t, -zp);
       xc[i] = ok ? x : -INFINITY;
       if (ok) okb |= 1u << i;
-      if (ok && x >= a.d.neg_T) lv |= 1u << i;
+      if (ok && (DENSE || x >= a.d.neg_T)) lv |= 1u << i;
       if (ok && x >= ntaup) rf |= 1u << i;
       if (V8 && ok && x >= ntauvp) rv |= 1u << i;
       if (DBG && a.xc_out && ok) a.xc_out[prow * g.max_seq_len + cl * kChunk + 4 * grp + i] = x;
@@ -332,7 +344,7 @@ struct Q8Packed {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const float x = dpp_movf<from_packed<Q>(), banks<0>()>(-INFINITY, xs[i]);
-      const float pw = x >= a.d.neg_T ? exp2_fast(x) : 0.0f;
+      const float pw = DENSE || x >= a.d.neg_T ? exp2_fast(x) : 0.0f;
       hi[i] = __float_as_uint(pw) & 0xffff0000u;
       res[i] = pw - __uint_as_float(hi[i]);
     }
@@ -373,10 +385,9 @@ struct Q8Packed {
     const int cl = chunk_of(step, slot);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const bool live = x[i] >= a.d.neg_T;
       const float w = exp2_fast(x[i]);
       lsum += w;
-      lcut += live ? 0.0f : w;
+      if (!DENSE) lcut += x[i] >= a.d.neg_T ? 0.0f : w;
       if (DBG && a.d.x_out && ((okl >> i) & 1u))
         a.d.x_out[prow * g.max_seq_len + cl * kChunk + 4 * grp + i] = x[i];
     }
@@ -391,10 +402,10 @@ struct Q8Packed {
   }
 };
 
-template <int D, int PK, bool DBG, bool V8>
+template <int D, int PK, bool DENSE, bool DBG, bool V8>
 __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void decode_q8_packed_kernel(const Q8DecodeArgs a) {
-  using S = Q8Packed<D, PK, DBG, V8>;
+  using S = Q8Packed<D, PK, DENSE, DBG, V8>;
   constexpr int NKI = S::NKI;
   constexpr int NKV = S::NKV;
   constexpr int kTileBytes = kScanWaves * 16 * S::VSTRIDE;
@@ -448,27 +459,58 @@ void decode_q8_packed_kernel(const Q8DecodeArgs a) {
   u32x4 A0[PK][NKI], A1[PK][NKI];
   uint32_t sc0, sc1;
   Q8Loc l0[PK], l1[PK];
-  sc.issue_a(0, A0, sc0, l0);
-  sc.issue_a(1, A1, sc1, l1);
-  // Step j: coarse pass (plane A of j), its plane-B and value requests, plane
-  // A of step j+2 into the freed set, then refine and products of step j.
-  // The requests of step j precede plane A of step j+2, so waiting for them
-  // leaves that load in flight.
-  for (int j = 0; j < steps; j += 2) {
-    {
-      u32x4 B[PK][NKI], V[PK][NKV], R[PK][V8 ? D / 64 : 1];
-      sc.coarse(j, A0, sc0);
-      sc.issue_bv(l0, B, V, R);
-      sc.issue_a(j + 2, A0, sc0, l0);
-      sc.finish(j, B, V, R);
+  if constexpr (DENSE) {
+    // Step j: coarse pass (plane A of j), its plane-B (and refine-V) requests,
+    // plane A of step j+2 into the freed set, refine and products of step j
+    // (values of j, requested with its plane A two steps earlier), then the
+    // values of step j+2 into the freed value set.
+    u32x4 V0[PK][NKV], V1[PK][NKV];
+    sc.issue_a(0, A0, sc0, l0);
+    sc.issue_v(l0, V0);
+    sc.issue_a(1, A1, sc1, l1);
+    sc.issue_v(l1, V1);
+    for (int j = 0; j < steps; j += 2) {
+      {
+        u32x4 B[PK][NKI], R[PK][V8 ? D / 64 : 1];
+        sc.coarse(j, A0, sc0);
+        sc.issue_bv(l0, B, V0, R);
+        sc.issue_a(j + 2, A0, sc0, l0);
+        sc.finish(j, B, V0, R);
+        sc.issue_v(l0, V0);
+      }
+      if (j + 1 >= steps) break;
+      {
+        u32x4 B[PK][NKI], R[PK][V8 ? D / 64 : 1];
+        sc.coarse(j + 1, A1, sc1);
+        sc.issue_bv(l1, B, V1, R);
+        sc.issue_a(j + 3, A1, sc1, l1);
+        sc.finish(j + 1, B, V1, R);
+        sc.issue_v(l1, V1);
+      }
     }
-    if (j + 1 >= steps) break;
-    {
-      u32x4 B[PK][NKI], V[PK][NKV], R[PK][V8 ? D / 64 : 1];
-      sc.coarse(j + 1, A1, sc1);
-      sc.issue_bv(l1, B, V, R);
-      sc.issue_a(j + 3, A1, sc1, l1);
-      sc.finish(j + 1, B, V, R);
+  } else {
+    sc.issue_a(0, A0, sc0, l0);
+    sc.issue_a(1, A1, sc1, l1);
+    // Step j: coarse pass (plane A of j), its plane-B and value requests,
+    // plane A of step j+2 into the freed set, then refine and products of
+    // step j.  The requests of step j precede plane A of step j+2, so waiting
+    // for them leaves that load in flight.
+    for (int j = 0; j < steps; j += 2) {
+      {
+        u32x4 B[PK][NKI], V[PK][NKV], R[PK][V8 ? D / 64 : 1];
+        sc.coarse(j, A0, sc0);
+        sc.issue_bv(l0, B, V, R);
+        sc.issue_a(j + 2, A0, sc0, l0);
+        sc.finish(j, B, V, R);
+      }
+      if (j + 1 >= steps) break;
+      {
+        u32x4 B[PK][NKI], V[PK][NKV], R[PK][V8 ? D / 64 : 1];
+        sc.coarse(j + 1, A1, sc1);
+        sc.issue_bv(l1, B, V, R);
+        sc.issue_a(j + 3, A1, sc1, l1);
+        sc.finish(j + 1, B, V, R);
+      }
     }
   }
 
@@ -518,27 +560,30 @@ void decode_q8_packed_kernel(const Q8DecodeArgs a) {
   }
 }
 
-template <int D, int PK, bool V8>
+template <int D, int PK, bool DENSE, bool V8>
 hipError_t launch_qp(const Q8DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
   if (dbg)
-    hipLaunchKernelGGL((decode_q8_packed_kernel<D, PK, true, V8>), dim3(blocks),
+    hipLaunchKernelGGL((decode_q8_packed_kernel<D, PK, DENSE, true, V8>), dim3(blocks),
                        dim3(kScanThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL((decode_q8_packed_kernel<D, PK, false, V8>), dim3(blocks),
+    hipLaunchKernelGGL((decode_q8_packed_kernel<D, PK, DENSE, false, V8>), dim3(blocks),
                        dim3(kScanThreads), 0, stream, a);
   return hipGetLastError();
 }
 
 template <int D, int PK>
 hipError_t launch_qp_v(const Q8DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
-  return a.vp ? launch_qp<D, PK, true>(a, dbg, blocks, stream)
-              : launch_qp<D, PK, false>(a, dbg, blocks, stream);
+  if (a.d.dense)
+    return a.vp ? launch_qp<D, PK, true, true>(a, dbg, blocks, stream)
+                : launch_qp<D, PK, true, false>(a, dbg, blocks, stream);
+  return a.vp ? launch_qp<D, PK, false, true>(a, dbg, blocks, stream)
+              : launch_qp<D, PK, false, false>(a, dbg, blocks, stream);
 }
 
 }  // namespace
 
-// Gated two-plane scan of read groups of at most eight rows (one read group
-// per kv sequence and head).
+// Two-plane scan of read groups of at most eight rows (one read group per kv
+// sequence and head), at any depth.
 hipError_t launch_q8_decode_packed(const Q8DecodeArgs& a, int head_dim, hipStream_t stream) {
   const long long blocks = static_cast<long long>(a.d.geo.num_seqs) * a.d.geo.hkv * a.d.num_splits;
   if (blocks == 0) return hipSuccess;
