@@ -644,6 +644,49 @@ def cpu_baseline(wl, budget_s):
                       f"calls in {dt:.1f} s, scaled to one call"}
 
 
+def paired_depths(path, steps, warmup, flush, torch, T_cut=16.0):
+    """Paired rounds: each round times one T=inf step and one T=T_cut step
+    (order alternating by round, caches evicted before each); returns the
+    medians of the per-round ratios (step and scan) and p10/p90 of the
+    steps (ms)."""
+    stream = torch.cuda.current_stream()
+    ratios_step, ratios_dec = [], []
+    steps_inf, steps_cut = [], []
+    for it in range(warmup + steps):
+        t = {}
+        order = (math.inf, T_cut) if it % 2 == 0 else (T_cut, math.inf)
+        for T in order:
+            evict_caches(flush)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ev[0].record(stream)
+            path.estimate(stream)
+            path.decode(T, stream)
+            path.combine(stream)
+            ev[1].record(stream)
+            evict_caches(flush)
+            ed = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ed[0].record(stream)
+            path.decode(T, stream)
+            ed[1].record(stream)
+            ed[1].synchronize()
+            t[T] = (ev[0].elapsed_time(ev[1]), ed[0].elapsed_time(ed[1]))
+        if it >= warmup:
+            ratios_step.append(t[math.inf][0] / t[T_cut][0])
+            ratios_dec.append(t[math.inf][1] / t[T_cut][1])
+            steps_inf.append(t[math.inf][0])
+            steps_cut.append(t[T_cut][0])
+
+    def pct(v, q):
+        v = sorted(v)
+        return v[min(len(v) - 1, max(0, int(round(q * (len(v) - 1)))))]
+
+    return {"rounds": steps, "T": T_cut,
+            "speedup_step_median": round(statistics.median(ratios_step), 3),
+            "speedup_decode_median": round(statistics.median(ratios_dec), 3),
+            "step_us_inf_p10_p50_p90": [round(pct(steps_inf, q) * 1e3, 2) for q in (0.1, 0.5, 0.9)],
+            "step_us_T_p10_p50_p90": [round(pct(steps_cut, q) * 1e3, 2) for q in (0.1, 0.5, 0.9)]}
+
+
 def run_workload(i, args, torch, F, make_config, flush, steps, warmup, splits=None):
     wl = make_config(i, device="cuda")
     if splits is not None and len(wl.level_splits) == 1:
@@ -726,6 +769,7 @@ def main():
         "t16_value_read_fraction": round(t16["lam"], 5),
         "t16_speedup_decode": round(dense["med"]["dec"] / t16["med"]["dec"], 3),
         "t16_speedup_step": round(dense["med"]["step"] / t16["med"]["step"], 3),
+        "t16_paired": paired_depths(Path(wl, F, torch), max(args.steps, 21), 1, flush, torch),
         "keys_per_s": round(dense["keys"] / (step_ms * 1e-3), 1),
         "wall_s": round(wall, 2),
     }
