@@ -176,6 +176,12 @@ class Q8Path:
     def estimate(self, stream):
         self.F.fold_q8_ref_estimate(self.flat, self.keys, self.qq, self.z, stream=stream)
 
+    def front(self, stream):
+        """Query split and reference estimate in one launch (fold_q8_front)."""
+        self.F.fold_q8_front(self.flat, self.keys, self.wl.q, self.wl.sm_scale, self.qq, self.z,
+                             req_lens=self.wl.flat.seq_lens, kappa=self.kappa,
+                             kappa_v=self.kappa_v, stream=stream)
+
     def decode(self, T, stream):
         off = 0
         for kv, s in zip(self.levels, self.splits):
@@ -290,43 +296,47 @@ def q8_bytes(wl, nv, nb, nr=None):
 
 def time_q8(qp, T, steps, warmup, flush, torch):
     """Median per-kernel and per-step durations (ms) of the two-plane step
-    (the step timed on its own, as in time_variant)."""
+    (the step timed on its own, as in time_variant).  The step is the fused
+    front (query split + estimate in one launch), the scan and the combine;
+    ``split_then_est`` times the same step with the split and the estimate
+    as two launches."""
     stream = torch.cuda.current_stream()
-    res = {"split": [], "est": [], "dec": [], "comb": [], "step": [], "append": []}
+    res = {"front": [], "dec": [], "comb": [], "step": [], "append": [], "split_then_est": []}
     for it in range(warmup + steps):
         evict_caches(flush)
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
         ev[0].record(stream)
-        qp.split(stream)
+        qp.front(stream)
         ev[1].record(stream)
-        qp.estimate(stream)
+        qp.decode(T, stream)
         ev[2].record(stream)
-        qp.decode(T, stream)
+        qp.combine(stream)
         ev[3].record(stream)
-        qp.combine(stream)
-        ev[4].record(stream)
         qp.append(stream)
-        ev[5].record(stream)
+        ev[4].record(stream)
         if it >= warmup:
-            ev[5].synchronize()
-            res["split"].append(ev[0].elapsed_time(ev[1]))
-            res["est"].append(ev[1].elapsed_time(ev[2]))
-            res["dec"].append(ev[2].elapsed_time(ev[3]))
-            res["comb"].append(ev[3].elapsed_time(ev[4]))
-            res["append"].append(ev[4].elapsed_time(ev[5]))
+            ev[4].synchronize()
+            res["front"].append(ev[0].elapsed_time(ev[1]))
+            res["dec"].append(ev[1].elapsed_time(ev[2]))
+            res["comb"].append(ev[2].elapsed_time(ev[3]))
+            res["append"].append(ev[3].elapsed_time(ev[4]))
     for it in range(warmup + steps):
-        evict_caches(flush)
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        qp.split(stream)
-        qp.estimate(stream)
-        qp.decode(T, stream)
-        qp.combine(stream)
-        e1.record(stream)
-        if it >= warmup:
-            e1.synchronize()
-            res["step"].append(e0.elapsed_time(e1))
+        for key, fused in (("step", True), ("split_then_est", False)):
+            evict_caches(flush)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            if fused:
+                qp.front(stream)
+            else:
+                qp.split(stream)
+                qp.estimate(stream)
+            qp.decode(T, stream)
+            qp.combine(stream)
+            e1.record(stream)
+            if it >= warmup:
+                e1.synchronize()
+                res[key].append(e0.elapsed_time(e1))
     return {k: statistics.median(v) for k, v in res.items()}
 
 
@@ -335,14 +345,13 @@ def q8_leg(wl, F, torch, flush, steps, warmup, name=None, values8=False):
     on the benchmark workload."""
     qp = Q8Path(wl, F, torch, values8=values8)
     stream = torch.cuda.current_stream()
-    qp.split(stream)
-    qp.estimate(stream)
+    qp.front(stream)
     out = {"kappa": qp.kappa,
            "cache": "two INT8 key planes + BF16 scale per key; " +
                     ("two E4M3 value planes, scale 2^%d" % qp.vals.scale_exp if values8
                      else "BF16 values"),
-           "step": "query split + estimate (coarse logits) + split scan + combine; the "
-                   "one-token append is timed apart"}
+           "step": "front (query split + estimate from coarse logits, one launch) + split "
+                   "scan + combine; the one-token append is timed apart"}
     if values8:
         out["kappa_v"] = qp.kappa_v
     for T in (math.inf, 16.0):

@@ -163,6 +163,24 @@ fold_status fold_q8_ref_estimate(const fold_kv_view* kv, const fold_q8_keys* key
                                  const fold_q8_query* q, const fold_est_params* params,
                                  float* z_out, void* stream);
 
+/*
+ * fold_q8_front - the per-step front of a two-plane key cache in one launch
+ * (the paper fuses the query quantisation and the reference estimate into
+ * one front kernel; Section 4, "Cache format"; Section 3, "Choosing the
+ * reference"): the result of fold_q8_split_query(q, kv->head_dim, sm_scale,
+ * req_lens, kappa, kappa_v, planes_out, eta_out, tau_out, tau_v_out)
+ * followed by fold_q8_ref_estimate(kv, keys, {planes_out, eta_out, tau_out,
+ * q->batch, q->num_heads, tau_v_out}, params, z_out), bit for bit.
+ *   kv, keys   the per-request view of the cache (no CSR rows) and its planes
+ *   q          bf16 query rows [batch][num_heads][kv->head_dim], 16-byte aligned
+ *   other arguments and outputs: as those two calls.  Errors: as those two
+ *   calls; the GQA group must be at most 16 rows.
+ */
+fold_status fold_q8_front(const fold_kv_view* kv, const fold_q8_keys* keys, const fold_q_view* q,
+                          float sm_scale, const int32_t* req_lens, float kappa, float kappa_v,
+                          int8_t* planes_out, float* eta_out, float* tau_out, float* tau_v_out,
+                          const fold_est_params* params, float* z_out, void* stream);
+
 /* Rows per read group (16 or 32) and read groups per (kv sequence, kv head)
  * of fold_q8_decode_split; -1 on an invalid view.  The GQA group size
  * num_heads / num_kv_heads must be 1, 2, 4, 8, 16 or 32, so that every read

@@ -33,6 +33,7 @@ from .fold import (  # noqa: F401
     fold_q8_decode_row_groups,
     fold_q8_decode_rows_per_group,
     fold_q8_decode_split,
+    fold_q8_front,
     fold_q8_ref_estimate,
     fold_q8_split_query,
     fold_q8_write_keys,

@@ -451,6 +451,56 @@ fold_status fold_q8_ref_estimate(const fold_kv_view* kv, const fold_q8_keys* key
   return ok();
 }
 
+fold_status fold_q8_front(const fold_kv_view* kv, const fold_q8_keys* keys, const fold_q_view* q,
+                          float sm_scale, const int32_t* req_lens, float kappa, float kappa_v,
+                          int8_t* planes_out, float* eta_out, float* tau_out, float* tau_v_out,
+                          const fold_est_params* params, float* z_out, void* stream) {
+  if (!q || !q->q) return fail(FOLD_E_INVAL, "q view with query rows is required");
+  if (!planes_out || !eta_out) return fail(FOLD_E_INVAL, "planes_out and eta_out are required");
+  if ((req_lens == nullptr) != (tau_out == nullptr))
+    return fail(FOLD_E_INVAL, "req_lens and tau_out must both be set or both be NULL");
+  if (tau_v_out && !req_lens) return fail(FOLD_E_INVAL, "tau_v_out needs req_lens");
+  if (!isfinite(sm_scale)) return fail(FOLD_E_INVAL, "sm_scale must be finite");
+  if (isnan(kappa) || isnan(kappa_v)) return fail(FOLD_E_INVAL, "kappa and kappa_v must not be NaN");
+  if (!aligned16(q->q)) return fail(FOLD_E_INVAL, "q must be 16-byte aligned");
+  const fold_q8_query codes{planes_out, eta_out, tau_out, q->batch, q->num_heads, tau_v_out};
+  fold::Q8EstimateArgs a{};
+  fold_status st = check_q8_view(kv, keys, &codes, &a.e.geo, false);
+  if (st != FOLD_OK) return st;
+  if (!z_out) return fail(FOLD_E_INVAL, "z_out is required");
+  if (kv->row_indptr) return fail(FOLD_E_INVAL, "the estimate needs a per-request view (no CSR rows)");
+  if (a.e.geo.group > fold::kMaxEstRows)
+    return fail(FOLD_E_UNSUPPORTED, "GQA group %d exceeds %d", a.e.geo.group, fold::kMaxEstRows);
+  fold_est_params p;
+  st = check_est_params(params, &p);
+  if (st != FOLD_OK) return st;
+  if (static_cast<long long>(q->batch) * kv->num_kv_heads > 0x7fffffffLL)
+    return fail(FOLD_E_INVAL, "grid too large");
+  a.e.q = nullptr;
+  a.e.z_out = z_out;
+  a.e.score_scale = 0.0f;
+  a.e.sink = p.sink;
+  a.e.recent = p.recent;
+  a.e.strata = p.strata;
+  a.e.trim_lo = p.trim_lo;
+  a.e.trim_hi = p.trim_hi;
+  a.keys = {keys->plane_a, keys->plane_b, keys->scale};
+  a.qp = planes_out;
+  a.eta = eta_out;
+  a.q_src = static_cast<const uint16_t*>(q->q);
+  a.qp_out = planes_out;
+  a.eta_out = eta_out;
+  a.sm_scale = sm_scale;
+  a.req_lens = req_lens;
+  a.tau = tau_out;
+  a.tau_v = tau_v_out;
+  a.kappa = kappa;
+  a.kappa_v = kappa_v;
+  hipError_t e = fold::launch_q8_front(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "q8 front launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* keys,
                                  const fold_q8_query* q, const fold_v8_values* values,
                                  const float* z, float depth_T, int32_t num_splits,

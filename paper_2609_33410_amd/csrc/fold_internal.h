@@ -185,6 +185,18 @@ struct Q8EstimateArgs {
   Q8Keys keys;
   const int8_t* qp;
   const float* eta;
+  // Fused front (the query split in the same launch; q_src non-NULL): the
+  // codes of each (request, kv head)'s rows are computed from q_src, written
+  // to qp_out / eta_out and scored from LDS; the thresholds as Q8SplitArgs.
+  const uint16_t* q_src;  // [batch][heads][D] bf16
+  int8_t* qp_out;         // [batch][heads][2][D]
+  float* eta_out;         // [batch][heads]
+  float sm_scale;
+  const int32_t* req_lens;
+  float* tau;
+  float* tau_v;
+  float kappa;
+  float kappa_v;
 };
 
 // Keys a kv sequence of this view can hold: max_seq_len, and for a paged view
@@ -202,6 +214,7 @@ hipError_t launch_decode(const DecodeArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_estimate(const EstimateArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_q8_decode(const Q8DecodeArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_q8_front(const Q8EstimateArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_value_mean(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_value_mean_append(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_write(const Q8WriteArgs& a, int head_dim, hipStream_t stream);

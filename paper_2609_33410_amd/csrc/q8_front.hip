@@ -16,61 +16,20 @@
 // inputs is exact while the inputs of one vector span at most 38 binades, so
 // the codes do not depend on the order of the butterflies.  Division, rint and
 // the rounded-up scale are exact IEEE FP64 operations.
-#include "fold_device.h"
 #include "fold_internal.h"
+#include "q8_split.h"
 
 namespace fold {
 namespace {
 
 constexpr int kFrontThreads = 256;
 constexpr int kWavesPerBlock = kFrontThreads / 64;
-constexpr double kLog2e = 0x1.71547652b82fep+0;
-
-template <int D>
-__device__ __forceinline__ void hadamard_wave(double (&x)[D / 64], int lane) {
-#pragma unroll
-  for (int s = 1; s < 64; s <<= 1) {
-#pragma unroll
-    for (int i = 0; i < D / 64; ++i) {
-      const double o = __shfl_xor(x[i], s, 64);
-      x[i] = (lane & s) ? o - x[i] : x[i] + o;
-    }
-  }
-  if constexpr (D == 128) {
-    const double u = x[0], v = x[1];
-    x[0] = u + v;
-    x[1] = u - v;
-  }
-}
-
-template <int D>
-__device__ __forceinline__ double wave_absmax_f64(const double (&x)[D / 64]) {
-  double m = 0.0;
-#pragma unroll
-  for (int i = 0; i < D / 64; ++i) m = fmax(m, fabs(x[i]));
-#pragma unroll
-  for (int s = 32; s >= 1; s >>= 1) m = fmax(m, __shfl_xor(m, s, 64));
-  return m;
-}
 
 // Smallest value with 8 significant bits (a BF16 significand) >= t, t > 0 normal.
 __device__ __forceinline__ double ceil_to_bf16(double t) {
   constexpr unsigned long long kLow = (1ull << 45) - 1;
   const unsigned long long u = static_cast<unsigned long long>(__double_as_longlong(t));
   return __longlong_as_double(static_cast<long long>((u + kLow) & ~kLow));
-}
-
-__device__ __forceinline__ void split_value(double x, double s, int8_t* a, int8_t* b) {
-  if (s > 0.0) {
-    const double y = x / s;
-    const double ai = rint(y);
-    const double bi = fmin(fmax(rint(256.0 * (y - ai)), -128.0), 127.0);
-    *a = static_cast<int8_t>(ai);
-    *b = static_cast<int8_t>(bi);
-  } else {
-    *a = 0;
-    *b = 0;
-  }
 }
 
 template <int D>
@@ -140,7 +99,7 @@ __global__ __launch_bounds__(kFrontThreads) void q8_split_kernel(const Q8SplitAr
     dst[D + 64 * i + lane] = qb;
   }
   if (lane == 0)
-    a.eta[row] = static_cast<float>(((kLog2e * static_cast<double>(a.sm_scale)) * f) / D);
+    a.eta[row] = static_cast<float>(((kLog2eF64 * static_cast<double>(a.sm_scale)) * f) / D);
 }
 
 // E4M3 (OCP E4M3FN: bias 7, subnormals m 2^-9, largest finite 448) code of

@@ -13,7 +13,10 @@
 //
 // Over a two-plane INT8 key cache the samples are scored with the scan's own
 // coarse logits, eta_i e_j (a_j . qa_i + a_j . qb_i / 256), from plane A and
-// the scales (v_mfma_i32_16x16x64_i8, the same operand layout).
+// the scales (v_mfma_i32_16x16x64_i8, the same operand layout).  The fused
+// front (FRONT) first splits the workgroup's own query rows into those codes,
+// with the query split's transform and rounding, writes them for the scan and
+// scores them from LDS: one launch instead of two, the same bits.
 //
 // Latency, not bandwidth, bounds this kernel (48 KiB per (request, kv head) at
 // D = 128).  Scores come from the matrix cores, 16 samples x 16 rows per
@@ -25,6 +28,7 @@
 // lanes; wave reductions use DPP and v_readlane.  Every sum has a fixed order, so the result is deterministic.
 #include "fold_device.h"
 #include "fold_internal.h"
+#include "q8_split.h"
 
 namespace fold {
 namespace {
@@ -125,7 +129,7 @@ __device__ __forceinline__ int sample_index(int t, int n, bool stratified, int s
   return (lo + hi - 1) / 2;
 }
 
-template <int D, bool Q8>
+template <int D, bool Q8, bool FRONT = false>
 __global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs qa8) {
   const EstimateArgs& a = qa8.e;
   constexpr int NK = Q8 ? D / 64 : D / 32;  // 16-byte key loads per lane per sample tile
@@ -139,6 +143,45 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs
   const int G = g.group;
 
   __shared__ float sc[kMaxEstRows][kMaxEstSamples];
+
+  // Fused front: split the query rows of this (request, kv head) first, wave w
+  // taking rows w, w+4, ... (the query split's own transform and rounding, so
+  // the codes are the same bits); the codes go out for the scan and into LDS
+  // for the scoring below.
+  __shared__ __attribute__((aligned(16))) int8_t qs[FRONT ? kMaxEstRows : 1][FRONT ? 2 * D : 16];
+  __shared__ float etas[FRONT ? kMaxEstRows : 1];
+  if constexpr (FRONT) {
+    for (int r = wave; r < G; r += kThreads / 64) {
+      const size_t row = static_cast<size_t>(req) * g.heads + kvh * G + r;
+      double x[D / 64];
+#pragma unroll
+      for (int i = 0; i < D / 64; ++i)
+        x[i] = static_cast<double>(bf16_lo(qa8.q_src[row * D + 64 * i + lane]));
+      hadamard_wave<D>(x, lane);
+      const double f = wave_absmax_f64<D>(x) / 127.0;
+#pragma unroll
+      for (int i = 0; i < D / 64; ++i) {
+        int8_t ca, cb;
+        split_value(x[i], f, &ca, &cb);
+        qa8.qp_out[row * 2 * D + 64 * i + lane] = ca;
+        qa8.qp_out[row * 2 * D + D + 64 * i + lane] = cb;
+        qs[r][64 * i + lane] = ca;
+        qs[r][D + 64 * i + lane] = cb;
+      }
+      if (lane == 0) {
+        const float eta = static_cast<float>(((kLog2eF64 * static_cast<double>(qa8.sm_scale)) * f) / D);
+        qa8.eta_out[row] = eta;
+        etas[r] = eta;
+      }
+    }
+    if (kvh == 0 && qa8.tau && threadIdx.x == 0) {
+      const int nr = qa8.req_lens[req];
+      const int c = nr > 1 ? 32 - __builtin_clz(static_cast<unsigned>(nr - 1)) : 0;
+      qa8.tau[req] = qa8.kappa + static_cast<float>(c);
+      if (qa8.tau_v) qa8.tau_v[req] = qa8.kappa_v + static_cast<float>(c);
+    }
+    __syncthreads();
+  }
 
   int n = 0;
   if (req < g.num_seqs) n = clamp_len(ld_uniform(g.seq_lens, req), view_capacity(g));
@@ -166,7 +209,10 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs
     qb2[c] = u32x4{0, 0, 0, 0};
     if (n16 < G) {
       const size_t row = static_cast<size_t>(req) * g.heads + kvh * G + n16;
-      if constexpr (Q8) {
+      if constexpr (FRONT) {
+        qb[c] = *reinterpret_cast<const u32x4*>(&qs[n16][64 * c + 16 * grp]);
+        qb2[c] = *reinterpret_cast<const u32x4*>(&qs[n16][D + 64 * c + 16 * grp]);
+      } else if constexpr (Q8) {
         qb[c] = *reinterpret_cast<const u32x4*>(qa8.qp + row * 2 * D + 64 * c + 16 * grp);
         qb2[c] = *reinterpret_cast<const u32x4*>(qa8.qp + row * 2 * D + D + 64 * c + 16 * grp);
       } else {
@@ -175,7 +221,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs
     }
   }
   if constexpr (Q8) {
-    if (n16 < G) eta_r = qa8.eta[static_cast<size_t>(req) * g.heads + kvh * G + n16];
+    if (n16 < G) eta_r = FRONT ? etas[n16] : qa8.eta[static_cast<size_t>(req) * g.heads + kvh * G + n16];
   }
 
   // Tiles of 16 samples; wave w scores tiles w, w+4, ...; lane l loads sample l%16.
@@ -361,6 +407,20 @@ hipError_t launch_estimate(const EstimateArgs& a, int head_dim, hipStream_t stre
 
 hipError_t launch_q8_estimate(const Q8EstimateArgs& a, int head_dim, hipStream_t stream) {
   return launch_est<true>(a, head_dim, stream);
+}
+
+hipError_t launch_q8_front(const Q8EstimateArgs& a, int head_dim, hipStream_t stream) {
+  const long long blocks = static_cast<long long>(a.e.geo.batch) * a.e.geo.hkv;
+  if (blocks == 0) return hipSuccess;
+  if (head_dim == 128)
+    hipLaunchKernelGGL((estimate_kernel<128, true, true>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(kThreads), 0, stream, a);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL((estimate_kernel<64, true, true>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(kThreads), 0, stream, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
 }
 
 }  // namespace fold

@@ -38,6 +38,7 @@ EXPORTED = (
     "fold_v8_write_values",
     "fold_q8_split_query",
     "fold_q8_ref_estimate",
+    "fold_q8_front",
     "fold_q8_decode_rows_per_group",
     "fold_q8_decode_row_groups",
     "fold_q8_decode_split",
@@ -178,6 +179,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.fold_q8_ref_estimate.restype = ctypes.c_int
     lib.fold_q8_ref_estimate.argtypes = [P(fold_kv_view), P(fold_q8_keys), P(fold_q8_query),
                                          P(fold_est_params), ctypes.c_void_p, ctypes.c_void_p]
+    lib.fold_q8_front.restype = ctypes.c_int
+    lib.fold_q8_front.argtypes = [P(fold_kv_view), P(fold_q8_keys), P(fold_q_view), ctypes.c_float,
+                                  ctypes.c_void_p, ctypes.c_float, ctypes.c_float,
+                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                  ctypes.c_void_p, P(fold_est_params), ctypes.c_void_p,
+                                  ctypes.c_void_p]
     for name in ("fold_q8_decode_rows_per_group", "fold_q8_decode_row_groups"):
         fn = getattr(lib, name)
         fn.restype = ctypes.c_int32
@@ -667,6 +674,34 @@ def fold_q8_ref_estimate(kv: KV, keys: Q8Keys, q: Q8Query, z_out: torch.Tensor, 
     kk, qq = keys.view(), q.view()
     _check(load_library().fold_q8_ref_estimate(
         ctypes.byref(kv.view), ctypes.byref(kk), ctypes.byref(qq),
+        None if p is None else ctypes.byref(p), _ptr(z_out), _stream(stream)))
+    return z_out
+
+
+def fold_q8_front(kv: KV, keys: Q8Keys, q: torch.Tensor, sm_scale: float, out: Q8Query,
+                  z_out: torch.Tensor, req_lens: Optional[torch.Tensor] = None,
+                  kappa: float = -4.0, kappa_v: float = -4.0, params=None,
+                  stream=None) -> torch.Tensor:
+    """fold_q8_split_query followed by fold_q8_ref_estimate, in one launch."""
+    qv = q_view(q)
+    _need(out.planes, "planes", torch.int8)
+    _need(out.eta, "eta", torch.float32)
+    _need(z_out, "z_out", torch.float32)
+    if req_lens is not None:
+        _need(req_lens, "req_lens", torch.int32)
+        _need(out.tau, "tau", torch.float32)
+    if req_lens is not None and out.tau_v is not None:
+        _need(out.tau_v, "tau_v", torch.float32)
+    p = None
+    if params is not None:
+        p = fold_est_params(params["sink"], params["recent"], params["strata"],
+                            params["trim_lo"], params["trim_hi"])
+    kk = keys.view()
+    _check(load_library().fold_q8_front(
+        ctypes.byref(kv.view), ctypes.byref(kk), ctypes.byref(qv.view), sm_scale,
+        _ptr(req_lens), kappa, kappa_v, _ptr(out.planes), _ptr(out.eta),
+        None if req_lens is None else _ptr(out.tau),
+        None if req_lens is None else _ptr(out.tau_v),
         None if p is None else ctypes.byref(p), _ptr(z_out), _stream(stream)))
     return z_out
 

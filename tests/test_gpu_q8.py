@@ -17,6 +17,7 @@ import torch
 from oracle import bf16_bits_to_f64, combine
 from oracle import q8_oracle as q8
 from tests import _adapt, _gpu, _gpu_q8
+import paper_2609_33410_amd as F
 from workloads import host_bits, make_cascade, make_config, make_custom
 
 pytestmark = pytest.mark.gpu
@@ -290,6 +291,56 @@ def test_q8_small_stacked_groups(heads, kv_heads, requests):
                       seed=heads + kv_heads + requests, device="cuda")
     for T in (INF, 16.0, 6.0):
         _full_parity(wl, T)
+
+
+@pytest.mark.parametrize("d,group,paged,thresholds", [(128, 4, True, "both"), (128, 8, True, "tau"),
+                                                      (64, 2, False, "none"), (128, 16, True, "both"),
+                                                      (64, 1, True, "tau")])
+def test_q8_front_equals_split_then_estimate(d, group, paged, thresholds):
+    """The fused front writes the same query codes, eta, thresholds and Z, bit
+    for bit, as the query split followed by the coarse-logit estimate
+    (ragged lengths, an empty request, 16-row groups)."""
+    lens = [0, 1, 17, 191, 192, 193, 700, 2049]
+    wl = make_custom(batch=len(lens), heads=2 * group, kv_heads=2, dim=d, lens=lens, paged=paged,
+                     spike_count=3, n_sink=1, seed=d + group, device="cuda")
+    keys = _gpu_q8.encode_cache(wl)
+    _, flat = _gpu_q8.level_views(wl, keys)
+    req = wl.flat.seq_lens if thresholds != "none" else None
+    kappa, kappa_v = -3.5, 1.25
+    a = F.q8_empty_query(wl.q)
+    b = F.q8_empty_query(wl.q)
+    for t in (a.planes, b.planes):
+        t.fill_(0x33)
+    for t in (a.eta, a.tau, a.tau_v, b.eta, b.tau, b.tau_v):
+        t.fill_(float("nan"))
+    if thresholds == "tau":
+        a.tau_v = b.tau_v = None
+    F.fold_q8_split_query(wl.q, wl.sm_scale, a, req_lens=req, kappa=kappa, kappa_v=kappa_v)
+    za = torch.empty(wl.batch, wl.num_heads, dtype=torch.float32, device="cuda")
+    F.fold_q8_ref_estimate(flat, keys, a, za)
+    zb = torch.full_like(za, float("nan"))
+    F.fold_q8_front(flat, keys, wl.q, wl.sm_scale, b, zb, req_lens=req, kappa=kappa,
+                    kappa_v=kappa_v)
+    torch.cuda.synchronize()
+    assert torch.equal(a.planes, b.planes)
+    assert torch.equal(a.eta, b.eta)
+    assert torch.equal(za, zb)
+    if req is not None:
+        assert torch.equal(a.tau, b.tau)
+        if a.tau_v is not None:
+            assert torch.equal(a.tau_v, b.tau_v)
+
+
+def test_q8_front_rejects_bad_arguments():
+    wl = make_config(2, batch=2, seq_len=300, device="cuda")
+    keys = _gpu_q8.encode_cache(wl)
+    _, flat = _gpu_q8.level_views(wl, keys)
+    qq = F.q8_empty_query(wl.q)
+    z = torch.empty(wl.batch, wl.num_heads, dtype=torch.float32, device="cuda")
+    with pytest.raises(F.FoldError):
+        F.fold_q8_front(flat, keys, wl.q, float("nan"), qq, z)
+    with pytest.raises(F.FoldError):
+        F.fold_q8_front(flat, keys, wl.q, wl.sm_scale, qq, z, kappa=float("nan"))
 
 
 # ------------------------------------------------------- invariants ---------
