@@ -264,7 +264,8 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2)
   using S = PackedScan<D, PK, DENSE, DBG>;
   constexpr int NK = S::NK;
   constexpr int kTileBytes = kScanWaves * 16 * S::VSTRIDE;
-  constexpr int kRedBytes = (16 * D + 64) * 4;
+  constexpr int kWaveFloats = S::NB * 4 * 64 + 64;  // one wave's accumulators, L and cut mass
+  constexpr int kRedBytes = kScanWaves * kWaveFloats * 4;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kTileBytes > kRedBytes ? kTileBytes : kRedBytes];
 
   const ScanGeometry& g = a.geo;
@@ -335,42 +336,59 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2)
   sc.lcut += __shfl_xor(sc.lcut, 16, 64);
   sc.lcut += __shfl_xor(sc.lcut, 32, 64);
 
-  // Add the four waves in order through LDS (the value tiles are dead now),
-  // in the accumulators' own lane order so that no two lanes share a bank.
+  // Add the four waves through LDS (the tiles are dead now): each wave stores
+  // its accumulators in its own region (in their lane order, so that no two
+  // lanes share a bank), one barrier, then every thread adds four channels of
+  // one row over the waves in wave order and stores them as one 16-byte group.
+  // Row n16's accumulator sits at (blk * 4 + i) * 64 + l with l % 16 = n16 and
+  // channel 16 blk + 4 (l / 16) + i; lanes 0-15 of a region hold L, lanes
+  // 16-31 the cut mass (lane n16 < BW holds packed row n16).
+  __shared__ long long out_row[16];  // query row of row n16, or -1
   __syncthreads();
-  float* red = reinterpret_cast<float*>(smem);  // [NB][4][64]
-  float* redl = red + S::NB * 4 * 64;           // [64]
-  for (int w = 0; w < kScanWaves; ++w) {
-    if (wave == w) {
-#pragma unroll
-      for (int blk = 0; blk < S::NB; ++blk)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float* r = red + (blk * 4 + i) * 64 + sc.lane;
-          *r = (w == 0 ? 0.0f : *r) + sc.acc[blk][i];
-        }
-      // lanes 0-15 add row n16's L (lane n16 < BW holds packed row n16), lanes
-      // 16-31 its cut mass
-      if (sc.lane < 32) {
-        float* d = redl + sc.lane;
-        *d = (w == 0 ? 0.0f : *d) + (sc.lane < 16 ? sc.lsum : sc.lcut);
-      }
-    }
-    __syncthreads();
-  }
-
-  // The LDS sums sit at (blk * 4 + i) * 64 + l for row l%16 and channel
-  // 16 blk + 4 (l/16) + i.  Wave i, lane l writes those entries of every blk.
-  const size_t slot_rows = (static_cast<size_t>(a.slot_offset) + sc.p.split) * g.batch * g.heads;
-  const int wl = threadIdx.x & 63;
-  const int wi = threadIdx.x >> 6;
-  if (sc.rok) {
-    const size_t row = slot_rows + sc.xrow;
+  float* red = reinterpret_cast<float*>(smem);
+  {
+    float* mine = red + wave * kWaveFloats;
 #pragma unroll
     for (int blk = 0; blk < S::NB; ++blk)
-      a.part_A[row * D + 16 * blk + 4 * (wl >> 4) + wi] = red[(blk * 4 + wi) * 64 + wl];
-    if (wi == 0 && wl < 16) a.part_L[row] = redl[wl];
-    if (a.part_Lcut && wi == 1 && wl < 16) a.part_Lcut[row] = redl[16 + wl];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mine[(blk * 4 + i) * 64 + sc.lane] = sc.acc[blk][i];
+    if (sc.lane < 32) mine[S::NB * 4 * 64 + sc.lane] = sc.lane < 16 ? sc.lsum : sc.lcut;
+    if (wave == 0 && sc.lane < 16) out_row[sc.lane] = sc.rok ? static_cast<long long>(sc.xrow) : -1;
+  }
+  __syncthreads();
+  const size_t slot_rows = (static_cast<size_t>(a.slot_offset) + sc.p.split) * g.batch * g.heads;
+  const bool vec_ok = (reinterpret_cast<uintptr_t>(a.part_A) & 15u) == 0;
+  for (int f = threadIdx.x; f < 16 * (D / 4); f += kScanThreads) {
+    const int r = f / (D / 4);
+    const int d = 4 * (f % (D / 4));
+    const long long xr = out_row[r];
+    if (xr < 0) continue;
+    const int base = (d / 16) * 4 * 64 + 16 * ((d % 16) / 4) + r;
+    float v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = base + i * 64;
+      v[i] = ((red[e] + red[kWaveFloats + e]) + red[2 * kWaveFloats + e]) + red[3 * kWaveFloats + e];
+    }
+    float* dst = a.part_A + (slot_rows + static_cast<size_t>(xr)) * D + d;
+    if (vec_ok) {
+      *reinterpret_cast<f32x4*>(dst) = f32x4{v[0], v[1], v[2], v[3]};
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dst[i] = v[i];
+    }
+  }
+  if (threadIdx.x < 32) {
+    const int r = threadIdx.x & 15;
+    const long long xr = out_row[r];
+    const int e = S::NB * 4 * 64 + threadIdx.x;
+    const float v = ((red[e] + red[kWaveFloats + e]) + red[2 * kWaveFloats + e]) + red[3 * kWaveFloats + e];
+    if (xr >= 0) {
+      if (threadIdx.x < 16)
+        a.part_L[slot_rows + static_cast<size_t>(xr)] = v;
+      else if (a.part_Lcut)
+        a.part_Lcut[slot_rows + static_cast<size_t>(xr)] = v;
+    }
   }
 }
 
