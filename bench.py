@@ -70,6 +70,30 @@ class Path:
         self.part_A = torch.empty(total, b, h, d, dtype=torch.float32, device=dev)
         self.part_L = torch.empty(total, b, h, dtype=torch.float32, device=dev)
         self.out = torch.empty(b, h, d, dtype=torch.float32, device=dev)
+        # one level over a per-request view with GQA groups of 2 to 8 rows: the
+        # whole step also runs as one launch (fold_decode_fused, the same bits)
+        lv = wl.levels[0]
+        self.fusable = (len(wl.levels) == 1 and lv.row_indptr is None and 2 <= wl.group <= 8
+                        and lv.num_seqs == b)
+        self.arrivals = (torch.zeros(lv.num_seqs, wl.num_kv_heads, dtype=torch.int32, device=dev)
+                         if self.fusable else None)
+
+    def step(self, T, stream):
+        """One whole call: the fused launch where it applies, else the three calls."""
+        if self.fusable:
+            self.fused(T, stream)
+        else:
+            self.three_calls(T, stream)
+
+    def three_calls(self, T, stream):
+        self.estimate(stream)
+        self.decode(T, stream)
+        self.combine(stream)
+
+    def fused(self, T, stream):
+        self.F.fold_decode_fused(self.levels[0], self.qv, self.wl.sm_scale, T, self.splits[0],
+                                 self.part_A, self.part_L, self.arrivals, self.z, self.out,
+                                 stream=stream)
 
     def estimate(self, stream):
         self.F.fold_ref_estimate(self.flat, self.qv, self.wl.sm_scale, self.z, stream=stream)
@@ -497,6 +521,22 @@ def progress(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def fused_bytes(wl, lam):
+    """Algorithmic bytes of one fused launch: the scan's (kv_bytes), the
+    estimate's sampled key rows and their block-table entries (once per
+    (request, kv head)), the combine's read of the slots and its output, and
+    the arrival counts (read-modify-write and reset)."""
+    d = wl.head_dim
+    b, h, _ = wl.q.shape
+    total, keys = kv_bytes(wl, lam)
+    full = 1 + 63 + 128  # default sample: sink, recent keys, strata
+    samples = sum(min(n, full) for n in wl.flat.seq_lens_host) * wl.num_kv_heads
+    total += samples * 2 * d + (4 * samples if wl.page_size else 0)
+    total += 4 * sum(wl.level_splits) * b * h * (d + 1) + 4 * b * h * d
+    total += 2 * 4 * wl.flat.num_seqs * wl.num_kv_heads
+    return total, keys
+
+
 def scan_kernel_name(wl):
     """The scan kernel the library launches for a single-level workload."""
     if wl.group == 1:
@@ -520,7 +560,8 @@ def time_variant(path, T, steps, warmup, flush, torch):
     from separate steps with events between the kernels; its parts add up to
     more than the step."""
     stream = torch.cuda.current_stream()
-    res = {"est": [], "dec": [], "comb": [], "step": [], "step_with_markers": []}
+    res = {"est": [], "dec": [], "comb": [], "step": [], "step_three_calls": [],
+           "step_with_markers": []}
     for it in range(warmup + steps):
         evict_caches(flush)
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
@@ -538,31 +579,32 @@ def time_variant(path, T, steps, warmup, flush, torch):
             res["comb"].append(ev[2].elapsed_time(ev[3]))
             res["step_with_markers"].append(ev[0].elapsed_time(ev[3]))
     for it in range(warmup + steps):
-        evict_caches(flush)
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        path.estimate(stream)
-        path.decode(T, stream)
-        path.combine(stream)
-        e1.record(stream)
-        if it >= warmup:
-            e1.synchronize()
-            res["step"].append(e0.elapsed_time(e1))
+        for key, fn in (("step_three_calls", path.three_calls), ("step", path.step)):
+            if key == "step" and not path.fusable:
+                continue
+            evict_caches(flush)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn(T, stream)
+            e1.record(stream)
+            if it >= warmup:
+                e1.synchronize()
+                res[key].append(e0.elapsed_time(e1))
+    if not path.fusable:
+        res["step"] = res["step_three_calls"]
     torch.cuda.synchronize()
     return {k: statistics.median(v) for k, v in res.items()}, res
 
 
 def time_graph(path, T, steps, warmup, flush, torch):
     """Median duration (ms) of one whole step replayed as a captured HIP graph
-    (estimate, every level's scan, combine), caches evicted before each replay."""
+    (the fused launch, or the estimate, every level's scan and the combine),
+    caches evicted before each replay."""
     stream = torch.cuda.current_stream()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        cs = torch.cuda.current_stream()
-        path.estimate(cs)
-        path.decode(T, cs)
-        path.combine(cs)
+        path.step(T, torch.cuda.current_stream())
     ts = []
     for it in range(warmup + steps):
         evict_caches(flush)
@@ -668,9 +710,7 @@ def paired_depths(path, steps, warmup, flush, torch, T_cut=16.0):
             evict_caches(flush)
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
             ev[0].record(stream)
-            path.estimate(stream)
-            path.decode(T, stream)
-            path.combine(stream)
+            path.step(T, stream)
             ev[1].record(stream)
             evict_caches(flush)
             ed = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -709,8 +749,11 @@ def run_workload(i, args, torch, F, make_config, flush, steps, warmup, splits=No
         med, _ = time_variant(path, T, steps, warmup, flush, torch)
         graph_ms = time_graph(path, T, steps, warmup, flush, torch)
         nbytes, keys = kv_bytes(wl, lam)
-        out[T] = {"med": med, "graph": graph_ms, "lam": lam, "bytes": nbytes, "keys": keys}
-        progress(f"workload {i} T={T:g}: step {med['step'] * 1e3:.1f} us")
+        fbytes = fused_bytes(wl, lam)[0] if path.fusable else None
+        out[T] = {"med": med, "graph": graph_ms, "lam": lam, "bytes": nbytes, "keys": keys,
+                  "fused_bytes": fbytes, "fusable": path.fusable}
+        progress(f"workload {i} T={T:g}: step {med['step'] * 1e3:.1f} us "
+                 f"(three calls {med['step_three_calls'] * 1e3:.1f} us)")
     return wl, out
 
 
@@ -736,10 +779,21 @@ def main():
                            args.warmup, splits=args.splits)
     wall = time.perf_counter() - wall0
     dense, t16 = res[math.inf], res[16.0]
+    fusable = dense["fusable"]
     dec_ms = dense["med"]["dec"]
-    achieved = dense["bytes"] / (dec_ms * 1e-3) / 1e9
+    scan_achieved = dense["bytes"] / (dec_ms * 1e-3) / 1e9
     step_ms = dense["med"]["step"]
-    traffic, trec = counter_traffic(CONFIG_NAMES[args.config])
+    # the dominant kernel: the fused launch (the whole step) where it applies,
+    # else the scan of the three-call step
+    if fusable:
+        r_bytes, r_ms, r_kernel = dense["fused_bytes"], step_ms, "decode_fused_kernel"
+        r_timing = "HIP events around the eager launch on its stream (the step is this one launch)"
+    else:
+        r_bytes, r_ms, r_kernel = dense["bytes"], dec_ms, scan_kernel_name(wl)
+        r_timing = "HIP events around the eager launch on its stream"
+    achieved = r_bytes / (r_ms * 1e-3) / 1e9
+    traffic, trec = counter_traffic(CONFIG_NAMES[args.config] + (" [fused]" if fusable else ""))
+    scan_traffic, _ = counter_traffic(CONFIG_NAMES[args.config])
     line = {
         "metric": METRIC,
         "value": round(step_ms * 1e3, 2),
@@ -757,7 +811,9 @@ def main():
                    "q_heads": wl.num_heads, "kv_heads": wl.num_kv_heads,
                    "head_dim": wl.head_dim, "keys_per_request": wl.flat.seq_lens_host[0],
                    "page_size": wl.page_size, "splits": wl.level_splits,
-                   "step": "estimate + split scan + combine at T=inf, launched on one stream",
+                   "step": ("estimate + split scan + combine at T=inf in one launch "
+                            "(fold_decode_fused)" if fusable else
+                            "estimate + split scan + combine at T=inf, launched on one stream"),
                    "timing": "median over steps of HIP events around the step on its stream "
                              "(no event inside the step); a 1 GiB read before each step evicts "
                              "all caches; the breakdown comes from separate steps with events "
@@ -765,10 +821,19 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": None if traffic is None else int(traffic),
-                     "kernel": scan_kernel_name(wl),
-                     "algorithmic_bytes_per_launch": int(dense["bytes"]),
-                     "avg_launch_us": round(dec_ms * 1e3, 2),
-                     "launch_timing": "HIP events around the eager launch on its stream"},
+                     "kernel": r_kernel,
+                     "algorithmic_bytes_per_launch": int(r_bytes),
+                     "avg_launch_us": round(r_ms * 1e3, 2),
+                     "launch_timing": r_timing},
+        "scan_roofline": {"kernel": scan_kernel_name(wl), "achieved": round(scan_achieved, 1),
+                          "frac": round(scan_achieved / HBM_PEAK_GBPS, 4),
+                          "traffic": None if scan_traffic is None else int(scan_traffic),
+                          "algorithmic_bytes_per_launch": int(dense["bytes"]),
+                          "avg_launch_us": round(dec_ms * 1e3, 2),
+                          "launch_timing": "HIP events around the scan launch of the three-call "
+                                           "step, events between its kernels"},
+        "three_calls_us_per_call": {"T=inf": round(dense["med"]["step_three_calls"] * 1e3, 2),
+                                    "T=16": round(t16["med"]["step_three_calls"] * 1e3, 2)},
         "t16_us_per_call": round(t16["med"]["step"] * 1e3, 2),
         "graph_replay_us_per_call": {"T=inf": round(dense["graph"] * 1e3, 2),
                                      "T=16": round(t16["graph"] * 1e3, 2)},
@@ -814,6 +879,8 @@ def main():
             for T, v in r.items():
                 rec = {"workload": CONFIG_NAMES[i], "T": "inf" if math.isinf(T) else T,
                        "us_per_call": round(v["med"]["step"] * 1e3, 2),
+                       "step": "fused" if v["fusable"] else "three calls",
+                       "us_per_call_three_calls": round(v["med"]["step_three_calls"] * 1e3, 2),
                        "us_per_call_graph": round(v["graph"] * 1e3, 2),
                        "decode_us": round(v["med"]["dec"] * 1e3, 2),
                        "estimate_us": round(v["med"]["est"] * 1e3, 2),

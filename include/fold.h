@@ -218,6 +218,35 @@ fold_status fold_combine(const float* part_A, const float* part_L, int32_t num_s
                          const fold_value_model* model, void* stream);
 
 /*
+ * fold_decode_fused - the whole decode of a single level in one launch:
+ * fold_ref_estimate, fold_decode_split over splits [0, num_splits) and
+ * fold_combine, with the same bits in z_out, out, lse_out and cert_out
+ * (Section 3, "Choosing the reference"; Section 4; Algorithm 1).  Every
+ * (request, kv head, split) workgroup computes its group's references Z_i
+ * while its first keys load, scans its tiles, writes its slot, and the split
+ * that finishes last adds the slots in increasing order into the output.
+ *   kv, q, sm_scale, params  as fold_ref_estimate: a per-request view
+ *           (row_indptr NULL, num_seqs == batch) whose kv heads each serve
+ *           2 to 8 query rows (GQA); other group sizes are FOLD_E_UNSUPPORTED
+ *           (use the three calls)
+ *   depth_T, num_splits      as fold_decode_split
+ *   part_A  [num_splits][batch][num_heads][head_dim] fp32, part_L
+ *           [num_splits][batch][num_heads] fp32: workspace for the slots
+ *           (their contents after the call are the slots of fold_decode_split)
+ *   arrivals [num_seqs][num_kv_heads] int32 (device): must be zero before the
+ *           first call; every call leaves it zero.  Calls that share it or
+ *           the slots must not run concurrently.
+ *   z_out   [batch][num_heads] fp32: the references, as fold_ref_estimate
+ *   out, out_dtype, lse_out, cert_out  as fold_combine (no value model);
+ *           part_A and out must be 16-byte aligned.
+ */
+fold_status fold_decode_fused(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
+                              const fold_est_params* params, float depth_T, int32_t num_splits,
+                              float* part_A, float* part_L, int32_t* arrivals, float* z_out,
+                              void* out, fold_dtype out_dtype, float* lse_out,
+                              uint8_t* cert_out, void* stream);
+
+/*
  * fold_value_mean - request mean value rows (the running mean of Section 4's
  * value model): mean_out[s][g] = mean of value rows 0..n_s-1 of kv sequence
  * s, head g (0 for an empty sequence), FP32 sums in a fixed order.

@@ -25,6 +25,7 @@ from .fold import (  # noqa: F401
     fold_cert_update,
     fold_certified_decode,
     fold_combine,
+    fold_decode_fused,
     fold_decode,
     fold_draft_views,
     fold_decode_row_groups,

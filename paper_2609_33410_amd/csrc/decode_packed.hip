@@ -37,6 +37,7 @@
 // without a live key issues no value load, so at small depths the key stream
 // of the next step is the only load a wave waits for.
 #include "decode_common.h"
+#include "estimate_device.h"
 
 namespace fold {
 namespace {
@@ -259,14 +260,131 @@ struct PackedScan {
   }
 };
 
-template <int D, int PK, bool DENSE, bool DBG>
-__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2))) void decode_packed_kernel(const DecodeArgs a) {
+// Slot values of the one-launch decode are stored and read as device-scope
+// atomics: the accesses go to the chip's coherence point past the per-XCD L2s,
+// so a split that finishes on one XCD and the split that combines on another
+// need no L2 write-back or invalidation (each costs far more than the few
+// kilobytes it would publish).
+__device__ __forceinline__ void slot_store(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float slot_load(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The last of a (kv sequence, kv head)'s splits adds their slots for the
+// group's rows, as the combine does: A and L summed in increasing slot order
+// from zero, o = A / L, the base-2 log-sum-exp Z + log2 L and the range
+// certificate.  Every split waits until its slot stores are complete, then
+// counts its arrival; the split that counts last reads the slots (its loads
+// are issued only after it has seen the count) and leaves the count at zero
+// for the next call.
+template <int D>
+__device__ __forceinline__ void fused_combine(const DecodeArgs& a, const FusedExtra& x,
+                                              const ScanPlace& p, const long long (&out_row)[16],
+                                              const float (&zs)[16]) {
+  const ScanGeometry& g = a.geo;
+  __shared__ int last;
+  __shared__ float lrow[16];
+  __shared__ int bad[16];
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's slot stores are complete
+  __syncthreads();
+  int32_t* ctr = x.arrivals + static_cast<size_t>(p.seq) * g.hkv + p.kvh;
+  if (threadIdx.x == 0)
+    last = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                   a.num_splits - 1
+               ? 1
+               : 0;
+  if (threadIdx.x < 16) bad[threadIdx.x] = 0;
+  __syncthreads();
+  if (!last) return;
+  const size_t nrows = static_cast<size_t>(g.batch) * g.heads;
+  for (int f = threadIdx.x; f < 16 * (D / 4); f += kScanThreads) {
+    const int r = f / (D / 4);
+    const int d = 4 * (f % (D / 4));
+    const long long xr = out_row[r];
+    if (xr < 0) continue;
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    float l = 0.0f;
+    int s = 0;
+    for (; s + 8 <= a.num_splits; s += 8) {
+      f32x4 av[8];
+      float lv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const size_t sr = static_cast<size_t>(a.slot_offset + s + u) * nrows + xr;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) av[u][i] = slot_load(a.part_A + sr * D + d + i);
+        lv[u] = slot_load(a.part_L + sr);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        acc += av[u];
+        l += lv[u];
+      }
+    }
+    for (; s < a.num_splits; ++s) {
+      const size_t sr = static_cast<size_t>(a.slot_offset + s) * nrows + xr;
+      f32x4 av;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = slot_load(a.part_A + sr * D + d + i);
+      acc += av;
+      l += slot_load(a.part_L + sr);
+    }
+    float o[4];
+    bool nf = false;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[i] = acc[i] / l;
+      nf = nf || !isfinite(o[i]);
+    }
+    const size_t oi = static_cast<size_t>(xr) * D + d;
+    if (x.out_bf16) {
+      uint32_t h[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) h[i] = f32_to_bf16_rne(o[i]);
+      const u32x2 ob = {h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+      *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(x.out) + oi) = ob;
+    } else {
+      *reinterpret_cast<f32x4*>(static_cast<float*>(x.out) + oi) = f32x4{o[0], o[1], o[2], o[3]};
+    }
+    if (nf) bad[r] = 1;
+    if (d == 0) lrow[r] = l;
+  }
+  __syncthreads();
+  if (threadIdx.x < 16) {
+    const int r = threadIdx.x;
+    const long long xr = out_row[r];
+    if (xr >= 0) {
+      const float l = lrow[r];
+      if (x.lse_out) x.lse_out[xr] = zs[r] + log2f(l);
+      if (x.cert_out) {
+        uint8_t c = 0;
+        if (l < 0.5f) c |= 1;
+        if (l > 0x1p100f) c |= 2;
+        if (bad[r]) c |= 4;
+        x.cert_out[xr] = c;
+      }
+    }
+  }
+  if (threadIdx.x == 0) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The scan of one (kv sequence, kv head, split) workgroup.  FUSED (the
+// one-launch decode of a single level, per-request view): the prologue
+// computes the group's references with the estimate routine while the first
+// keys load, and the last split to finish adds the slots into the output.
+template <int D, int PK, bool DENSE, bool DBG, bool FUSED>
+__device__ __forceinline__ void packed_scan(const DecodeArgs& a, const FusedExtra* fx) {
   using S = PackedScan<D, PK, DENSE, DBG>;
   constexpr int NK = S::NK;
   constexpr int kTileBytes = kScanWaves * 16 * S::VSTRIDE;
   constexpr int kWaveFloats = S::NB * 4 * 64 + 64;  // one wave's accumulators, L and cut mass
   constexpr int kRedBytes = kScanWaves * kWaveFloats * 4;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[kTileBytes > kRedBytes ? kTileBytes : kRedBytes];
+  constexpr int kEstBytes = FUSED ? kMaxEstRows * kMaxEstSamples * 4 : 0;  // the estimate's scores
+  constexpr int kSmemBytes = kTileBytes > kRedBytes ? (kTileBytes > kEstBytes ? kTileBytes : kEstBytes)
+                                                    : (kRedBytes > kEstBytes ? kRedBytes : kEstBytes);
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kSmemBytes];
 
   const ScanGeometry& g = a.geo;
   S sc(a);
@@ -292,7 +410,7 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2)
     const RowInfo rp = row_info(g, sc.p.seq, sc.p.kvh, sc.n16 % S::BW, sc.p.nrows, sc.p.req0);
     sc.pok = rp.ok;
     sc.prow = static_cast<size_t>(rp.req) * g.heads + rp.head;
-    sc.zp = rp.ok ? a.z[sc.prow] : 0.0f;
+    if (!FUSED) sc.zp = rp.ok ? a.z[sc.prow] : 0.0f;
   }
   sc.lsum = 0.0f;
   sc.lcut = 0.0f;
@@ -306,7 +424,21 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2)
 
   u32x4 X0[PK][NK], X1[PK][NK];
   rsrc_t rv0[PK], rv1[PK];
-  sc.issue_keys(0, X0, rv0);
+  __shared__ float zs[16];  // FUSED: Z of row n16
+  if constexpr (FUSED) {
+    // Z of the group's rows (split 0 also writes them out); the wave's first
+    // keys are issued as soon as the estimate's sample loads are, so they
+    // fly during its second round trip.  The scores' LDS is free again after
+    // the barrier.
+    est::estimate_rows<D, false, false>(fx->est, sc.p.seq, sc.p.kvh,
+                                        reinterpret_cast<float (*)[kMaxEstSamples]>(smem), nullptr,
+                                        nullptr, sc.p.split == 0, zs,
+                                        [&] { sc.issue_keys(0, X0, rv0); });
+    __syncthreads();
+    sc.zp = sc.pok ? zs[sc.n16 % S::BW] : 0.0f;
+  } else {
+    sc.issue_keys(0, X0, rv0);
+  }
   bool pend = false;  // the last scored step has value rows in flight
   for (int j = 0; j < steps; j += 2) {
     if (pend) sc.product(X1);  // step j - 1
@@ -371,7 +503,10 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2)
       v[i] = ((red[e] + red[kWaveFloats + e]) + red[2 * kWaveFloats + e]) + red[3 * kWaveFloats + e];
     }
     float* dst = a.part_A + (slot_rows + static_cast<size_t>(xr)) * D + d;
-    if (vec_ok) {
+    if constexpr (FUSED) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) slot_store(dst + i, v[i]);
+    } else if (vec_ok) {
       *reinterpret_cast<f32x4*>(dst) = f32x4{v[0], v[1], v[2], v[3]};
     } else {
 #pragma unroll
@@ -384,12 +519,25 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2)
     const int e = S::NB * 4 * 64 + threadIdx.x;
     const float v = ((red[e] + red[kWaveFloats + e]) + red[2 * kWaveFloats + e]) + red[3 * kWaveFloats + e];
     if (xr >= 0) {
-      if (threadIdx.x < 16)
+      if (FUSED && threadIdx.x < 16)
+        slot_store(a.part_L + slot_rows + static_cast<size_t>(xr), v);
+      else if (threadIdx.x < 16)
         a.part_L[slot_rows + static_cast<size_t>(xr)] = v;
       else if (a.part_Lcut)
         a.part_Lcut[slot_rows + static_cast<size_t>(xr)] = v;
     }
   }
+  if constexpr (FUSED) fused_combine<D>(a, *fx, sc.p, out_row, zs);
+}
+
+template <int D, int PK, bool DENSE, bool DBG>
+__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2))) void decode_packed_kernel(const DecodeArgs a) {
+  packed_scan<D, PK, DENSE, DBG, false>(a, nullptr);
+}
+
+template <int D, int PK, bool DENSE>
+__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2))) void decode_fused_kernel(const FusedArgs fa) {
+  packed_scan<D, PK, DENSE, false, true>(fa.d, &fa.x);
 }
 
 template <int D, int PK, bool DENSE>
@@ -410,7 +558,30 @@ hipError_t launch_pk(const DecodeArgs& a, unsigned blocks, hipStream_t stream) {
                  : launch_pkd<D, PK, false>(a, dbg, blocks, stream);
 }
 
+template <int D, int PK>
+hipError_t launch_fused_pk(const FusedArgs& a, unsigned blocks, hipStream_t stream) {
+  if (a.d.dense)
+    hipLaunchKernelGGL((decode_fused_kernel<D, PK, true>), dim3(blocks), dim3(kScanThreads), 0,
+                       stream, a);
+  else
+    hipLaunchKernelGGL((decode_fused_kernel<D, PK, false>), dim3(blocks), dim3(kScanThreads), 0,
+                       stream, a);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+// One-launch decode of a single level: read groups of two to eight rows of a
+// per-request view.
+hipError_t launch_decode_fused(const FusedArgs& a, int head_dim, hipStream_t stream) {
+  const long long blocks = static_cast<long long>(a.d.geo.num_seqs) * a.d.geo.hkv * a.d.num_splits;
+  if (blocks == 0) return hipSuccess;
+  const unsigned nb = static_cast<unsigned>(blocks);
+  const bool four = a.d.rows_per_seq <= 4;
+  if (head_dim == 128) return four ? launch_fused_pk<128, 4>(a, nb, stream) : launch_fused_pk<128, 2>(a, nb, stream);
+  if (head_dim == 64) return four ? launch_fused_pk<64, 4>(a, nb, stream) : launch_fused_pk<64, 2>(a, nb, stream);
+  return hipErrorInvalidValue;
+}
 
 // Scan of read groups of at most eight rows (one read group per kv sequence
 // and head), at any depth.

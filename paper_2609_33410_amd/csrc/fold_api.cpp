@@ -283,6 +283,69 @@ fold_status fold_combine(const float* part_A, const float* part_L, int32_t num_s
   return ok();
 }
 
+fold_status fold_decode_fused(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
+                              const fold_est_params* params, float depth_T, int32_t num_splits,
+                              float* part_A, float* part_L, int32_t* arrivals, float* z_out,
+                              void* out, fold_dtype out_dtype, float* lse_out,
+                              uint8_t* cert_out, void* stream) {
+  fold::FusedArgs f{};
+  fold::DecodeArgs& a = f.d;
+  fold_status st = check_view(kv, q, &a.geo, true);
+  if (st != FOLD_OK) return st;
+  if (!part_A || !part_L || !arrivals || !z_out || !out)
+    return fail(FOLD_E_INVAL, "part_A, part_L, arrivals, z_out and out are required");
+  if (kv->row_indptr) return fail(FOLD_E_INVAL, "the fused decode needs a per-request view (no CSR rows)");
+  if (kv->num_seqs != q->batch)
+    return fail(FOLD_E_INVAL, "the fused decode needs num_seqs %d == batch %d", kv->num_seqs, q->batch);
+  st = check_depth(depth_T);
+  if (st != FOLD_OK) return st;
+  if (!isfinite(sm_scale)) return fail(FOLD_E_INVAL, "sm_scale must be finite");
+  if (num_splits < 1) return fail(FOLD_E_INVAL, "num_splits must be >= 1");
+  if (out_dtype != FOLD_DTYPE_F32 && out_dtype != FOLD_DTYPE_BF16)
+    return fail(FOLD_E_INVAL, "unknown out_dtype");
+  if ((reinterpret_cast<uintptr_t>(part_A) & 15u) != 0 || (reinterpret_cast<uintptr_t>(out) & 15u) != 0)
+    return fail(FOLD_E_INVAL, "part_A and out must be 16-byte aligned");
+  const int rows = rows_per_seq(kv, q);
+  if (rows < 2 || rows > 8)
+    return fail(FOLD_E_UNSUPPORTED, "the fused decode serves 2 to 8 rows per kv head (got %d)", rows);
+  fold_est_params p;
+  st = check_est_params(params, &p);
+  if (st != FOLD_OK) return st;
+  const long long blocks = static_cast<long long>(kv->num_seqs) * kv->num_kv_heads * num_splits;
+  if (blocks > 0x7fffffffLL) return fail(FOLD_E_INVAL, "grid too large");
+  a.q = static_cast<const uint16_t*>(q->q);
+  a.z = nullptr;
+  a.part_A = part_A;
+  a.part_L = part_L;
+  a.part_Lcut = nullptr;
+  a.score_scale = kLog2e * sm_scale;
+  a.dense = isinf(depth_T) ? 1 : 0;
+  a.neg_T = a.dense ? 0.0f : -depth_T;
+  a.num_splits = num_splits;
+  a.slot_offset = 0;
+  a.rows_per_seq = rows;
+  a.rows_per_group = fold::decode_rows_per_group(rows);
+  a.row_groups = 1;
+  fold::EstimateArgs& e = f.x.est.e;
+  e.geo = a.geo;
+  e.q = a.q;
+  e.z_out = z_out;
+  e.score_scale = a.score_scale;
+  e.sink = p.sink;
+  e.recent = p.recent;
+  e.strata = p.strata;
+  e.trim_lo = p.trim_lo;
+  e.trim_hi = p.trim_hi;
+  f.x.arrivals = arrivals;
+  f.x.out = out;
+  f.x.lse_out = lse_out;
+  f.x.cert_out = cert_out;
+  f.x.out_bf16 = out_dtype == FOLD_DTYPE_BF16 ? 1 : 0;
+  hipError_t err = fold::launch_decode_fused(f, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (err != hipSuccess) return fail(FOLD_E_HIP, "fused decode launch: %s", hipGetErrorString(err));
+  return ok();
+}
+
 fold_status fold_value_mean(const fold_kv_view* kv, float* mean_out, void* stream) {
   if (!kv) return fail(FOLD_E_INVAL, "kv view is required");
   fold::MeanArgs a{};

@@ -199,6 +199,24 @@ struct Q8EstimateArgs {
   float kappa_v;
 };
 
+// The one-launch decode of a single level over a per-request view: every
+// split's workgroup computes its (request, kv head)'s reference in its
+// prologue (the estimate routine, the same bits as the estimate kernel), and
+// the last split to finish adds the slots (the combine's order and bits).
+struct FusedExtra {
+  Q8EstimateArgs est;   // the estimate of the scan's view (est.e.z_out: Z)
+  int32_t* arrivals;    // [num_seqs][hkv]: zero before a call, zero after it
+  void* out;            // [batch][heads][D] fp32 or bf16
+  float* lse_out;       // [batch][heads] or NULL
+  uint8_t* cert_out;    // [batch][heads] or NULL
+  int out_bf16;
+};
+
+struct FusedArgs {
+  DecodeArgs d;         // the scan (d.z is not read; d.part_Lcut is NULL)
+  FusedExtra x;
+};
+
 // Keys a kv sequence of this view can hold: max_seq_len, and for a paged view
 // also max_pages * page_size.  Device-supplied lengths are clamped to it.
 __host__ __device__ inline int view_capacity(const ScanGeometry& g) {
@@ -215,6 +233,7 @@ hipError_t launch_estimate(const EstimateArgs& a, int head_dim, hipStream_t stre
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_q8_decode(const Q8DecodeArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_front(const Q8EstimateArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_decode_fused(const FusedArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_value_mean(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_value_mean_append(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_write(const Q8WriteArgs& a, int head_dim, hipStream_t stream);

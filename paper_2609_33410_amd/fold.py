@@ -32,6 +32,7 @@ EXPORTED = (
     "fold_ref_estimate",
     "fold_decode_split",
     "fold_combine",
+    "fold_decode_fused",
     "fold_value_mean",
     "fold_value_mean_append",
     "fold_q8_write_keys",
@@ -157,6 +158,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                  ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
                                  ctypes.c_void_p, ctypes.c_void_p, P(fold_value_model),
                                  ctypes.c_void_p]
+    lib.fold_decode_fused.restype = ctypes.c_int
+    lib.fold_decode_fused.argtypes = [P(fold_kv_view), P(fold_q_view), ctypes.c_float,
+                                      P(fold_est_params), ctypes.c_float, ctypes.c_int32,
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.fold_value_mean.restype = ctypes.c_int
     lib.fold_value_mean.argtypes = [P(fold_kv_view), ctypes.c_void_p, ctypes.c_void_p]
     lib.fold_value_mean_append.restype = ctypes.c_int
@@ -369,6 +376,45 @@ def fold_combine(part_A: torch.Tensor, part_L: torch.Tensor, out: torch.Tensor,
                                        _ptr(out), odt, _ptr(lse_out), _ptr(cert_out),
                                        None if model is None else ctypes.byref(model),
                                        _stream(stream)))
+    return out
+
+
+def fold_decode_fused(kv: KV, q: Q, sm_scale: float, depth_T: float, num_splits: int,
+                      part_A: torch.Tensor, part_L: torch.Tensor, arrivals: torch.Tensor,
+                      z_out: torch.Tensor, out: torch.Tensor,
+                      lse_out: Optional[torch.Tensor] = None,
+                      cert_out: Optional[torch.Tensor] = None, params=None,
+                      stream=None) -> torch.Tensor:
+    """Estimate, scan and combine of one per-request level in one launch.
+    ``arrivals`` ([num_seqs, Hkv] int32) must be zero before the first call and
+    is zero after every call; ``part_A``/``part_L`` hold ``num_splits`` slots."""
+    _need(part_A, "part_A", torch.float32)
+    _need(part_L, "part_L", torch.float32)
+    _need(arrivals, "arrivals", torch.int32)
+    _need(z_out, "z_out", torch.float32)
+    if lse_out is not None:
+        _need(lse_out, "lse_out", torch.float32)
+    if cert_out is not None:
+        _need(cert_out, "cert_out", torch.uint8)
+    if out.dtype == torch.float32:
+        odt = FOLD_DTYPE_F32
+    elif out.dtype == torch.bfloat16:
+        odt = FOLD_DTYPE_BF16
+    else:
+        raise TypeError("out must be float32 or bfloat16")
+    if not out.is_contiguous():
+        raise ValueError("out must be contiguous")
+    if int(part_A.shape[0]) < num_splits or int(part_L.shape[0]) < num_splits:
+        raise ValueError("part_A and part_L need num_splits slots")
+    p = None
+    if params is not None:
+        p = fold_est_params(params["sink"], params["recent"], params["strata"],
+                            params["trim_lo"], params["trim_hi"])
+    _check(load_library().fold_decode_fused(
+        ctypes.byref(kv.view), ctypes.byref(q.view), sm_scale,
+        None if p is None else ctypes.byref(p), depth_T, num_splits, _ptr(part_A), _ptr(part_L),
+        _ptr(arrivals), _ptr(z_out), _ptr(out), odt, _ptr(lse_out), _ptr(cert_out),
+        _stream(stream)))
     return out
 
 
