@@ -230,9 +230,9 @@ fold_status fold_combine(const float* part_A, const float* part_L, int32_t num_s
  *           2 to 8 query rows (GQA); other group sizes are FOLD_E_UNSUPPORTED
  *           (use the three calls)
  *   depth_T, num_splits      as fold_decode_split
- *   part_A  [num_splits][batch][num_heads][head_dim] fp32, part_L
- *           [num_splits][batch][num_heads] fp32: workspace for the slots
- *           (their contents after the call are the slots of fold_decode_split)
+ *   part_A  [num_splits][batch][num_heads][head_dim] fp32 (under 2 GiB),
+ *           part_L [num_splits][batch][num_heads] fp32: workspace for the
+ *           slots (their contents after the call are those of fold_decode_split)
  *   arrivals [num_seqs][num_kv_heads] int32 (device): must be zero before the
  *           first call; every call leaves it zero.  Calls that share it or
  *           the slots must not run concurrently.

@@ -260,16 +260,35 @@ struct PackedScan {
   }
 };
 
-// Slot values of the one-launch decode are stored and read as device-scope
-// atomics: the accesses go to the chip's coherence point past the per-XCD L2s,
-// so a split that finishes on one XCD and the split that combines on another
-// need no L2 write-back or invalidation (each costs far more than the few
-// kilobytes it would publish).
-__device__ __forceinline__ void slot_store(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Slot values of the one-launch decode are stored and read with the
+// device-scope cache bit (SC1): the accesses are coherent at the chip's
+// coherence point past the per-XCD L2s, as device-scope atomics are, so a
+// split that finishes on one XCD and the split that combines on another need
+// no L2 write-back or invalidation (each costs far more than the few kilobytes
+// it would publish).  Offsets are bytes from the slot array's base (the host
+// keeps the array under 2 GiB).
+constexpr int kDeviceScope = 16;  // the SC1 bit of the gfx950 cache-policy field
+
+__device__ __forceinline__ void slot_store4(rsrc_t r, uint32_t off, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, kDeviceScope);
 }
-__device__ __forceinline__ float slot_load(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ void slot_store1(rsrc_t r, uint32_t off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, off, 0, kDeviceScope);
+}
+__device__ __forceinline__ f32x4 slot_load4(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kDeviceScope));
+}
+__device__ __forceinline__ float slot_load1(rsrc_t r, uint32_t off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kDeviceScope));
+}
+
+// Buffer resources over the slot arrays A and L of the call's slots.
+template <int D>
+__device__ __forceinline__ void slot_rsrc(const DecodeArgs& a, rsrc_t* ra, rsrc_t* rl) {
+  const uint32_t rows = static_cast<uint32_t>(
+      static_cast<size_t>(a.slot_offset + a.num_splits) * a.geo.batch * a.geo.heads);
+  *ra = make_rsrc(a.part_A, rows * static_cast<uint32_t>(D) * 4u);
+  *rl = make_rsrc(a.part_L, rows * 4u);
 }
 
 // The last of a (kv sequence, kv head)'s splits adds their slots for the
@@ -299,6 +318,8 @@ __device__ __forceinline__ void fused_combine(const DecodeArgs& a, const FusedEx
   __syncthreads();
   if (!last) return;
   const size_t nrows = static_cast<size_t>(g.batch) * g.heads;
+  rsrc_t ra, rl;
+  slot_rsrc<D>(a, &ra, &rl);
   for (int f = threadIdx.x; f < 16 * (D / 4); f += kScanThreads) {
     const int r = f / (D / 4);
     const int d = 4 * (f % (D / 4));
@@ -312,10 +333,9 @@ __device__ __forceinline__ void fused_combine(const DecodeArgs& a, const FusedEx
       float lv[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const size_t sr = static_cast<size_t>(a.slot_offset + s + u) * nrows + xr;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) av[u][i] = slot_load(a.part_A + sr * D + d + i);
-        lv[u] = slot_load(a.part_L + sr);
+        const uint32_t sr = static_cast<uint32_t>(static_cast<size_t>(a.slot_offset + s + u) * nrows + xr);
+        av[u] = slot_load4(ra, (sr * D + d) * 4u);
+        lv[u] = slot_load1(rl, sr * 4u);
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -324,12 +344,9 @@ __device__ __forceinline__ void fused_combine(const DecodeArgs& a, const FusedEx
       }
     }
     for (; s < a.num_splits; ++s) {
-      const size_t sr = static_cast<size_t>(a.slot_offset + s) * nrows + xr;
-      f32x4 av;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) av[i] = slot_load(a.part_A + sr * D + d + i);
-      acc += av;
-      l += slot_load(a.part_L + sr);
+      const uint32_t sr = static_cast<uint32_t>(static_cast<size_t>(a.slot_offset + s) * nrows + xr);
+      acc += slot_load4(ra, (sr * D + d) * 4u);
+      l += slot_load1(rl, sr * 4u);
     }
     float o[4];
     bool nf = false;
@@ -490,6 +507,8 @@ __device__ __forceinline__ void packed_scan(const DecodeArgs& a, const FusedExtr
   __syncthreads();
   const size_t slot_rows = (static_cast<size_t>(a.slot_offset) + sc.p.split) * g.batch * g.heads;
   const bool vec_ok = (reinterpret_cast<uintptr_t>(a.part_A) & 15u) == 0;
+  rsrc_t ra, rl;  // FUSED: the slot arrays
+  if constexpr (FUSED) slot_rsrc<D>(a, &ra, &rl);
   for (int f = threadIdx.x; f < 16 * (D / 4); f += kScanThreads) {
     const int r = f / (D / 4);
     const int d = 4 * (f % (D / 4));
@@ -504,8 +523,8 @@ __device__ __forceinline__ void packed_scan(const DecodeArgs& a, const FusedExtr
     }
     float* dst = a.part_A + (slot_rows + static_cast<size_t>(xr)) * D + d;
     if constexpr (FUSED) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) slot_store(dst + i, v[i]);
+      slot_store4(ra, static_cast<uint32_t>((slot_rows + static_cast<size_t>(xr)) * D + d) * 4u,
+                  f32x4{v[0], v[1], v[2], v[3]});
     } else if (vec_ok) {
       *reinterpret_cast<f32x4*>(dst) = f32x4{v[0], v[1], v[2], v[3]};
     } else {
@@ -520,7 +539,7 @@ __device__ __forceinline__ void packed_scan(const DecodeArgs& a, const FusedExtr
     const float v = ((red[e] + red[kWaveFloats + e]) + red[2 * kWaveFloats + e]) + red[3 * kWaveFloats + e];
     if (xr >= 0) {
       if (FUSED && threadIdx.x < 16)
-        slot_store(a.part_L + slot_rows + static_cast<size_t>(xr), v);
+        slot_store1(rl, static_cast<uint32_t>(slot_rows + static_cast<size_t>(xr)) * 4u, v);
       else if (threadIdx.x < 16)
         a.part_L[slot_rows + static_cast<size_t>(xr)] = v;
       else if (a.part_Lcut)

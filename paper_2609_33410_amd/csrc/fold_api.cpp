@@ -313,6 +313,8 @@ fold_status fold_decode_fused(const fold_kv_view* kv, const fold_q_view* q, floa
   if (st != FOLD_OK) return st;
   const long long blocks = static_cast<long long>(kv->num_seqs) * kv->num_kv_heads * num_splits;
   if (blocks > 0x7fffffffLL) return fail(FOLD_E_INVAL, "grid too large");
+  if (static_cast<long long>(num_splits) * q->batch * q->num_heads * kv->head_dim * 4 >= (1LL << 31))
+    return fail(FOLD_E_UNSUPPORTED, "the fused decode's slots must stay under 2 GiB");
   a.q = static_cast<const uint16_t*>(q->q);
   a.z = nullptr;
   a.part_A = part_A;
