@@ -198,7 +198,9 @@ __device__ __forceinline__ void estimate_rows(const Q8EstimateArgs& qa8, int req
   // Tiles of 16 samples; wave w scores tiles w, w+4, ...; lane l loads sample l%16.
   const int ntiles = (m + 15) / 16;
   // One pass: the loads of tiles tau0, tau0 + 4, ... (clamped samples for
-  // tiles past the end), then hook(), then the scores of the tiles that exist.
+  // tiles past the end), then hook(), then the scores of every tile loaded
+  // (those past the end are not stored), so that no load is left in flight
+  // unread: a later wait would count it.
   auto pass = [&](int tau0, auto&& hook) {
     int jb[kTilesPerPass];
 #pragma unroll
@@ -212,8 +214,12 @@ __device__ __forceinline__ void estimate_rows(const Q8EstimateArgs& qa8, int req
       phys[u] = g.page_size > 0
                     ? g.block_table[static_cast<size_t>(req) * g.max_pages + jb[u] / g.page_size]
                     : 0;
+    // Raw loads; a lane whose sample is past the end or on a page outside
+    // the pool (okl false) contributes zeros, applied after hook() so that no
+    // wait for a load precedes the caller's loads.
     u32x4 kv[kTilesPerPass][NK];
-    float ks[kTilesPerPass];  // Q8: the scale of this lane's sample
+    uint16_t ksr[kTilesPerPass];  // Q8: the scale of this lane's sample
+    bool okl[kTilesPerPass];
 #pragma unroll
     for (int u = 0; u < kTilesPerPass; ++u) {
       const int t = 16 * (tau0 + kScanWavesEst * u) + n16;
@@ -235,37 +241,40 @@ __device__ __forceinline__ void estimate_rows(const Q8EstimateArgs& qa8, int req
           v = *reinterpret_cast<const u32x4*>(qa8.keys.ka + krow * D + 64 * c + 16 * grp);
         else
           v = *reinterpret_cast<const u32x4*>(g.k + krow * D + 32 * c + 8 * grp);
-        kv[u][c] = ok ? v : u32x4{0, 0, 0, 0};
+        kv[u][c] = v;
       }
-      ks[u] = 0.0f;
-      if constexpr (Q8) ks[u] = ok ? bf16_lo(qa8.keys.ks[krow]) : 0.0f;
+      okl[u] = ok;
+      ksr[u] = 0;
+      if constexpr (Q8) ksr[u] = qa8.keys.ks[krow];
     }
     hook();
 #pragma unroll
     for (int u = 0; u < kTilesPerPass; ++u) {
       const int tau = tau0 + kScanWavesEst * u;
-      if (tau >= ntiles) break;  // uniform
       float sv[4];
       if constexpr (Q8) {
         i32x4 caa = {0, 0, 0, 0}, cab = {0, 0, 0, 0};
 #pragma unroll
         for (int c = 0; c < NK; ++c) {
-          caa = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, kv[u][c]),
+          const u32x4 ka = okl[u] ? kv[u][c] : u32x4{0, 0, 0, 0};
+          caa = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, ka),
                                                      __builtin_bit_cast(i32x4, qb[c]), caa, 0, 0, 0);
-          cab = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, kv[u][c]),
+          cab = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, ka),
                                                      __builtin_bit_cast(i32x4, qb2[c]), cab, 0, 0, 0);
         }
+        const float ks = okl[u] ? bf16_lo(ksr[u]) : 0.0f;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           // the scale of sample 4(l/16)+i sits in lane 4(l/16)+i
-          const float e = __shfl(ks[u], 4 * grp + i, 64);
+          const float e = __shfl(ks, 4 * grp + i, 64);
           const float t = static_cast<float>(caa[i]) + static_cast<float>(cab[i]) * (1.0f / 256.0f);
           sv[i] = (eta_r * e) * t;
         }
       } else {
         f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int c = 0; c < NK; ++c) s = mfma_16x16x32(kv[u][c], qb[c], s);
+        for (int c = 0; c < NK; ++c)
+          s = mfma_16x16x32(okl[u] ? kv[u][c] : u32x4{0, 0, 0, 0}, qb[c], s);
 #pragma unroll
         for (int i = 0; i < 4; ++i) sv[i] = s[i] * a.score_scale;
       }
