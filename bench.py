@@ -200,6 +200,22 @@ class Q8Path:
     def estimate(self, stream):
         self.F.fold_q8_ref_estimate(self.flat, self.keys, self.qq, self.z, stream=stream)
 
+    def fusable(self):
+        lv = self.wl.levels[0]
+        return (len(self.wl.levels) == 1 and lv.row_indptr is None and self.wl.group <= 8
+                and lv.num_seqs == self.wl.batch)
+
+    def fused(self, T, stream):
+        """Front, scan and combine in one launch (fold_q8_decode_fused)."""
+        if not hasattr(self, "arrivals"):
+            self.arrivals = self.torch.zeros(self.wl.levels[0].num_seqs, self.wl.num_kv_heads,
+                                             dtype=self.torch.int32, device=self.wl.q.device)
+        self.F.fold_q8_decode_fused(self.levels[0], self.keys, self.wl.q, self.wl.sm_scale,
+                                    self.qq, self.wl.flat.seq_lens, T, self.splits[0],
+                                    self.part_A, self.part_L, self.arrivals, self.z, self.out,
+                                    values=self.vals, kappa=self.kappa, kappa_v=self.kappa_v,
+                                    stream=stream)
+
     def front(self, stream):
         """Query split and reference estimate in one launch (fold_q8_front)."""
         self.F.fold_q8_front(self.flat, self.keys, self.wl.q, self.wl.sm_scale, self.qq, self.z,
@@ -325,7 +341,8 @@ def time_q8(qp, T, steps, warmup, flush, torch):
     ``split_then_est`` times the same step with the split and the estimate
     as two launches."""
     stream = torch.cuda.current_stream()
-    res = {"front": [], "dec": [], "comb": [], "step": [], "append": [], "split_then_est": []}
+    res = {"front": [], "dec": [], "comb": [], "step": [], "append": [], "split_then_est": [],
+           "fused": []}
     for it in range(warmup + steps):
         evict_caches(flush)
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
@@ -344,23 +361,29 @@ def time_q8(qp, T, steps, warmup, flush, torch):
             res["dec"].append(ev[1].elapsed_time(ev[2]))
             res["comb"].append(ev[2].elapsed_time(ev[3]))
             res["append"].append(ev[3].elapsed_time(ev[4]))
+    one = qp.fusable()
     for it in range(warmup + steps):
-        for key, fused in (("step", True), ("split_then_est", False)):
+        for key in ("step", "split_then_est") + (("fused",) if one else ()):
             evict_caches(flush)
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-            if fused:
-                qp.front(stream)
+            if key == "fused":
+                qp.fused(T, stream)
             else:
-                qp.split(stream)
-                qp.estimate(stream)
-            qp.decode(T, stream)
-            qp.combine(stream)
+                if key == "step":
+                    qp.front(stream)
+                else:
+                    qp.split(stream)
+                    qp.estimate(stream)
+                qp.decode(T, stream)
+                qp.combine(stream)
             e1.record(stream)
             if it >= warmup:
                 e1.synchronize()
                 res[key].append(e0.elapsed_time(e1))
+    if not one:
+        del res["fused"]
     return {k: statistics.median(v) for k, v in res.items()}
 
 
@@ -375,7 +398,8 @@ def q8_leg(wl, F, torch, flush, steps, warmup, name=None, values8=False):
                     ("two E4M3 value planes, scale 2^%d" % qp.vals.scale_exp if values8
                      else "BF16 values"),
            "step": "front (query split + estimate from coarse logits, one launch) + split "
-                   "scan + combine; the one-token append is timed apart"}
+                   "scan + combine; the one-token append is timed apart; breakdown `fused`: "
+                   "the same call as one launch (fold_q8_decode_fused), slower here"}
     if values8:
         out["kappa_v"] = qp.kappa_v
     for T in (math.inf, 16.0):

@@ -33,6 +33,7 @@
 
 #include "fold_device.h"
 #include "fold_internal.h"
+#include "q8_split.h"
 
 namespace fold {
 namespace est {
@@ -128,6 +129,58 @@ __device__ __forceinline__ int sample_index(int t, int n, bool stratified, int s
   const int lo = sink + static_cast<int>(floor(static_cast<double>(b) * rmid / strata));
   const int hi = sink + static_cast<int>(floor(static_cast<double>(b + 1) * rmid / strata));
   return (lo + hi - 1) / 2;
+}
+
+// Refine threshold of a request of nr query rows: kappa + ceil(log2 nr)
+// (the query split's rule).
+__device__ __forceinline__ float refine_threshold(float kappa, int nr) {
+  const int c = nr > 1 ? 32 - __builtin_clz(static_cast<unsigned>(nr - 1)) : 0;
+  return kappa + static_cast<float>(c);
+}
+
+// The fused front's query split of the GQA rows of (req, kvh), wave w taking
+// rows w, w+4, ...: the query split's own transform and rounding (so the
+// codes are the same bits), into qs / etas in LDS and, when write_out, to
+// qa8.qp_out / eta_out and the request's thresholds.  The caller puts a
+// barrier before reading qs / etas.
+template <int D>
+__device__ __forceinline__ void front_split_rows(const Q8EstimateArgs& qa8, int req, int kvh,
+                                                 int8_t (*qs)[2 * D], float* etas,
+                                                 bool write_out) {
+  const ScanGeometry& g = qa8.e.geo;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int G = g.group;
+  for (int r = wave; r < G; r += kThreads / 64) {
+    const size_t row = static_cast<size_t>(req) * g.heads + kvh * G + r;
+    double x[D / 64];
+#pragma unroll
+    for (int i = 0; i < D / 64; ++i)
+      x[i] = static_cast<double>(bf16_lo(qa8.q_src[row * D + 64 * i + lane]));
+    hadamard_wave<D>(x, lane);
+    const double f = wave_absmax_f64<D>(x) / 127.0;
+#pragma unroll
+    for (int i = 0; i < D / 64; ++i) {
+      int8_t ca, cb;
+      split_value(x[i], f, &ca, &cb);
+      if (write_out) {
+        qa8.qp_out[row * 2 * D + 64 * i + lane] = ca;
+        qa8.qp_out[row * 2 * D + D + 64 * i + lane] = cb;
+      }
+      qs[r][64 * i + lane] = ca;
+      qs[r][D + 64 * i + lane] = cb;
+    }
+    if (lane == 0) {
+      const float eta = static_cast<float>(((kLog2eF64 * static_cast<double>(qa8.sm_scale)) * f) / D);
+      if (write_out) qa8.eta_out[row] = eta;
+      etas[r] = eta;
+    }
+  }
+  if (write_out && kvh == 0 && qa8.tau && threadIdx.x == 0) {
+    const int nr = qa8.req_lens[req];
+    qa8.tau[req] = refine_threshold(qa8.kappa, nr);
+    if (qa8.tau_v) qa8.tau_v[req] = refine_threshold(qa8.kappa_v, nr);
+  }
 }
 
 // Z of the GQA rows of (req, kvh), computed by all four waves of the

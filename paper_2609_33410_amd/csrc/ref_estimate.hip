@@ -32,35 +32,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs
   __shared__ __attribute__((aligned(16))) int8_t qs[FRONT ? kMaxEstRows : 1][2 * D];
   __shared__ float etas[FRONT ? kMaxEstRows : 1];
   if constexpr (FRONT) {
-    for (int r = wave; r < G; r += kThreads / 64) {
-      const size_t row = static_cast<size_t>(req) * g.heads + kvh * G + r;
-      double x[D / 64];
-#pragma unroll
-      for (int i = 0; i < D / 64; ++i)
-        x[i] = static_cast<double>(bf16_lo(qa8.q_src[row * D + 64 * i + lane]));
-      hadamard_wave<D>(x, lane);
-      const double f = wave_absmax_f64<D>(x) / 127.0;
-#pragma unroll
-      for (int i = 0; i < D / 64; ++i) {
-        int8_t ca, cb;
-        split_value(x[i], f, &ca, &cb);
-        qa8.qp_out[row * 2 * D + 64 * i + lane] = ca;
-        qa8.qp_out[row * 2 * D + D + 64 * i + lane] = cb;
-        qs[r][64 * i + lane] = ca;
-        qs[r][D + 64 * i + lane] = cb;
-      }
-      if (lane == 0) {
-        const float eta = static_cast<float>(((kLog2eF64 * static_cast<double>(qa8.sm_scale)) * f) / D);
-        qa8.eta_out[row] = eta;
-        etas[r] = eta;
-      }
-    }
-    if (kvh == 0 && qa8.tau && threadIdx.x == 0) {
-      const int nr = qa8.req_lens[req];
-      const int c = nr > 1 ? 32 - __builtin_clz(static_cast<unsigned>(nr - 1)) : 0;
-      qa8.tau[req] = qa8.kappa + static_cast<float>(c);
-      if (qa8.tau_v) qa8.tau_v[req] = qa8.kappa_v + static_cast<float>(c);
-    }
+    est::front_split_rows<D>(qa8, req, kvh, qs, etas, true);
     __syncthreads();
   }
 

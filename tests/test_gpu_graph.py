@@ -57,3 +57,46 @@ def test_graph_replays_match_eager(cfg, T):
         step(torch.cuda.current_stream())  # eager work between replays
         torch.cuda.synchronize()
         assert torch.equal(out, eager)
+
+
+@pytest.mark.parametrize("T", [math.inf, 16.0])
+def test_graph_replays_of_the_fused_call(T):
+    """The one-launch decode captured in a graph: every replay gives the eager
+    bits and leaves the arrival counts at zero (they reset themselves, so the
+    graph holds no memset), with eager calls on the same counters in between."""
+    import paper_2609_33410_amd as F
+
+    wl = make_config(2, device="cuda", batch=4, seq_len=3000)
+    (kv,), _ = _gpu.kv_views(wl)
+    qv = F.q_view(wl.q)
+    b, h, d = wl.q.shape
+    s = 4
+    z = torch.empty(b, h, dtype=torch.float32, device="cuda")
+    part_a = torch.empty(s, b, h, d, dtype=torch.float32, device="cuda")
+    part_l = torch.empty(s, b, h, dtype=torch.float32, device="cuda")
+    arrivals = torch.zeros(b, wl.num_kv_heads, dtype=torch.int32, device="cuda")
+    out = torch.empty(b, h, d, dtype=torch.float32, device="cuda")
+    lse = torch.empty(b, h, dtype=torch.float32, device="cuda")
+
+    def call(stream):
+        F.fold_decode_fused(kv, qv, wl.sm_scale, T, s, part_a, part_l, arrivals, z, out,
+                            lse_out=lse, stream=stream)
+
+    call(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    eager, eager_lse = out.clone(), lse.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(torch.cuda.current_stream())
+    for it in range(4):
+        out.fill_(float("nan"))
+        lse.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), f"replay {it} differs from the eager call"
+        assert torch.equal(lse, eager_lse)
+        assert int(arrivals.abs().sum()) == 0
+        call(torch.cuda.current_stream())  # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager)
