@@ -17,18 +17,14 @@ using est::kThreads;
 template <int D, bool Q8, bool FRONT = false>
 __global__ __launch_bounds__(kThreads) void estimate_kernel(const Q8EstimateArgs qa8) {
   const ScanGeometry& g = qa8.e.geo;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int req = blockIdx.x / g.hkv;
   const int kvh = blockIdx.x % g.hkv;
-  const int G = g.group;
 
   __shared__ float sc[kMaxEstRows][kMaxEstSamples];
 
-  // Fused front: split the query rows of this (request, kv head) first, wave w
-  // taking rows w, w+4, ... (the query split's own transform and rounding, so
-  // the codes are the same bits); the codes go out for the scan and into LDS
-  // for the scoring below.
+  // Fused front: split the query rows of this (request, kv head) first (the
+  // query split's own transform and rounding, so the codes are the same bits);
+  // the codes go out for the scan and into LDS for the scoring below.
   __shared__ __attribute__((aligned(16))) int8_t qs[FRONT ? kMaxEstRows : 1][2 * D];
   __shared__ float etas[FRONT ? kMaxEstRows : 1];
   if constexpr (FRONT) {
