@@ -362,3 +362,52 @@ def test_draft_gather_rejects_bad_args(lib):
                                  None) == F.FOLD_E_INVAL                    # misaligned rows
     assert lib.fold_draft_gather(ctypes.byref(kv), None, V(FAKE), V(FAKE), V(FAKE), 2, 1, 256,
                                  V(FAKE), V(FAKE), None, None) == F.FOLD_E_INVAL
+
+
+# ------------------------------------------------------ one-launch decodes --
+def _fused(lib, kv=None, q=None, T=math.inf, splits=2, part_a=FAKE, arrivals=FAKE, out=FAKE,
+           out_dtype=0):
+    return lib.fold_decode_fused(ctypes.byref(kv or _kv()), ctypes.byref(q or _q()), 0.125, None,
+                                 T, splits, part_a, FAKE, arrivals, FAKE, out, out_dtype, None,
+                                 None, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    ({"arrivals": None}, F.FOLD_E_INVAL),
+    ({"T": float("nan")}, F.FOLD_E_INVAL),
+    ({"splits": 0}, F.FOLD_E_INVAL),
+    ({"out_dtype": 7}, F.FOLD_E_INVAL),
+    ({"out": FAKE + 4}, F.FOLD_E_INVAL),                  # misaligned output
+    ({"part_a": FAKE + 8}, F.FOLD_E_INVAL),               # misaligned slots
+    ({"q": _q(num_heads=2)}, F.FOLD_E_UNSUPPORTED),       # MHA
+    ({"q": _q(num_heads=32)}, F.FOLD_E_UNSUPPORTED),      # groups of 16 rows
+    ({"kv": _kv(num_seqs=1)}, F.FOLD_E_INVAL),            # num_seqs != batch
+    ({"kv": _kv(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=2)}, F.FOLD_E_INVAL),
+    ({"splits": 1 << 20}, F.FOLD_E_UNSUPPORTED),          # slots of 8 GiB
+])
+def test_fused_decode_rejects_bad_args(lib, kw, want):
+    """Every refusal happens in validation, before anything is launched."""
+    assert _fused(lib, **kw) == want
+    assert len(lib.fold_last_error()) > 0
+
+
+@pytest.mark.parametrize("kw,want", [
+    ({"req_lens": None}, F.FOLD_E_INVAL),
+    ({"planes": None}, F.FOLD_E_INVAL),
+    ({"arrivals": None}, F.FOLD_E_INVAL),
+    ({"heads": 32}, F.FOLD_E_UNSUPPORTED),                # groups of 16 rows
+    ({"kappa": float("nan")}, F.FOLD_E_INVAL),
+    ({"splits": 0}, F.FOLD_E_INVAL),
+])
+def test_q8_fused_decode_rejects_bad_args(lib, kw, want):
+    args = {"req_lens": FAKE, "planes": FAKE, "arrivals": FAKE, "heads": 8, "kappa": 0.0,
+            "splits": 2}
+    args.update(kw)
+    keys, _ = _q8()
+    q = _q(num_heads=args["heads"])
+    st = lib.fold_q8_decode_fused(ctypes.byref(_kv()), ctypes.byref(keys), ctypes.byref(q), 0.125,
+                                  args["req_lens"], args["kappa"], 0.0, None, None, math.inf,
+                                  args["splits"], FAKE, FAKE, args["arrivals"], args["planes"],
+                                  FAKE, None, None, FAKE, FAKE, 0, None, None, None)
+    assert st == want
+    assert len(lib.fold_last_error()) > 0
