@@ -35,8 +35,10 @@ Readings of points the paper leaves open are listed in the design notes of
 the repository (score scale, tie at the threshold, cut keys' value, gate
 granularity, estimator details, empty rows, combine order).
 
-Parity status: O1-O8 are pinned by the CPU tests (closed forms, textbook and
-library softmax, invariants, hand-computed fixtures).  The estimator's
+Parity status: O1-O9 are pinned by the CPU tests (closed forms, textbook and
+library softmax, invariants, hand-computed fixtures; O9 by a hand-computed
+fixture of exact binary fractions and by an independent FP64 evaluation of
+the Proposition 1(iii) left side on every row of every workload).  The estimator's
 stratified/trimmed branch (n > 192) is pinned only structurally (exact
 cases, which keys it reads, what its trim discards); the paper prints no
 value to check it against, so its exact value is "parity unpinned".

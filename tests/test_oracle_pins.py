@@ -292,22 +292,93 @@ def test_additive_combine_equals_lse_merge_and_online_softmax():
 # ------------------------------------------------------------- P8 ----------
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
 def test_prop1_range_condition_every_row(cfg):
-    """Prop. 1(iii) holds on every row with the estimated reference."""
-    wl = make_config(cfg, batch=2 if cfg != 1 else None, seq_len=2048 if cfg != 1 else None)
+    """Prop. 1(iii) holds on every row with the estimated reference.
+
+    The left side m - Z + log2(n nu) and L = 2^(lse - Z) are formed here
+    from the generator's logical cache (before paging) with torch in FP64
+    and torch's logsumexp, independently of the oracle's gather, scores and
+    diagnostics; the oracle's O9 figures must agree with them."""
+    wl = make_config(cfg, batch=2 if cfg != 1 else None, seq_len=2048 if cfg != 1 else None,
+                     keep_logical=True)
     oi = _adapt.oracle_inputs(wl)
     z = _adapt.estimate(oi)
     q = oracle.bf16_bits_to_f64(oi["q_bits"])
     fl = oi["flat"]
     group = wl.group
+    qt = wl.q.double()
+    log2e = 1.0 / math.log(2.0)
     for r, n in enumerate(fl["seq_lens"]):
         for h in range(wl.num_heads):
             g = h // group
+            kl = wl.logical_k[r, g, :n].double()
+            vl = wl.logical_v[r, g, :n].double()
+            s_ind = (kl @ qt[r, h]) * (wl.sm_scale * log2e)
+            m_ind = float(s_ind.max())
+            nu_ind = max(1.0, float(vl.abs().max()))
+            lhs_ind = m_ind - float(z[r, h]) + math.log2(n * nu_ind)
+            lse_ind = float(torch.logsumexp(s_ind * math.log(2.0), dim=0)) * log2e
+            assert lhs_ind < 127.0
             k = oracle.gather(oi["k_bits"], r, g, n, fl["block_table"], wl.page_size)
             v = oracle.gather(oi["v_bits"], r, g, n, fl["block_table"], wl.page_size)
             s = oracle.scores(q[r, h:h + 1], k, wl.sm_scale)[0]
             d = oracle.row_diagnostics(s, z[r, h], INF, v)
-            assert d["prop1_lhs"] < 127.0
-            assert CERT_OK(d["L"])
+            assert abs(d["prop1_lhs"] - lhs_ind) <= 1e-9 * max(1.0, abs(lhs_ind))
+            assert abs(d["lse"] - lse_ind) <= 1e-9 * max(1.0, abs(lse_ind))
+            assert abs(d["headroom"] - (lse_ind - float(z[r, h]))) <= 1e-9 * max(1.0, abs(lse_ind))
+            l_ind = 2.0 ** (lse_ind - float(z[r, h]))
+            assert abs(d["L"] - l_ind) <= 1e-9 * l_ind
+            assert CERT_OK(l_ind)
+
+
+# ------------------------------------------------------------- O9 ----------
+def _row_diag_fixture():
+    with open(os.path.join(GOLDEN, "row_diagnostics_example.json")) as f:
+        return json.load(f)
+
+
+@pytest.mark.parametrize("row", [0, 1])
+def test_row_diagnostics_hand_computed(row):
+    """Hand-computed fixture (exact binary fractions): every O9 figure --
+    m, lse, headroom, the Prop. 1(iii) left side, L, the cut mass, the
+    truncation bound and the live fraction -- at several depths, ties on
+    the threshold included."""
+    fx = _row_diag_fixture()
+    s = np.array(fx["scores"], dtype=np.float64)
+    rw = fx["rows"][row]
+    v = np.array(rw["values"], dtype=np.float64)
+    for case in rw["cases"]:
+        d = oracle.row_diagnostics(s, rw["z"], _T(case["T"]), v)
+        want = dict(rw["common"])
+        want.update({k: case[k] for k in ("w_cut", "bound_T", "live_frac")})
+        for key, val in want.items():
+            assert d[key] == pytest.approx(val, rel=1e-15, abs=1e-300), (rw["name"], case["T"], key)
+
+
+def test_row_diagnostics_fixture_is_what_its_derivation_says():
+    """The fixture's own arithmetic, redone in exact rationals: sum 2^s = 16,
+    L = 2^(lse - Z), the cut sets on the ties, and nu over every key."""
+    from fractions import Fraction as Fr
+
+    fx = _row_diag_fixture()
+    s = [int(x) for x in fx["scores"]]
+    tot = sum(Fr(2) ** e for e in s)
+    assert tot == 16
+    for rw in fx["rows"]:
+        z = int(rw["z"])
+        w = [Fr(2) ** (e - z) for e in s]
+        assert sum(w) == Fr(rw["common"]["L"]) == Fr(2) ** (4 - z)
+        vals = [[Fr(x) for x in row] for row in rw["values"]]
+        nu = max(Fr(1), max(abs(x) for row in vals for x in row))
+        lhs = max(s) - z + math.log2(len(s) * nu)
+        assert lhs == rw["common"]["prop1_lhs"]
+        for case in rw["cases"]:
+            T = _T(case["T"])
+            cut = [i for i, e in enumerate(s) if not (math.isinf(T) or e - z >= -T)]
+            wc = sum((w[i] for i in cut), Fr(0))
+            assert wc == Fr(case["w_cut"])
+            vmax = max((max(abs(x) for x in vals[i]) for i in cut), default=Fr(0))
+            assert wc / sum(w) * vmax == Fr(case["bound_T"])
+            assert Fr(len(s) - len(cut), len(s)) == Fr(case["live_frac"])
 
 
 def CERT_OK(l):
