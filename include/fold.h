@@ -29,7 +29,11 @@
  *     can address (max_seq_len, or max_pages_per_seq * page_size); a page id
  *     outside [0, num_pages) and a row request outside [0, batch) are skipped
  *     (they contribute nothing and are never dereferenced).
- *   - Results are deterministic: no atomics; every sum has a fixed order.
+ *   - Results are deterministic: every sum has a fixed order.  The
+ *     three-call path uses no atomics; the one-launch decodes count split
+ *     arrivals with one atomic add per workgroup, and the split that counts
+ *     last adds the slots in slot order, so arrival order never changes a
+ *     bit of the result.
  */
 #ifndef FOLD_H
 #define FOLD_H

@@ -54,7 +54,21 @@ __device__ __forceinline__ void fused_combine(const DecodeArgs& a, const FusedEx
   __shared__ int last;
   __shared__ float lrow[16];
   __shared__ int bad[16];
+  // Ordering of the handoff.  The slot stores and loads carry SC1, the
+  // encoding the memory model gives device-scope atomic stores and loads on
+  // this target, so each one is coherent across XCDs by itself and the
+  // protocol needs no L2 write-back or invalidate (a device-scope release
+  // fence per workgroup, which issues one, costs 15 us per call on the
+  // Llama-3-8B-shaped decode).  What remains is ordering:
+  //  * hardware: s_waitcnt vmcnt(0) returns only after every slot store of
+  //    the wave is acknowledged, and the barrier makes all four waves wait
+  //    before the one atomic add; the last arriver's slot loads are issued
+  //    after it has read the count through LDS and a second barrier;
+  //  * compiler: the signal fences are compiler barriers (no instruction),
+  //    so no slot store sinks below the count and no slot load rises above
+  //    it whatever code generation does around the barriers.
   __builtin_amdgcn_s_waitcnt(0);  // this wave's slot stores are complete
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
   __syncthreads();
   int32_t* ctr = x.arrivals + static_cast<size_t>(p.seq) * g.hkv + p.kvh;
   if (threadIdx.x == 0)
@@ -64,6 +78,7 @@ __device__ __forceinline__ void fused_combine(const DecodeArgs& a, const FusedEx
                : 0;
   if (threadIdx.x < 16) bad[threadIdx.x] = 0;
   __syncthreads();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
   if (!last) return;
   const size_t nrows = static_cast<size_t>(g.batch) * g.heads;
   rsrc_t ra, rl;

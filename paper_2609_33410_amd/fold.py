@@ -251,6 +251,54 @@ def _need(t: torch.Tensor, name: str, dtype: torch.dtype) -> None:
         raise ValueError(f"{name} must be contiguous")
 
 
+def _need_device(named) -> None:
+    """Every tensor handed to a launch must live in device memory."""
+    for nm, t in named:
+        if t is not None and not t.is_cuda:
+            raise ValueError(f"{nm} must be a device tensor")
+
+
+def _slot_checks(q: torch.Tensor, part_A: torch.Tensor, part_L: torch.Tensor,
+                 part_Lcut: Optional[torch.Tensor], z: Optional[torch.Tensor]) -> None:
+    """Slots are [slots, B, H, D] / [slots, B, H] for the query [B, H, D]."""
+    b, h, d = (int(x) for x in q.shape)
+    if part_A.dim() != 4 or tuple(part_A.shape[1:]) != (b, h, d):
+        raise ValueError(f"part_A must be [slots, {b}, {h}, {d}], got {tuple(part_A.shape)}")
+    for t, nm in ((part_L, "part_L"), (part_Lcut, "part_Lcut")):
+        if t is not None and (t.dim() != 3 or tuple(t.shape) != (int(part_A.shape[0]), b, h)):
+            raise ValueError(f"{nm} must be [{int(part_A.shape[0])}, {b}, {h}], "
+                             f"got {tuple(t.shape)}")
+    if z is not None and z.numel() < b * h:
+        raise ValueError(f"z needs {b * h} elements, got {z.numel()}")
+
+
+def _fused_checks(kv: KV, q: torch.Tensor, num_splits: int, part_A: torch.Tensor,
+                  part_L: torch.Tensor, arrivals: torch.Tensor, z_out: torch.Tensor,
+                  out: torch.Tensor, lse_out: Optional[torch.Tensor],
+                  cert_out: Optional[torch.Tensor], extra=()) -> None:
+    """Sizes of the one-launch decodes' workspace and outputs: the kernels
+    write every slot, arrival count and output row the view and the query
+    imply, so a short tensor would be written past its end."""
+    b, h, d = (int(x) for x in q.shape)
+    if part_A.dim() != 4 or tuple(part_A.shape[1:]) != (b, h, d):
+        raise ValueError(f"part_A must be [slots, {b}, {h}, {d}], got {tuple(part_A.shape)}")
+    if part_L.dim() != 3 or tuple(part_L.shape[1:]) != (b, h):
+        raise ValueError(f"part_L must be [slots, {b}, {h}], got {tuple(part_L.shape)}")
+    if int(part_A.shape[0]) < num_splits or int(part_L.shape[0]) < num_splits:
+        raise ValueError("part_A and part_L need num_splits slots")
+    need = int(kv.view.num_seqs) * int(kv.view.num_kv_heads)
+    if arrivals.numel() < need:
+        raise ValueError(f"arrivals needs num_seqs * num_kv_heads = {need} counters, "
+                         f"got {arrivals.numel()}")
+    for t, nm, n in ((z_out, "z_out", b * h), (out, "out", b * h * d),
+                     (lse_out, "lse_out", b * h), (cert_out, "cert_out", b * h)):
+        if t is not None and t.numel() < n:
+            raise ValueError(f"{nm} needs {n} elements, got {t.numel()}")
+    _need_device([("q", q), ("part_A", part_A), ("part_L", part_L), ("arrivals", arrivals),
+                  ("z_out", z_out), ("out", out), ("lse_out", lse_out), ("cert_out", cert_out)]
+                 + [(f"view tensor {i}", t) for i, t in enumerate(kv.tensors)] + list(extra))
+
+
 @dataclass
 class KV:
     """A cache view plus the tensors it points into (kept alive here)."""
@@ -342,6 +390,11 @@ def fold_decode_split(kv: KV, q: Q, sm_scale: float, z: torch.Tensor, depth_T: f
     _need(part_L, "part_L", torch.float32)
     if part_Lcut is not None:
         _need(part_Lcut, "part_Lcut", torch.float32)
+    _slot_checks(q.tensor, part_A, part_L, part_Lcut, z)
+    _need_device([("q", q.tensor), ("z", z), ("part_A", part_A), ("part_L", part_L),
+                  ("part_Lcut", part_Lcut), ("x_out", x_out), ("key_gate_out", key_gate_out),
+                  ("page_gate_out", page_gate_out)]
+                 + [(f"view tensor {i}", t) for i, t in enumerate(kv.tensors)])
     dbg = None
     if x_out is not None or key_gate_out is not None or page_gate_out is not None:
         for t, nm, dt in ((x_out, "x_out", torch.float32), (key_gate_out, "key_gate_out", torch.uint8),
@@ -414,8 +467,8 @@ def fold_decode_fused(kv: KV, q: Q, sm_scale: float, depth_T: float, num_splits:
         raise TypeError("out must be float32 or bfloat16")
     if not out.is_contiguous():
         raise ValueError("out must be contiguous")
-    if int(part_A.shape[0]) < num_splits or int(part_L.shape[0]) < num_splits:
-        raise ValueError("part_A and part_L need num_splits slots")
+    _fused_checks(kv, q.tensor, num_splits, part_A, part_L, arrivals, z_out, out, lse_out,
+                  cert_out)
     p = None
     if params is not None:
         p = fold_est_params(params["sink"], params["recent"], params["strata"],
@@ -793,8 +846,18 @@ def fold_q8_decode_fused(kv: KV, keys: Q8Keys, q: torch.Tensor, sm_scale: float,
         raise TypeError("out must be float32 or bfloat16")
     if not out.is_contiguous():
         raise ValueError("out must be contiguous")
-    if int(part_A.shape[0]) < num_splits or int(part_L.shape[0]) < num_splits:
-        raise ValueError("part_A and part_L need num_splits slots")
+    b, h, d = (int(x) for x in q.shape)
+    for t, nm, n in ((codes.planes, "planes", 2 * b * h * d), (codes.eta, "eta", b * h),
+                     (codes.tau, "tau", b), (codes.tau_v, "tau_v", b), (req_lens, "req_lens", b)):
+        if t is not None and t.numel() < n:
+            raise ValueError(f"{nm} needs {n} elements, got {t.numel()}")
+    extra = [("planes", codes.planes), ("eta", codes.eta), ("tau", codes.tau),
+             ("tau_v", codes.tau_v), ("req_lens", req_lens), ("plane_a", keys.plane_a),
+             ("plane_b", keys.plane_b), ("scale", keys.scale)]
+    if values is not None:
+        extra += [("plane_p", values.plane_p), ("plane_r", values.plane_r)]
+    _fused_checks(kv, q, num_splits, part_A, part_L, arrivals, z_out, out, lse_out, cert_out,
+                  extra)
     p = None
     if params is not None:
         p = fold_est_params(params["sink"], params["recent"], params["strata"],

@@ -411,3 +411,82 @@ def test_q8_fused_decode_rejects_bad_args(lib, kw, want):
                                   FAKE, None, None, FAKE, FAKE, 0, None, None, None)
     assert st == want
     assert len(lib.fold_last_error()) > 0
+
+
+# ------------------------------------- binding checks of the one-launch calls --
+def _fused_tensors(b=2, h=8, hkv=2, d=128, slots=2, npages=4):
+    import torch
+
+    bf = torch.bfloat16
+    t = {
+        "q": torch.zeros(b, h, d, dtype=bf),
+        "k": torch.zeros(npages, hkv, 16, d, dtype=bf),
+        "v": torch.zeros(npages, hkv, 16, d, dtype=bf),
+        "seq_lens": torch.full((b,), 32, dtype=torch.int32),
+        "block_table": torch.zeros(b, 2, dtype=torch.int32),
+        "part_A": torch.zeros(slots, b, h, d),
+        "part_L": torch.zeros(slots, b, h),
+        "arrivals": torch.zeros(b, hkv, dtype=torch.int32),
+        "z_out": torch.zeros(b, h),
+        "out": torch.zeros(b, h, d),
+        "lse_out": torch.zeros(b, h),
+        "cert_out": torch.zeros(b, h, dtype=torch.uint8),
+    }
+    return t
+
+
+def _call_fused(t, splits=2):
+    kv = F.kv_view(t["k"], t["v"], t["seq_lens"], num_kv_heads=t["k"].shape[1],
+                   max_seq_len=32, block_table=t["block_table"])
+    return F.fold_decode_fused(kv, F.q_view(t["q"]), 0.125, math.inf, splits, t["part_A"],
+                               t["part_L"], t["arrivals"], t["z_out"], t["out"],
+                               lse_out=t["lse_out"], cert_out=t["cert_out"])
+
+
+@pytest.mark.parametrize("name,shape,match", [
+    ("arrivals", (3,), "arrivals needs"),
+    ("part_A", (2, 2, 8, 64), "part_A must be"),
+    ("part_A", (2, 1, 8, 128), "part_A must be"),
+    ("part_L", (2, 2, 4), "part_L must be"),
+    ("part_L", (1, 2, 8), "num_splits slots"),
+    ("z_out", (2, 7), "z_out needs"),
+    ("out", (2, 8, 127), "out needs"),
+    ("lse_out", (15,), "lse_out needs"),
+    ("cert_out", (1, 8), "cert_out needs"),
+])
+def test_fused_binding_rejects_short_workspace(name, shape, match):
+    """The binding refuses a workspace or output too small for the view and
+    the query before the library is called (a short tensor would be written
+    past its end)."""
+    import torch
+
+    t = _fused_tensors()
+    t[name] = torch.zeros(shape, dtype=t[name].dtype)
+    with pytest.raises(ValueError, match=match):
+        _call_fused(t)
+
+
+def test_fused_binding_rejects_host_tensors():
+    """Correctly sized host tensors are refused as not in device memory."""
+    with pytest.raises(ValueError, match="device tensor"):
+        _call_fused(_fused_tensors())
+
+
+def test_q8_fused_binding_rejects_short_codes():
+    import torch
+
+    t = _fused_tensors()
+    kv = F.kv_view(t["k"], t["v"], t["seq_lens"], num_kv_heads=2, max_seq_len=32,
+                   block_table=t["block_table"])
+    keys = F.q8_empty_keys(t["k"])
+    codes = F.q8_empty_query(t["q"])
+    good = dict(codes=codes, req_lens=t["seq_lens"], arrivals=t["arrivals"])
+    bad = [("req_lens", dict(good, req_lens=torch.zeros(1, dtype=torch.int32)), "req_lens needs"),
+           ("arrivals", dict(good, arrivals=torch.zeros(1, dtype=torch.int32)), "arrivals needs"),
+           ("eta", dict(good, codes=F.fold.Q8Query(codes.planes, torch.zeros(3), codes.tau,
+                                                  codes.tau_v)), "eta needs")]
+    for _, kw, match in bad + [("host", good, "device tensor")]:
+        with pytest.raises(ValueError, match=match):
+            F.fold_q8_decode_fused(kv, keys, t["q"], 0.125, kw["codes"], kw["req_lens"],
+                                   math.inf, 2, t["part_A"], t["part_L"], kw["arrivals"],
+                                   t["z_out"], t["out"])
