@@ -2,18 +2,24 @@
 
 A step is one pass of the whole decode hot path over one batch: the
 reference estimate, the gated split-KV scan of every level, and the additive
-combine.  The default workload is the Llama-3-8B-shaped GQA decode (batch 16,
-32 query / 8 kv heads, head dim 128, 8192 cached keys per request, paged BF16
-cache of 16-key pages).  Inputs are synthetic, seeded and resident in HBM
-before timing.  Before every timed step a 1 GiB buffer is read, so that no
-cache (4 MB L2 per XCD, 256 MB MALL) holds any of the step's data and no dirty
-line is left to drain during the step; each step is bracketed by HIP events on
-the stream the kernels are launched on.
+combine.  The headline workload is the largest single-GPU one, the MHA
+long-context stress decode (batch 4, 32 heads, head dim 128, 64K-128K cached
+keys per request drawn uniformly, split-KV 32 ways, paged BF16 cache of
+16-key pages), at T = inf, with its T = 16 step beside it.  The
+Llama-3-8B-shaped GQA decode and the Qwen3-8B-shaped 32K-key decode (its
+depth sweep T in {inf, 24, 16, 12}) ride along as extra keys.  Inputs are
+synthetic, seeded and resident in HBM before timing.  Before every timed
+step a 1 GiB buffer is read, so that no cache (4 MB L2 per XCD, 256 MB MALL)
+holds any of the step's data and no dirty line is left to drain during the
+step; each step is bracketed by HIP events on the stream the kernels are
+launched on.
 
-Prints ONE JSON line (rank 0).  The line also carries the same workload over
-a two-plane INT8 key cache (``q8_keys``; Section 4, cache format).  ``--all``
-adds one JSON line per workload and depth on stderr (used for the design
-notes' tables).
+Prints ONE JSON line (rank 0).  The line also carries the headline workload
+over a two-plane INT8 key cache (``q8_keys``; Section 4, cache format) and
+with 8-bit values (``v8_values``), the cut-key value model's effect
+(``value_model``) and the FP64 oracle timed on the host (``cpu_baseline``).
+``--all`` adds one JSON line per workload and depth on stderr (used for the
+design notes' tables).
 """
 
 from __future__ import annotations
@@ -38,12 +44,17 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--config", type=int, default=4,
+                    help="headline workload (default 4: MHA 4 x 64K-128K keys, the largest "
+                         "single-GPU workload)")
+    ap.add_argument("--only", action="store_true",
+                    help="time only the headline workload (no workload-2/3 extra keys)")
     ap.add_argument("--all", action="store_true", help="also time workloads 1-5 (stderr)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-q8", action="store_true",
                     help="skip the two-plane INT8 key legs (BF16 and 8-bit values)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-graph", action="store_true", help="skip the graph-replay leg")
     ap.add_argument("--splits", type=int, default=None, help="override the split count")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="end with one 1 GiB device copy (byte-counter calibration under rocprofv3)")
@@ -424,8 +435,7 @@ def q8_leg(wl, F, torch, flush, steps, warmup, name=None, values8=False):
             out["roofline"] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
                                "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
                                "traffic": None if traffic is None else int(traffic),
-                               "kernel": "decode_q8_kernel (dense%s)"
-                                         % (", 8-bit values" if values8 else "")}
+                               "kernel": q8_kernel_name(wl, values8)}
     del qp
     torch.cuda.empty_cache()
     return out
@@ -546,26 +556,35 @@ def progress(msg):
 
 
 def fused_bytes(wl, lam):
-    """Algorithmic bytes of one fused launch: the scan's (kv_bytes), the
-    estimate's sampled key rows and their block-table entries (once per
-    (request, kv head)), the combine's read of the slots and its output, and
-    the arrival counts (read-modify-write and reset)."""
+    """Algorithmic bytes of one fused launch: the scan's (every key row, the
+    value rows the gates keep, queries, references, block-table entries,
+    slots written) plus the combine's read of the slots and its FP32 output.
+    The estimate's sampled key rows are rows the scan reads anyway; they are
+    not counted a second time."""
     d = wl.head_dim
     b, h, _ = wl.q.shape
     total, keys = kv_bytes(wl, lam)
-    full = 1 + 63 + 128  # default sample: sink, recent keys, strata
-    samples = sum(min(n, full) for n in wl.flat.seq_lens_host) * wl.num_kv_heads
-    total += samples * 2 * d + (4 * samples if wl.page_size else 0)
     total += 4 * sum(wl.level_splits) * b * h * (d + 1) + 4 * b * h * d
-    total += 2 * 4 * wl.flat.num_seqs * wl.num_kv_heads
     return total, keys
 
 
-def scan_kernel_name(wl):
-    """The scan kernel the library launches for a single-level workload."""
+def scan_kernel_name(wl, dense=True):
+    """The scan kernel (with its template arguments as rocprofv3 prints them)
+    the library launches for a single-level workload."""
+    d, dn = wl.head_dim, "true" if dense else "false"
     if wl.group == 1:
-        return "decode_split_kernel"
-    return "decode_packed_kernel" if wl.group <= 8 else "decode_mfma_kernel"
+        return f"decode_split_kernel<{d}, 1, {dn}, false>"
+    if wl.group <= 8:
+        return f"decode_packed_kernel<{d}, {4 if wl.group <= 4 else 2}, {dn}, false>"
+    return f"decode_mfma_kernel<{d}, ...>"
+
+
+def q8_kernel_name(wl, values8):
+    """The dense two-plane scan kernel of a single-level workload."""
+    v8 = "true" if values8 else "false"
+    if wl.group <= 8:
+        return f"decode_q8_packed_kernel<{wl.head_dim}, 2, true, false, {v8}>"
+    return f"decode_q8_kernel<{wl.head_dim}, ..., true, false, {v8}>"
 
 
 def evict_caches(flush):
@@ -644,22 +663,106 @@ def time_graph(path, T, steps, warmup, flush, torch):
     return statistics.median(ts)
 
 
-def kernel_sources_sha():
-    """SHA-256 over the HIP sources of the library (identifies the kernels)."""
+def graph_leg(workloads, F, torch, flush, steps, warmup):
+    """Timed last, after every eager leg: each workload's step replayed from a
+    captured HIP graph, the same step eagerly again afterwards, and what a
+    replay adds around one trivial kernel.  On this platform the first graph
+    capture (like the first launch on a second stream) leaves every later
+    kernel of the process about 8 % slower, with unchanged clocks; timing the
+    graphs last keeps the eager figures free of that."""
+    out = {}
+    for name, wl in workloads:
+        path = Path(wl, F, torch)
+        path.estimate(torch.cuda.current_stream())
+        rec = {}
+        for T in (math.inf, 16.0):
+            rec[depth_key(T)] = {"graph_replay_us": round(
+                time_graph(path, T, steps, warmup, flush, torch) * 1e3, 2)}
+        for T in (math.inf, 16.0):
+            med, _ = time_variant(path, T, steps, warmup, flush, torch)
+            rec[depth_key(T)]["eager_us_after_capture"] = round(med["step"] * 1e3, 2)
+            rec[depth_key(T)]["eager_decode_us_after_capture"] = round(med["dec"] * 1e3, 2)
+        out[name] = rec
+        del path
+        torch.cuda.empty_cache()
+    out["one_fill_kernel"] = graph_overhead(max(steps, 11), flush, torch)
+    out["note"] = ("graph replays and the eager steps after them run after the process's first "
+                   "graph capture, which slows every kernel of the process by about 8 % on this "
+                   "platform; the eager figures elsewhere in this line precede any capture")
+    return out
+
+
+def graph_overhead(steps, flush, torch):
+    """What a graph replay adds around its kernels: one 4-byte fill kernel timed
+    eagerly and as a one-node graph replay (events around each, caches evicted
+    before each), medians in us."""
+    stream = torch.cuda.current_stream()
+    x = torch.zeros(1, dtype=torch.int32, device="cuda")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        x.fill_(1)
+    res = {"eager": [], "graph": []}
+    for it in range(steps + 1):
+        for key in ("eager", "graph"):
+            evict_caches(flush)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            if key == "graph":
+                g.replay()
+            else:
+                x.fill_(1)
+            e1.record(stream)
+            e1.synchronize()
+            if it:
+                res[key].append(e0.elapsed_time(e1))
+    med = {k: statistics.median(v) * 1e3 for k, v in res.items()}
+    return {"one_fill_kernel_eager_us": round(med["eager"], 2),
+            "one_fill_kernel_graph_us": round(med["graph"], 2),
+            "graph_adds_us": round(med["graph"] - med["eager"], 2)}
+
+
+def _local_includes(path):
+    import re
+
+    out = []
+    with open(path) as f:
+        for line in f:
+            m = re.match(r'\s*#\s*include\s+"([^"]+)"', line)
+            if m:
+                out.append(m.group(1))
+    return out
+
+
+def kernel_sources_sha(source="*"):
+    """SHA-256 over a kernel's source file and every local header it includes
+    (transitively), or over every library source with ``source="*"``; it
+    identifies the code a counter record was taken on."""
     import glob
     import hashlib
 
-    h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_33410_amd", "csrc")
-    for f in sorted(glob.glob(os.path.join(csrc, "*"))):
-        with open(f, "rb") as fh:
-            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    if source == "*":
+        files = sorted(os.path.basename(f) for f in glob.glob(os.path.join(csrc, "*")))
+    else:
+        seen, todo = set(), [source]
+        while todo:
+            f = todo.pop()
+            if f in seen or not os.path.exists(os.path.join(csrc, f)):
+                continue
+            seen.add(f)
+            todo.extend(_local_includes(os.path.join(csrc, f)))
+        files = sorted(seen)
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()
 
 
 def counter_traffic(workload_name):
     """HBM bytes per dense decode launch from the committed counter summary,
-    or None when it is absent or was taken on other kernel sources."""
+    or None when it is absent or the kernel's sources changed since."""
     path = os.path.join(ROOT, "profiles", "decode_traffic_counters.txt")
     if not os.path.exists(path):
         return None, None
@@ -670,15 +773,30 @@ def counter_traffic(workload_name):
                 r = json.loads(line[len("record:"):])
                 rec[r["workload"]] = r
     r = rec.get(workload_name)
-    if r is None or r.get("source_sha256") != kernel_sources_sha():
+    if r is None or r.get("source_sha256") != kernel_sources_sha(r.get("sources", "*")):
         return None, r
     kib = r["fetch_kib"] * r["fetch_scale"] + r["write_kib"] * r["write_scale"]
     return kib * 1024.0, r
 
 
-def cpu_baseline(wl, budget_s):
-    """The FP64 oracle timed on this host on a bounded sample of the workload's
-    (kv sequence, kv head) chunks; scaled to one whole call."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:  # pragma: no cover
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, budget_s, T_cut=16.0):
+    """The FP64 oracle, as it stands, timed on this host's cores on a bounded
+    sample of the workload's (request, kv head) chunks and scaled to one whole
+    call: the oracle's estimator (its own reference for the sampled rows), and
+    the decode (gather, scores, depth rule, fold, splits) at T = inf and at
+    T = T_cut with that reference.  Chunks are taken in a seeded random order,
+    so long and short requests of a ragged batch are both sampled."""
     import numpy as np
 
     import oracle
@@ -691,32 +809,56 @@ def cpu_baseline(wl, budget_s):
         threads = 1
     cores = len(os.sched_getaffinity(0))
     q_bits, k_bits, v_bits = host_bits(wl.q), host_bits(wl.k), host_bits(wl.v)
-    lv = wl.levels[0]
-    bt = None if lv.block_table is None else lv.block_table.cpu().numpy()
+    fl = wl.flat
+    bt = None if fl.block_table is None else fl.block_table.cpu().numpy()
+    group = wl.group
+    chunks_all = [(s, g) for s in range(fl.num_seqs) for g in range(wl.num_kv_heads)]
+    order = np.random.default_rng(0).permutation(len(chunks_all))
+    chunks_all = [chunks_all[i] for i in order]
     z = np.zeros((wl.batch, wl.num_heads))
-    chunks_all = [(s, g) for s in range(lv.num_seqs) for g in range(wl.num_kv_heads)]
-    done = 0
-    t0 = time.perf_counter()
-    while True:  # whole calls (or a prefix of one) until the time budget is used
+    keys_of = {c: int(fl.seq_lens_host[c[0]]) for c in chunks_all}
+    all_keys = sum(keys_of.values())
+
+    def run(leg, budget):
+        done, keys = [], 0
+        t0 = time.perf_counter()
         for c in chunks_all:
-            oracle.decode_level(q_bits, k_bits, v_bits, num_kv_heads=wl.num_kv_heads,
-                                page_size=wl.page_size, sm_scale=wl.sm_scale,
-                                seq_lens=lv.seq_lens_host, block_table=bt, z=z, T=math.inf,
-                                num_splits=wl.level_splits[0], chunks=[c])
-            done += 1
-            if time.perf_counter() - t0 > budget_s:
+            if leg == "estimate":
+                rows = [(c[0], c[1] * group + hh) for hh in range(group)]
+                zc = oracle.estimate_level(q_bits, k_bits, num_kv_heads=wl.num_kv_heads,
+                                           page_size=wl.page_size, sm_scale=wl.sm_scale,
+                                           seq_lens=fl.seq_lens_host, block_table=bt, rows=rows)
+                for r, h in rows:
+                    z[r, h] = zc[r, h]
+            else:
+                oracle.decode_level(q_bits, k_bits, v_bits, num_kv_heads=wl.num_kv_heads,
+                                    page_size=wl.page_size, sm_scale=wl.sm_scale,
+                                    seq_lens=fl.seq_lens_host, block_table=bt, z=z, T=leg,
+                                    num_splits=wl.level_splits[0], chunks=[c])
+            done.append(c)
+            keys += keys_of[c]
+            if time.perf_counter() - t0 > budget:
                 break
-        if time.perf_counter() - t0 > budget_s:
-            break
-    dt = time.perf_counter() - t0
-    per_call_s = dt * len(chunks_all) / done
-    keys = sum(lv.seq_lens_host) * wl.num_kv_heads
-    return {"value": round(per_call_s * 1e6, 1), "unit": "us/call", "cores": threads,
-            "host_cores_visible": cores, "kind": "oracle",
-            "keys_per_s": round(keys / per_call_s, 1),
-            "sample": f"FP64 oracle decode (T=inf, gather + scores + fold + splits) of "
-                      f"{done} (request, kv head) chunks = {done / len(chunks_all):.2f} whole "
-                      f"calls in {dt:.1f} s, scaled to one call"}
+        dt = time.perf_counter() - t0
+        return dt * all_keys / keys, len(done), dt  # scaled by keys to one whole call
+
+    est_s, n_est, dt_est = run("estimate", budget_s / 4)
+    chunks_all = chunks_all[:n_est]  # the decode needs the sampled rows' references
+    inf_s, n_inf, dt_inf = run(math.inf, budget_s * 3 / 8)
+    cut_s, n_cut, dt_cut = run(T_cut, budget_s * 3 / 8)
+    keys = sum(fl.seq_lens_host) * wl.num_kv_heads
+    del q_bits, k_bits, v_bits
+    return {"value": round((est_s + inf_s) * 1e6, 1), "unit": "us/call", "cores": threads,
+            "host_cores_visible": cores, "cpu_model": cpu_model(), "kind": "oracle",
+            "decode_us_per_call": {"T=inf": round(inf_s * 1e6, 1),
+                                   f"T={T_cut:g}": round(cut_s * 1e6, 1)},
+            "estimate_us_per_call": round(est_s * 1e6, 1),
+            "keys_per_s": {"T=inf": round(keys / inf_s, 1), f"T={T_cut:g}": round(keys / cut_s, 1)},
+            "sample": f"FP64 oracle on {cores} visible host cores ({threads} BLAS threads): "
+                      f"estimator on {n_est} of {fl.num_seqs * wl.num_kv_heads} (request, kv head) "
+                      f"chunks in {dt_est:.1f} s; decode of {n_inf} of them at T=inf in "
+                      f"{dt_inf:.1f} s and of {n_cut} at T={T_cut:g} in {dt_cut:.1f} s; each "
+                      f"leg scaled by keys to one whole call; value = estimator + T=inf decode"}
 
 
 def paired_depths(path, steps, warmup, flush, torch, T_cut=16.0):
@@ -760,32 +902,79 @@ def paired_depths(path, steps, warmup, flush, torch, T_cut=16.0):
             "step_us_T_p10_p50_p90": [round(pct(steps_cut, q) * 1e3, 2) for q in (0.1, 0.5, 0.9)]}
 
 
-def run_workload(i, args, torch, F, make_config, flush, steps, warmup, splits=None):
-    wl = make_config(i, device="cuda")
+def run_workload(i, args, torch, F, make_config, flush, steps, warmup, splits=None,
+                 depths=None, wl=None):
+    if wl is None:
+        wl = make_config(i, device="cuda")
     if splits is not None and len(wl.level_splits) == 1:
         wl.level_splits = [splits]
     path = Path(wl, F, torch)
     stream = torch.cuda.current_stream()
     path.estimate(stream)
     out = {}
-    for T in (math.inf, 16.0) + ((24.0, 12.0) if i == 3 else ()):
+    if depths is None:
+        depths = (math.inf, 16.0) + ((24.0, 12.0) if i == 3 else ())
+    for T in depths:
         lam = path.read_fraction(T)
         med, _ = time_variant(path, T, steps, warmup, flush, torch)
-        graph_ms = time_graph(path, T, steps, warmup, flush, torch)
         nbytes, keys = kv_bytes(wl, lam)
         fbytes = fused_bytes(wl, lam)[0] if path.fusable else None
-        out[T] = {"med": med, "graph": graph_ms, "lam": lam, "bytes": nbytes, "keys": keys,
+        out[T] = {"med": med, "lam": lam, "bytes": nbytes, "keys": keys,
                   "fused_bytes": fbytes, "fusable": path.fusable}
         progress(f"workload {i} T={T:g}: step {med['step'] * 1e3:.1f} us "
                  f"(three calls {med['step_three_calls'] * 1e3:.1f} us)")
     return wl, out
 
 
+def depth_key(T):
+    return "T=inf" if math.isinf(T) else f"T={T:g}"
+
+
+def gbps(nbytes, ms):
+    return round(nbytes / (ms * 1e-3) / 1e9, 1)
+
+
+def depth_record(wl, v, T):
+    """One depth of a workload: the step, its kernels, bytes and rates."""
+    med = v["med"]
+    rec = {"us_per_call": round(med["step"] * 1e3, 2),
+           "step": "fused" if v["fusable"] else "three calls",
+           "us_per_call_three_calls": round(med["step_three_calls"] * 1e3, 2),
+           "decode_us": round(med["dec"] * 1e3, 2),
+           "estimate_us_with_marker": round(med["est"] * 1e3, 2),
+           "combine_us_with_marker": round(med["comb"] * 1e3, 2),
+           "decode_bytes": int(v["bytes"]),
+           "decode_gbps": gbps(v["bytes"], med["dec"]),
+           "decode_frac_of_peak": round(v["bytes"] / (med["dec"] * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+           "value_read_fraction": round(v["lam"], 5),
+           "keys_per_s": round(v["keys"] / (med["step"] * 1e-3), 1)}
+    if v["fusable"]:
+        rec["fused_bytes"] = int(v["fused_bytes"])
+        rec["fused_gbps"] = gbps(v["fused_bytes"], med["step"])
+    return rec
+
+
+def workload_summary(i, wl, res, paired):
+    """Extra-key record of a workload: every depth, and the paired speedups."""
+    names = __import__("workloads").CONFIG_NAMES
+    out = {"workload": names[i], "batch": wl.batch, "q_heads": wl.num_heads,
+           "kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim,
+           "keys_per_request": list(wl.flat.seq_lens_host) if len(set(wl.flat.seq_lens_host)) > 1
+           else wl.flat.seq_lens_host[0], "splits": wl.level_splits,
+           "scan_kernel": scan_kernel_name(wl)}
+    for T, v in res.items():
+        out[depth_key(T)] = depth_record(wl, v, T)
+    for T, pr in paired.items():
+        out[depth_key(T)]["paired_vs_T=inf"] = pr
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the decode path has no multi-GPU leg in this build)", file=sys.stderr)
+              "(every GPU box here has one GPU; the sharding of this path is design only)",
+              file=sys.stderr)
         sys.exit(2)
     import torch
 
@@ -798,26 +987,31 @@ def main():
     F.load_library()
     flush = torch.ones(1 << 28, dtype=torch.int32, device="cuda")  # 1 GiB
 
+    cfg = args.config
     wall0 = time.perf_counter()
-    wl, res = run_workload(args.config, args, torch, F, make_config, flush, args.steps,
-                           args.warmup, splits=args.splits)
+    wl, res = run_workload(cfg, args, torch, F, make_config, flush, args.steps, args.warmup,
+                           splits=args.splits)
     wall = time.perf_counter() - wall0
     dense, t16 = res[math.inf], res[16.0]
     fusable = dense["fusable"]
     dec_ms = dense["med"]["dec"]
-    scan_achieved = dense["bytes"] / (dec_ms * 1e-3) / 1e9
     step_ms = dense["med"]["step"]
     # the dominant kernel: the fused launch (the whole step) where it applies,
     # else the scan of the three-call step
     if fusable:
         r_bytes, r_ms, r_kernel = dense["fused_bytes"], step_ms, "decode_fused_kernel"
         r_timing = "HIP events around the eager launch on its stream (the step is this one launch)"
+        tkey = CONFIG_NAMES[cfg] + " [fused]"
     else:
         r_bytes, r_ms, r_kernel = dense["bytes"], dec_ms, scan_kernel_name(wl)
-        r_timing = "HIP events around the eager launch on its stream"
+        r_timing = ("HIP events on the launch stream around the scan launch of the "
+                    "three-call step (events between its kernels)")
+        tkey = CONFIG_NAMES[cfg]
     achieved = r_bytes / (r_ms * 1e-3) / 1e9
-    traffic, trec = counter_traffic(CONFIG_NAMES[args.config] + (" [fused]" if fusable else ""))
-    scan_traffic, _ = counter_traffic(CONFIG_NAMES[args.config])
+    traffic, _ = counter_traffic(tkey)
+    keys = dense["keys"]
+    pairs = sum(wl.flat.seq_lens_host) * wl.num_heads
+    paired16 = paired_depths(Path(wl, F, torch), max(args.steps, 21), 1, flush, torch)
     line = {
         "metric": METRIC,
         "value": round(step_ms * 1e3, 2),
@@ -831,17 +1025,19 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": CONFIG_NAMES[args.config], "batch": wl.batch,
+        "config": {"workload": CONFIG_NAMES[cfg], "batch": wl.batch,
                    "q_heads": wl.num_heads, "kv_heads": wl.num_kv_heads,
-                   "head_dim": wl.head_dim, "keys_per_request": wl.flat.seq_lens_host[0],
-                   "page_size": wl.page_size, "splits": wl.level_splits,
+                   "head_dim": wl.head_dim,
+                   "keys_per_request": list(wl.flat.seq_lens_host),
+                   "page_size": wl.page_size, "splits": wl.level_splits, "depth": "T=inf",
                    "step": ("estimate + split scan + combine at T=inf in one launch "
                             "(fold_decode_fused)" if fusable else
-                            "estimate + split scan + combine at T=inf, launched on one stream"),
+                            "fold_ref_estimate + fold_decode_split + fold_combine at T=inf, "
+                            "launched on one stream"),
                    "timing": "median over steps of HIP events around the step on its stream "
                              "(no event inside the step); a 1 GiB read before each step evicts "
-                             "all caches; the breakdown comes from separate steps with events "
-                             "between the kernels"},
+                             "all caches; the kernel breakdown comes from separate steps with "
+                             "events between the kernels"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": None if traffic is None else int(traffic),
@@ -849,43 +1045,65 @@ def main():
                      "algorithmic_bytes_per_launch": int(r_bytes),
                      "avg_launch_us": round(r_ms * 1e3, 2),
                      "launch_timing": r_timing},
-        "scan_roofline": {"kernel": scan_kernel_name(wl), "achieved": round(scan_achieved, 1),
-                          "frac": round(scan_achieved / HBM_PEAK_GBPS, 4),
-                          "traffic": None if scan_traffic is None else int(scan_traffic),
-                          "algorithmic_bytes_per_launch": int(dense["bytes"]),
-                          "avg_launch_us": round(dec_ms * 1e3, 2),
-                          "launch_timing": "HIP events around the scan launch of the three-call "
-                                           "step, events between its kernels"},
-        "three_calls_us_per_call": {"T=inf": round(dense["med"]["step_three_calls"] * 1e3, 2),
-                                    "T=16": round(t16["med"]["step_three_calls"] * 1e3, 2)},
+        "T=16": dict(depth_record(wl, t16, 16.0), paired_vs_T_inf=paired16),
+        "T=inf": depth_record(wl, dense, math.inf),
         "t16_us_per_call": round(t16["med"]["step"] * 1e3, 2),
-        "graph_replay_us_per_call": {"T=inf": round(dense["graph"] * 1e3, 2),
-                                     "T=16": round(t16["graph"] * 1e3, 2)},
-        "breakdown_us_eager": {"T=inf": {k: round(v * 1e3, 2) for k, v in dense["med"].items()},
-                               "T=16": {k: round(v * 1e3, 2) for k, v in t16["med"].items()}},
-        "t16_decode_gbps": round(t16["bytes"] / (t16["med"]["dec"] * 1e-3) / 1e9, 1),
-        "t16_value_read_fraction": round(t16["lam"], 5),
-        "t16_speedup_decode": round(dense["med"]["dec"] / t16["med"]["dec"], 3),
-        "t16_speedup_step": round(dense["med"]["step"] / t16["med"]["step"], 3),
-        "t16_paired": paired_depths(Path(wl, F, torch), max(args.steps, 21), 1, flush, torch),
-        "keys_per_s": round(dense["keys"] / (step_ms * 1e-3), 1),
+        "t16_speedup_step": paired16["speedup_step_median"],
+        "t16_speedup_decode": paired16["speedup_decode_median"],
+        "keys_per_s": round(keys / (step_ms * 1e-3), 1),
+        "query_key_pairs_per_s": round(pairs / (step_ms * 1e-3), 1),
         "wall_s": round(wall, 2),
     }
+    keep = [(CONFIG_NAMES[cfg], wl)]
+    del res
+    torch.cuda.empty_cache()
+    # the other long-context and GQA workloads, as extra keys
+    for extra in (2, 3):
+        if extra == cfg or args.only:
+            continue
+        wl_x, r = run_workload(extra, args, torch, F, make_config, flush, args.steps,
+                               args.warmup)
+        paired = {}
+        for T in r:
+            if not math.isinf(T):
+                paired[T] = paired_depths(Path(wl_x, F, torch), max(args.steps, 21), 1, flush,
+                                          torch, T_cut=T)
+        rec = workload_summary(extra, wl_x, r, paired)
+        if r[math.inf]["fusable"]:
+            fb = r[math.inf]["fused_bytes"]
+            fms = r[math.inf]["med"]["step"]
+            ft, _ = counter_traffic(CONFIG_NAMES[extra] + " [fused]")
+            rec["roofline"] = {"bound": "hbm", "kernel": "decode_fused_kernel",
+                               "achieved": gbps(fb, fms), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                               "frac": round(fb / (fms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                               "traffic": None if ft is None else int(ft),
+                               "algorithmic_bytes_per_launch": int(fb),
+                               "avg_launch_us": round(fms * 1e3, 2)}
+        line[f"workload{extra}"] = rec
+        progress(f"workload {extra} leg done")
+        keep.append((CONFIG_NAMES[extra], wl_x))
+        del r
+        torch.cuda.empty_cache()
     line["value_model"] = model_leg(Path(wl, F, torch), wl, F, torch, flush, args.steps,
                                     args.warmup)
     progress("value model leg done")
     if not args.no_q8:
         line["q8_keys"] = q8_leg(wl, F, torch, flush, args.steps, args.warmup,
-                                 name=CONFIG_NAMES[args.config])
+                                 name=CONFIG_NAMES[cfg])
         progress("two-plane key leg done")
         line["v8_values"] = q8_leg(wl, F, torch, flush, args.steps, args.warmup,
-                                   name=CONFIG_NAMES[args.config], values8=True)
+                                   name=CONFIG_NAMES[cfg], values8=True)
         progress("8-bit value leg done")
     if args.all:
         line["drafts"] = drafts_leg(F, torch, flush, args.steps, args.warmup)
         progress("draft leg done")
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        progress("CPU baseline done")
+    if not args.no_graph:
+        line["graph_replay"] = graph_leg(keep, F, torch, flush, args.steps, args.warmup)
+        progress("graph leg done")
+    del keep
     print(json.dumps(line), flush=True)
 
     if args.calibrate_copy:  # a plain copy of known size for byte-counter calibration
@@ -897,22 +1115,14 @@ def main():
         del src, dst
 
     if args.all:
+        del wl
+        torch.cuda.empty_cache()
         for i in (1, 2, 3, 4, 5):
             wl_i, r = run_workload(i, args, torch, F, make_config, flush, args.steps,
                                    args.warmup)
             for T, v in r.items():
-                rec = {"workload": CONFIG_NAMES[i], "T": "inf" if math.isinf(T) else T,
-                       "us_per_call": round(v["med"]["step"] * 1e3, 2),
-                       "step": "fused" if v["fusable"] else "three calls",
-                       "us_per_call_three_calls": round(v["med"]["step_three_calls"] * 1e3, 2),
-                       "us_per_call_graph": round(v["graph"] * 1e3, 2),
-                       "decode_us": round(v["med"]["dec"] * 1e3, 2),
-                       "estimate_us": round(v["med"]["est"] * 1e3, 2),
-                       "combine_us": round(v["med"]["comb"] * 1e3, 2),
-                       "decode_bytes": int(v["bytes"]),
-                       "decode_gbps": round(v["bytes"] / (v["med"]["dec"] * 1e-3) / 1e9, 1),
-                       "value_read_fraction": round(v["lam"], 5),
-                       "keys_per_s": round(v["keys"] / (v["med"]["step"] * 1e-3), 1)}
+                rec = dict({"workload": CONFIG_NAMES[i], "T": "inf" if math.isinf(T) else T},
+                           **depth_record(wl_i, v, T))
                 print(json.dumps(rec), file=sys.stderr, flush=True)
             if not args.no_q8:
                 rec = {"workload": CONFIG_NAMES[i],

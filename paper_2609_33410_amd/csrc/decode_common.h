@@ -82,6 +82,45 @@ __device__ __forceinline__ ScanPlace scan_place(const DecodeArgs& a) {
   return p;
 }
 
+// Longest sequences first.  For a per-request view of at most kOrderMax
+// sequences the block index runs over kv heads fastest, then splits, then the
+// sequences by decreasing length (ties by index), then read groups.  Blocks
+// are dispatched in index order as slots free up, so the workgroups of the
+// longest sequences start first and the last to start are the shortest ones:
+// a ragged batch drains with less of the call left to a half-empty chip.
+// Which workgroup scans which keys changes nothing else (same sums, same
+// bits).  Every thread of the workgroup must call it (one barrier).
+
+__device__ __forceinline__ ScanPlace scan_place_by_length(const DecodeArgs& a, int* order) {
+  const ScanGeometry& g = a.geo;
+  const int cap = view_capacity(g);
+  if (static_cast<int>(threadIdx.x) < g.num_seqs) {
+    const int i = threadIdx.x;
+    const int li = clamp_len(g.seq_lens[i], cap);
+    int r = 0;
+    for (int j = 0; j < g.num_seqs; ++j) {
+      const int lj = clamp_len(g.seq_lens[j], cap);
+      r += (lj > li || (lj == li && j < i)) ? 1 : 0;
+    }
+    order[r] = i;
+  }
+  __syncthreads();
+  ScanPlace p;
+  int bid = blockIdx.x;
+  p.kvh = bid % g.hkv;
+  bid /= g.hkv;
+  p.split = bid % a.num_splits;
+  bid /= a.num_splits;
+  const int rank = bid % g.num_seqs;
+  p.rg = bid / g.num_seqs;
+  p.seq = __builtin_amdgcn_readfirstlane(order[rank]);
+  p.req0 = p.seq;
+  p.nrows = g.group;
+  p.n = clamp_len(ld_uniform(g.seq_lens, p.seq), cap);
+  p.nchunks = (p.n + kChunk - 1) / kChunk;
+  return p;
+}
+
 // Block-table entry of the page holding 16-key chunk c of the sequence (0 for
 // a contiguous view or past the sequence end).  A scalar load: issuing it well
 // before chunk_rsrc_at() hides its latency.

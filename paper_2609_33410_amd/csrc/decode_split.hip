@@ -2,10 +2,15 @@
 // "Value product", "Depth as a dial"; Algorithm 1).
 //
 // One workgroup = one (kv sequence, kv head, split, read group of GR query
-// rows); four wave64s.  The split walks the 64-key tiles t == split (mod S);
-// wave w owns the 16-key chunk 4t + w of each tile, a contiguous [16][D] bf16
-// slab in both cache layouts (pages hold a multiple of 16 keys).  D/8 lanes
-// hold one key row (8 channels each), so one wave-wide 128-bit load covers
+// rows); W wave64s (4 or 8).  The split walks the 64-key tiles
+// t == split (mod S); a tile holds four 16-key chunks, each a contiguous
+// [16][D] bf16 slab in both cache layouts (pages hold a multiple of 16 keys).
+// Wave w owns chunk (w mod 4) of the split's tiles k == w / 4 (mod W / 4), so
+// the W waves share the split's tiles and a workgroup finishes its split W/4
+// times sooner than four waves would: with the split count fixed by the
+// caller, a long batch then drains in shorter workgroups (the last ones to be
+// dispatched leave less of the call to a half-empty chip).  D/8 lanes hold
+// one key row (8 channels each), so one wave-wide 128-bit load covers
 // 64/(D/8) keys and 1 KiB of contiguous bytes.
 //
 // Loads go through buffer resources whose size is the chunk's valid bytes:
@@ -21,15 +26,12 @@
 //                accumulate chunk t: A += [live] 2^x v, L += 2^x (FP32).
 // Dense scan (T = inf): every key is live, so K and V of chunk t+1 are issued
 // together before chunk t is scored and accumulated.
-// At the end the lanes of a wave and then the four waves are reduced in a fixed
+// At the end the lanes of a wave and then the W waves are reduced in a fixed
 // order and the pair (A, L) of every row is written to its split's slot.
 #include "decode_common.h"
 
 namespace fold {
 namespace {
-
-constexpr int kWaves = kScanWaves;
-constexpr int kThreads = kScanThreads;
 
 template <int D, int GR, bool DENSE, bool DBG>
 struct Scan {
@@ -119,8 +121,10 @@ struct Scan {
   }
 };
 
-template <int D, int GR, bool DENSE, bool DBG>
-__global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs a) {
+template <int D, int GR, bool DENSE, bool DBG, int W>
+__global__ __launch_bounds__(64 * W) void decode_split_kernel(const DecodeArgs a) {
+  constexpr int kWaves = W;
+  constexpr int kThreads = 64 * W;
   using S = Scan<D, GR, DENSE, DBG>;
   constexpr int NI = S::NI;
   const ScanGeometry& g = a.geo;
@@ -131,7 +135,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs
   sc.part = sc.lane % S::LPK;
   sc.kslot = sc.lane / S::LPK;
 
-  const ScanPlace pl = scan_place(a);
+  __shared__ int order[kOrderMax];
+  const ScanPlace pl = a.by_length ? scan_place_by_length(a, order) : scan_place(a);
   sc.seq = pl.seq;
   sc.kvh = pl.kvh;
   const int split = pl.split;
@@ -159,9 +164,10 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs
     for (int e = 0; e < 8; ++e) sc.acc[r][e] = 0.0f;
   }
 
-  // Chunks of this wave: c_t = c0 + t * cstride, t < m.
+  // Chunks of this wave: c_t = c0 + t * cstride, t < m (chunk w mod 4 of the
+  // split's tiles k == w / 4 (mod W / 4)).
   const int cstride = kWaves * a.num_splits;
-  const int c0 = kWaves * split + wave;
+  const int c0 = 4 * split + 4 * a.num_splits * (wave >> 2) + (wave & 3);
   const int m = sc.nchunks > c0 ? (sc.nchunks - c0 + cstride - 1) / cstride : 0;
 
   if (DENSE) {
@@ -279,25 +285,36 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(const DecodeArgs
   }
 }
 
+template <int D, bool DENSE, bool DBG>
+hipError_t launch_valu_w(const DecodeArgs& a, unsigned blocks, int waves, hipStream_t stream) {
+  if (waves == 8)
+    hipLaunchKernelGGL((decode_split_kernel<D, 1, DENSE, DBG, 8>), dim3(blocks), dim3(64 * 8), 0,
+                       stream, a);
+  else
+    hipLaunchKernelGGL((decode_split_kernel<D, 1, DENSE, DBG, 4>), dim3(blocks), dim3(64 * 4), 0,
+                       stream, a);
+  return hipGetLastError();
+}
+
+// Waves per workgroup: 8 when every wave still gets at least 4 chunks of the
+// longest sequence the view can hold, else 4 (so that no wave idles).
+// Measured on the MHA 4 x 64K-128K decode (32 splits, longest sequences
+// first): 8 waves 965 us dense / 563 us at T = 16, 4 waves 964 / 569, 16
+// waves (one 1024-thread workgroup per CU) 966 / 576.
+int mha_waves(const DecodeArgs& a) {
+  const long long chunks = (static_cast<long long>(a.geo.max_seq_len) + kChunk - 1) / kChunk;
+  return chunks / a.num_splits >= 8LL * 4 ? 8 : 4;
+}
+
 template <int D>
 hipError_t launch_valu(const DecodeArgs& a, unsigned blocks, hipStream_t stream) {
   const bool dbg = a.x_out || a.key_gate_out || a.page_gate_out;
-  if (a.dense) {
-    if (dbg)
-      hipLaunchKernelGGL((decode_split_kernel<D, 1, true, true>), dim3(blocks), dim3(kThreads), 0,
-                         stream, a);
-    else
-      hipLaunchKernelGGL((decode_split_kernel<D, 1, true, false>), dim3(blocks), dim3(kThreads), 0,
-                         stream, a);
-  } else {
-    if (dbg)
-      hipLaunchKernelGGL((decode_split_kernel<D, 1, false, true>), dim3(blocks), dim3(kThreads), 0,
-                         stream, a);
-    else
-      hipLaunchKernelGGL((decode_split_kernel<D, 1, false, false>), dim3(blocks), dim3(kThreads), 0,
-                         stream, a);
-  }
-  return hipGetLastError();
+  const int w = mha_waves(a);
+  if (a.dense)
+    return dbg ? launch_valu_w<D, true, true>(a, blocks, w, stream)
+               : launch_valu_w<D, true, false>(a, blocks, w, stream);
+  return dbg ? launch_valu_w<D, false, true>(a, blocks, w, stream)
+             : launch_valu_w<D, false, false>(a, blocks, w, stream);
 }
 
 }  // namespace

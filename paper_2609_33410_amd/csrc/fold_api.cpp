@@ -236,6 +236,7 @@ fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, floa
   a.rows_per_seq = rows;
   a.rows_per_group = gr;
   a.row_groups = groups;
+  a.by_length = (!kv->row_indptr && kv->num_seqs >= 2 && kv->num_seqs <= fold::kOrderMax) ? 1 : 0;
   hipError_t e = fold::launch_decode(a, kv->head_dim, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(FOLD_E_HIP, "decode launch: %s", hipGetErrorString(e));
   return ok();
@@ -283,12 +284,15 @@ fold_status fold_combine(const float* part_A, const float* part_L, int32_t num_s
   return ok();
 }
 
-fold_status fold_decode_fused(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
+// Validation and arguments of the one-launch decode (shared by
+// fold_decode_fused and fold_decode_fused_noalloc); launches nothing.
+static fold_status fused_args(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
                               const fold_est_params* params, float depth_T, int32_t num_splits,
                               float* part_A, float* part_L, int32_t* arrivals, float* z_out,
                               void* out, fold_dtype out_dtype, float* lse_out,
-                              uint8_t* cert_out, void* stream) {
-  fold::FusedArgs f{};
+                              uint8_t* cert_out, fold::FusedArgs* fa) {
+  fold::FusedArgs& f = *fa;
+  f = fold::FusedArgs{};
   fold::DecodeArgs& a = f.d;
   fold_status st = check_view(kv, q, &a.geo, true);
   if (st != FOLD_OK) return st;
@@ -343,6 +347,18 @@ fold_status fold_decode_fused(const fold_kv_view* kv, const fold_q_view* q, floa
   f.x.lse_out = lse_out;
   f.x.cert_out = cert_out;
   f.x.out_bf16 = out_dtype == FOLD_DTYPE_BF16 ? 1 : 0;
+  return FOLD_OK;
+}
+
+fold_status fold_decode_fused(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
+                              const fold_est_params* params, float depth_T, int32_t num_splits,
+                              float* part_A, float* part_L, int32_t* arrivals, float* z_out,
+                              void* out, fold_dtype out_dtype, float* lse_out,
+                              uint8_t* cert_out, void* stream) {
+  fold::FusedArgs f;
+  fold_status st = fused_args(kv, q, sm_scale, params, depth_T, num_splits, part_A, part_L,
+                              arrivals, z_out, out, out_dtype, lse_out, cert_out, &f);
+  if (st != FOLD_OK) return st;
   hipError_t err = fold::launch_decode_fused(f, kv->head_dim, static_cast<hipStream_t>(stream));
   if (err != hipSuccess) return fail(FOLD_E_HIP, "fused decode launch: %s", hipGetErrorString(err));
   return ok();

@@ -11,6 +11,9 @@ namespace fold {
 // interleave by 64-key tiles; pages are 16 keys).
 constexpr int kTile = 64;
 constexpr int kChunk = 16;
+// Largest per-request view whose scan dispatches its sequences by decreasing
+// length (each workgroup ranks the lengths itself).
+constexpr int kOrderMax = 64;
 
 struct ScanGeometry {
   const uint16_t* k;
@@ -48,6 +51,7 @@ struct DecodeArgs {
   int rows_per_seq;   // bound on rows attending one (kv seq, kv head)
   int rows_per_group; // rows one workgroup serves (template GR)
   int row_groups;
+  int by_length = 0;  // block order over sequences by decreasing length (per-request views)
 };
 
 struct EstimateArgs {

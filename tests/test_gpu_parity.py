@@ -178,6 +178,21 @@ def test_ragged_edge_lengths(d, group, paged):
         assert (res["cert"][1:].numpy() & 2 == 0).all()
 
 
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("splits", [1, 3, 5])
+def test_mha_waves_per_workgroup(d, splits):
+    """The MHA scan with 8 and 4 waves sharing a split's tiles (chosen from the
+    longest sequence per split: 2100 keys give 132 chunks, so S = 1 and 3 take
+    8 waves, S = 5 four), sequences dispatched longest first, ragged lengths
+    with partial last tiles, an empty and a short sequence; output, slots, x
+    and read bits against the oracle."""
+    lens = [2100, 1100, 2053, 0, 77]
+    wl = make_custom(batch=len(lens), heads=3, kv_heads=3, dim=d, lens=lens, paged=True,
+                     spike_count=6, n_sink=1, seed=40 + d + splits, device="cuda")
+    for T in (INF, 16.0, 4.0):
+        _full_parity(wl, T, splits=[splits], own_mode=not math.isinf(T))
+
+
 def test_page_size_64_and_dim64_gqa8():
     wl = make_custom(batch=3, heads=16, kv_heads=2, dim=64, lens=[500, 129, 64], page_size=64,
                      spike_count=5, n_sink=4, seed=9, device="cuda")
