@@ -251,6 +251,35 @@ fold_status fold_decode_fused(const fold_kv_view* kv, const fold_q_view* q, floa
                               uint8_t* cert_out, void* stream);
 
 /*
+ * fold_decode_fused_noalloc - fold_decode_fused for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  The slots and arrival counts live in a
+ * fixed scratch array inside the library (8 MiB per GPU, held from the first
+ * call on that GPU until the process ends); the call allocates nothing and
+ * takes no workspace argument.
+ *   kv, q, sm_scale, params, depth_T, num_splits, z_out, out, out_dtype,
+ *   lse_out, cert_out  as fold_decode_fused (same validation, same results,
+ *           bit for bit: the same kernel).
+ *   Scratch: num_splits*batch*num_heads*(head_dim + 1)*4 bytes of slots plus
+ *           num_seqs*num_kv_heads*4 bytes of counts (each rounded up to 256
+ *           bytes) must fit in 8 MiB, else FOLD_E_INVAL and nothing is
+ *           launched (e.g. 16 splits x 8 requests x 32 heads at head_dim 128
+ *           use 2.1 MB).  The counts are cleared by a small fill kernel on
+ *           `stream` before the decode, so each call starts from zero.
+ *   Concurrency: every call on one GPU uses that GPU's one scratch array, and
+ *           it keeps the last call's contents; calls that overlap on one GPU
+ *           (other streams, other host threads) race and must be serialised
+ *           by the caller.
+ *   The first call on a GPU looks up the scratch address (no allocation, no
+ *           synchronisation); FOLD_E_HIP if that lookup fails.
+ */
+fold_status fold_decode_fused_noalloc(const fold_kv_view* kv, const fold_q_view* q,
+                                      float sm_scale, const fold_est_params* params,
+                                      float depth_T, int32_t num_splits, float* z_out, void* out,
+                                      fold_dtype out_dtype, float* lse_out, uint8_t* cert_out,
+                                      void* stream);
+
+/*
  * fold_value_mean - request mean value rows (the running mean of Section 4's
  * value model): mean_out[s][g] = mean of value rows 0..n_s-1 of kv sequence
  * s, head g (0 for an empty sequence), FP32 sums in a fixed order.

@@ -26,6 +26,7 @@ from .fold import (  # noqa: F401
     fold_certified_decode,
     fold_combine,
     fold_decode_fused,
+    fold_decode_fused_noalloc,
     fold_decode,
     fold_draft_views,
     fold_decode_row_groups,

@@ -19,7 +19,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libfold.so")
 
 SOURCES = ["decode_split.hip", "decode_mfma.hip", "decode_packed.hip", "decode_stacked.hip", "ref_estimate.hip", "combine.hip",
-           "decode_q8.hip", "decode_q8_packed.hip", "q8_front.hip", "value_model.hip", "step.hip", "fold_api.cpp"]
+           "decode_q8.hip", "decode_q8_packed.hip", "q8_front.hip", "value_model.hip", "step.hip", "noalloc.hip",
+           "fold_api.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

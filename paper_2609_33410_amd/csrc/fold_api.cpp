@@ -364,6 +364,56 @@ fold_status fold_decode_fused(const fold_kv_view* kv, const fold_q_view* q, floa
   return ok();
 }
 
+fold_status fold_decode_fused_noalloc(const fold_kv_view* kv, const fold_q_view* q,
+                                      float sm_scale, const fold_est_params* params,
+                                      float depth_T, int32_t num_splits, float* z_out, void* out,
+                                      fold_dtype out_dtype, float* lse_out, uint8_t* cert_out,
+                                      void* stream) {
+  if (!kv || !q) return fail(FOLD_E_INVAL, "kv and q views are required");
+  if (num_splits < 1) return fail(FOLD_E_INVAL, "num_splits must be >= 1");
+  if (q->batch < 0 || q->num_heads < 0 || kv->num_seqs < 0 || kv->num_kv_heads < 0 ||
+      (kv->head_dim != 64 && kv->head_dim != 128))
+    return fail(FOLD_E_INVAL, "bad view sizes");
+  // scratch layout: slots A, slots L, arrival counts, each from a 256-byte boundary
+  auto up = [](long long b) { return (b + 255) / 256 * 256; };
+  const long long rows = static_cast<long long>(q->batch) * q->num_heads;
+  if (num_splits > (1 << 20) || rows > (1LL << 31) ||
+      static_cast<long long>(kv->num_seqs) * kv->num_kv_heads > (1LL << 31))
+    return fail(FOLD_E_INVAL, "the call is far larger than the fixed scratch");
+  const long long bytes_a = up(static_cast<long long>(num_splits) * rows * kv->head_dim * 4);
+  const long long bytes_l = up(static_cast<long long>(num_splits) * rows * 4);
+  const long long bytes_c = up(static_cast<long long>(kv->num_seqs) * kv->num_kv_heads * 4);
+  const long long need = bytes_a + bytes_l + bytes_c;
+  if (need > static_cast<long long>(fold::scratch_capacity()))
+    return fail(FOLD_E_INVAL,
+                "the call needs %lld bytes of scratch (slots and arrival counts); the fixed "
+                "scratch holds %lld: use fold_decode_fused with caller workspace",
+                need, static_cast<long long>(fold::scratch_capacity()));
+  // validate every argument first (placeholder workspace addresses with the
+  // scratch's alignment), so a refused call touches no HIP state
+  char* base = reinterpret_cast<char*>(uintptr_t{256});
+  fold::FusedArgs f;
+  fold_status st = fused_args(kv, q, sm_scale, params, depth_T, num_splits,
+                              reinterpret_cast<float*>(base), reinterpret_cast<float*>(base + bytes_a),
+                              reinterpret_cast<int32_t*>(base + bytes_a + bytes_l), z_out, out,
+                              out_dtype, lse_out, cert_out, &f);
+  if (st != FOLD_OK) return st;
+  hipError_t err = fold::scratch_device_ptr(reinterpret_cast<void**>(&base));
+  if (err != hipSuccess) return fail(FOLD_E_HIP, "scratch address: %s", hipGetErrorString(err));
+  float* part_A = reinterpret_cast<float*>(base);
+  float* part_L = reinterpret_cast<float*>(base + bytes_a);
+  int32_t* arrivals = reinterpret_cast<int32_t*>(base + bytes_a + bytes_l);
+  f.d.part_A = part_A;
+  f.d.part_L = part_L;
+  f.x.arrivals = arrivals;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  err = fold::launch_clear_i32(arrivals, kv->num_seqs * kv->num_kv_heads, s);
+  if (err != hipSuccess) return fail(FOLD_E_HIP, "scratch clear launch: %s", hipGetErrorString(err));
+  err = fold::launch_decode_fused(f, kv->head_dim, s);
+  if (err != hipSuccess) return fail(FOLD_E_HIP, "fused decode launch: %s", hipGetErrorString(err));
+  return ok();
+}
+
 fold_status fold_value_mean(const fold_kv_view* kv, float* mean_out, void* stream) {
   if (!kv) return fail(FOLD_E_INVAL, "kv view is required");
   fold::MeanArgs a{};

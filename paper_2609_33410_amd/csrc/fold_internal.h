@@ -243,6 +243,12 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_q8_decode(const Q8DecodeArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_front(const Q8EstimateArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_decode_fused(const FusedArgs& a, int head_dim, hipStream_t stream);
+// The library's fixed device scratch (noalloc.hip): its capacity in bytes, its
+// address on the current device (looked up once per device), and a fill
+// kernel that zeroes n int32 values of it.
+size_t scratch_capacity();
+hipError_t scratch_device_ptr(void** out);
+hipError_t launch_clear_i32(int32_t* p, int n, hipStream_t stream);
 hipError_t launch_q8_decode_fused(const Q8FusedArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_value_mean(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_value_mean_append(const MeanArgs& a, int head_dim, hipStream_t stream);

@@ -33,6 +33,7 @@ EXPORTED = (
     "fold_decode_split",
     "fold_combine",
     "fold_decode_fused",
+    "fold_decode_fused_noalloc",
     "fold_value_mean",
     "fold_value_mean_append",
     "fold_q8_write_keys",
@@ -165,6 +166,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.fold_decode_fused_noalloc.restype = ctypes.c_int
+    lib.fold_decode_fused_noalloc.argtypes = [P(fold_kv_view), P(fold_q_view), ctypes.c_float,
+                                              P(fold_est_params), ctypes.c_float, ctypes.c_int32,
+                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.fold_value_mean.restype = ctypes.c_int
     lib.fold_value_mean.argtypes = [P(fold_kv_view), ctypes.c_void_p, ctypes.c_void_p]
     lib.fold_value_mean_append.restype = ctypes.c_int
@@ -478,6 +484,46 @@ def fold_decode_fused(kv: KV, q: Q, sm_scale: float, depth_T: float, num_splits:
         None if p is None else ctypes.byref(p), depth_T, num_splits, _ptr(part_A), _ptr(part_L),
         _ptr(arrivals), _ptr(z_out), _ptr(out), odt, _ptr(lse_out), _ptr(cert_out),
         _stream(stream)))
+    return out
+
+
+def fold_decode_fused_noalloc(kv: KV, q: Q, sm_scale: float, depth_T: float, num_splits: int,
+                              z_out: torch.Tensor, out: torch.Tensor,
+                              lse_out: Optional[torch.Tensor] = None,
+                              cert_out: Optional[torch.Tensor] = None, params=None,
+                              stream=None) -> torch.Tensor:
+    """fold_decode_fused with its slots and arrival counts in the library's
+    fixed device scratch (8 MiB per GPU): no workspace, no allocation.  Calls
+    that overlap on one GPU race on that scratch."""
+    _need(z_out, "z_out", torch.float32)
+    if lse_out is not None:
+        _need(lse_out, "lse_out", torch.float32)
+    if cert_out is not None:
+        _need(cert_out, "cert_out", torch.uint8)
+    if out.dtype == torch.float32:
+        odt = FOLD_DTYPE_F32
+    elif out.dtype == torch.bfloat16:
+        odt = FOLD_DTYPE_BF16
+    else:
+        raise TypeError("out must be float32 or bfloat16")
+    if not out.is_contiguous():
+        raise ValueError("out must be contiguous")
+    b, h, d = (int(x) for x in q.tensor.shape)
+    for t, nm, n in ((z_out, "z_out", b * h), (out, "out", b * h * d),
+                     (lse_out, "lse_out", b * h), (cert_out, "cert_out", b * h)):
+        if t is not None and t.numel() < n:
+            raise ValueError(f"{nm} needs {n} elements, got {t.numel()}")
+    _need_device([("q", q.tensor), ("z_out", z_out), ("out", out), ("lse_out", lse_out),
+                  ("cert_out", cert_out)]
+                 + [(f"view tensor {i}", t) for i, t in enumerate(kv.tensors)])
+    p = None
+    if params is not None:
+        p = fold_est_params(params["sink"], params["recent"], params["strata"],
+                            params["trim_lo"], params["trim_hi"])
+    _check(load_library().fold_decode_fused_noalloc(
+        ctypes.byref(kv.view), ctypes.byref(q.view), sm_scale,
+        None if p is None else ctypes.byref(p), depth_T, num_splits, _ptr(z_out), _ptr(out), odt,
+        _ptr(lse_out), _ptr(cert_out), _stream(stream)))
     return out
 
 

@@ -490,3 +490,32 @@ def test_q8_fused_binding_rejects_short_codes():
             F.fold_q8_decode_fused(kv, keys, t["q"], 0.125, kw["codes"], kw["req_lens"],
                                    math.inf, 2, t["part_A"], t["part_L"], kw["arrivals"],
                                    t["z_out"], t["out"])
+
+
+# --------------------------------------------- one-launch decode, no allocation --
+def _noalloc(lib, kv=None, q=None, T=math.inf, splits=2, z=FAKE, out=FAKE, out_dtype=0):
+    return lib.fold_decode_fused_noalloc(None if kv is False else ctypes.byref(kv or _kv()),
+                                         ctypes.byref(q or _q()), 0.125, None, T, splits, z, out,
+                                         out_dtype, None, None, None)
+
+
+@pytest.mark.parametrize("kw,want,text", [
+    ({"splits": 4096}, F.FOLD_E_INVAL, "scratch"),            # 33.8 MB of slots > 8 MiB
+    ({"splits": 1 << 21}, F.FOLD_E_INVAL, "scratch"),
+    ({"q": _q(batch=1 << 20, num_heads=8), "kv": _kv(num_seqs=1 << 20)}, F.FOLD_E_INVAL, "scratch"),
+    ({"splits": 0}, F.FOLD_E_INVAL, "num_splits"),
+    ({"T": float("nan")}, F.FOLD_E_INVAL, ""),
+    ({"z": None}, F.FOLD_E_INVAL, ""),
+    ({"out": FAKE + 4}, F.FOLD_E_INVAL, "aligned"),
+    ({"out_dtype": 7}, F.FOLD_E_INVAL, ""),
+    ({"kv": False}, F.FOLD_E_INVAL, ""),
+    ({"q": _q(num_heads=2)}, F.FOLD_E_UNSUPPORTED, ""),       # MHA
+    ({"kv": _kv(num_seqs=1)}, F.FOLD_E_INVAL, ""),            # num_seqs != batch
+])
+def test_noalloc_decode_rejects_before_touching_the_device(lib, kw, want, text):
+    """Every refusal (scratch too small included) happens on the host before
+    the scratch address is looked up or anything is launched: these calls run
+    here without a GPU."""
+    assert _noalloc(lib, **kw) == want
+    msg = lib.fold_last_error().decode()
+    assert len(msg) > 0 and text in msg
