@@ -66,19 +66,22 @@ def _gate_check(wl, oi, res, T):
                     assert np.array_equal(pg, page), f"page gates differ (level {li} seq {seq} head {g})"
 
 
-def _x_check(wl, oi, res, z64):
-    """The exported x equals the oracle's s - Z to FP32 rounding."""
+def _x_check(wl, oi, res, z64, chunks=None):
+    """The exported x equals the oracle's s - Z to FP32 rounding (on the listed
+    (kv sequence, kv head) chunks, or all)."""
     q = oracle.bf16_bits_to_f64(oi["q_bits"])
     G = wl.group
     worst = 0.0
     for li, lv in enumerate(oi["levels"]):
-        x = res["dbg"][li]["x"].double().numpy()
+        x = res["dbg"][li]["x"].numpy()
         for seq, n in enumerate(lv["seq_lens"]):
             if lv["row_indptr"] is None:
                 reqs = [seq]
             else:
                 reqs = list(lv["row_req"][lv["row_indptr"][seq]:lv["row_indptr"][seq + 1]])
             for g in range(wl.num_kv_heads):
+                if chunks is not None and (seq, g) not in chunks:
+                    continue
                 keys = oracle.gather(oi["k_bits"], seq, g, n, lv["block_table"], wl.page_size)
                 for r in reqs:
                     hs = [g * G + hh for hh in range(G)]
@@ -125,7 +128,7 @@ def _full_parity(wl, T, splits=None, own_mode=True, check_gates=True):
     return res, oi
 
 
-def _flip_counts(wl, oi, res, z64, T):
+def _flip_counts(wl, oi, res, z64, T, chunks=None):
     q = oracle.bf16_bits_to_f64(oi["q_bits"])
     b, h = z64.shape
     flips = np.zeros((b, h))
@@ -136,6 +139,8 @@ def _flip_counts(wl, oi, res, z64, T):
             reqs = [seq] if lv["row_indptr"] is None else \
                 list(lv["row_req"][lv["row_indptr"][seq]:lv["row_indptr"][seq + 1]])
             for g in range(wl.num_kv_heads):
+                if chunks is not None and (seq, g) not in chunks:
+                    continue
                 keys = oracle.gather(oi["k_bits"], seq, g, n, lv["block_table"], wl.page_size)
                 for r in reqs:
                     hs = [g * G + hh for hh in range(G)]
@@ -315,10 +320,18 @@ def test_certificate_forced_bad_reference_and_rerun():
 
 
 # ------------------------------------------------- full-size, sampled ------
-def _sampled(wl, T, chunks, check_gates=False):
+def _sampled(wl, T, chunks, check_gates=False, own_mode=False):
     """Full-size run on the GPU; the oracle recomputes the sampled
-    (kv sequence, kv head) chunks of a flat workload one by one."""
-    res = _gpu.run(wl, T, debug=check_gates)
+    (kv sequence, kv head) chunks of a flat workload one by one.
+
+    With ``check_gates`` the kernel's debug exports are taken: the key and page
+    read bits of EVERY chunk of the call must equal the FP32 rule applied to
+    the exported x (bit-exact), and the exported x of the sampled chunks must
+    equal the oracle's s - Z.  With ``own_mode`` (finite T) the sampled rows
+    are also held to the stated bound against the oracle's own FP64
+    decisions: the 1e-2 row bar plus 2 * 2^-T * N_flip * max|v| / L."""
+    debug = check_gates or own_mode
+    res = _gpu.run(wl, T, debug=debug)
     oi = _adapt.oracle_inputs(wl)
     G = wl.group
     rows = [(r, g * G + hh) for r, g in chunks for hh in range(G)]
@@ -326,11 +339,11 @@ def _sampled(wl, T, chunks, check_gates=False):
     z64 = res["z"].double().numpy()
     lv = oi["levels"][0]
     S = res["splits"][0]
-    imposed = None if not check_gates else res["dbg"][0]["x"].numpy()
+    x = res["dbg"][0]["x"].numpy() if debug else None
     pa, pl = oracle.decode_level(oi["q_bits"], oi["k_bits"], oi["v_bits"],
                                  num_kv_heads=wl.num_kv_heads, page_size=wl.page_size,
                                  sm_scale=wl.sm_scale, z=z64, T=T, num_splits=S,
-                                 chunks=chunks, imposed_x=imposed, **lv)
+                                 chunks=chunks, imposed_x=x, **lv)
     o_ref, l_ref = oracle.combine(pa, pl)
     ri = np.array([r for r, _ in rows])
     hi = np.array([h for _, h in rows])
@@ -339,25 +352,52 @@ def _sampled(wl, T, chunks, check_gates=False):
     assert (err <= TOL).all()
     gl = res["part_L"].double().numpy()[:, ri, hi]
     assert np.allclose(gl, pl[:, ri, hi], rtol=2e-5, atol=0)
+    if check_gates:
+        _gate_check(wl, oi, res, T)
+        _x_check(wl, oi, res, z64, chunks=chunks)
+    if own_mode and not math.isinf(T):
+        pa_o, pl_o = oracle.decode_level(oi["q_bits"], oi["k_bits"], oi["v_bits"],
+                                         num_kv_heads=wl.num_kv_heads, page_size=wl.page_size,
+                                         sm_scale=wl.sm_scale, z=z64, T=T, num_splits=S,
+                                         chunks=chunks, **lv)
+        o_own, l_own = oracle.combine(pa_o, pl_o)
+        flips = _flip_counts(wl, oi, res, z64, T, chunks=chunks)
+        vmax = float(np.abs(oracle.bf16_bits_to_f64(oi["v_bits"])).max())
+        scale = np.maximum(np.abs(o_own[ri, hi]).max(axis=-1), 1e-300)
+        bound = TOL + 2.0 * 2.0 ** -T * flips[ri, hi] * vmax / np.maximum(l_own[ri, hi], 1e-300) \
+            / scale
+        err_own = _gpu.row_errors(res["out"].numpy()[ri, hi], o_own[ri, hi])
+        print(f"  own-mode max row err = {err_own.max():.3e}, flips = {int(flips[ri, hi].sum())}, "
+              f"min bound = {bound.min():.3e}")
+        assert (err_own <= bound).all()
     return res
 
 
 @pytest.mark.parametrize("T", [INF, 16.0])
 def test_config2_full_size_sampled(T):
+    """One (request, kv head) chunk of every request; at T = 16 the read bits of
+    the whole call bit-exact and the own-mode stated bound."""
     wl = make_config(2, device="cuda")
-    _sampled(wl, T, chunks=[(0, 0), (5, 3), (15, 7)])
+    _sampled(wl, T, chunks=[(r, (3 * r) % 8) for r in range(16)],
+             check_gates=not math.isinf(T), own_mode=not math.isinf(T))
 
 
-@pytest.mark.parametrize("T", [INF, 12.0])
+@pytest.mark.parametrize("T", [INF, 24.0, 16.0, 12.0])
 def test_config3_full_size_sampled(T):
+    """Every configured depth of the Qwen3-8B-shaped 32K decode."""
     wl = make_config(3, device="cuda")
-    _sampled(wl, T, chunks=[(0, 0), (7, 7)])
+    _sampled(wl, T, chunks=[(0, 0), (3, 5), (7, 7)], check_gates=not math.isinf(T),
+             own_mode=not math.isinf(T))
 
 
 @pytest.mark.parametrize("T", [INF, 16.0])
 def test_config4_full_size_sampled(T):
+    """The MHA 64K-128K decode (ragged, 32 splits): sampled rows of every
+    request; at T = 16 the read bits of the whole call bit-exact and the
+    own-mode stated bound."""
     wl = make_config(4, device="cuda")
-    _sampled(wl, T, chunks=[(0, 0), (1, 17), (3, 31)])
+    _sampled(wl, T, chunks=[(0, 0), (1, 17), (2, 9), (3, 31)],
+             check_gates=not math.isinf(T), own_mode=not math.isinf(T))
 
 
 @pytest.mark.parametrize("T", [INF, 16.0])

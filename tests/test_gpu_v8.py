@@ -212,29 +212,45 @@ def _on_pages(fn, t, pages, outs):
     return full
 
 
+def _on_chunk_pages(fn, t, chunks, bt, seq_lens, outs):
+    """fn over the stored rows of each chunk's pages at the chunk's kv head
+    only (the rows its scan reads); other entries zero."""
+    full = [np.zeros(shape, dtype=dtype) for shape, dtype in outs]
+    for seq, g in chunks:
+        pg = sorted({int(x) for x in bt[seq, :(seq_lens[seq] + 15) // 16]})
+        idx = torch.as_tensor(pg, dtype=torch.long, device=t.device)
+        sub = fn(host_bits(t.index_select(0, idx)[:, g:g + 1].contiguous()))
+        for dst, arr in zip(full, sub):
+            dst[np.array(pg), g:g + 1] = arr
+    return full
+
+
+@pytest.mark.parametrize("cfg,chunks", [(2, [(0, 0), (5, 3), (15, 7)]),
+                                        (3, [(0, 0), (7, 7)]),
+                                        (4, [(0, 5), (2, 30)])])
 @pytest.mark.parametrize("T", [INF, 16.0])
-def test_v8_config2_full_size_sampled(T):
-    """Full-size GQA batch (16 x 8192 keys, paged): sampled (request, kv head)
+def test_v8_full_size_sampled(cfg, chunks, T):
+    """Full-size workloads 2 (16 x 8192 keys, GQA), 3 (8 x 32768, 16 splits)
+    and 4 (MHA, 64K-128K ragged, 32 splits): sampled (request, kv head)
     chunks against the oracle's own FP64 decisions, within the row bar; the
-    sampled pages' value codes bit-exact."""
-    wl = make_config(2, device="cuda")
+    sampled chunks' key and value codes bit-exact."""
+    wl = make_config(cfg, device="cuda")
     vals = _gpu_q8.encode_values(wl)
     res, keys = _gpu_q8.run(wl, T, values=vals)
     oi = _adapt.oracle_inputs(wl)
     lv = oi["levels"][0]
-    chunks = [(0, 0), (5, 3), (15, 7)]
     bt = lv["block_table"]
-    pages = set()
-    for rq, _ in chunks:
-        pages |= {int(pg) for pg in bt[rq, :(lv["seq_lens"][rq] + 15) // 16]}
     shp = tuple(wl.k.shape)
-    planes = _on_pages(q8.split_keys, wl.k, pages,
-                       [(shp, np.int8), (shp, np.int8), (shp[:-1], np.uint16)])
-    p, r = _on_pages(lambda b: q8.split_values(b, vals.scale_exp), wl.v, pages,
-                     [(shp, np.uint8), (shp, np.uint8)])
-    idx = np.array(sorted(pages))
+    planes = _on_chunk_pages(q8.split_keys, wl.k, chunks, bt, lv["seq_lens"],
+                             [(shp, np.int8), (shp, np.int8), (shp[:-1], np.uint16)])
+    p, r = _on_chunk_pages(lambda b: q8.split_values(b, vals.scale_exp), wl.v, chunks, bt,
+                           lv["seq_lens"], [(shp, np.uint8), (shp, np.uint8)])
     gp, gr = _planes_of(vals)
-    assert np.array_equal(gp[idx], p[idx]) and np.array_equal(gr[idx], r[idx])
+    ga = keys.plane_a.cpu().numpy()
+    for seq, g in chunks:
+        idx = np.array(sorted({int(x) for x in bt[seq, :(lv["seq_lens"][seq] + 15) // 16]}))
+        assert np.array_equal(gp[idx, g], p[idx, g]) and np.array_equal(gr[idx, g], r[idx, g])
+        assert np.array_equal(ga[idx, g], planes[0][idx, g])
     qa, qb, eta = q8.split_queries(host_bits(wl.q), wl.sm_scale)
     tau = np.array([q8.refine_tau(n, 0.0) for n in wl.flat.seq_lens_host], dtype=np.float32)
     assert np.array_equal(res["tau_v"].numpy(), tau)
