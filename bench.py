@@ -211,22 +211,6 @@ class Q8Path:
     def estimate(self, stream):
         self.F.fold_q8_ref_estimate(self.flat, self.keys, self.qq, self.z, stream=stream)
 
-    def fusable(self):
-        lv = self.wl.levels[0]
-        return (len(self.wl.levels) == 1 and lv.row_indptr is None and self.wl.group <= 8
-                and lv.num_seqs == self.wl.batch)
-
-    def fused(self, T, stream):
-        """Front, scan and combine in one launch (fold_q8_decode_fused)."""
-        if not hasattr(self, "arrivals"):
-            self.arrivals = self.torch.zeros(self.wl.levels[0].num_seqs, self.wl.num_kv_heads,
-                                             dtype=self.torch.int32, device=self.wl.q.device)
-        self.F.fold_q8_decode_fused(self.levels[0], self.keys, self.wl.q, self.wl.sm_scale,
-                                    self.qq, self.wl.flat.seq_lens, T, self.splits[0],
-                                    self.part_A, self.part_L, self.arrivals, self.z, self.out,
-                                    values=self.vals, kappa=self.kappa, kappa_v=self.kappa_v,
-                                    stream=stream)
-
     def front(self, stream):
         """Query split and reference estimate in one launch (fold_q8_front)."""
         self.F.fold_q8_front(self.flat, self.keys, self.wl.q, self.wl.sm_scale, self.qq, self.z,
@@ -352,8 +336,7 @@ def time_q8(qp, T, steps, warmup, flush, torch):
     ``split_then_est`` times the same step with the split and the estimate
     as two launches."""
     stream = torch.cuda.current_stream()
-    res = {"front": [], "dec": [], "comb": [], "step": [], "append": [], "split_then_est": [],
-           "fused": []}
+    res = {"front": [], "dec": [], "comb": [], "step": [], "append": [], "split_then_est": []}
     for it in range(warmup + steps):
         evict_caches(flush)
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
@@ -372,29 +355,23 @@ def time_q8(qp, T, steps, warmup, flush, torch):
             res["dec"].append(ev[1].elapsed_time(ev[2]))
             res["comb"].append(ev[2].elapsed_time(ev[3]))
             res["append"].append(ev[3].elapsed_time(ev[4]))
-    one = qp.fusable()
     for it in range(warmup + steps):
-        for key in ("step", "split_then_est") + (("fused",) if one else ()):
+        for key in ("step", "split_then_est"):
             evict_caches(flush)
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-            if key == "fused":
-                qp.fused(T, stream)
+            if key == "step":
+                qp.front(stream)
             else:
-                if key == "step":
-                    qp.front(stream)
-                else:
-                    qp.split(stream)
-                    qp.estimate(stream)
-                qp.decode(T, stream)
-                qp.combine(stream)
+                qp.split(stream)
+                qp.estimate(stream)
+            qp.decode(T, stream)
+            qp.combine(stream)
             e1.record(stream)
             if it >= warmup:
                 e1.synchronize()
                 res[key].append(e0.elapsed_time(e1))
-    if not one:
-        del res["fused"]
     return {k: statistics.median(v) for k, v in res.items()}
 
 
@@ -409,8 +386,7 @@ def q8_leg(wl, F, torch, flush, steps, warmup, name=None, values8=False):
                     ("two E4M3 value planes, scale 2^%d" % qp.vals.scale_exp if values8
                      else "BF16 values"),
            "step": "front (query split + estimate from coarse logits, one launch) + split "
-                   "scan + combine; the one-token append is timed apart; breakdown `fused`: "
-                   "the same call as one launch (fold_q8_decode_fused), slower here"}
+                   "scan + combine; the one-token append is timed apart"}
     if values8:
         out["kappa_v"] = qp.kappa_v
     for T in (math.inf, 16.0):
@@ -573,7 +549,10 @@ def scan_kernel_name(wl, dense=True):
     the library launches for a single-level workload."""
     d, dn = wl.head_dim, "true" if dense else "false"
     if wl.group == 1:
-        return f"decode_split_kernel<{d}, 1, {dn}, false>"
+        # waves per workgroup: 8 when each wave gets at least 4 chunks of the
+        # longest sequence per split, else 4 (the library's rule)
+        w = 8 if ((wl.flat.max_seq_len + 15) // 16) // wl.level_splits[0] >= 32 else 4
+        return f"decode_split_kernel<{d}, 1, {dn}, false, {w}>"
     if wl.group <= 8:
         return f"decode_packed_kernel<{d}, {4 if wl.group <= 4 else 2}, {dn}, false>"
     return f"decode_mfma_kernel<{d}, ...>"
@@ -735,9 +714,10 @@ def _local_includes(path):
 
 
 def kernel_sources_sha(source="*"):
-    """SHA-256 over a kernel's source file and every local header it includes
-    (transitively), or over every library source with ``source="*"``; it
-    identifies the code a counter record was taken on."""
+    """SHA-256 over the source files of some kernels (a file name or a list of
+    them) and every local header they include (transitively), or over every
+    library source with ``source="*"``; it identifies the code a counter
+    record was taken on."""
     import glob
     import hashlib
 
@@ -745,7 +725,7 @@ def kernel_sources_sha(source="*"):
     if source == "*":
         files = sorted(os.path.basename(f) for f in glob.glob(os.path.join(csrc, "*")))
     else:
-        seen, todo = set(), [source]
+        seen, todo = set(), [source] if isinstance(source, str) else list(source)
         while todo:
             f = todo.pop()
             if f in seen or not os.path.exists(os.path.join(csrc, f)):

@@ -181,36 +181,6 @@ fold_status fold_q8_front(const fold_kv_view* kv, const fold_q8_keys* keys, cons
                           int8_t* planes_out, float* eta_out, float* tau_out, float* tau_v_out,
                           const fold_est_params* params, float* z_out, void* stream);
 
-/*
- * fold_q8_decode_fused - the whole step of a single level over a two-plane
- * key cache in one launch: fold_q8_front, fold_q8_decode_split over splits
- * [0, num_splits) and fold_combine, with the same bits in planes_out,
- * eta_out, tau_out, tau_v_out, z_out, out, lse_out and cert_out (Section 4,
- * "Cache format", "Weight-gated reads"; Section 3, "Choosing the reference";
- * Algorithm 1).  Every (request, kv head, split) workgroup splits its group's
- * query rows, estimates their references from the coarse logits while its
- * first plane-A keys load, scans its tiles, writes its slot, and the split
- * that finishes last adds the slots in increasing order into the output.
- *   kv, keys, q, sm_scale, req_lens, kappa, kappa_v, params  as fold_q8_front
- *            (req_lens required; a per-request view with num_seqs == batch
- *            and at most 8 rows per kv head, else FOLD_E_UNSUPPORTED)
- *   values, depth_T, num_splits  as fold_q8_decode_split
- *   part_A, part_L, arrivals     as fold_decode_fused (slots under 2 GiB;
- *            arrivals [num_seqs][num_kv_heads] int32, zero before the first
- *            call and after every call)
- *   planes_out, eta_out (required), tau_out, tau_v_out (or NULL): the query
- *            split's outputs, written by split 0
- *   z_out, out, out_dtype, lse_out, cert_out  as fold_decode_fused
- */
-fold_status fold_q8_decode_fused(const fold_kv_view* kv, const fold_q8_keys* keys,
-                                 const fold_q_view* q, float sm_scale, const int32_t* req_lens,
-                                 float kappa, float kappa_v, const fold_v8_values* values,
-                                 const fold_est_params* params, float depth_T, int32_t num_splits,
-                                 float* part_A, float* part_L, int32_t* arrivals,
-                                 int8_t* planes_out, float* eta_out, float* tau_out,
-                                 float* tau_v_out, float* z_out, void* out, fold_dtype out_dtype,
-                                 float* lse_out, uint8_t* cert_out, void* stream);
-
 /* Rows per read group (16 or 32) and read groups per (kv sequence, kv head)
  * of fold_q8_decode_split; -1 on an invalid view.  The GQA group size
  * num_heads / num_kv_heads must be 1, 2, 4, 8, 16 or 32, so that every read

@@ -36,7 +36,6 @@ from .fold import (  # noqa: F401
     fold_q8_decode_rows_per_group,
     fold_q8_decode_split,
     fold_q8_front,
-    fold_q8_decode_fused,
     fold_q8_ref_estimate,
     fold_q8_split_query,
     fold_q8_write_keys,

@@ -25,8 +25,6 @@
 //             live key requests nothing beyond plane A and the scales and
 //             waits for nothing but plane A.
 #include "q8_common.h"
-#include "estimate_device.h"
-#include "fused_combine.h"
 
 namespace fold {
 namespace {
@@ -404,26 +402,17 @@ struct Q8Packed {
   }
 };
 
-// The scan of one (kv sequence, kv head, split) workgroup.  FUSED (the
-// one-launch decode of a per-request level): the prologue splits the group's
-// query rows (the fused front's code) and computes their references from the
-// coarse logits while the first plane-A keys load; the scan takes the codes
-// from LDS; the last split to finish adds the slots into the output.
-template <int D, int PK, bool DENSE, bool DBG, bool V8, bool FUSED>
-__device__ __forceinline__ void q8_packed_scan(const Q8DecodeArgs& a, const FusedExtra* fx) {
+// The scan of one (kv sequence, kv head, split) workgroup.
+template <int D, int PK, bool DENSE, bool DBG, bool V8>
+__device__ __forceinline__ void q8_packed_scan(const Q8DecodeArgs& a) {
   using S = Q8Packed<D, PK, DENSE, DBG, V8>;
   constexpr int NKI = S::NKI;
   constexpr int NKV = S::NKV;
   constexpr int kTileBytes = kScanWaves * 16 * S::VSTRIDE;
   constexpr int kWaveFloats = S::NB * 4 * 64 + 64;  // one wave's accumulators, L and cut mass
   constexpr int kRedBytes = kScanWaves * kWaveFloats * 4;
-  constexpr int kEstBytes = FUSED ? kMaxEstRows * kMaxEstSamples * 4 : 0;  // the estimate's scores
-  constexpr int kSmemBytes = kTileBytes > kRedBytes ? (kTileBytes > kEstBytes ? kTileBytes : kEstBytes)
-                                                    : (kRedBytes > kEstBytes ? kRedBytes : kEstBytes);
+  constexpr int kSmemBytes = kTileBytes > kRedBytes ? kTileBytes : kRedBytes;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kSmemBytes];
-  __shared__ __attribute__((aligned(16))) int8_t qs[FUSED ? kMaxEstRows : 1][2 * D];  // FUSED: codes
-  __shared__ float etas[FUSED ? kMaxEstRows : 1];  // FUSED: their scales
-  __shared__ float zs[16];                         // FUSED: Z of row n16
 
   const ScanGeometry& g = a.d.geo;
   S sc(a);
@@ -438,10 +427,6 @@ __device__ __forceinline__ void q8_packed_scan(const Q8DecodeArgs& a, const Fuse
   sc.gate_row = static_cast<size_t>(sc.p.seq) * g.hkv + sc.p.kvh;
   sc.gspan = (g.group < 16 ? g.group : 16) - 1;
   sc.pshift = q8_page_shift(g);
-  if constexpr (FUSED) {
-    est::front_split_rows<D>(fx->est, sc.p.seq, sc.p.kvh, qs, etas, sc.p.split == 0);
-    __syncthreads();
-  }
 
   {
     const RowInfo ri = row_info(g, sc.p.seq, sc.p.kvh, sc.n16, sc.p.nrows, sc.p.req0);
@@ -450,7 +435,6 @@ __device__ __forceinline__ void q8_packed_scan(const Q8DecodeArgs& a, const Fuse
     sc.xrow = row;
 #pragma unroll
     for (int c = 0; c < NKI; ++c) {
-      if (FUSED) break;  // the codes come from LDS after the estimate
       sc.qa[c] = ri.ok ? *reinterpret_cast<const u32x4*>(a.qp + row * 2 * D + 64 * c + 16 * sc.grp)
                        : u32x4{0, 0, 0, 0};
       sc.qb[c] = ri.ok ? *reinterpret_cast<const u32x4*>(a.qp + row * 2 * D + D + 64 * c + 16 * sc.grp)
@@ -459,17 +443,10 @@ __device__ __forceinline__ void q8_packed_scan(const Q8DecodeArgs& a, const Fuse
     const RowInfo rp = row_info(g, sc.p.seq, sc.p.kvh, sc.n16 % S::BW, sc.p.nrows, sc.p.req0);
     sc.pok = rp.ok;
     sc.prow = static_cast<size_t>(rp.req) * g.heads + rp.head;
-    if constexpr (FUSED) {
-      const int nr = rp.ok ? fx->est.req_lens[rp.req] : 0;
-      sc.etap = rp.ok ? etas[sc.n16 % S::BW] : 0.0f;
-      sc.ntaup = rp.ok ? -est::refine_threshold(fx->est.kappa, nr) : 0.0f;
-      sc.ntauvp = V8 && rp.ok ? -est::refine_threshold(fx->est.kappa_v, nr) : 0.0f;
-    } else {
-      sc.zp = rp.ok ? a.d.z[sc.prow] : 0.0f;
-      sc.etap = rp.ok ? a.eta[sc.prow] : 0.0f;
-      sc.ntaup = rp.ok ? -a.tau[rp.req] : 0.0f;
-      sc.ntauvp = V8 && rp.ok ? -a.tau_v[rp.req] : 0.0f;
-    }
+    sc.zp = rp.ok ? a.d.z[sc.prow] : 0.0f;
+    sc.etap = rp.ok ? a.eta[sc.prow] : 0.0f;
+    sc.ntaup = rp.ok ? -a.tau[rp.req] : 0.0f;
+    sc.ntauvp = V8 && rp.ok ? -a.tau_v[rp.req] : 0.0f;
   }
   sc.lsum = 0.0f;
   sc.lcut = 0.0f;
@@ -484,38 +461,14 @@ __device__ __forceinline__ void q8_packed_scan(const Q8DecodeArgs& a, const Fuse
   u32x4 A0[PK][NKI], A1[PK][NKI];
   uint32_t sc0, sc1;
   Q8Loc l0[PK], l1[PK];
-  // FUSED: Z of the group's rows from the coarse logits of the sampled keys
-  // (split 0 also writes them out), the first loads issued as soon as the
-  // estimate's sample loads are; otherwise just the first loads.
-  auto prologue = [&](auto&& first_loads) {
-    if constexpr (FUSED) {
-      est::estimate_rows<D, true, true>(fx->est, sc.p.seq, sc.p.kvh,
-                                        reinterpret_cast<float (*)[kMaxEstSamples]>(smem), qs, etas,
-                                        sc.p.split == 0, zs, first_loads);
-      __syncthreads();
-      sc.zp = sc.pok ? zs[sc.n16 % S::BW] : 0.0f;
-      // a per-request view: row n16 of the group is query row n16
-#pragma unroll
-      for (int c = 0; c < NKI; ++c) {
-        sc.qa[c] = sc.rok ? *reinterpret_cast<const u32x4*>(&qs[sc.n16][64 * c + 16 * sc.grp])
-                          : u32x4{0, 0, 0, 0};
-        sc.qb[c] = sc.rok ? *reinterpret_cast<const u32x4*>(&qs[sc.n16][D + 64 * c + 16 * sc.grp])
-                          : u32x4{0, 0, 0, 0};
-      }
-    } else {
-      first_loads();
-    }
-  };
   if constexpr (DENSE) {
     // Step j: coarse pass (plane A of j), its plane-B (and refine-V) requests,
     // plane A of step j+2 into the freed set, refine and products of step j
     // (values of j, requested with its plane A two steps earlier), then the
     // values of step j+2 into the freed value set.
     u32x4 V0[PK][NKV], V1[PK][NKV];
-    prologue([&] {
-      sc.issue_a(0, A0, sc0, l0);
-      sc.issue_v(l0, V0);
-    });
+    sc.issue_a(0, A0, sc0, l0);
+    sc.issue_v(l0, V0);
     sc.issue_a(1, A1, sc1, l1);
     sc.issue_v(l1, V1);
     for (int j = 0; j < steps; j += 2) {
@@ -538,7 +491,7 @@ __device__ __forceinline__ void q8_packed_scan(const Q8DecodeArgs& a, const Fuse
       }
     }
   } else {
-    prologue([&] { sc.issue_a(0, A0, sc0, l0); });
+    sc.issue_a(0, A0, sc0, l0);
     sc.issue_a(1, A1, sc1, l1);
     // Step j: coarse pass (plane A of j), its plane-B and value requests,
     // plane A of step j+2 into the freed set, then refine and products of
@@ -593,8 +546,6 @@ __device__ __forceinline__ void q8_packed_scan(const Q8DecodeArgs& a, const Fuse
   __syncthreads();
   const size_t slot_rows = (static_cast<size_t>(a.d.slot_offset) + sc.p.split) * g.batch * g.heads;
   const bool vec_ok = (reinterpret_cast<uintptr_t>(a.d.part_A) & 15u) == 0;
-  rsrc_t ra, rl;  // FUSED: the slot arrays
-  if constexpr (FUSED) slot_rsrc<D>(a.d, &ra, &rl);
   for (int f = threadIdx.x; f < 16 * (D / 4); f += kScanThreads) {
     const int r = f / (D / 4);
     const int d = 4 * (f % (D / 4));
@@ -609,10 +560,7 @@ __device__ __forceinline__ void q8_packed_scan(const Q8DecodeArgs& a, const Fuse
       if (V8) v[i] *= a.v_scale;  // 2^e: exact
     }
     float* dst = a.d.part_A + (slot_rows + static_cast<size_t>(xr)) * D + d;
-    if constexpr (FUSED) {
-      slot_store4(ra, static_cast<uint32_t>((slot_rows + static_cast<size_t>(xr)) * D + d) * 4u,
-                  f32x4{v[0], v[1], v[2], v[3]});
-    } else if (vec_ok) {
+    if (vec_ok) {
       *reinterpret_cast<f32x4*>(dst) = f32x4{v[0], v[1], v[2], v[3]};
     } else {
 #pragma unroll
@@ -625,27 +573,18 @@ __device__ __forceinline__ void q8_packed_scan(const Q8DecodeArgs& a, const Fuse
     const int e = S::NB * 4 * 64 + threadIdx.x;
     const float v = ((red[e] + red[kWaveFloats + e]) + red[2 * kWaveFloats + e]) + red[3 * kWaveFloats + e];
     if (xr >= 0) {
-      if (FUSED && threadIdx.x < 16)
-        slot_store1(rl, static_cast<uint32_t>(slot_rows + static_cast<size_t>(xr)) * 4u, v);
-      else if (threadIdx.x < 16)
+      if (threadIdx.x < 16)
         a.d.part_L[slot_rows + static_cast<size_t>(xr)] = v;
       else if (a.d.part_Lcut)
         a.d.part_Lcut[slot_rows + static_cast<size_t>(xr)] = v;
     }
   }
-  if constexpr (FUSED) fused_combine<D>(a.d, *fx, sc.p, out_row, zs);
 }
 
 template <int D, int PK, bool DENSE, bool DBG, bool V8>
 __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void decode_q8_packed_kernel(const Q8DecodeArgs a) {
-  q8_packed_scan<D, PK, DENSE, DBG, V8, false>(a, nullptr);
-}
-
-template <int D, int PK, bool DENSE, bool V8>
-__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2)))
-void decode_q8_fused_kernel(const Q8FusedArgs fa) {
-  q8_packed_scan<D, PK, DENSE, false, V8, true>(fa.q, &fa.x);
+  q8_packed_scan<D, PK, DENSE, DBG, V8>(a);
 }
 
 template <int D, int PK, bool DENSE, bool V8>
@@ -668,36 +607,7 @@ hipError_t launch_qp_v(const Q8DecodeArgs& a, bool dbg, unsigned blocks, hipStre
               : launch_qp<D, PK, false, false>(a, dbg, blocks, stream);
 }
 
-template <int D>
-hipError_t launch_q8_fused_d(const Q8FusedArgs& a, unsigned blocks, hipStream_t stream) {
-  const bool v8 = a.q.vp != nullptr;
-  if (a.q.d.dense) {
-    if (v8)
-      hipLaunchKernelGGL((decode_q8_fused_kernel<D, 2, true, true>), dim3(blocks), dim3(kScanThreads), 0, stream, a);
-    else
-      hipLaunchKernelGGL((decode_q8_fused_kernel<D, 2, true, false>), dim3(blocks), dim3(kScanThreads), 0, stream, a);
-  } else {
-    if (v8)
-      hipLaunchKernelGGL((decode_q8_fused_kernel<D, 2, false, true>), dim3(blocks), dim3(kScanThreads), 0, stream, a);
-    else
-      hipLaunchKernelGGL((decode_q8_fused_kernel<D, 2, false, false>), dim3(blocks), dim3(kScanThreads), 0, stream, a);
-  }
-  return hipGetLastError();
-}
-
 }  // namespace
-
-// One-launch decode of a per-request level over a two-plane key cache: read
-// groups of at most eight rows.
-hipError_t launch_q8_decode_fused(const Q8FusedArgs& a, int head_dim, hipStream_t stream) {
-  const long long blocks = static_cast<long long>(a.q.d.geo.num_seqs) * a.q.d.geo.hkv * a.q.d.num_splits;
-  if (blocks == 0) return hipSuccess;
-  const unsigned nb = static_cast<unsigned>(blocks);
-  if (head_dim == 128) return launch_q8_fused_d<128>(a, nb, stream);
-  if (head_dim == 64) return launch_q8_fused_d<64>(a, nb, stream);
-  return hipErrorInvalidValue;
-}
-
 
 // Two-plane scan of read groups of at most eight rows (one read group per kv
 // sequence and head), at any depth.

@@ -632,105 +632,6 @@ fold_status fold_q8_front(const fold_kv_view* kv, const fold_q8_keys* keys, cons
   return ok();
 }
 
-fold_status fold_q8_decode_fused(const fold_kv_view* kv, const fold_q8_keys* keys,
-                                 const fold_q_view* q, float sm_scale, const int32_t* req_lens,
-                                 float kappa, float kappa_v, const fold_v8_values* values,
-                                 const fold_est_params* params, float depth_T, int32_t num_splits,
-                                 float* part_A, float* part_L, int32_t* arrivals,
-                                 int8_t* planes_out, float* eta_out, float* tau_out,
-                                 float* tau_v_out, float* z_out, void* out, fold_dtype out_dtype,
-                                 float* lse_out, uint8_t* cert_out, void* stream) {
-  if (!q || !q->q) return fail(FOLD_E_INVAL, "q view with query rows is required");
-  if (!aligned16(q->q)) return fail(FOLD_E_INVAL, "q must be 16-byte aligned");
-  if (!planes_out || !eta_out || !req_lens)
-    return fail(FOLD_E_INVAL, "planes_out, eta_out and req_lens are required");
-  if (!part_A || !part_L || !arrivals || !z_out || !out)
-    return fail(FOLD_E_INVAL, "part_A, part_L, arrivals, z_out and out are required");
-  if (!isfinite(sm_scale)) return fail(FOLD_E_INVAL, "sm_scale must be finite");
-  if (isnan(kappa) || isnan(kappa_v)) return fail(FOLD_E_INVAL, "kappa and kappa_v must not be NaN");
-  if (out_dtype != FOLD_DTYPE_F32 && out_dtype != FOLD_DTYPE_BF16)
-    return fail(FOLD_E_INVAL, "unknown out_dtype");
-  if ((reinterpret_cast<uintptr_t>(part_A) & 15u) != 0 || (reinterpret_cast<uintptr_t>(out) & 15u) != 0)
-    return fail(FOLD_E_INVAL, "part_A and out must be 16-byte aligned");
-  const fold_q8_query codes{planes_out, eta_out, tau_out, q->batch, q->num_heads, tau_v_out};
-  fold::Q8FusedArgs f{};
-  fold::Q8DecodeArgs& a = f.q;
-  fold_status st = check_q8_view(kv, keys, &codes, &a.d.geo, values == nullptr);
-  if (st != FOLD_OK) return st;
-  if (kv->row_indptr) return fail(FOLD_E_INVAL, "the fused decode needs a per-request view (no CSR rows)");
-  if (kv->num_seqs != q->batch)
-    return fail(FOLD_E_INVAL, "the fused decode needs num_seqs %d == batch %d", kv->num_seqs, q->batch);
-  const int rows = rows_per_seq_of(kv, q->num_heads);
-  if (rows > 8)
-    return fail(FOLD_E_UNSUPPORTED, "the fused two-plane decode serves at most 8 rows per kv head (got %d)", rows);
-  st = check_depth(depth_T);
-  if (st != FOLD_OK) return st;
-  if (num_splits < 1) return fail(FOLD_E_INVAL, "num_splits must be >= 1");
-  fold_est_params p;
-  st = check_est_params(params, &p);
-  if (st != FOLD_OK) return st;
-  const long long blocks = static_cast<long long>(kv->num_seqs) * kv->num_kv_heads * num_splits;
-  if (blocks > 0x7fffffffLL) return fail(FOLD_E_INVAL, "grid too large");
-  if (static_cast<long long>(num_splits) * q->batch * q->num_heads * kv->head_dim * 4 >= (1LL << 31))
-    return fail(FOLD_E_UNSUPPORTED, "the fused decode's slots must stay under 2 GiB");
-  a.vp = nullptr;
-  a.vr = nullptr;
-  a.v_scale = 1.0f;
-  a.tau_v = nullptr;
-  if (values) {
-    if (!values->plane_p || !values->plane_r)
-      return fail(FOLD_E_INVAL, "8-bit values need plane_p and plane_r");
-    if (!aligned16(values->plane_p) || !aligned16(values->plane_r))
-      return fail(FOLD_E_INVAL, "value planes must be 16-byte aligned");
-    if (values->scale_exp < -100 || values->scale_exp > 100)
-      return fail(FOLD_E_INVAL, "scale_exp %d out of range", values->scale_exp);
-    a.vp = values->plane_p;
-    a.vr = values->plane_r;
-    a.v_scale = ldexpf(1.0f, values->scale_exp);
-  }
-  a.d.q = nullptr;
-  a.d.z = nullptr;
-  a.d.part_A = part_A;
-  a.d.part_L = part_L;
-  a.d.part_Lcut = nullptr;
-  a.d.score_scale = 0.0f;
-  a.d.dense = isinf(depth_T) ? 1 : 0;
-  a.d.neg_T = a.d.dense ? 0.0f : -depth_T;
-  a.d.num_splits = num_splits;
-  a.d.slot_offset = 0;
-  a.d.rows_per_seq = rows;
-  a.d.rows_per_group = q8_rows_per_group(rows);
-  a.d.row_groups = 1;
-  a.keys = {keys->plane_a, keys->plane_b, keys->scale};
-  fold::Q8EstimateArgs& e = f.x.est;
-  e.e.geo = a.d.geo;
-  e.e.q = nullptr;
-  e.e.z_out = z_out;
-  e.e.score_scale = 0.0f;
-  e.e.sink = p.sink;
-  e.e.recent = p.recent;
-  e.e.strata = p.strata;
-  e.e.trim_lo = p.trim_lo;
-  e.e.trim_hi = p.trim_hi;
-  e.keys = a.keys;
-  e.q_src = static_cast<const uint16_t*>(q->q);
-  e.qp_out = planes_out;
-  e.eta_out = eta_out;
-  e.sm_scale = sm_scale;
-  e.req_lens = req_lens;
-  e.tau = tau_out;
-  e.tau_v = tau_v_out;
-  e.kappa = kappa;
-  e.kappa_v = kappa_v;
-  f.x.arrivals = arrivals;
-  f.x.out = out;
-  f.x.lse_out = lse_out;
-  f.x.cert_out = cert_out;
-  f.x.out_bf16 = out_dtype == FOLD_DTYPE_BF16 ? 1 : 0;
-  hipError_t err = fold::launch_q8_decode_fused(f, kv->head_dim, static_cast<hipStream_t>(stream));
-  if (err != hipSuccess) return fail(FOLD_E_HIP, "fused two-plane decode launch: %s", hipGetErrorString(err));
-  return ok();
-}
 
 fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* keys,
                                  const fold_q8_query* q, const fold_v8_values* values,

@@ -221,11 +221,6 @@ struct FusedArgs {
   FusedExtra x;
 };
 
-struct Q8FusedArgs {
-  Q8DecodeArgs q;       // the scan (q.d.z, q.qp, q.eta, q.tau, q.tau_v are not read)
-  FusedExtra x;         // x.est: the fused front's arguments (codes, thresholds, Z)
-};
-
 // Keys a kv sequence of this view can hold: max_seq_len, and for a paged view
 // also max_pages * page_size.  Device-supplied lengths are clamped to it.
 __host__ __device__ inline int view_capacity(const ScanGeometry& g) {
@@ -249,7 +244,6 @@ hipError_t launch_decode_fused(const FusedArgs& a, int head_dim, hipStream_t str
 size_t scratch_capacity();
 hipError_t scratch_device_ptr(void** out);
 hipError_t launch_clear_i32(int32_t* p, int n, hipStream_t stream);
-hipError_t launch_q8_decode_fused(const Q8FusedArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_value_mean(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_value_mean_append(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_write(const Q8WriteArgs& a, int head_dim, hipStream_t stream);

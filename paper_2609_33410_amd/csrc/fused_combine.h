@@ -1,5 +1,5 @@
-// The slot handoff and combine of the one-launch decodes (fold_decode_fused,
-// fold_q8_decode_fused): every split stores its slot, counts its arrival, and
+// The slot handoff and combine of the one-launch decode (fold_decode_fused,
+// fold_decode_fused_noalloc): every split stores its slot, counts its arrival, and
 // the split that counts last adds the slots into the output (Algorithm 1, last
 // step; Section 3 certificate).
 #pragma once

@@ -41,7 +41,6 @@ EXPORTED = (
     "fold_q8_split_query",
     "fold_q8_ref_estimate",
     "fold_q8_front",
-    "fold_q8_decode_fused",
     "fold_q8_decode_rows_per_group",
     "fold_q8_decode_row_groups",
     "fold_q8_decode_split",
@@ -199,15 +198,6 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                   ctypes.c_void_p, P(fold_est_params), ctypes.c_void_p,
                                   ctypes.c_void_p]
-    lib.fold_q8_decode_fused.restype = ctypes.c_int
-    lib.fold_q8_decode_fused.argtypes = [P(fold_kv_view), P(fold_q8_keys), P(fold_q_view),
-                                         ctypes.c_float, ctypes.c_void_p, ctypes.c_float,
-                                         ctypes.c_float, P(fold_v8_values), P(fold_est_params),
-                                         ctypes.c_float, ctypes.c_int32, ctypes.c_void_p,
-                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
-                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     for name in ("fold_q8_decode_rows_per_group", "fold_q8_decode_row_groups"):
         fn = getattr(lib, name)
         fn.restype = ctypes.c_int32
@@ -859,64 +849,6 @@ def fold_q8_front(kv: KV, keys: Q8Keys, q: torch.Tensor, sm_scale: float, out: Q
         None if req_lens is None else _ptr(out.tau_v),
         None if p is None else ctypes.byref(p), _ptr(z_out), _stream(stream)))
     return z_out
-
-
-def fold_q8_decode_fused(kv: KV, keys: Q8Keys, q: torch.Tensor, sm_scale: float, codes: Q8Query,
-                         req_lens: torch.Tensor, depth_T: float, num_splits: int,
-                         part_A: torch.Tensor, part_L: torch.Tensor, arrivals: torch.Tensor,
-                         z_out: torch.Tensor, out: torch.Tensor,
-                         values: Optional[V8Values] = None, kappa: float = -4.0,
-                         kappa_v: float = -4.0, lse_out: Optional[torch.Tensor] = None,
-                         cert_out: Optional[torch.Tensor] = None, params=None,
-                         stream=None) -> torch.Tensor:
-    """fold_q8_front, fold_q8_decode_split and fold_combine of one per-request
-    level in one launch; ``codes`` receives the query split (its ``tau`` and
-    ``tau_v`` when present), ``arrivals`` ([num_seqs, Hkv] int32) must be zero
-    before the first call and is zero after every call."""
-    qv = q_view(q)
-    _need(codes.planes, "planes", torch.int8)
-    _need(codes.eta, "eta", torch.float32)
-    _need(req_lens, "req_lens", torch.int32)
-    for t, nm in ((part_A, "part_A"), (part_L, "part_L"), (z_out, "z_out")):
-        _need(t, nm, torch.float32)
-    _need(arrivals, "arrivals", torch.int32)
-    for t, nm, dt in ((codes.tau, "tau", torch.float32), (codes.tau_v, "tau_v", torch.float32),
-                      (lse_out, "lse_out", torch.float32), (cert_out, "cert_out", torch.uint8)):
-        if t is not None:
-            _need(t, nm, dt)
-    if out.dtype == torch.float32:
-        odt = FOLD_DTYPE_F32
-    elif out.dtype == torch.bfloat16:
-        odt = FOLD_DTYPE_BF16
-    else:
-        raise TypeError("out must be float32 or bfloat16")
-    if not out.is_contiguous():
-        raise ValueError("out must be contiguous")
-    b, h, d = (int(x) for x in q.shape)
-    for t, nm, n in ((codes.planes, "planes", 2 * b * h * d), (codes.eta, "eta", b * h),
-                     (codes.tau, "tau", b), (codes.tau_v, "tau_v", b), (req_lens, "req_lens", b)):
-        if t is not None and t.numel() < n:
-            raise ValueError(f"{nm} needs {n} elements, got {t.numel()}")
-    extra = [("planes", codes.planes), ("eta", codes.eta), ("tau", codes.tau),
-             ("tau_v", codes.tau_v), ("req_lens", req_lens), ("plane_a", keys.plane_a),
-             ("plane_b", keys.plane_b), ("scale", keys.scale)]
-    if values is not None:
-        extra += [("plane_p", values.plane_p), ("plane_r", values.plane_r)]
-    _fused_checks(kv, q, num_splits, part_A, part_L, arrivals, z_out, out, lse_out, cert_out,
-                  extra)
-    p = None
-    if params is not None:
-        p = fold_est_params(params["sink"], params["recent"], params["strata"],
-                            params["trim_lo"], params["trim_hi"])
-    kk = keys.view()
-    vals = None if values is None else values.view()
-    _check(load_library().fold_q8_decode_fused(
-        ctypes.byref(kv.view), ctypes.byref(kk), ctypes.byref(qv.view), sm_scale, _ptr(req_lens),
-        kappa, kappa_v, None if vals is None else ctypes.byref(vals),
-        None if p is None else ctypes.byref(p), depth_T, num_splits, _ptr(part_A), _ptr(part_L),
-        _ptr(arrivals), _ptr(codes.planes), _ptr(codes.eta), _ptr(codes.tau), _ptr(codes.tau_v),
-        _ptr(z_out), _ptr(out), odt, _ptr(lse_out), _ptr(cert_out), _stream(stream)))
-    return out
 
 
 def fold_q8_decode_rows_per_group(kv: KV, q: Q8Query) -> int:

@@ -391,26 +391,6 @@ def test_fused_decode_rejects_bad_args(lib, kw, want):
     assert len(lib.fold_last_error()) > 0
 
 
-@pytest.mark.parametrize("kw,want", [
-    ({"req_lens": None}, F.FOLD_E_INVAL),
-    ({"planes": None}, F.FOLD_E_INVAL),
-    ({"arrivals": None}, F.FOLD_E_INVAL),
-    ({"heads": 32}, F.FOLD_E_UNSUPPORTED),                # groups of 16 rows
-    ({"kappa": float("nan")}, F.FOLD_E_INVAL),
-    ({"splits": 0}, F.FOLD_E_INVAL),
-])
-def test_q8_fused_decode_rejects_bad_args(lib, kw, want):
-    args = {"req_lens": FAKE, "planes": FAKE, "arrivals": FAKE, "heads": 8, "kappa": 0.0,
-            "splits": 2}
-    args.update(kw)
-    keys, _ = _q8()
-    q = _q(num_heads=args["heads"])
-    st = lib.fold_q8_decode_fused(ctypes.byref(_kv()), ctypes.byref(keys), ctypes.byref(q), 0.125,
-                                  args["req_lens"], args["kappa"], 0.0, None, None, math.inf,
-                                  args["splits"], FAKE, FAKE, args["arrivals"], args["planes"],
-                                  FAKE, None, None, FAKE, FAKE, 0, None, None, None)
-    assert st == want
-    assert len(lib.fold_last_error()) > 0
 
 
 # ------------------------------------- binding checks of the one-launch calls --
@@ -470,26 +450,6 @@ def test_fused_binding_rejects_host_tensors():
     """Correctly sized host tensors are refused as not in device memory."""
     with pytest.raises(ValueError, match="device tensor"):
         _call_fused(_fused_tensors())
-
-
-def test_q8_fused_binding_rejects_short_codes():
-    import torch
-
-    t = _fused_tensors()
-    kv = F.kv_view(t["k"], t["v"], t["seq_lens"], num_kv_heads=2, max_seq_len=32,
-                   block_table=t["block_table"])
-    keys = F.q8_empty_keys(t["k"])
-    codes = F.q8_empty_query(t["q"])
-    good = dict(codes=codes, req_lens=t["seq_lens"], arrivals=t["arrivals"])
-    bad = [("req_lens", dict(good, req_lens=torch.zeros(1, dtype=torch.int32)), "req_lens needs"),
-           ("arrivals", dict(good, arrivals=torch.zeros(1, dtype=torch.int32)), "arrivals needs"),
-           ("eta", dict(good, codes=F.fold.Q8Query(codes.planes, torch.zeros(3), codes.tau,
-                                                  codes.tau_v)), "eta needs")]
-    for _, kw, match in bad + [("host", good, "device tensor")]:
-        with pytest.raises(ValueError, match=match):
-            F.fold_q8_decode_fused(kv, keys, t["q"], 0.125, kw["codes"], kw["req_lens"],
-                                   math.inf, 2, t["part_A"], t["part_L"], kw["arrivals"],
-                                   t["z_out"], t["out"])
 
 
 # --------------------------------------------- one-launch decode, no allocation --
