@@ -12,6 +12,7 @@ from .fold_oracle import (  # noqa: F401
     PAGE_GATE,
     TILE,
     bf16_bits_to_f64,
+    block_means,
     combine,
     decode,
     decode_level,

@@ -29,14 +29,20 @@ notation:
 * O8  read gates: a key is read iff some row of the read group is live on it;
       a 16-key page is read iff one of its keys is (Section 4; Algorithm 1);
 * O9  per-row diagnostics (Proposition 1(iii), the certificate window of
-      Section 3, the truncation bound, live fractions).
+      Section 3, the truncation bound, live fractions);
+* O10 cut-key value models (Section 4, "Depth as a dial"; Algorithm 1's
+      virtual row): the request mean (``value_mean``, ``running_mean``) whose
+      weight is a slot's cut mass, and the block model of BF16 values
+      (``block_means``; ``decode_level(block_mean=...)``), one virtual row per
+      64-key tile carrying the tile's cut mass times the block's mean.
 
 Readings of points the paper leaves open are listed in the design notes of
 the repository (score scale, tie at the threshold, cut keys' value, gate
 granularity, estimator details, empty rows, combine order).
 
-Parity status: O1-O9 are pinned by the CPU tests (closed forms, textbook and
-library softmax, invariants, hand-computed fixtures; O9 by a hand-computed
+Parity status: O1-O10 are pinned by the CPU tests (closed forms, textbook and
+library softmax, invariants, hand-computed fixtures; O10 against library
+softmax over values with the cut keys replaced by their model; O9 by a hand-computed
 fixture of exact binary fractions and by an independent FP64 evaluation of
 the Proposition 1(iii) left side on every row of every workload).  The estimator's
 stratified/trimmed branch (n > 192) is pinned only structurally (exact
@@ -142,6 +148,21 @@ def running_mean(prev: np.ndarray, count: int, v_new: np.ndarray) -> np.ndarray:
     return prev + (np.asarray(v_new, dtype=np.float64) - prev) / (count + 1)
 
 
+def block_means(v_bits: np.ndarray, seq: int, g: int, n: int, block_table, page_size: int
+                ) -> np.ndarray:
+    """Mean value row of every 64-key block of keys 0..n-1 of (seq, g), FP64
+    ``[ceil(n / 64), D]``; the last block averages the keys it holds.
+
+    The mean part of the block model of BF16 values (Section 4, "Depth as a
+    dial"): a cut key of block t is modelled by block t's mean value row."""
+    vals = gather(v_bits, seq, g, n, block_table, page_size)
+    nblk = (n + TILE - 1) // TILE
+    out = np.zeros((nblk, v_bits.shape[-1]))
+    for t in range(nblk):
+        out[t] = vals[t * TILE:(t + 1) * TILE].mean(axis=0)
+    return out
+
+
 # ------------------------------------------------------------ level driver -
 def _rows_of(seq: int, g: int, group: int, row_indptr, row_req) -> List[Tuple[int, int]]:
     """(request, head) pairs of the query rows that attend kv seq ``seq``, head ``g``."""
@@ -157,7 +178,7 @@ def decode_level(q_bits, k_bits, v_bits, *, num_kv_heads: int, page_size: int,
                  row_indptr=None, row_req=None, z: np.ndarray, T: float, num_splits: int,
                  imposed_x: Optional[np.ndarray] = None,
                  chunks: Optional[Iterable[Tuple[int, int]]] = None,
-                 with_cut: bool = False):
+                 with_cut: bool = False, block_mean=None):
     """Split partials of one scan level (steps O1-O6).
 
     Returns ``part_A [S, B, H, D]`` and ``part_L [S, B, H]`` (FP64); rows the
@@ -166,7 +187,13 @@ def decode_level(q_bits, k_bits, v_bits, *, num_kv_heads: int, page_size: int,
     those values.  ``chunks`` restricts the work to the listed
     ``(kv seq, kv head)`` pairs.  With ``with_cut`` a third array
     ``part_Lcut [S, B, H]`` holds the cut keys' summed weights (the mass the
-    value model of Section 4 attaches to its virtual row).
+    value model of Section 4 attaches to its virtual row).  With
+    ``block_mean`` (a mapping ``(kv seq, kv head) -> [ceil(n / 64), D]``
+    block mean rows, see ``block_means``) the block model of BF16 values is
+    on: every 64-key tile ``t`` of a split has one virtual row whose weight is
+    the row's summed weight of the tile's cut keys ``c_it`` and whose value is
+    the block's mean ``mu_t``, so the split's *A* gains ``sum_t c_it mu_t``
+    (Section 4, "Depth as a dial"; Algorithm 1, the tile's virtual row).
     """
     q = bf16_bits_to_f64(q_bits)
     b, h, d = q.shape
@@ -197,6 +224,12 @@ def decode_level(q_bits, k_bits, v_bits, *, num_kv_heads: int, page_size: int,
             if not m.any():
                 continue
             a, l = fold(x[:, m], live[:, m], vals[m])
+            if block_mean is not None:
+                mu = np.asarray(block_mean[(seq, g)], dtype=np.float64)
+                cut_w = np.exp2(x) * ~live
+                for t in range(sp, (n + TILE - 1) // TILE, num_splits):
+                    c_t = cut_w[:, t * TILE:(t + 1) * TILE].sum(axis=-1)
+                    a = a + c_t[:, None] * mu[t][None, :]
             part_a[sp, ri, hi] = a
             part_l[sp, ri, hi] = l
             part_c[sp, ri, hi] = (np.exp2(x[:, m]) * ~live[:, m]).sum(axis=-1)

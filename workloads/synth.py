@@ -21,6 +21,17 @@ Recipe (identical for every workload; the generator is a fresh
    of the group's query rows (for MHA, ``q_h / |q_h|``);
 5. a random permutation maps (request, logical page) to a physical page.
 
+Structured values (``values="structured"``, for the cut-key value models of
+Section 4, "Depth as a dial"): the N(0,1) values of step 2 carry no
+structure, so every value model sees zero-mean noise.  Real value caches
+carry per-channel offsets and content that changes by stretches of the
+text; this option imitates that.  After step 4 and before step 5, per
+(request, kv head): a channel offset ``beta ~ 0.5 N(0,1)^D``; segment
+lengths ``1 + floor(E)`` with ``E`` exponential of mean ``segment`` keys,
+cut until the sequence is covered; one topic row ``tau ~ 0.5 N(0,1)^D`` per
+segment; then ``v_j = beta + tau_seg(j) + 0.7 v_j`` in FP32 from the BF16
+draw of step 2, rounded to BF16.
+
 Nothing here computes attention scores, weights or references.
 """
 
@@ -147,9 +158,29 @@ def _group_directions(q: torch.Tensor, hkv: int) -> torch.Tensor:
     return s / s.norm(dim=-1, keepdim=True)
 
 
+def _structure_values(v_log, lens, g, dev, segment):
+    """Channel offset + per-segment topic rows + scaled noise (module recipe)."""
+    batch, kv_heads, _, dim = v_log.shape
+    for r in range(batch):
+        n = lens[r]
+        for kh in range(kv_heads):
+            beta = 0.5 * torch.randn(dim, generator=g, device=dev)
+            seg = torch.empty(n, dtype=torch.long, device=dev)
+            pos, idx = 0, 0
+            while pos < n:
+                e = torch.empty(1, device=dev).exponential_(1.0 / segment, generator=g)
+                ln = 1 + int(e.item())
+                seg[pos:pos + ln] = idx
+                pos += ln
+                idx += 1
+            tau = 0.5 * torch.randn(idx, dim, generator=g, device=dev)
+            v = v_log[r, kh, :n].float()
+            v_log[r, kh, :n] = _bf16(beta[None, :] + tau[seg] + 0.7 * v)
+
+
 def _generate(*, name, batch, heads, kv_heads, dim, lens, paged, page_size, spike_count,
               alpha_spike, n_sink, alpha_sink, seed, device, level_splits, depths,
-              keep_logical, draw_lens=None):
+              keep_logical, draw_lens=None, values="normal", segment=256):
     dev = torch.device(device)
     g = torch.Generator(device=dev)
     g.manual_seed(seed)
@@ -177,8 +208,12 @@ def _generate(*, name, batch, heads, kv_heads, dim, lens, paged, page_size, spik
             _spike_keys(k_log[r, kh], perm, alpha_spike, u[r, kh], dim)
             if ns:
                 _spike_keys(k_log[r, kh], torch.arange(ns, device=dev), alpha_sink, u[r, kh], dim)
+    if values == "structured":
+        _structure_values(v_log, lens, g, dev, segment)
+    elif values != "normal":
+        raise ValueError(f"values={values!r}: 'normal' or 'structured'")
     meta = {"spikes": spikes, "n_sink": n_sink, "alpha_spike": alpha_spike,
-            "alpha_sink": alpha_sink, "seed": seed, "device": str(dev)}
+            "alpha_sink": alpha_sink, "seed": seed, "device": str(dev), "values": values}
     sl = torch.tensor(lens, dtype=torch.int32, device=dev)
     if not paged:
         view = KVView(None, sl, lens, n_max)
@@ -266,19 +301,25 @@ INF = float("inf")
 
 
 def make_config(i: int, seed: int = 0, device: str = "cpu", *, batch: Optional[int] = None,
-                seq_len: Optional[int] = None, keep_logical: bool = False) -> Workload:
+                seq_len: Optional[int] = None, keep_logical: bool = False,
+                values: str = "normal") -> Workload:
     """Workload ``i`` (1..5) at full size, or shrunk by ``batch`` / ``seq_len``.
 
     A shrunk workload keeps the structure (group size, spike density, sinks,
     paging) but is a different draw; it exists for CPU-sized tests.
+    ``values="structured"`` (workloads 1-4) draws values with the structure
+    described in the module recipe.
     """
+    if values != "normal" and i == 5:
+        raise ValueError("structured values are drawn for workloads 1-4")
+    vx = {"values": values}
     if i == 1:
         n = seq_len or 512
         return _generate(name=CONFIG_NAMES[1], batch=batch or 1, heads=4, kv_heads=4, dim=64,
                          lens=[n] * (batch or 1), paged=False, page_size=0,
                          spike_count=lambda m: 8, alpha_spike=4.0, n_sink=0, alpha_sink=0.0,
                          seed=seed, device=device, level_splits=[1], depths=[INF, 16.0],
-                         keep_logical=keep_logical)
+                         keep_logical=keep_logical, **vx)
     if i in (2, 3):
         n = seq_len or (8192 if i == 2 else 32768)
         b = batch or (16 if i == 2 else 8)
@@ -288,7 +329,7 @@ def make_config(i: int, seed: int = 0, device: str = "cpu", *, batch: Optional[i
                          alpha_sink=6.0, seed=seed, device=device,
                          level_splits=[4 if i == 2 else 16],
                          depths=[INF, 16.0] if i == 2 else [INF, 24.0, 16.0, 12.0],
-                         keep_logical=keep_logical)
+                         keep_logical=keep_logical, **vx)
     if i == 4:
         b = batch or 4
         hi = seq_len or 131072
@@ -297,7 +338,7 @@ def make_config(i: int, seed: int = 0, device: str = "cpu", *, batch: Optional[i
                          lens=None, draw_lens=(lo, hi), paged=True, page_size=16,
                          spike_count=lambda m: int(round(0.005 * m)), alpha_spike=3.0, n_sink=0,
                          alpha_sink=0.0, seed=seed, device=device, level_splits=[32],
-                         depths=[INF, 16.0], keep_logical=keep_logical)
+                         depths=[INF, 16.0], keep_logical=keep_logical, **vx)
     if i == 5:
         reqs = batch or 64
         pre = 16384 if seq_len is None else max(16, (seq_len // 16) * 16)
@@ -324,14 +365,14 @@ def make_custom(*, batch: int, heads: int, kv_heads: int, dim: int, lens: List[i
                 paged: bool = True, page_size: int = 16, spike_count: int = 0,
                 alpha_spike: float = 3.0, n_sink: int = 0, alpha_sink: float = 6.0,
                 seed: int = 0, device: str = "cpu", keep_logical: bool = True,
-                splits: int = 1) -> Workload:
+                splits: int = 1, values: str = "normal", segment: int = 256) -> Workload:
     """A small workload of any shape (ragged lengths allowed) for tests."""
     return _generate(name="custom", batch=batch, heads=heads, kv_heads=kv_heads, dim=dim,
                      lens=list(lens), paged=paged, page_size=page_size,
                      spike_count=lambda m: min(spike_count, max(0, m - n_sink)),
                      alpha_spike=alpha_spike, n_sink=n_sink, alpha_sink=alpha_sink, seed=seed,
                      device=device, level_splits=[splits], depths=[INF, 16.0],
-                     keep_logical=keep_logical)
+                     keep_logical=keep_logical, values=values, segment=segment)
 
 
 @dataclass
