@@ -303,6 +303,75 @@ fold_status fold_value_mean_append(const fold_kv_view* kv, const void* v_src,
                                    int32_t n_tok, float* mean, void* stream);
 
 /*
+ * fold_value_block_mean - block means of the block model of BF16 values
+ * (Section 4, "Depth as a dial"): mean_out[s][g][t] = mean of value rows
+ * 64 t .. min(64 t + 64, n_s) - 1 of kv sequence s, head g, FP32 sums in key
+ * order; blocks t >= ceil(n_s / 64) get zeros.  A key on a page id outside
+ * [0, num_pages) adds zeros to its block's sum.
+ *   kv          any view (kv->v read; kv->k and the row lists not read)
+ *   max_blocks  row stride of mean_out in blocks, >= ceil(max_seq_len / 64)
+ *   mean_out    [num_seqs][num_kv_heads][max_blocks][head_dim] fp32, 16-byte
+ *               aligned
+ */
+fold_status fold_value_block_mean(const fold_kv_view* kv, int32_t max_blocks, float* mean_out,
+                                  void* stream);
+
+/*
+ * fold_value_block_mean_append - running update of the block means for
+ * appended tokens: for a token of kv sequence s at position pos,
+ * mean[s][g][pos / 64] += (v - mean[s][g][pos / 64]) / (pos mod 64 + 1), so a
+ * block's mean stays the mean of the keys it holds.
+ *   kv, max_blocks, mean  as fold_value_block_mean (kv gives the layout)
+ *   v_src, tok_seq, tok_pos, n_tok  as fold_value_mean_append; a token with
+ *               pos / 64 >= max_blocks is skipped.  At most one token per
+ *               sequence per call.
+ */
+fold_status fold_value_block_mean_append(const fold_kv_view* kv, int32_t max_blocks,
+                                         const void* v_src, const int32_t* tok_seq,
+                                         const int32_t* tok_pos, int32_t n_tok, float* mean,
+                                         void* stream);
+
+/* Block model of BF16 values for fold_decode_split_blocks.
+ *   block_mean  [num_seqs][num_kv_heads][max_blocks][head_dim] fp32 block means
+ *               of the view's kv sequences (fold_value_block_mean), 16-byte
+ *               aligned
+ *   max_blocks  >= ceil(max_seq_len / 64)
+ *   chunk_cut   [batch][num_heads][ceil(max_seq_len / 16)] fp32 workspace: the
+ *               scan writes each row's cut mass of every 16-key chunk of its
+ *               kv sequence there (finite depth; not read at T = inf, may be
+ *               NULL then).  Entries of chunks past a sequence's end and of
+ *               rows the view does not cover are left unwritten. */
+typedef struct fold_block_model {
+  const float* block_mean;
+  int32_t max_blocks;
+  float* chunk_cut;
+} fold_block_model;
+
+/*
+ * fold_decode_split_blocks - fold_decode_split with the block model of BF16
+ * values (Section 4, "Depth as a dial"; Algorithm 1, the tile's virtual row):
+ * the cut keys of 64-key block t of (kv sequence s, kv head g) are modelled
+ * by the block's mean value row mu_t.  One virtual row per tile, whose weight
+ * is row i's summed weight of the tile's cut keys c_it, adds c_it mu_t to the
+ * A of the split that owns the tile:
+ *     A_i^s = sum_{live j in split s} w_ij v_j + sum_{tiles t of split s} c_it mu_t.
+ * L is fold_decode_split's (it holds every weight), so pairs stay additive
+ * and fold_combine (without its request-mean model) finishes the decode.
+ * At T = inf no key is cut and the call is fold_decode_split.  The scan
+ * writes the cut masses per 16-key chunk, then a second kernel adds the
+ * virtual rows into the slots (both on `stream`).
+ *   kv ... num_slots, part_A, part_L  as fold_decode_split
+ *   model    the block means and the chunk workspace (required)
+ *   dbg      NULL, or the optional exports of fold_decode_split
+ */
+fold_status fold_decode_split_blocks(const fold_kv_view* kv, const fold_q_view* q,
+                                     float sm_scale, const float* z, float depth_T,
+                                     int32_t num_splits, int32_t slot_offset, int32_t num_slots,
+                                     float* part_A, float* part_L,
+                                     const fold_block_model* model, const fold_debug* dbg,
+                                     void* stream);
+
+/*
  * fold_append_kv - cache append (Section 4, "Weight-gated reads": the front
  * appends each step's new token): token t's key and value rows are stored at
  * position tok_pos[t] of kv sequence tok_seq[t].

@@ -24,6 +24,9 @@
 //            weight of every key, live or cut.  The A operand V^T is read from
 //            the wave's value tile in LDS, transposed by 16-bit reads.
 //
+// CX (block model of BF16 values, finite T): each scored chunk's cut mass per
+// row, the summed weights of its cut keys, is also written to chunk_cut.
+//
 // The scan is software-pipelined per wave exactly as the VALU scan: gated
 // (finite T) issues the keys of chunk t+2, scores chunk t+1 and issues its live
 // value rows, then forms the product of chunk t; dense (T = inf) issues keys
@@ -36,7 +39,7 @@ namespace {
 __device__ __forceinline__ f32x4 mfma_qk(u32x4 a, u32x4 b, f32x4 c) { return mfma_16x16x32(a, b, c); }
 __device__ __forceinline__ f32x4 mfma_pv(u32x2 a, u32x2 b, f32x4 c) { return mfma_16x16x16(a, b, c); }
 
-template <int D, int RB, bool DENSE, bool DBG>
+template <int D, int RB, bool DENSE, bool DBG, bool CX>
 struct MfmaScan {
   static constexpr int NK = D / 32;           // 128-bit loads per lane per chunk (K, and V)
   static constexpr int NB = D / 16;           // 16-channel blocks of the value product
@@ -108,6 +111,7 @@ struct MfmaScan {
 #pragma unroll
       for (int c2 = 0; c2 < NK; ++c2) s = mfma_qk(ka[c2], qb[b][c2], s);
       uint32_t hi[4], lo[4];
+      float cc = 0.0f;  // cut weights of this lane's keys of the chunk
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int kk = 4 * grp + i;
@@ -117,11 +121,20 @@ struct MfmaScan {
         const float w = ok ? exp2_fast(x) : 0.0f;
         lsum[b] += w;
         if (!DENSE) lcut[b] += live ? 0.0f : w;
+        if (!DENSE && (CX || DBG)) cc += live ? 0.0f : w;
         const float pw = live ? w : 0.0f;
         hi[i] = __float_as_uint(pw) & 0xffff0000u;
         lo[i] = f32_to_bf16_rne(pw - __uint_as_float(hi[i]));
         any[i] |= __ballot(live);
         if (DBG && a.x_out && ok) a.x_out[xrow[b] * g.max_seq_len + key0 + kk] = x;
+      }
+      if constexpr (!DENSE && (CX || DBG)) {
+        if (a.chunk_cut) {
+          // the four key groups of row n16 hold the chunk's 16 keys
+          cc += __shfl_xor(cc, 16, 64);
+          cc += __shfl_xor(cc, 32, 64);
+          if (grp == 0 && rok[b] && c < p.nchunks) a.chunk_cut[xrow[b] * a.chunk_stride + c] = cc;
+        }
       }
       phi[b] = u32x2{(hi[0] >> 16) | hi[1], (hi[2] >> 16) | hi[3]};
       plo[b] = u32x2{lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16)};
@@ -168,9 +181,9 @@ struct MfmaScan {
   }
 };
 
-template <int D, int RB, bool DENSE, bool DBG>
+template <int D, int RB, bool DENSE, bool DBG, bool CX = false>
 __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeArgs a) {
-  using S = MfmaScan<D, RB, DENSE, DBG>;
+  using S = MfmaScan<D, RB, DENSE, DBG, CX>;
   constexpr int NK = S::NK;
   constexpr int R = S::R;
   constexpr int kTileBytes = kScanWaves * 16 * S::VSTRIDE;
@@ -328,10 +341,16 @@ __global__ __launch_bounds__(kScanThreads) void decode_mfma_kernel(const DecodeA
 
 template <int D, int RB, bool DENSE>
 hipError_t launch_rb(const DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
-  if (dbg)
+  bool cx = false;
+  if constexpr (!DENSE) cx = !dbg && a.chunk_cut;
+  if (dbg) {
     hipLaunchKernelGGL((decode_mfma_kernel<D, RB, DENSE, true>), dim3(blocks), dim3(kScanThreads),
                        0, stream, a);
-  else
+  } else if (cx) {
+    if constexpr (!DENSE)
+      hipLaunchKernelGGL((decode_mfma_kernel<D, RB, DENSE, false, true>), dim3(blocks),
+                         dim3(kScanThreads), 0, stream, a);
+  } else
     hipLaunchKernelGGL((decode_mfma_kernel<D, RB, DENSE, false>), dim3(blocks), dim3(kScanThreads),
                        0, stream, a);
   return hipGetLastError();

@@ -32,6 +32,9 @@
 //             A^T += V^T P^T runs on v_mfma_f32_16x16x16_bf16 with V^T read
 //             transposed from the wave's value tile in LDS.
 //
+// CX (block model of BF16 values, finite T): each scored chunk's cut mass per
+// row, the summed weights of its cut keys, is also written to chunk_cut.
+//
 // Two register sets of PK chunks alternate: the keys of step j+1 load while
 // step j is scored, and a step's value rows reuse its key registers.  A step
 // without a live key issues no value load, so at small depths the key stream
@@ -63,7 +66,7 @@ constexpr int kDppRowShl = 0x100;    // row_shl:n = 0x100 + n (lane i reads lane
 constexpr int kDppRowShr = 0x110;    // row_shr:n = 0x110 + n (lane i reads lane i - n)
 constexpr int kDppIdentity = 0xE4;   // quad_perm [0, 1, 2, 3]
 
-template <int D, int PK, bool DENSE, bool DBG>
+template <int D, int PK, bool DENSE, bool DBG, bool CX>
 struct PackedScan {
   static constexpr int NK = D / 32;           // 128-bit loads per lane per chunk
   static constexpr int NB = D / 16;           // 16-channel blocks of the value product
@@ -168,6 +171,7 @@ struct PackedScan {
     const int nkl = cl < p.nchunks ? min(kChunk, p.n - cl * kChunk) : 0;
     uint32_t bits = 0;
     float w[4];
+    float cc = 0.0f;  // cut weights of this lane's keys of chunk cl
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int kk = 4 * grp + i;
@@ -176,9 +180,18 @@ struct PackedScan {
       const bool live = DENSE ? ok : x >= a.neg_T;
       w[i] = exp2_fast(x);
       if (!DENSE) lcut += live ? 0.0f : w[i];
+      if (!DENSE && (CX || DBG)) cc += live ? 0.0f : w[i];
       xs[i] = x;
       bits |= live ? (1u << i) : 0u;
       if (DBG && a.x_out && ok) a.x_out[prow * g.max_seq_len + cl * kChunk + kk] = x;
+    }
+    if constexpr (!DENSE && (CX || DBG)) {
+      if (a.chunk_cut) {
+        // the four key groups of a packed (row, chunk) lane hold its 16 keys
+        cc += __shfl_xor(cc, 16, 64);
+        cc += __shfl_xor(cc, 32, 64);
+        if (grp == 0 && pok && cl < p.nchunks) a.chunk_cut[prow * a.chunk_stride + cl] = cc;
+      }
     }
     // L adds the weights in the dense scan's order (chunk by chunk, then key
     // 4 grp + i), in the lanes of chunk slot 0, so that L has the same bits at
@@ -265,9 +278,9 @@ struct PackedScan {
 // one-launch decode of a single level, per-request view): the prologue
 // computes the group's references with the estimate routine while the first
 // keys load, and the last split to finish adds the slots into the output.
-template <int D, int PK, bool DENSE, bool DBG, bool FUSED>
+template <int D, int PK, bool DENSE, bool DBG, bool FUSED, bool CX = false>
 __device__ __forceinline__ void packed_scan(const DecodeArgs& a, const FusedExtra* fx) {
-  using S = PackedScan<D, PK, DENSE, DBG>;
+  using S = PackedScan<D, PK, DENSE, DBG, CX>;
   constexpr int NK = S::NK;
   constexpr int kTileBytes = kScanWaves * 16 * S::VSTRIDE;
   constexpr int kWaveFloats = S::NB * 4 * 64 + 64;  // one wave's accumulators, L and cut mass
@@ -423,9 +436,9 @@ __device__ __forceinline__ void packed_scan(const DecodeArgs& a, const FusedExtr
   if constexpr (FUSED) fused_combine<D>(a, *fx, sc.p, out_row, zs);
 }
 
-template <int D, int PK, bool DENSE, bool DBG>
+template <int D, int PK, bool DENSE, bool DBG, bool CX = false>
 __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2))) void decode_packed_kernel(const DecodeArgs a) {
-  packed_scan<D, PK, DENSE, DBG, false>(a, nullptr);
+  packed_scan<D, PK, DENSE, DBG, false, CX>(a, nullptr);
 }
 
 template <int D, int PK, bool DENSE>
@@ -435,10 +448,16 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2)
 
 template <int D, int PK, bool DENSE>
 hipError_t launch_pkd(const DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
-  if (dbg)
+  bool cx = false;
+  if constexpr (!DENSE) cx = !dbg && a.chunk_cut;
+  if (dbg) {
     hipLaunchKernelGGL((decode_packed_kernel<D, PK, DENSE, true>), dim3(blocks),
                        dim3(kScanThreads), 0, stream, a);
-  else
+  } else if (cx) {
+    if constexpr (!DENSE)
+      hipLaunchKernelGGL((decode_packed_kernel<D, PK, DENSE, false, true>), dim3(blocks),
+                         dim3(kScanThreads), 0, stream, a);
+  } else
     hipLaunchKernelGGL((decode_packed_kernel<D, PK, DENSE, false>), dim3(blocks),
                        dim3(kScanThreads), 0, stream, a);
   return hipGetLastError();

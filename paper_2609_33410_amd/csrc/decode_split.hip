@@ -28,12 +28,14 @@
 // together before chunk t is scored and accumulated.
 // At the end the lanes of a wave and then the W waves are reduced in a fixed
 // order and the pair (A, L) of every row is written to its split's slot.
+// CX (block model of BF16 values, finite T): each scored chunk's cut mass per
+// row, the summed weights of its cut keys, is also written to chunk_cut.
 #include "decode_common.h"
 
 namespace fold {
 namespace {
 
-template <int D, int GR, bool DENSE, bool DBG>
+template <int D, int GR, bool DENSE, bool DBG, bool CX>
 struct Scan {
   static constexpr int LPK = D / 8;        // lanes per key row
   static constexpr int KPI = 64 / LPK;     // keys per wave-wide 128-bit load
@@ -68,6 +70,9 @@ struct Scan {
   // any key of the chunk is read (wave-uniform).
   __device__ __forceinline__ bool score(int c, const u32x4 (&kv)[NI], float (&p)[NI][GR],
                                         bool (&anyl)[NI]) {
+    float cc[GR];  // cut weights of this lane's keys of the chunk
+#pragma unroll
+    for (int r = 0; r < GR; ++r) cc[r] = 0.0f;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int j = c * kChunk + KPI * i + kslot;
@@ -82,12 +87,26 @@ struct Scan {
         const float w = ok ? exp2_fast(x) : 0.0f;
         lsum[r] += w;
         if (!DENSE) lcut[r] += live ? 0.0f : w;
+        if (!DENSE && (CX || DBG)) cc[r] += live ? 0.0f : w;
         p[i][r] = live ? w : 0.0f;
         anyl[i] = anyl[i] || live;
         if (DBG && a.x_out && ok && part == 0) a.x_out[xrow[r] * g.max_seq_len + j] = x;
       }
       if (DBG && a.key_gate_out && kok && part == 0)
         a.key_gate_out[gate_row * g.max_seq_len + j] = anyl[i] ? 1 : 0;
+    }
+    if constexpr (!DENSE && (CX || DBG)) {
+      if (a.chunk_cut) {
+        // the chunk's keys sit in the lanes of equal `part`
+#pragma unroll
+        for (int r = 0; r < GR; ++r) {
+          float t = cc[r];
+#pragma unroll
+          for (int off = LPK; off < 64; off <<= 1) t += __shfl_xor(t, off, 64);
+          if (lane == 0 && rok[r] && c < nchunks)
+            a.chunk_cut[xrow[r] * a.chunk_stride + c] = t;
+        }
+      }
     }
     bool lane_any = false;
 #pragma unroll
@@ -121,11 +140,11 @@ struct Scan {
   }
 };
 
-template <int D, int GR, bool DENSE, bool DBG, int W>
+template <int D, int GR, bool DENSE, bool DBG, int W, bool CX = false>
 __global__ __launch_bounds__(64 * W) void decode_split_kernel(const DecodeArgs a) {
   constexpr int kWaves = W;
   constexpr int kThreads = 64 * W;
-  using S = Scan<D, GR, DENSE, DBG>;
+  using S = Scan<D, GR, DENSE, DBG, CX>;
   constexpr int NI = S::NI;
   const ScanGeometry& g = a.geo;
   S sc(a);
@@ -285,14 +304,14 @@ __global__ __launch_bounds__(64 * W) void decode_split_kernel(const DecodeArgs a
   }
 }
 
-template <int D, bool DENSE, bool DBG>
+template <int D, bool DENSE, bool DBG, bool CX = false>
 hipError_t launch_valu_w(const DecodeArgs& a, unsigned blocks, int waves, hipStream_t stream) {
   if (waves == 8)
-    hipLaunchKernelGGL((decode_split_kernel<D, 1, DENSE, DBG, 8>), dim3(blocks), dim3(64 * 8), 0,
-                       stream, a);
+    hipLaunchKernelGGL((decode_split_kernel<D, 1, DENSE, DBG, 8, CX>), dim3(blocks), dim3(64 * 8),
+                       0, stream, a);
   else
-    hipLaunchKernelGGL((decode_split_kernel<D, 1, DENSE, DBG, 4>), dim3(blocks), dim3(64 * 4), 0,
-                       stream, a);
+    hipLaunchKernelGGL((decode_split_kernel<D, 1, DENSE, DBG, 4, CX>), dim3(blocks), dim3(64 * 4),
+                       0, stream, a);
   return hipGetLastError();
 }
 
@@ -313,8 +332,9 @@ hipError_t launch_valu(const DecodeArgs& a, unsigned blocks, hipStream_t stream)
   if (a.dense)
     return dbg ? launch_valu_w<D, true, true>(a, blocks, w, stream)
                : launch_valu_w<D, true, false>(a, blocks, w, stream);
-  return dbg ? launch_valu_w<D, false, true>(a, blocks, w, stream)
-             : launch_valu_w<D, false, false>(a, blocks, w, stream);
+  if (dbg) return launch_valu_w<D, false, true>(a, blocks, w, stream);
+  return a.chunk_cut ? launch_valu_w<D, false, false, true>(a, blocks, w, stream)
+                     : launch_valu_w<D, false, false>(a, blocks, w, stream);
 }
 
 }  // namespace

@@ -31,6 +31,10 @@
 //            (ds_read_b64_tr_b16).  The weight enters as bf16(hi) +
 //            bf16(residual), two products; L adds the FP32 weight of every key.
 //
+// CX (block model of BF16 values, finite T): each weighed 16-key chunk's cut
+// mass per row, the summed weights of its cut keys, is also written to
+// chunk_cut.
+//
 // Pipelines.  Dense (T = inf): keys run one tile ahead of values; while the
 // product of tile t runs on the matrix cores, the weights of tile t+1 are
 // formed, and keys of t+4 / values of t+3 are in flight (four stages each).
@@ -142,7 +146,7 @@ struct TileW {
   uint64_t mask;
 };
 
-template <int D, bool DENSE, bool DBG>
+template <int D, bool DENSE, bool DBG, bool CX = false>
 __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const DecodeArgs a) {
   constexpr int NK = D / 32;          // K-dim steps of the score product
   constexpr int NB = D / 16;          // 16-channel blocks of the value product
@@ -326,6 +330,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
     const int nk = tile_keys(j);
     uint32_t hb[2][4];
     float lf[2][4];
+    float cc[2] = {0.0f, 0.0f};  // cut weights of this lane's keys of the half's two chunks
     uint32_t lb = 0;  // bit 4 st + i: key 16 st + 4 grp + i of the half is live for this row
 #pragma unroll
     for (int st = 0; st < 2; ++st)
@@ -338,12 +343,26 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
         const float w = FULL ? exp2_fast(x) : (ok ? exp2_fast(x) : 0.0f);
         lsum += w;
         if (!DENSE) lcut += live ? 0.0f : w;
+        if (!DENSE && (CX || DBG)) cc[st] += live ? 0.0f : w;
         const float pw = (FULL && DENSE) ? w : (live ? w : 0.0f);
         hb[st][i] = __float_as_uint(pw) & 0xffff0000u;
         lf[st][i] = pw - __uint_as_float(hb[st][i]);
         lb |= (live ? 1u : 0u) << (4 * st + i);
         if (DBG && a.x_out && ri.ok && kk < nk) a.x_out[qrow * g.max_seq_len + key0 + kk] = x;
       }
+    if constexpr (!DENSE && (CX || DBG)) {
+      if (a.chunk_cut) {
+        // the four key groups of row n16 hold a chunk's 16 keys
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+          float t = cc[st];
+          t += __shfl_xor(t, 16, 64);
+          t += __shfl_xor(t, 32, 64);
+          const int c = (key0 + 32 * kh + 16 * st) / kChunk;
+          if (grp == 0 && ri.ok && c < p.nchunks) a.chunk_cut[qrow * a.chunk_stride + c] = t;
+        }
+      }
+    }
     if (need_mask) {
       lb = group_or16(lb);
       uint32_t mask = 0;
@@ -584,10 +603,16 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
 
 template <int D, bool DENSE>
 hipError_t launch_stk(const DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
-  if (dbg)
+  bool cx = false;
+  if constexpr (!DENSE) cx = !dbg && a.chunk_cut;
+  if (dbg) {
     hipLaunchKernelGGL((decode_stacked_kernel<D, DENSE, true>), dim3(blocks), dim3(kStkThreads), 0,
                        stream, a);
-  else
+  } else if (cx) {
+    if constexpr (!DENSE)
+      hipLaunchKernelGGL((decode_stacked_kernel<D, DENSE, false, true>), dim3(blocks),
+                         dim3(kStkThreads), 0, stream, a);
+  } else
     hipLaunchKernelGGL((decode_stacked_kernel<D, DENSE, false>), dim3(blocks), dim3(kStkThreads), 0,
                        stream, a);
   return hipGetLastError();

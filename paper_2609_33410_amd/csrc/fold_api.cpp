@@ -199,12 +199,15 @@ fold_status fold_ref_estimate(const fold_kv_view* kv, const fold_q_view* q, floa
   return ok();
 }
 
-fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
+// Validation and arguments of one level's split scan (shared by
+// fold_decode_split and fold_decode_split_blocks); launches nothing.
+static fold_status split_args(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
                               const float* z, float depth_T, int32_t num_splits,
                               int32_t slot_offset, int32_t num_slots, float* part_A,
                               float* part_L, float* part_Lcut, const fold_debug* dbg,
-                              void* stream) {
-  fold::DecodeArgs a;
+                              fold::DecodeArgs* out) {
+  fold::DecodeArgs& a = *out;
+  a = fold::DecodeArgs{};
   fold_status st = check_view(kv, q, &a.geo, true);
   if (st != FOLD_OK) return st;
   if (!z || !part_A || !part_L) return fail(FOLD_E_INVAL, "z, part_A and part_L are required");
@@ -237,8 +240,69 @@ fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, floa
   a.rows_per_group = gr;
   a.row_groups = groups;
   a.by_length = (!kv->row_indptr && kv->num_seqs >= 2 && kv->num_seqs <= fold::kOrderMax) ? 1 : 0;
+  return FOLD_OK;
+}
+
+fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, float sm_scale,
+                              const float* z, float depth_T, int32_t num_splits,
+                              int32_t slot_offset, int32_t num_slots, float* part_A,
+                              float* part_L, float* part_Lcut, const fold_debug* dbg,
+                              void* stream) {
+  fold::DecodeArgs a;
+  fold_status st = split_args(kv, q, sm_scale, z, depth_T, num_splits, slot_offset, num_slots,
+                              part_A, part_L, part_Lcut, dbg, &a);
+  if (st != FOLD_OK) return st;
   hipError_t e = fold::launch_decode(a, kv->head_dim, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(FOLD_E_HIP, "decode launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_decode_split_blocks(const fold_kv_view* kv, const fold_q_view* q,
+                                     float sm_scale, const float* z, float depth_T,
+                                     int32_t num_splits, int32_t slot_offset, int32_t num_slots,
+                                     float* part_A, float* part_L,
+                                     const fold_block_model* model, const fold_debug* dbg,
+                                     void* stream) {
+  fold::DecodeArgs a;
+  fold_status st = split_args(kv, q, sm_scale, z, depth_T, num_splits, slot_offset, num_slots,
+                              part_A, part_L, nullptr, dbg, &a);
+  if (st != FOLD_OK) return st;
+  if (!model || !model->block_mean) return fail(FOLD_E_INVAL, "the block model is required");
+  const long long need_blocks = (static_cast<long long>(kv->max_seq_len) + fold::kTile - 1) / fold::kTile;
+  if (model->max_blocks < need_blocks)
+    return fail(FOLD_E_INVAL, "max_blocks %d < ceil(max_seq_len / 64) = %lld", model->max_blocks,
+                need_blocks);
+  if (!aligned16(model->block_mean)) return fail(FOLD_E_INVAL, "block_mean must be 16-byte aligned");
+  if (!a.dense && !model->chunk_cut)
+    return fail(FOLD_E_INVAL, "chunk_cut is required at a finite depth");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (a.dense) {  // no key is cut: the plain scan
+    hipError_t e = fold::launch_decode(a, kv->head_dim, s);
+    if (e != hipSuccess) return fail(FOLD_E_HIP, "decode launch: %s", hipGetErrorString(e));
+    return ok();
+  }
+  a.chunk_cut = model->chunk_cut;
+  a.chunk_stride = static_cast<int>((static_cast<long long>(kv->max_seq_len) + fold::kChunk - 1) /
+                                    fold::kChunk);
+  fold::BlockModelArgs b;
+  b.geo = a.geo;
+  b.part_A = part_A;
+  b.chunk_cut = model->chunk_cut;
+  b.block_mean = model->block_mean;
+  b.chunk_stride = a.chunk_stride;
+  b.max_blocks = model->max_blocks;
+  b.num_splits = num_splits;
+  b.slot_offset = slot_offset;
+  b.rows_per_seq = a.rows_per_seq;
+  const int rb = fold::block_model_rows(a.rows_per_seq);
+  b.row_tiles = (a.rows_per_seq + rb - 1) / rb;
+  const long long blocks = static_cast<long long>(kv->num_seqs) * kv->num_kv_heads * num_splits *
+                           b.row_tiles;
+  if (blocks > 0x7fffffffLL) return fail(FOLD_E_INVAL, "grid too large");
+  hipError_t e = fold::launch_decode(a, kv->head_dim, s);
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "decode launch: %s", hipGetErrorString(e));
+  e = fold::launch_block_model(b, kv->head_dim, s);
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "block model launch: %s", hipGetErrorString(e));
   return ok();
 }
 
@@ -447,6 +511,53 @@ fold_status fold_value_mean_append(const fold_kv_view* kv, const void* v_src,
   a.n_tok = n_tok;
   hipError_t e = fold::launch_value_mean_append(a, kv->head_dim, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(FOLD_E_HIP, "value mean append launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_value_block_mean(const fold_kv_view* kv, int32_t max_blocks, float* mean_out,
+                                  void* stream) {
+  if (!kv) return fail(FOLD_E_INVAL, "kv view is required");
+  fold::MeanArgs a{};
+  fold_status st = check_layout(kv, kv->num_seqs, kv->num_kv_heads, &a.geo);
+  if (st != FOLD_OK) return st;
+  const long long need = (static_cast<long long>(kv->max_seq_len) + fold::kTile - 1) / fold::kTile;
+  if (max_blocks < need)
+    return fail(FOLD_E_INVAL, "max_blocks %d < ceil(max_seq_len / 64) = %lld", max_blocks, need);
+  if (kv->num_seqs > 0 && (!kv->v || !kv->seq_lens || !mean_out))
+    return fail(FOLD_E_INVAL, "v, seq_lens and mean_out are required");
+  if (kv->num_seqs > 0 && (!aligned16(kv->v) || !aligned16(mean_out)))
+    return fail(FOLD_E_INVAL, "v and mean_out must be 16-byte aligned");
+  if (static_cast<long long>(kv->num_seqs) * kv->num_kv_heads * max_blocks > 0x1fffffffLL)
+    return fail(FOLD_E_INVAL, "grid too large");
+  a.mean = mean_out;
+  a.max_blocks = max_blocks;
+  hipError_t e = fold::launch_block_mean(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "block mean launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_value_block_mean_append(const fold_kv_view* kv, int32_t max_blocks,
+                                         const void* v_src, const int32_t* tok_seq,
+                                         const int32_t* tok_pos, int32_t n_tok, float* mean,
+                                         void* stream) {
+  if (!kv) return fail(FOLD_E_INVAL, "kv view is required");
+  if (n_tok < 0) return fail(FOLD_E_INVAL, "n_tok must be >= 0");
+  if (max_blocks < 1) return fail(FOLD_E_INVAL, "max_blocks must be >= 1");
+  fold::MeanArgs a{};
+  fold_status st = check_layout(kv, kv->num_seqs, kv->num_kv_heads, &a.geo);
+  if (st != FOLD_OK) return st;
+  if (n_tok > 0 && (!v_src || !tok_seq || !tok_pos || !mean))
+    return fail(FOLD_E_INVAL, "v_src, tok_seq, tok_pos and mean are required");
+  if (static_cast<long long>(n_tok) * kv->num_kv_heads > 0x1fffffffLL)
+    return fail(FOLD_E_INVAL, "grid too large");
+  a.mean = mean;
+  a.v_src = static_cast<const uint16_t*>(v_src);
+  a.tok_seq = tok_seq;
+  a.tok_pos = tok_pos;
+  a.n_tok = n_tok;
+  a.max_blocks = max_blocks;
+  hipError_t e = fold::launch_block_mean_append(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "block mean append launch: %s", hipGetErrorString(e));
   return ok();
 }
 

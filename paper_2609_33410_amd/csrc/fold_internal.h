@@ -52,6 +52,10 @@ struct DecodeArgs {
   int rows_per_group; // rows one workgroup serves (template GR)
   int row_groups;
   int by_length = 0;  // block order over sequences by decreasing length (per-request views)
+  // Block model of BF16 values: the scan also writes each row's cut mass of
+  // every 16-key chunk, chunk_cut[row * chunk_stride + chunk] (finite depth).
+  float* chunk_cut = nullptr;
+  int chunk_stride = 0;  // ceil(max_seq_len / 16)
 };
 
 struct EstimateArgs {
@@ -81,11 +85,27 @@ struct CombineArgs {
 // Request mean value rows (the cut-key value model).
 struct MeanArgs {
   ScanGeometry geo;       // per-request view (geo.k unused)
-  float* mean;            // [num_seqs][hkv][D]
+  float* mean;            // [num_seqs][hkv][D], or block means [num_seqs][hkv][max_blocks][D]
   const uint16_t* v_src;  // append: [n_tok][hkv][D] bf16
   const int32_t* tok_seq;
   const int32_t* tok_pos;
   int n_tok;
+  int max_blocks;         // block means: row stride in blocks
+};
+
+// Virtual rows of the block model: adds sum over the split's tiles t of
+// c_it * mu_t to the split's slot of every row of the level (after the scan).
+struct BlockModelArgs {
+  ScanGeometry geo;
+  float* part_A;              // the scan's slots
+  const float* chunk_cut;     // [batch * heads][chunk_stride] cut masses per 16-key chunk
+  const float* block_mean;    // [num_seqs][hkv][max_blocks][D]
+  int chunk_stride;
+  int max_blocks;
+  int num_splits;
+  int slot_offset;
+  int rows_per_seq;           // host bound on rows attending one (kv seq, kv head)
+  int row_tiles;              // row blocks of RB rows per (kv seq, kv head)
 };
 
 // Two-plane INT8 key cache (Section 4, "Cache format"): the planes use the
@@ -246,6 +266,12 @@ hipError_t scratch_device_ptr(void** out);
 hipError_t launch_clear_i32(int32_t* p, int n, hipStream_t stream);
 hipError_t launch_value_mean(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_value_mean_append(const MeanArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_block_mean(const MeanArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_block_mean_append(const MeanArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_block_model(const BlockModelArgs& a, int head_dim, hipStream_t stream);
+// Rows per workgroup of the block model's virtual-row kernel for a bound on
+// the rows attending one (kv sequence, kv head).
+int block_model_rows(int rows_per_seq);
 hipError_t launch_q8_write(const Q8WriteArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_split(const Q8SplitArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_v8_write(const V8WriteArgs& a, int head_dim, hipStream_t stream);

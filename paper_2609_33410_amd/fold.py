@@ -36,6 +36,9 @@ EXPORTED = (
     "fold_decode_fused_noalloc",
     "fold_value_mean",
     "fold_value_mean_append",
+    "fold_value_block_mean",
+    "fold_value_block_mean_append",
+    "fold_decode_split_blocks",
     "fold_q8_write_keys",
     "fold_v8_write_values",
     "fold_q8_split_query",
@@ -99,6 +102,11 @@ class fold_value_model(ctypes.Structure):
                 ("num_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32)]
 
 
+class fold_block_model(ctypes.Structure):
+    _fields_ = [("block_mean", ctypes.c_void_p), ("max_blocks", ctypes.c_int32),
+                ("chunk_cut", ctypes.c_void_p)]
+
+
 class fold_q8_keys(ctypes.Structure):
     _fields_ = [("plane_a", ctypes.c_void_p), ("plane_b", ctypes.c_void_p),
                 ("scale", ctypes.c_void_p)]
@@ -154,6 +162,20 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                       ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                       ctypes.c_void_p, ctypes.c_void_p, P(fold_debug),
                                       ctypes.c_void_p]
+    lib.fold_decode_split_blocks.restype = ctypes.c_int
+    lib.fold_decode_split_blocks.argtypes = [P(fold_kv_view), P(fold_q_view), ctypes.c_float,
+                                             ctypes.c_void_p, ctypes.c_float, ctypes.c_int32,
+                                             ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                             ctypes.c_void_p, P(fold_block_model),
+                                             P(fold_debug), ctypes.c_void_p]
+    lib.fold_value_block_mean.restype = ctypes.c_int
+    lib.fold_value_block_mean.argtypes = [P(fold_kv_view), ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.c_void_p]
+    lib.fold_value_block_mean_append.restype = ctypes.c_int
+    lib.fold_value_block_mean_append.argtypes = [P(fold_kv_view), ctypes.c_int32,
+                                                 ctypes.c_void_p, ctypes.c_void_p,
+                                                 ctypes.c_void_p, ctypes.c_int32,
+                                                 ctypes.c_void_p, ctypes.c_void_p]
     lib.fold_combine.restype = ctypes.c_int
     lib.fold_combine.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                  ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
@@ -404,6 +426,96 @@ def fold_decode_split(kv: KV, q: Q, sm_scale: float, z: torch.Tensor, depth_T: f
         None if dbg is None else ctypes.byref(dbg), _stream(stream)))
 
 
+def block_count(max_seq_len: int) -> int:
+    """Blocks of the block model a view of ``max_seq_len`` keys needs."""
+    return (int(max_seq_len) + 63) // 64
+
+
+def chunk_count(max_seq_len: int) -> int:
+    """16-key chunks per row of the block model's cut-mass workspace."""
+    return (int(max_seq_len) + 15) // 16
+
+
+def _block_mean_checks(kv: KV, block_mean: torch.Tensor) -> int:
+    v = kv.view
+    want = (v.num_seqs, v.num_kv_heads)
+    if block_mean.dim() != 4 or tuple(block_mean.shape[:2]) != want or \
+            int(block_mean.shape[3]) != v.head_dim:
+        raise ValueError(f"block_mean must be [{want[0]}, {want[1]}, max_blocks, {v.head_dim}], "
+                         f"got {tuple(block_mean.shape)}")
+    if not block_mean.is_contiguous():
+        raise ValueError("block_mean must be contiguous")
+    mb = int(block_mean.shape[2])
+    if mb < block_count(v.max_seq_len):
+        raise ValueError(f"block_mean holds {mb} blocks; the view needs {block_count(v.max_seq_len)}")
+    return mb
+
+
+def fold_value_block_mean(kv: KV, mean_out: torch.Tensor, stream=None) -> torch.Tensor:
+    """Mean value row of every 64-key block, ``[num_seqs, Hkv, max_blocks, D]``."""
+    _need(mean_out, "mean_out", torch.float32)
+    mb = _block_mean_checks(kv, mean_out)
+    _need_device([("mean_out", mean_out)] + [(f"view tensor {i}", t) for i, t in enumerate(kv.tensors)])
+    _check(load_library().fold_value_block_mean(ctypes.byref(kv.view), mb, _ptr(mean_out),
+                                                _stream(stream)))
+    return mean_out
+
+
+def fold_value_block_mean_append(kv: KV, v_src: torch.Tensor, tok_seq: torch.Tensor,
+                                 tok_pos: torch.Tensor, mean: torch.Tensor, stream=None) -> None:
+    """Running update of the appended tokens' blocks (one token per sequence)."""
+    _need(v_src, "v_src", torch.bfloat16)
+    _need(tok_seq, "tok_seq", torch.int32)
+    _need(tok_pos, "tok_pos", torch.int32)
+    _need(mean, "mean", torch.float32)
+    mb = _block_mean_checks(kv, mean)
+    _need_device([("v_src", v_src), ("tok_seq", tok_seq), ("tok_pos", tok_pos), ("mean", mean)])
+    _check(load_library().fold_value_block_mean_append(
+        ctypes.byref(kv.view), mb, _ptr(v_src), _ptr(tok_seq), _ptr(tok_pos),
+        int(tok_seq.shape[0]), _ptr(mean), _stream(stream)))
+
+
+def fold_decode_split_blocks(kv: KV, q: Q, sm_scale: float, z: torch.Tensor, depth_T: float,
+                             num_splits: int, slot_offset: int, part_A: torch.Tensor,
+                             part_L: torch.Tensor, block_mean: torch.Tensor,
+                             chunk_cut: Optional[torch.Tensor],
+                             x_out: Optional[torch.Tensor] = None,
+                             key_gate_out: Optional[torch.Tensor] = None,
+                             page_gate_out: Optional[torch.Tensor] = None, stream=None) -> None:
+    """``fold_decode_split`` with the block model of BF16 values: each tile's
+    cut mass times its block's mean is added to the owning split's A.
+    ``chunk_cut`` (``[B * H * chunk_count(max_seq_len)]`` float32 workspace)
+    receives the cut masses per row and 16-key chunk."""
+    _need(z, "z", torch.float32)
+    _need(part_A, "part_A", torch.float32)
+    _need(part_L, "part_L", torch.float32)
+    _need(block_mean, "block_mean", torch.float32)
+    mb = _block_mean_checks(kv, block_mean)
+    _slot_checks(q.tensor, part_A, part_L, None, z)
+    b, h, _ = (int(x) for x in q.tensor.shape)
+    if chunk_cut is not None:
+        _need(chunk_cut, "chunk_cut", torch.float32)
+        need = b * h * chunk_count(kv.view.max_seq_len)
+        if chunk_cut.numel() < need:
+            raise ValueError(f"chunk_cut needs {need} elements, got {chunk_cut.numel()}")
+    _need_device([("q", q.tensor), ("z", z), ("part_A", part_A), ("part_L", part_L),
+                  ("block_mean", block_mean), ("chunk_cut", chunk_cut), ("x_out", x_out),
+                  ("key_gate_out", key_gate_out), ("page_gate_out", page_gate_out)]
+                 + [(f"view tensor {i}", t) for i, t in enumerate(kv.tensors)])
+    dbg = None
+    if x_out is not None or key_gate_out is not None or page_gate_out is not None:
+        for t, nm, dt in ((x_out, "x_out", torch.float32), (key_gate_out, "key_gate_out", torch.uint8),
+                          (page_gate_out, "page_gate_out", torch.uint8)):
+            if t is not None:
+                _need(t, nm, dt)
+        dbg = fold_debug(_ptr(x_out), _ptr(key_gate_out), _ptr(page_gate_out))
+    model = fold_block_model(_ptr(block_mean), mb, _ptr(chunk_cut))
+    _check(load_library().fold_decode_split_blocks(
+        ctypes.byref(kv.view), ctypes.byref(q.view), sm_scale, _ptr(z), depth_T, num_splits,
+        slot_offset, int(part_A.shape[0]), _ptr(part_A), _ptr(part_L), ctypes.byref(model),
+        None if dbg is None else ctypes.byref(dbg), _stream(stream)))
+
+
 def fold_combine(part_A: torch.Tensor, part_L: torch.Tensor, out: torch.Tensor,
                  z: Optional[torch.Tensor] = None, lse_out: Optional[torch.Tensor] = None,
                  cert_out: Optional[torch.Tensor] = None,
@@ -538,13 +650,17 @@ def fold_value_mean_append(kv: KV, v_src: torch.Tensor, tok_seq: torch.Tensor,
 
 def fold_decode(levels, q: torch.Tensor, z: torch.Tensor, depth_T: float, splits,
                 sm_scale: float, out_dtype=torch.float32, lse: bool = False, cert: bool = False,
-                value_mean: Optional[torch.Tensor] = None, stream=None):
+                value_mean: Optional[torch.Tensor] = None, block_means=None, stream=None):
     """Every level's split scan into one slot array, then the combine.
 
     ``levels`` is a list of ``KV`` views; ``splits`` their split counts;
-    ``value_mean`` ([B, Hkv, D], from ``fold_value_mean``) turns on the cut-key
-    value model.  Returns ``(out, part_A, part_L, lse_out, cert_out)``.
+    ``value_mean`` ([B, Hkv, D], from ``fold_value_mean``) turns on the
+    request-mean value model, ``block_means`` (one ``fold_value_block_mean``
+    array per level) the block model of BF16 values; at most one of them.
+    Returns ``(out, part_A, part_L, lse_out, cert_out)``.
     """
+    if value_mean is not None and block_means is not None:
+        raise ValueError("value_mean and block_means are two value models: pass one")
     b, h, d = q.shape
     qv = q_view(q)
     total = sum(splits)
@@ -552,10 +668,20 @@ def fold_decode(levels, q: torch.Tensor, z: torch.Tensor, depth_T: float, splits
     part_L = torch.empty(total, b, h, dtype=torch.float32, device=q.device)
     part_C = (torch.empty(total, b, h, dtype=torch.float32, device=q.device)
               if value_mean is not None else None)
+    cut = None
+    if block_means is not None:
+        if len(block_means) != len(levels):
+            raise ValueError("block_means needs one array per level")
+        cut = torch.empty(b * h * max(chunk_count(kv.view.max_seq_len) for kv in levels),
+                          dtype=torch.float32, device=q.device)
     off = 0
-    for kv, s in zip(levels, splits):
-        fold_decode_split(kv, qv, sm_scale, z, depth_T, s, off, part_A, part_L,
-                          part_Lcut=part_C, stream=stream)
+    for i, (kv, s) in enumerate(zip(levels, splits)):
+        if block_means is not None:
+            fold_decode_split_blocks(kv, qv, sm_scale, z, depth_T, s, off, part_A, part_L,
+                                     block_means[i], cut, stream=stream)
+        else:
+            fold_decode_split(kv, qv, sm_scale, z, depth_T, s, off, part_A, part_L,
+                              part_Lcut=part_C, stream=stream)
         off += s
     out = torch.empty(b, h, d, dtype=out_dtype, device=q.device)
     lse_out = torch.empty(b, h, dtype=torch.float32, device=q.device) if lse else None

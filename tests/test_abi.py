@@ -137,6 +137,67 @@ def test_value_mean_rejects_bad_args(lib):
     assert ap(ctypes.byref(_kv()), None, None, None, 0, None, None) == F.FOLD_OK
 
 
+def _blocks(lib, kv=None, q=None, T=4.0, model="ok", dbg=None):
+    from paper_2609_33410_amd.fold import fold_block_model
+    m = fold_block_model(FAKE, 1, FAKE) if model == "ok" else model
+    return lib.fold_decode_split_blocks(ctypes.byref(kv or _kv()), ctypes.byref(q or _q()), 0.125,
+                                        FAKE, T, 1, 0, 1, FAKE, FAKE,
+                                        None if m is None else ctypes.byref(m), dbg, None)
+
+
+def test_block_model_decode_rejects_bad_args(lib):
+    from paper_2609_33410_amd.fold import fold_block_model
+    assert _blocks(lib, kv=_kv(head_dim=96)) == F.FOLD_E_INVAL          # the scan's checks
+    assert _blocks(lib, T=float("nan")) == F.FOLD_E_INVAL
+    assert _blocks(lib, model=None) == F.FOLD_E_INVAL                    # no model
+    assert _blocks(lib, model=fold_block_model(None, 1, FAKE)) == F.FOLD_E_INVAL
+    assert _blocks(lib, model=fold_block_model(FAKE, 0, FAKE)) == F.FOLD_E_INVAL  # 64 keys: 1 block
+    assert _blocks(lib, kv=_kv(max_seq_len=65), model=fold_block_model(FAKE, 1, FAKE)) \
+        == F.FOLD_E_INVAL                                                # 65 keys: 2 blocks
+    assert _blocks(lib, model=fold_block_model(FAKE + 4, 1, FAKE)) == F.FOLD_E_INVAL  # misaligned
+    assert _blocks(lib, model=fold_block_model(FAKE, 1, None)) == F.FOLD_E_INVAL  # finite T: workspace
+    assert "chunk_cut" in lib.fold_last_error().decode()
+
+
+def test_block_mean_rejects_bad_args(lib):
+    bm = lib.fold_value_block_mean
+    assert bm(ctypes.byref(_kv()), 0, FAKE, None) == F.FOLD_E_INVAL          # needs 1 block
+    assert bm(ctypes.byref(_kv(max_seq_len=200)), 3, FAKE, None) == F.FOLD_E_INVAL  # needs 4
+    assert bm(ctypes.byref(_kv()), 1, None, None) == F.FOLD_E_INVAL
+    assert bm(ctypes.byref(_kv(v=None)), 1, FAKE, None) == F.FOLD_E_INVAL
+    assert bm(ctypes.byref(_kv()), 1, FAKE + 8, None) == F.FOLD_E_INVAL      # misaligned
+    assert bm(ctypes.byref(_kv(head_dim=80)), 1, FAKE, None) == F.FOLD_E_INVAL
+    ap = lib.fold_value_block_mean_append
+    assert ap(ctypes.byref(_kv()), 1, FAKE, FAKE, FAKE, -1, FAKE, None) == F.FOLD_E_INVAL
+    assert ap(ctypes.byref(_kv()), 0, FAKE, FAKE, FAKE, 1, FAKE, None) == F.FOLD_E_INVAL
+    assert ap(ctypes.byref(_kv()), 1, None, FAKE, FAKE, 3, FAKE, None) == F.FOLD_E_INVAL
+    assert ap(ctypes.byref(_kv()), 1, None, None, None, 0, None, None) == F.FOLD_OK
+
+
+def test_block_model_binding_checks_shapes_and_devices():
+    import torch
+    t = _fused_tensors()
+    kv = F.kv_view(t["k"], t["v"], t["seq_lens"], num_kv_heads=t["k"].shape[1], max_seq_len=32,
+                   block_table=t["block_table"])
+    qv = F.q_view(t["q"])
+    b, h = t["q"].shape[:2]
+    z = torch.zeros(b, h)
+    pa, pl = torch.zeros(1, b, h, 128), torch.zeros(1, b, h)
+    mb = F.block_count(kv.view.max_seq_len)
+    good = torch.zeros(kv.view.num_seqs, kv.view.num_kv_heads, mb, 128)
+    cut = torch.zeros(b * h * F.chunk_count(kv.view.max_seq_len))
+    with pytest.raises(ValueError, match="block_mean must be"):
+        F.fold_decode_split_blocks(kv, qv, 0.1, z, 4.0, 1, 0, pa, pl, good[:, :, :, :64], cut)
+    with pytest.raises(ValueError, match="blocks; the view needs"):
+        F.fold_decode_split_blocks(kv, qv, 0.1, z, 4.0, 1, 0, pa, pl, good[:, :, :mb - 1], cut)
+    with pytest.raises(ValueError, match="chunk_cut needs"):
+        F.fold_decode_split_blocks(kv, qv, 0.1, z, 4.0, 1, 0, pa, pl, good, cut[:-1])
+    with pytest.raises(ValueError, match="device tensor"):
+        F.fold_decode_split_blocks(kv, qv, 0.1, z, 4.0, 1, 0, pa, pl, good, cut)
+    with pytest.raises(ValueError, match="device tensor"):
+        F.fold_value_block_mean(kv, good)
+
+
 def test_row_group_queries(lib):
     kv = _kv()
     # GQA group of 4: one matrix-core read group of 16 rows
