@@ -16,8 +16,11 @@ launched on.
 
 Prints ONE JSON line (rank 0).  The line also carries the headline workload
 over a two-plane INT8 key cache (``q8_keys``; Section 4, cache format) and
-with 8-bit values (``v8_values``), the cut-key value model's effect
-(``value_model``) and the FP64 oracle timed on the host (``cpu_baseline``).
+with 8-bit values (``v8_values``), the cut-key value models' errors and costs
+(``value_model``: no model, the request mean, the block model of BF16 values,
+at T = 16 and 14; ``value_model_structured``: the same errors on the 32K-key
+GQA shapes with structured values) and the FP64 oracle timed on the host
+(``cpu_baseline``).
 ``--all`` adds one JSON line per workload and depth on stderr (used for the
 design notes' tables).
 """
@@ -255,10 +258,13 @@ class Q8Path:
         return nv, nb, total, nr
 
 
-def model_leg(path, wl, F, torch, flush, steps, warmup):
-    """The cut-key value model on the benchmark workload at T=16: scan time with
-    the cut masses written, and the output error against the dense output
-    (exact softmax up to FP32 rounding) without and with the model."""
+def model_leg(path, wl, F, torch, flush, steps, warmup, depths=(16.0, 14.0), timed=True):
+    """The cut-key value models on a workload: the output error against the
+    dense output (exact softmax up to FP32 rounding) at finite depths with no
+    model, the request mean (the model of 8-bit values) and the block model
+    of BF16 values (64-key block means, one virtual row per tile); and, when
+    ``timed``, the scan time with each model and the time of the block-mean
+    fit over the whole cache (a prompt-time call)."""
     dev = wl.q.device
     b, h, d = wl.q.shape
     fl = wl.flat
@@ -268,47 +274,86 @@ def model_leg(path, wl, F, torch, flush, steps, warmup):
     stream = torch.cuda.current_stream()
     path.estimate(stream)
     F.fold_value_mean(kv, mean)
-    part_C = torch.empty_like(path.part_L)
+    bms = [torch.empty(lv.num_seqs, wl.num_kv_heads, F.block_count(lv.max_seq_len), d,
+                       dtype=torch.float32, device=dev) for lv in wl.levels]
 
-    def decode_cut(stream):
+    def fit(stream):
+        for kvl, bm in zip(path.levels, bms):
+            F.fold_value_block_mean(kvl, bm, stream=stream)
+
+    fit(stream)
+    part_C = torch.empty_like(path.part_L)
+    cut = torch.empty(b * h * max(F.chunk_count(lv.max_seq_len) for lv in wl.levels),
+                      dtype=torch.float32, device=dev)
+
+    def decode_cut(T, stream):
         off = 0
         for kvl, s in zip(path.levels, path.splits):
-            F.fold_decode_split(kvl, path.qv, wl.sm_scale, path.z, 16.0, s, off, path.part_A,
+            F.fold_decode_split(kvl, path.qv, wl.sm_scale, path.z, T, s, off, path.part_A,
                                 path.part_L, part_Lcut=part_C, stream=stream)
             off += s
 
-    ts = []
-    for it in range(warmup + steps):
-        evict_caches(flush)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        decode_cut(stream)
-        e1.record(stream)
-        if it >= warmup:
-            e1.synchronize()
-            ts.append(e0.elapsed_time(e1))
+    def decode_blocks(T, stream):
+        off = 0
+        for kvl, s, bm in zip(path.levels, path.splits, bms):
+            F.fold_decode_split_blocks(kvl, path.qv, wl.sm_scale, path.z, T, s, off,
+                                       path.part_A, path.part_L, bm, cut, stream=stream)
+            off += s
+
+    def timed_us(fn):
+        ts = []
+        for it in range(warmup + steps):
+            evict_caches(flush)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn(stream)
+            e1.record(stream)
+            if it >= warmup:
+                e1.synchronize()
+                ts.append(e0.elapsed_time(e1))
+        return round(statistics.median(ts) * 1e3, 2)
+
     dense = torch.empty(b, h, d, dtype=torch.float32, device=dev)
     path.decode(math.inf, stream)
     F.fold_combine(path.part_A, path.part_L, dense, stream=stream)
-    plain = torch.empty_like(dense)
-    path.decode(16.0, stream)
-    F.fold_combine(path.part_A, path.part_L, plain, stream=stream)
-    model = torch.empty_like(dense)
-    decode_cut(stream)
-    F.fold_combine(path.part_A, path.part_L, model, part_Lcut=part_C, mean=mean, stream=stream)
     torch.cuda.synchronize()
     scale = dense.abs().amax(dim=-1).clamp_min(1e-30)
 
-    def err(o):
-        return float(((o - dense).abs().amax(dim=-1) / scale).max())
+    def errs(o):
+        e = (o - dense).abs().amax(dim=-1) / scale
+        return {"max_row": float(e.max()), "median_row": float(e.median()),
+                "rel_l2": float((o - dense).norm() / dense.norm())}
 
-    def l2(o):
-        return float((o - dense).norm() / dense.norm())
-
-    return {"T": 16.0, "model": "request mean (cut keys carry their request's mean value row)",
-            "decode_us_with_cut_masses": round(statistics.median(ts) * 1e3, 2),
-            "max_row_err_vs_dense": {"no_model": err(plain), "request_mean": err(model)},
-            "rel_l2_vs_dense": {"no_model": l2(plain), "request_mean": l2(model)}}
+    rec = {"models": {"no_model": "cut keys add nothing to A",
+                      "request_mean": "cut keys carry their request's mean value row",
+                      "block_mean": "each 64-key tile's cut mass carries its block's mean value "
+                                    "row (one virtual row per tile)"},
+           "reference": "dense decode of the same kernel (T = inf)"}
+    for T in depths:
+        plain = torch.empty_like(dense)
+        path.decode(T, stream)
+        F.fold_combine(path.part_A, path.part_L, plain, stream=stream)
+        model = torch.empty_like(dense)
+        decode_cut(T, stream)
+        F.fold_combine(path.part_A, path.part_L, model, part_Lcut=part_C, mean=mean,
+                       stream=stream)
+        blocks = torch.empty_like(dense)
+        decode_blocks(T, stream)
+        F.fold_combine(path.part_A, path.part_L, blocks, stream=stream)
+        torch.cuda.synchronize()
+        cut_share = float(part_C.double().sum() / path.part_L.double().sum())
+        r = {"err_vs_dense": {"no_model": errs(plain), "request_mean": errs(model),
+                              "block_mean": errs(blocks)},
+             "cut_mass_share": cut_share}
+        if timed:
+            r["scan_us"] = {"no_model": timed_us(lambda st: path.decode(T, st)),
+                            "request_mean_cut_masses": timed_us(lambda st: decode_cut(T, st)),
+                            "block_mean_scan_and_virtual_rows":
+                                timed_us(lambda st: decode_blocks(T, st))}
+        rec[depth_key(T)] = r
+    if timed:
+        rec["block_mean_fit_us"] = timed_us(fit)
+    return rec
 
 
 def q8_bytes(wl, nv, nb, nr=None):
@@ -1067,6 +1112,17 @@ def main():
     line["value_model"] = model_leg(Path(wl, F, torch), wl, F, torch, flush, args.steps,
                                     args.warmup)
     progress("value model leg done")
+    if not args.only:
+        # structured values (channel offset + per-segment topics + noise) on
+        # the 32K-key GQA shapes, where the models have something to capture
+        wl_s = make_config(3, device="cuda", values="structured")
+        rec = model_leg(Path(wl_s, F, torch), wl_s, F, torch, flush, args.steps, args.warmup,
+                        depths=(16.0, 14.0, 12.0), timed=False)
+        rec["workload"] = CONFIG_NAMES[3] + " with structured values"
+        line["value_model_structured"] = rec
+        del wl_s
+        torch.cuda.empty_cache()
+        progress("structured-value model leg done")
     if not args.no_q8:
         line["q8_keys"] = q8_leg(wl, F, torch, flush, args.steps, args.warmup,
                                  name=CONFIG_NAMES[cfg])
