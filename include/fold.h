@@ -117,6 +117,10 @@ typedef struct fold_est_params {
  *   value row was read (some row of the read group is live on key j).
  * page_gate_out [num_seqs][num_kv_heads][row_groups][ceil(max_seq_len/16)] u8:
  *   1 if any key of the 16-key page was read.
+ * A call with exports reads exactly these value rows.  Without exports, the
+ * scan of read groups of 64 rows (more than 32 rows on one kv sequence, a
+ * latency-bound contraction) fetches every value row with its key and applies
+ * the same verdicts to the weights: the results are the same bits.
  * row_groups = fold_decode_row_groups(kv, q).  The rows attending one
  * (kv sequence s, kv head g) are numbered rho = c * G + (h mod G), where c is
  * the position of the row's request in the sequence's row list (0 without CSR

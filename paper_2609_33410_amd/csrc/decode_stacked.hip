@@ -40,7 +40,15 @@
 // formed, and keys of t+4 / values of t+3 are in flight (four stages each).
 // Gated: keys run two tiles ahead; tile t+2 is scored and its live value rows
 // requested while the product of tile t runs (four key and three value
-// stages).  The DMAs are issued from assembly, so the compiler's wait
+// stages).  EAGER (finite T, the production kernel): the dense pipeline with
+// the depth rule deciding every weight, so value rows are fetched with their
+// keys.  A stacked level reads a few MB per call and is bound by per-wave
+// latency, not by HBM: waiting for a tile's verdict before its values move
+// costs more than the bytes it saves (measured slower at every depth from 2
+// to 16 on the 512 x 16384 cascade prefix, with as few as 0.8% of its pages
+// live).  Cut keys' values meet a zero weight, so the slots hold the same
+// bits as the gated fetch's, which the debug variant keeps (its read bits are
+// the ones the tests check).  The DMAs are issued from assembly, so the compiler's wait
 // insertion does not see them and never drains the prefetch; every wait for
 // them is explicit (s_waitcnt vmcnt + an LDS-only barrier).  The two key halves
 // of a row block add their partials in LDS at the end, in a fixed order.
@@ -146,8 +154,10 @@ struct TileW {
   uint64_t mask;
 };
 
-template <int D, bool DENSE, bool DBG, bool CX = false>
+template <int D, bool DENSE, bool DBG, bool CX = false, bool EAGER = false>
 __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const DecodeArgs a) {
+  constexpr bool PIPE = DENSE || EAGER;  // the dense pipeline: values fetched with their keys
+  constexpr bool DEPTH = !DENSE;         // the depth rule decides the weights
   constexpr int NK = D / 32;          // K-dim steps of the score product
   constexpr int NB = D / 16;          // 16-channel blocks of the value product
   constexpr int KEYB = 2 * D;         // bytes per key row
@@ -155,7 +165,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
   constexpr int TILEB = kTile * KEYB; // bytes of one 64-key K (or V) tile
   constexpr int NLD = TILEB / 1024 / kStkWaves;  // 1 KiB DMA loads per wave per tile
   constexpr int KST = 4;              // K stages in LDS
-  constexpr int VST = DENSE ? 4 : 3;  // V stages in LDS
+  constexpr int VST = PIPE ? 4 : 3;   // V stages in LDS
   static_assert(D == 64 || D == 128, "head dim");
   static_assert(NLD >= 1 && (NLD * 1024 / KEYB) * kStkWaves == kTile, "tile split");
   static_assert(7 * NLD < 64, "wait counts");
@@ -339,18 +349,18 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
         const int kk = 32 * kh + 16 * st + 4 * grp + i;
         const bool ok = FULL || (ri.ok && kk < nk);
         const float x = __builtin_fmaf(s[st][i], a.score_scale, -zr);
-        const bool live = ok && (DENSE || x >= a.neg_T);
+        const bool live = ok && (!DEPTH || x >= a.neg_T);
         const float w = FULL ? exp2_fast(x) : (ok ? exp2_fast(x) : 0.0f);
         lsum += w;
-        if (!DENSE) lcut += live ? 0.0f : w;
-        if (!DENSE && (CX || DBG)) cc[st] += live ? 0.0f : w;
-        const float pw = (FULL && DENSE) ? w : (live ? w : 0.0f);
+        if (DEPTH) lcut += live ? 0.0f : w;
+        if (DEPTH && (CX || DBG)) cc[st] += live ? 0.0f : w;
+        const float pw = (FULL && !DEPTH) ? w : (live ? w : 0.0f);
         hb[st][i] = __float_as_uint(pw) & 0xffff0000u;
         lf[st][i] = pw - __uint_as_float(hb[st][i]);
         lb |= (live ? 1u : 0u) << (4 * st + i);
         if (DBG && a.x_out && ri.ok && kk < nk) a.x_out[qrow * g.max_seq_len + key0 + kk] = x;
       }
-    if constexpr (!DENSE && (CX || DBG)) {
+    if constexpr (DEPTH && (CX || DBG)) {
       if (a.chunk_cut) {
         // the four key groups of row n16 hold a chunk's 16 keys
 #pragma unroll
@@ -431,7 +441,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
   using Full = std::true_type;
   using Part = std::false_type;
 
-  if (DENSE && m > 0) {
+  if (PIPE && m > 0) {
     // Issue order: K0, then pairs (K(i+1), V(i)).  Keys of tile j in K stage
     // j % 4, values in V stage j % 4.
     fetch_k(0, pg0, 0);
@@ -483,7 +493,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
       vs0 = next_stage(vs0, VST);
       s3 = next_stage(s3, KST);
     }
-  } else if (!DENSE && m > 0) {
+  } else if (!PIPE && m > 0) {
     // Issue order: K0 K1 V0 K2 V1 | K3 V2 | K4 V3 | ...  Keys of tile j in K
     // stage j % 4, values in V stage j % 3.
     const int ph0 = pg0, ph1 = pg1;
@@ -561,7 +571,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
   // L partials: the four lane groups of a row hold different keys.
   lsum += __shfl_xor(lsum, 16, 64);
   lsum += __shfl_xor(lsum, 32, 64);
-  if (!DENSE) {
+  if (DEPTH) {
     lcut += __shfl_xor(lcut, 16, 64);
     lcut += __shfl_xor(lcut, 32, 64);
   }
@@ -603,18 +613,19 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
 
 template <int D, bool DENSE>
 hipError_t launch_stk(const DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
-  bool cx = false;
-  if constexpr (!DENSE) cx = !dbg && a.chunk_cut;
   if (dbg) {
     hipLaunchKernelGGL((decode_stacked_kernel<D, DENSE, true>), dim3(blocks), dim3(kStkThreads), 0,
                        stream, a);
-  } else if (cx) {
-    if constexpr (!DENSE)
-      hipLaunchKernelGGL((decode_stacked_kernel<D, DENSE, false, true>), dim3(blocks),
-                         dim3(kStkThreads), 0, stream, a);
-  } else
-    hipLaunchKernelGGL((decode_stacked_kernel<D, DENSE, false>), dim3(blocks), dim3(kStkThreads), 0,
+  } else if constexpr (DENSE) {
+    hipLaunchKernelGGL((decode_stacked_kernel<D, true, false>), dim3(blocks), dim3(kStkThreads), 0,
                        stream, a);
+  } else if (a.chunk_cut) {
+    hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, true, true>), dim3(blocks),
+                       dim3(kStkThreads), 0, stream, a);
+  } else {
+    hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, false, true>), dim3(blocks),
+                       dim3(kStkThreads), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

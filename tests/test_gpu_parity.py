@@ -253,12 +253,15 @@ def test_mass_kept_L_independent_of_T():
 
 
 @pytest.mark.parametrize("cfg,T,batch", [(1, INF, None), (1, 16.0, None), (2, INF, 4),
-                                         (2, 16.0, 4), (5, 16.0, 4), (5, INF, 12), (5, 6.0, 12)])
+                                         (2, 16.0, 4), (5, 16.0, 4), (5, INF, 12), (5, 6.0, 12),
+                                         (5, 2.0, 12)])
 def test_debug_exports_do_not_change_results(cfg, T, batch):
     """The kernel variant that exports x and read gates computes the same bits
     as the production variant, so the exported decisions are the production
     kernel's decisions.  Config 5 with 4 requests stacks 32 rows on the prefix;
-    with 12 requests, 96 rows (the stacked-row scan, two read groups)."""
+    with 12 requests, 96 rows (the stacked-row scan, two read groups), whose
+    production kernel fetches values with their keys at finite depth while the
+    debug variant fetches only the live ones: the same bits."""
     wl = make_config(cfg, device="cuda", batch=batch, seq_len=None if cfg == 1 else 1500)
     z = _gpu.estimate(wl)
     a = _gpu.run(wl, T, z=z, debug=False)
