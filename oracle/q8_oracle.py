@@ -33,8 +33,19 @@ with BF16 values):
       split t mod S, slots added in order).
 * Q8  read bits: a value row is read iff live_j holds for some GQA group of
       the read group; a plane-B row iff refine_j does.
+* Q9  stacked level (Appendix E, tile layouts: past 64 stacked rows the level
+      runs laid out as prefill is, with one FP16 product per logit): each key's
+      code rounded once to FP16, k^_j = fp16(e_j (a_j + b_j/256)) (the scale is
+      folded in before that one rounding), each row's query codes rounded to
+      FP16, q^_i = fp16(qa_i + qb_i/256), and s_ij = eta_i (k^_j . q^_i) in
+      FP64 from those FP16 operands; then the depth rule and the fold of the
+      BF16 path (no coarse pass and no refine gate: the product already holds
+      both planes).
 
-Parity status: Q1-Q3 are pinned by closed forms (orthogonality, exact
+Parity status: Q9 is pinned by torch's FP16 rounding of the same exact
+values, by the paper's stated logit bound (within about 2^-11 of |q||k| per
+rounding), by library softmax over the FP16 operands and by additivity over
+splits.  Q1-Q3 are pinned by closed forms (orthogonality, exact
 rational sums, reconstruction bounds, minimality of the rounded-up scale);
 Q4-Q7 by the dequantized dot product, by library softmax over the
 dequantized operands, by the closed-form refine bound and by additivity over
@@ -49,8 +60,8 @@ from typing import Dict, Iterable, Optional, Sequence, Tuple
 
 import numpy as np
 
-from .fold_oracle import (EST_DEFAULT, TILE, bf16_bits_to_f64, estimate_z, gather,
-                          read_gates, split_of_key)
+from .fold_oracle import (EST_DEFAULT, TILE, bf16_bits_to_f64, estimate_z, fold, gather,
+                          live_mask, live_mask_imposed, read_gates, split_of_key)
 
 LOG2E_F64 = float.fromhex("0x1.71547652b82fep+0")   # log2(e) rounded to FP64
 QMAX = 127          # plane-A magnitude bound
@@ -338,6 +349,66 @@ def decode_level_q8(qa, qb, eta, planes, v_bits, *, num_kv_heads: int, page_size
     if want_scores:
         return out + (info,)
     return out
+
+
+# ---------------------------------------------------------------- Q9 -------
+def stack_keys(a: np.ndarray, b: np.ndarray, e_bits: np.ndarray) -> np.ndarray:
+    """The stacked level's FP16 keys ``fp16(e (a + b/256))`` of key codes
+    ``[..., D]``: the product is exact in FP32 (a 16-bit code times an 8-bit
+    scale), rounded once to FP16, nearest even."""
+    e = bf16_bits_to_f64(e_bits)[..., None]
+    exact = e * (a.astype(np.float64) + b.astype(np.float64) / 256.0)
+    return exact.astype(np.float32).astype(np.float16)
+
+
+def stack_queries(qa: np.ndarray, qb: np.ndarray) -> np.ndarray:
+    """The stacked level's FP16 query operand ``fp16(qa + qb/256)`` (the sum is
+    exact in FP32, then one rounding to FP16, nearest even)."""
+    return (qa.astype(np.float32) + qb.astype(np.float32) / np.float32(256.0)).astype(np.float16)
+
+
+def decode_level_q8_stacked(qhat, eta, khat, v_bits, *, num_kv_heads: int, page_size: int,
+                            seq_lens: Sequence[int], block_table=None, row_indptr=None,
+                            row_req=None, z: np.ndarray, T: float, num_splits: int,
+                            imposed_x: Optional[np.ndarray] = None,
+                            chunks: Optional[Iterable[Tuple[int, int]]] = None):
+    """Split partials of a stacked level over the FP16 keys ``khat`` (the
+    layout of the BF16 path's key cache): ``s_ij = eta_i (k^_j . q^_i)`` in
+    FP64 from the FP16 operands, ``x = s - Z``, the depth rule (or the FP32
+    rule on ``imposed_x`` [B, H, max_len]) and the fold, splits and slots of
+    the BF16 path.  Returns ``part_A [S, B, H, D]``, ``part_L [S, B, H]``."""
+    b_, h, d = qhat.shape
+    group = h // num_kv_heads
+    part_a = np.zeros((num_splits, b_, h, d))
+    part_l = np.zeros((num_splits, b_, h))
+    if chunks is None:
+        chunks = [(s, g) for s in range(len(seq_lens)) for g in range(num_kv_heads)]
+    for seq, g in chunks:
+        n = int(seq_lens[seq])
+        reqs = [seq] if row_indptr is None else [int(r) for r in
+                                                  row_req[row_indptr[seq]:row_indptr[seq + 1]]]
+        if n == 0 or not reqs:
+            continue
+        ri = np.array([r for r in reqs for _ in range(group)])
+        hi = np.array([g * group + hh for _ in reqs for hh in range(group)])
+        keys = _gather_raw(khat, seq, g, n, block_table, page_size).astype(np.float64)
+        vals = gather(v_bits, seq, g, n, block_table, page_size)
+        s = np.asarray(eta, dtype=np.float64)[ri, hi][:, None] * (
+            qhat[ri, hi].astype(np.float64) @ keys.T)
+        x = s - np.asarray(z, dtype=np.float64)[ri, hi][:, None]
+        if imposed_x is None:
+            live = live_mask(x, T)
+        else:
+            live = live_mask_imposed(imposed_x[ri, hi, :n], T)
+        owner = split_of_key(n, num_splits)
+        for sp in range(num_splits):
+            m = owner == sp
+            if not m.any():
+                continue
+            a, l = fold(x[:, m], live[:, m], vals[m])
+            part_a[sp, ri, hi] = a
+            part_l[sp, ri, hi] = l
+    return part_a, part_l
 
 
 def _gather_raw(arr: np.ndarray, seq: int, g: int, n: int, block_table, page_size: int):

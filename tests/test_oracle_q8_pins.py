@@ -444,3 +444,126 @@ def test_refine_v_gate_invariants():
         assert np.array_equal(lv_, live)
         assert not np.any(rv & ~live)
         assert np.array_equal(rv[0], live[0] & (xc >= -3.0).any(axis=0))
+
+
+# ------------------------------------------------------------------ Q9 -----
+def test_stacked_operands_are_torch_fp16_of_the_exact_codes():
+    """Library routine: the stacked level's FP16 keys and queries are torch's
+    round-to-nearest-even FP16 conversion of the exact FP32 values
+    e (a + b/256) and qa + qb/256, and stay within FP16's relative rounding
+    bound 2^-11 of them (normal range)."""
+    bits = _rand_bits((64, 128), seed=21, scale=3.0)
+    a, b, e_bits = q8.split_keys(bits)
+    k = q8.stack_keys(a, b, e_bits)
+    assert k.dtype == np.float16
+    exact = q8.dequant(a, b, bf16_bits_to_f64(e_bits))
+    assert np.array_equal(exact.astype(np.float32).astype(np.float64), exact)  # exact in FP32
+    want = torch.from_numpy(exact.astype(np.float32)).to(torch.float16).numpy()
+    assert np.array_equal(k.view(np.uint16), want.view(np.uint16))
+    normal = np.abs(exact) >= 2.0 ** -14
+    assert np.all(np.abs(k.astype(np.float64) - exact)[normal]
+                  <= 2.0 ** -11 * np.abs(exact)[normal])
+    qa, qb, _ = q8.split_queries(_rand_bits((8, 128), seed=22), 0.125)
+    qh = q8.stack_queries(qa, qb)
+    qex = qa.astype(np.float64) + qb.astype(np.float64) / 256.0
+    want_q = torch.from_numpy(qex.astype(np.float32)).to(torch.float16).numpy()
+    assert np.array_equal(qh.view(np.uint16), want_q.view(np.uint16))
+
+
+def test_stacked_logit_within_the_stated_bound():
+    """The paper's bound for the stacked level's FP16 product: each rounding
+    puts the logit within about 2^-11 of |q||k|.  Two roundings (key and
+    query) and the Cauchy-Schwarz inequality give
+    |eta k^.q^ - eta k''.q~| <= eta 2^-11 (2 + 2^-11) |k''| |q~|, q~ = qa + qb/256,
+    against the fully refined two-plane logit (both planes, exact)."""
+    wl = _wl(seed=23, d=128, lens=(400,))
+    planes, qa, qb, eta, tau = _q8_inputs(wl, INF)
+    oi = _adapt.oracle_inputs(wl)
+    bt = oi["flat"]["block_table"]
+    khat_cache = q8.stack_keys(*planes)
+    qh = q8.stack_queries(qa, qb)
+    n = wl.flat.seq_lens_host[0]
+    G = wl.num_heads // wl.num_kv_heads
+    worst = 0.0
+    for h in range(wl.num_heads):
+        g = h // G
+        a = q8._gather_raw(planes[0], 0, g, n, bt, wl.page_size)
+        b = q8._gather_raw(planes[1], 0, g, n, bt, wl.page_size)
+        e = bf16_bits_to_f64(q8._gather_raw(planes[2][..., None], 0, g, n, bt, wl.page_size)[:, 0])
+        kdeq = q8.dequant(a, b, e)
+        kh = q8._gather_raw(khat_cache, 0, g, n, bt, wl.page_size).astype(np.float64)
+        qt = qa[0, h].astype(np.float64) + qb[0, h].astype(np.float64) / 256.0
+        coarse, refine = q8.coarse_and_refine(qa[0, h][None], qb[0, h][None], eta[0, h][None],
+                                              a, b, e)
+        exact = (coarse + refine)[0]                       # eta e (a + b/256) . q~
+        stacked = float(eta[0, h]) * (kh @ qh[0, h].astype(np.float64))
+        bound = float(eta[0, h]) * 2.0 ** -11 * (2 + 2.0 ** -11) * \
+            np.linalg.norm(kdeq, axis=1) * np.linalg.norm(qt)
+        assert np.all(np.abs(stacked - exact) <= bound)
+        worst = max(worst, float((np.abs(stacked - exact) / bound).max()))
+    assert worst > 0.01  # the FP16 rounding is visible, not zero
+
+
+@pytest.mark.parametrize("T", [INF, 1.5])
+def test_stacked_level_equals_library_softmax_on_fp16_operands(T):
+    """Library routine: the stacked level's output is softmax attention (torch
+    SDPA, FP64) over the FP16 operands with scale eta ln 2 (base-2 logits), with
+    the keys the depth rule cuts removed from the numerator only; at T = inf it
+    is plain SDPA.  The cascade prefix of 3 requests x 8 heads stacks 24 rows."""
+    wl = make_cascade(requests=3, heads=8, kv_heads=1, dim=64, prefix_len=208, suffix_len=16,
+                      seed=24)
+    planes, qa, qb, eta, _ = _q8_inputs(wl, 0.0)
+    khat = q8.stack_keys(*planes)
+    qh = q8.stack_queries(qa, qb)
+    lv = _adapt.level_args(wl.levels[0])
+    z = np.full((3, 8), 2.5)
+    n_cut = 0
+    pa, pl = q8.decode_level_q8_stacked(qh, eta, khat, host_bits(wl.v), num_kv_heads=1,
+                                        page_size=wl.page_size, z=z, T=T, num_splits=3, **lv)
+    o, l = combine(pa, pl)
+    n = lv["seq_lens"][0]
+    keys = q8._gather_raw(khat, 0, 0, n, lv["block_table"], wl.page_size).astype(np.float64)
+    vals = bf16_bits_to_f64(q8._gather_raw(host_bits(wl.v), 0, 0, n, lv["block_table"],
+                                           wl.page_size))
+    for r in range(3):
+        for h in range(8):
+            qv = qh[r, h].astype(np.float64)
+            sc = float(eta[r, h]) * math.log(2.0)
+            if math.isinf(T):
+                want = torch.nn.functional.scaled_dot_product_attention(
+                    torch.from_numpy(qv)[None, None, None], torch.from_numpy(keys)[None, None],
+                    torch.from_numpy(vals)[None, None], scale=sc)[0, 0, 0].numpy()
+            else:
+                s = float(eta[r, h]) * (keys @ qv)
+                cut = s - z[r, h] < -T
+                n_cut += int(cut.sum())
+                p = torch.softmax(torch.from_numpy(s * math.log(2.0)), dim=0).numpy()
+                want = (p * ~cut) @ vals
+            np.testing.assert_allclose(o[r, h], want, rtol=0, atol=1e-10 * np.abs(want).max())
+            # L is every key's weight against the reference
+            np.testing.assert_allclose(l[r, h], np.exp2(float(eta[r, h]) * (keys @ qv)
+                                                        - z[r, h]).sum(), rtol=1e-12)
+    assert math.isinf(T) or 0 < n_cut < 3 * 8 * n
+
+
+def test_stacked_level_partials_add_over_splits():
+    """Additivity over splits, and each request's rows give the same partials
+    scanned alone (the stacked level has no group gate)."""
+    wl = make_cascade(requests=3, heads=4, kv_heads=1, dim=64, prefix_len=336, suffix_len=16,
+                      seed=25)
+    planes, qa, qb, eta, _ = _q8_inputs(wl, 0.0)
+    khat = q8.stack_keys(*planes)
+    qh = q8.stack_queries(qa, qb)
+    lv = _adapt.level_args(wl.levels[0])
+    z = _adapt.estimate(_adapt.oracle_inputs(wl))
+    kw = dict(num_kv_heads=1, page_size=wl.page_size, z=z, T=6.0)
+    a1, l1 = q8.decode_level_q8_stacked(qh, eta, khat, host_bits(wl.v), num_splits=1, **kw, **lv)
+    a4, l4 = q8.decode_level_q8_stacked(qh, eta, khat, host_bits(wl.v), num_splits=4, **kw, **lv)
+    np.testing.assert_allclose(a4.sum(0), a1[0], rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(l4.sum(0), l1[0], rtol=1e-12)
+    one = dict(lv)
+    one["row_indptr"] = np.array([0, 1])
+    one["row_req"] = np.array([1])
+    a_one, _ = q8.decode_level_q8_stacked(qh, eta, khat, host_bits(wl.v), num_splits=4, **kw,
+                                          **one)
+    assert np.array_equal(a_one[:, 1], a4[:, 1])
