@@ -189,6 +189,20 @@ class Q8Path:
                                  row_req=lv.row_req, max_reqs_per_seq=lv.max_reqs_per_seq,
                                  k_is_layout_only=True) for lv in wl.levels]
         self.flat = self.app_kv
+        # levels past 32 rows per kv sequence (a cascade prefix) run as a
+        # stacked level over FP16 keys written once per prefix (BF16 values)
+        self.stacked = [None] * len(wl.levels)
+        if not values8:
+            qv = F.q_view(wl.q)
+            for i, lv in enumerate(wl.levels):
+                if F.fold_decode_rows_per_group(self.levels[i], qv) == 64:
+                    k16 = torch.empty(self.keys.plane_a.shape, dtype=torch.float16, device=dev)
+                    F.fold_q8_stack_keys(self.levels[i], self.keys, k16)
+                    self.stacked[i] = F.kv_view(
+                        k16, wl.v, lv.seq_lens, num_kv_heads=wl.num_kv_heads,
+                        max_seq_len=lv.max_seq_len, block_table=lv.block_table,
+                        row_indptr=lv.row_indptr, row_req=lv.row_req,
+                        max_reqs_per_seq=lv.max_reqs_per_seq)
         self.qq = F.q8_empty_query(wl.q)
         bq, h, d = wl.q.shape
         self.splits = list(wl.level_splits)
@@ -222,10 +236,21 @@ class Q8Path:
 
     def decode(self, T, stream):
         off = 0
-        for kv, s in zip(self.levels, self.splits):
-            self.F.fold_q8_decode_split(kv, self.keys, self.qq, self.z, T, s, off, self.part_A,
-                                        self.part_L, values=self.vals, stream=stream)
+        for kv, stk, s in zip(self.levels, self.stacked, self.splits):
+            if stk is not None:
+                self.F.fold_q8_decode_stacked(stk, self.qq, self.z, T, s, off, self.part_A,
+                                              self.part_L, stream=stream)
+            else:
+                self.F.fold_q8_decode_split(kv, self.keys, self.qq, self.z, T, s, off,
+                                            self.part_A, self.part_L, values=self.vals,
+                                            stream=stream)
             off += s
+
+    def stack_keys(self, stream):
+        """Re-write the stacked levels' FP16 keys (a once-per-prefix cost)."""
+        for kv, stk in zip(self.levels, self.stacked):
+            if stk is not None:
+                self.F.fold_q8_stack_keys(kv, self.keys, stk.tensors[0], stream=stream)
 
     def combine(self, stream):
         self.F.fold_combine(self.part_A, self.part_L, self.out, stream=stream)
@@ -238,7 +263,14 @@ class Q8Path:
         dev = self.wl.q.device
         nv = nb = total = nr = 0
         off = 0
-        for lv, kv, s in zip(self.wl.levels, self.levels, self.splits):
+        for lv, kv, stk, s in zip(self.wl.levels, self.levels, self.stacked, self.splits):
+            if stk is not None:  # the stacked level reads every key and value row
+                n_keys = sum(lv.seq_lens_host) * self.wl.num_kv_heads
+                nv += n_keys
+                nb += n_keys
+                total += n_keys
+                off += s
+                continue
             rg = F.fold_q8_decode_row_groups(kv, self.qq)
             kg = torch.zeros(lv.num_seqs, self.wl.num_kv_heads, rg, lv.max_seq_len,
                              dtype=torch.uint8, device=dev)
@@ -434,6 +466,21 @@ def q8_leg(wl, F, torch, flush, steps, warmup, name=None, values8=False):
                    "scan + combine; the one-token append is timed apart"}
     if values8:
         out["kappa_v"] = qp.kappa_v
+    if any(stk is not None for stk in qp.stacked):
+        out["stacked_levels"] = ("levels past 32 rows per kv sequence run on FP16 keys "
+                                 "fp16(e (a + b/256)) written once per prefix "
+                                 "(fold_q8_stack_keys, timed apart)")
+        ts = []
+        for it in range(warmup + steps):
+            evict_caches(flush)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            qp.stack_keys(stream)
+            e1.record(stream)
+            if it >= warmup:
+                e1.synchronize()
+                ts.append(e0.elapsed_time(e1))
+        out["stack_keys_us_once_per_prefix"] = round(statistics.median(ts) * 1e3, 2)
     for T in (math.inf, 16.0):
         nv, nb, total, nr = qp.read_counts(T)
         med = time_q8(qp, T, steps, warmup, flush, torch)

@@ -209,6 +209,46 @@ fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* key
                                  float* part_L, float* part_Lcut, const fold_q8_debug* dbg,
                                  void* stream);
 
+/*
+ * Stacked levels over a two-plane key cache (Appendix E, tile layouts: past
+ * 64 stacked query rows a level runs laid out as prefill is, and its logit is
+ * one FP16 product of each key's code, rounded once per prefix, against the
+ * rows' queries).  A level that more than 32 rows attend per kv sequence (a
+ * shared prefix, a wide draft level) is decoded from FP16 keys written once:
+ *
+ * fold_q8_stack_keys - k_f16 = fp16(e (a + b/256)) for every key of the
+ * view's kv sequences, rounded to nearest even (a + b/256 and its product with
+ * the BF16 scale are exact in FP32; the scale is folded in before the one
+ * rounding).
+ *   kv     the level's view (sequences, lengths, block table; kv->k and kv->v
+ *          are not read)
+ *   keys   the cache's planes and scales
+ *   k_f16  FP16 bits in the element layout of the planes (2 bytes per
+ *          element), 16-byte aligned; elements of keys past a sequence's
+ *          length or on a page id outside [0, num_pages) are not written
+ */
+fold_status fold_q8_stack_keys(const fold_kv_view* kv, const fold_q8_keys* keys,
+                               uint16_t* k_f16, void* stream);
+
+/*
+ * fold_q8_decode_stacked - the split scan of a stacked level over the FP16
+ * keys: s_ij = eta_i (k^_j . q^_i), k^ from fold_q8_stack_keys, q^ =
+ * fp16(qa + qb/256) from the query codes, the product accumulated in FP32;
+ * then the depth rule, slots and outputs of fold_decode_split (read groups of
+ * 64 rows, as fold_decode_rows_per_group gives them).  There is no coarse
+ * pass and no refine gate: the product holds both planes (q->tau is not read).
+ *   kv       the level's view with kv->k = the FP16 keys and kv->v the BF16
+ *            values; more than 32 rows must attend each kv sequence, else
+ *            FOLD_E_UNSUPPORTED (fold_q8_decode_split serves such levels)
+ *   q        query codes and eta (fold_q8_split_query)
+ *   z, depth_T, num_splits, slot_offset, num_slots, part_A, part_L,
+ *   part_Lcut, dbg   as fold_decode_split
+ */
+fold_status fold_q8_decode_stacked(const fold_kv_view* kv, const fold_q8_query* q, const float* z,
+                                   float depth_T, int32_t num_splits, int32_t slot_offset,
+                                   int32_t num_slots, float* part_A, float* part_L,
+                                   float* part_Lcut, const fold_debug* dbg, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -31,6 +31,12 @@
 //            (ds_read_b64_tr_b16).  The weight enters as bf16(hi) +
 //            bf16(residual), two products; L adds the FP32 weight of every key.
 //
+// F16 (the stacked level of a two-plane key cache; Appendix E, tile layouts):
+// the K tiles hold FP16 keys fp16(e (a + b/256)) written once per prefix, the
+// query operand is fp16(qa + qb/256) formed from the query codes in the
+// prologue, the scores run on v_mfma_f32_16x16x32_f16 and x = eta_i s - Z_i.
+// Everything else is the BF16 kernel's.
+//
 // CX (block model of BF16 values, finite T): each weighed 16-key chunk's cut
 // mass per row, the summed weights of its cut keys, is also written to
 // chunk_cut.
@@ -130,6 +136,17 @@ __device__ __forceinline__ uint32_t gload4(const void* p) {
   asm volatile("global_load_dword %0, %1, off" : "=v"(r) : "v"(p) : "memory");
   return r;
 }
+__device__ __forceinline__ u32x2 gload8(const void* p) {
+  u32x2 r;
+  asm volatile("global_load_dwordx2 %0, %1, off" : "=v"(r) : "v"(p) : "memory");
+  return r;
+}
+template <int N>
+__device__ __forceinline__ void tie_regs2(u32x2 (&a)[N], u32x2 (&b)[N], uint32_t& z, uint32_t& e) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(a[i]), "+v"(b[i]) : : "memory");
+  asm volatile("" : "+v"(z), "+v"(e) : : "memory");
+}
 template <int N>
 __device__ __forceinline__ void tie_regs(u32x4 (&q)[N], uint32_t& z) {
   static_assert(N == 2 || N == 4, "operand count");
@@ -154,7 +171,7 @@ struct TileW {
   uint64_t mask;
 };
 
-template <int D, bool DENSE, bool DBG, bool CX = false, bool EAGER = false>
+template <int D, bool DENSE, bool DBG, bool CX = false, bool EAGER = false, bool F16 = false>
 __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const DecodeArgs a) {
   constexpr bool PIPE = DENSE || EAGER;  // the dense pipeline: values fetched with their keys
   constexpr bool DEPTH = !DENSE;         // the depth rule decides the weights
@@ -226,17 +243,52 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
   asm volatile("" : : "s"(pg0), "s"(pg1), "s"(pg2), "s"(pg3), "s"(pg4));
   u32x4 qb[NK];
   uint32_t zbits;
+  // F16 (stacked level of a two-plane key cache): the query codes qa, qb of
+  // the lane's channels and the row's score scale eta
+  u32x2 qca[F16 ? NK : 1], qcb[F16 ? NK : 1];
+  uint32_t ebits = 0;
   {
     // a row outside the group reads row 0 (there is at least one row) and is
     // replaced below
-    const uint16_t* qp = a.q + (ri.ok ? qrow * D : 0) + 8 * grp;
+    if constexpr (F16) {
+      const int8_t* qp = a.qplanes + (ri.ok ? qrow * 2 * D : 0) + 8 * grp;
 #pragma unroll
-    for (int c = 0; c < NK; ++c) qb[c] = gload16(qp + 32 * c);
+      for (int c = 0; c < NK; ++c) {
+        qca[c] = gload8(qp + 32 * c);
+        qcb[c] = gload8(qp + D + 32 * c);
+      }
+      ebits = gload4(a.qeta + (ri.ok ? qrow : 0));
+    } else {
+      const uint16_t* qp = a.q + (ri.ok ? qrow * D : 0) + 8 * grp;
+#pragma unroll
+      for (int c = 0; c < NK; ++c) qb[c] = gload16(qp + 32 * c);
+    }
     zbits = gload4(a.z + (ri.ok ? qrow : 0));
   }
   float zr = 0.0f;
+  float sscale = a.score_scale;  // F16: the row's eta
   auto settle_row = [&]() {
-    tie_regs(qb, zbits);
+    if constexpr (F16) {
+      tie_regs2(qca, qcb, zbits, ebits);
+      // the query operand fp16(qa + qb/256), element k of the 8 at byte k
+#pragma unroll
+      for (int c = 0; c < NK; ++c) {
+        uint32_t h[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const uint32_t wa = k < 4 ? qca[c].x : qca[c].y;
+          const uint32_t wb = k < 4 ? qcb[c].x : qcb[c].y;
+          const int ca = static_cast<int8_t>((wa >> (8 * (k & 3))) & 0xffu);
+          const int cb = static_cast<int8_t>((wb >> (8 * (k & 3))) & 0xffu);
+          h[k] = f32_to_f16_bits(static_cast<float>(ca) + static_cast<float>(cb) * (1.0f / 256.0f));
+        }
+        qb[c] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                      h[6] | (h[7] << 16)};
+      }
+      sscale = ri.ok ? __uint_as_float(ebits) : 0.0f;
+    } else {
+      tie_regs(qb, zbits);
+    }
     // A row outside the group gets Z = +inf and q = 0: x = -inf, its weights
     // are exactly 0 and it is never live, without per-key selects.
     zr = ri.ok ? __uint_as_float(zbits) : INFINITY;
@@ -317,10 +369,11 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
     for (int st = 0; st < 2; ++st) {
       f32x4 c4 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int cc = 0; cc < NK; ++cc)
-        c4 = mfma_16x16x32(*reinterpret_cast<const u32x4*>(
-                               kb + 16 * KEYB * st + (((4 * cc + grp) ^ fk(n16)) << 4)),
-                           qb[cc], c4);
+      for (int cc = 0; cc < NK; ++cc) {
+        const u32x4 kop = *reinterpret_cast<const u32x4*>(
+            kb + 16 * KEYB * st + (((4 * cc + grp) ^ fk(n16)) << 4));
+        c4 = F16 ? mfma_16x16x32_f16(kop, qb[cc], c4) : mfma_16x16x32(kop, qb[cc], c4);
+      }
       s[st] = c4;
     }
   };
@@ -348,7 +401,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
       for (int i = 0; i < 4; ++i) {
         const int kk = 32 * kh + 16 * st + 4 * grp + i;
         const bool ok = FULL || (ri.ok && kk < nk);
-        const float x = __builtin_fmaf(s[st][i], a.score_scale, -zr);
+        const float x = __builtin_fmaf(s[st][i], sscale, -zr);
         const bool live = ok && (!DEPTH || x >= a.neg_T);
         const float w = FULL ? exp2_fast(x) : (ok ? exp2_fast(x) : 0.0f);
         lsum += w;
@@ -611,22 +664,32 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
   }
 }
 
-template <int D, bool DENSE>
+template <int D, bool DENSE, bool F16>
 hipError_t launch_stk(const DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
   if (dbg) {
-    hipLaunchKernelGGL((decode_stacked_kernel<D, DENSE, true>), dim3(blocks), dim3(kStkThreads), 0,
-                       stream, a);
-  } else if constexpr (DENSE) {
-    hipLaunchKernelGGL((decode_stacked_kernel<D, true, false>), dim3(blocks), dim3(kStkThreads), 0,
-                       stream, a);
-  } else if (a.chunk_cut) {
-    hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, true, true>), dim3(blocks),
+    hipLaunchKernelGGL((decode_stacked_kernel<D, DENSE, true, false, false, F16>), dim3(blocks),
                        dim3(kStkThreads), 0, stream, a);
+  } else if constexpr (DENSE) {
+    hipLaunchKernelGGL((decode_stacked_kernel<D, true, false, false, false, F16>), dim3(blocks),
+                       dim3(kStkThreads), 0, stream, a);
+  } else if (!F16 && a.chunk_cut) {
+    if constexpr (!F16)
+      hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, true, true>), dim3(blocks),
+                         dim3(kStkThreads), 0, stream, a);
   } else {
-    hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, false, true>), dim3(blocks),
+    hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, false, true, F16>), dim3(blocks),
                        dim3(kStkThreads), 0, stream, a);
   }
   return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_stk_d(const DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
+  if (a.qplanes)
+    return a.dense ? launch_stk<D, true, true>(a, dbg, blocks, stream)
+                   : launch_stk<D, false, true>(a, dbg, blocks, stream);
+  return a.dense ? launch_stk<D, true, false>(a, dbg, blocks, stream)
+                 : launch_stk<D, false, false>(a, dbg, blocks, stream);
 }
 
 }  // namespace
@@ -638,10 +701,8 @@ hipError_t launch_decode_stacked(const DecodeArgs& a, int head_dim, hipStream_t 
   if (blocks == 0) return hipSuccess;
   const bool dbg = a.x_out || a.key_gate_out || a.page_gate_out;
   const unsigned nb = static_cast<unsigned>(blocks);
-  if (head_dim == 128)
-    return a.dense ? launch_stk<128, true>(a, dbg, nb, stream) : launch_stk<128, false>(a, dbg, nb, stream);
-  if (head_dim == 64)
-    return a.dense ? launch_stk<64, true>(a, dbg, nb, stream) : launch_stk<64, false>(a, dbg, nb, stream);
+  if (head_dim == 128) return launch_stk_d<128>(a, dbg, nb, stream);
+  if (head_dim == 64) return launch_stk_d<64>(a, dbg, nb, stream);
   return hipErrorInvalidValue;
 }
 

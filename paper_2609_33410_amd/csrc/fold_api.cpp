@@ -810,6 +810,79 @@ fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* key
   return ok();
 }
 
+fold_status fold_q8_stack_keys(const fold_kv_view* kv, const fold_q8_keys* keys, uint16_t* k_f16,
+                               void* stream) {
+  if (!kv || !keys) return fail(FOLD_E_INVAL, "kv view and keys are required");
+  fold::Q8StackArgs a;
+  fold_status st = check_layout(kv, kv->num_seqs, kv->num_kv_heads, &a.geo);
+  if (st != FOLD_OK) return st;
+  if (kv->num_seqs == 0) return ok();
+  if (!kv->seq_lens || !keys->plane_a || !keys->plane_b || !keys->scale || !k_f16)
+    return fail(FOLD_E_INVAL, "seq_lens, plane_a, plane_b, scale and k_f16 are required");
+  if (!aligned16(keys->plane_a) || !aligned16(keys->plane_b) || !aligned16(k_f16))
+    return fail(FOLD_E_INVAL, "planes and k_f16 must be 16-byte aligned");
+  const long long per = (static_cast<long long>(fold::view_capacity(a.geo)) + 31) / 16;
+  if (static_cast<long long>(kv->num_seqs) * kv->num_kv_heads * per > 0x7fffffffLL)
+    return fail(FOLD_E_INVAL, "grid too large");
+  a.ka = keys->plane_a;
+  a.kb = keys->plane_b;
+  a.ks = keys->scale;
+  a.out = k_f16;
+  hipError_t e = fold::launch_q8_stack_keys(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "stack keys launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fold_status fold_q8_decode_stacked(const fold_kv_view* kv, const fold_q8_query* q, const float* z,
+                                   float depth_T, int32_t num_splits, int32_t slot_offset,
+                                   int32_t num_slots, float* part_A, float* part_L,
+                                   float* part_Lcut, const fold_debug* dbg, void* stream) {
+  if (!kv || !q) return fail(FOLD_E_INVAL, "kv view and q are required");
+  fold::DecodeArgs a;
+  fold_status st = check_layout(kv, q->batch, q->num_heads, &a.geo);
+  if (st != FOLD_OK) return st;
+  if (!kv->k || !kv->v || !kv->seq_lens || !q->planes || !q->eta)
+    return fail(FOLD_E_INVAL, "k (the FP16 keys), v, seq_lens, query planes and eta are required");
+  if (!aligned16(kv->k) || !aligned16(kv->v) || !aligned16(q->planes))
+    return fail(FOLD_E_INVAL, "k, v and the query planes must be 16-byte aligned");
+  if (!z || !part_A || !part_L) return fail(FOLD_E_INVAL, "z, part_A and part_L are required");
+  st = check_depth(depth_T);
+  if (st != FOLD_OK) return st;
+  if (num_splits < 1) return fail(FOLD_E_INVAL, "num_splits must be >= 1");
+  if (slot_offset < 0 || static_cast<long long>(slot_offset) + num_splits > num_slots)
+    return fail(FOLD_E_INVAL, "slots [%d, %d) exceed num_slots %d", slot_offset,
+                slot_offset + num_splits, num_slots);
+  const int rows = rows_per_seq_of(kv, q->num_heads);
+  const int gr = fold::decode_rows_per_group(rows);
+  if (gr != 64)
+    return fail(FOLD_E_UNSUPPORTED, "%d rows per kv sequence: the stacked level needs more than "
+                "32 (use fold_q8_decode_split)", rows);
+  const int groups = (rows + gr - 1) / gr;
+  const long long blocks = static_cast<long long>(kv->num_seqs) * kv->num_kv_heads * num_splits * groups;
+  if (blocks > 0x7fffffffLL) return fail(FOLD_E_INVAL, "grid too large");
+  a.q = nullptr;
+  a.z = z;
+  a.part_A = part_A;
+  a.part_L = part_L;
+  a.part_Lcut = part_Lcut;
+  a.x_out = dbg ? dbg->x_out : nullptr;
+  a.key_gate_out = dbg ? dbg->key_gate_out : nullptr;
+  a.page_gate_out = dbg ? dbg->page_gate_out : nullptr;
+  a.score_scale = 0.0f;
+  a.dense = isinf(depth_T) ? 1 : 0;
+  a.neg_T = a.dense ? 0.0f : -depth_T;
+  a.num_splits = num_splits;
+  a.slot_offset = slot_offset;
+  a.rows_per_seq = rows;
+  a.rows_per_group = gr;
+  a.row_groups = groups;
+  a.qplanes = q->planes;
+  a.qeta = q->eta;
+  hipError_t e = fold::launch_decode(a, kv->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "stacked decode launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 fold_status fold_append_kv(const fold_kv_view* kv, const void* k_src, const void* v_src,
                            const int32_t* tok_seq, const int32_t* tok_pos, int32_t n_tok,
                            void* k_cache, void* v_cache, void* stream) {

@@ -22,6 +22,19 @@ __device__ __forceinline__ f32x4 mfma_16x16x32(u32x4 a, u32x4 b, f32x4 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// The same tile with FP16 operands (v_mfma_f32_16x16x32_f16).
+__device__ __forceinline__ f32x4 mfma_16x16x32_f16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+// FP16 bits of x rounded to nearest even (v_cvt_f16_f32; subnormals kept).
+__device__ __forceinline__ uint32_t f32_to_f16_bits(float x) {
+  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(x)));
+}
+
 // C += A . B on a 16x16 tile with K = 16 BF16 (v_mfma_f32_16x16x16_bf16).  Lane l
 // holds A[l%16][4(l/16)..+4] and B[4(l/16)..+4][l%16]; C as above.
 __device__ __forceinline__ f32x4 mfma_16x16x16(u32x2 a, u32x2 b, f32x4 c) {

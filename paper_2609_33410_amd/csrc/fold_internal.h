@@ -56,6 +56,11 @@ struct DecodeArgs {
   // every 16-key chunk, chunk_cut[row * chunk_stride + chunk] (finite depth).
   float* chunk_cut = nullptr;
   int chunk_stride = 0;  // ceil(max_seq_len / 16)
+  // Stacked level of a two-plane key cache: geo.k holds the FP16 keys
+  // fp16(e (a + b/256)); the query operand is fp16(qa + qb/256) from the
+  // query codes and the score scale is eta per row (q is not read).
+  const int8_t* qplanes = nullptr;  // [batch][heads][2][D]
+  const float* qeta = nullptr;      // [batch][heads]
 };
 
 struct EstimateArgs {
@@ -269,6 +274,15 @@ hipError_t launch_value_mean_append(const MeanArgs& a, int head_dim, hipStream_t
 hipError_t launch_block_mean(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_block_mean_append(const MeanArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_block_model(const BlockModelArgs& a, int head_dim, hipStream_t stream);
+// The stacked level's FP16 keys of a two-plane cache (q8_front.hip).
+struct Q8StackArgs {
+  ScanGeometry geo;       // the level's view (its sequences' keys are converted)
+  const int8_t* ka;
+  const int8_t* kb;
+  const uint16_t* ks;
+  uint16_t* out;          // FP16 bits, the element layout of the planes
+};
+hipError_t launch_q8_stack_keys(const Q8StackArgs& a, int head_dim, hipStream_t stream);
 // Rows per workgroup of the block model's virtual-row kernel for a bound on
 // the rows attending one (kv sequence, kv head).
 int block_model_rows(int rows_per_seq);

@@ -1,5 +1,10 @@
 // Front of a two-plane INT8 key cache (Section 4, "Cache format"): the key
-// writer, the per-step query split and the writer of 8-bit values.
+// writer, the per-step query split and the writer of 8-bit values; and the
+// stacked level's FP16 keys (Appendix E, tile layouts: a level past 64
+// stacked rows runs laid out as prefill is, with one FP16 product per logit
+// of each key's code rounded once per prefix): q8_stack_kernel writes
+// fp16(e (a + b/256)) per element, the product being exact in FP32 (a 16-bit
+// code times an 8-bit scale) and rounded once, to nearest even.
 //
 // Both rotate a D-vector by the Sylvester Hadamard matrix H_D (entries +-1;
 // the paper's orthonormal rotation is H_D / sqrt(D), and its 1/D on a dot
@@ -162,7 +167,67 @@ __global__ __launch_bounds__(kFrontThreads) void v8_write_kernel(const V8WriteAr
   }
 }
 
+// One thread per 8 elements of a key: D/8 threads per key, 256/(D/8) keys per
+// workgroup.  Grid: (kv sequence, kv head, key block).
+template <int D>
+__global__ __launch_bounds__(kFrontThreads) void q8_stack_kernel(const Q8StackArgs a, int blocks_per_seq) {
+  constexpr int TPK = D / 8;
+  constexpr int KPB = kFrontThreads / TPK;
+  const ScanGeometry& g = a.geo;
+  int bid = blockIdx.x;
+  const int kb = bid % blocks_per_seq;
+  bid /= blocks_per_seq;
+  const int kvh = bid % g.hkv;
+  const int seq = bid / g.hkv;
+  const int j = kb * KPB + static_cast<int>(threadIdx.x) / TPK;
+  const int part = threadIdx.x % TPK;
+  const int n = clamp_len(ld_uniform(g.seq_lens, seq), view_capacity(g));
+  if (j >= n) return;
+  size_t row;
+  if (g.page_size > 0) {
+    const int phys = g.block_table[static_cast<size_t>(seq) * g.max_pages + j / g.page_size];
+    if (phys < 0 || phys >= g.num_pages) return;
+    row = (static_cast<size_t>(phys) * g.hkv + kvh) * g.page_size + j % g.page_size;
+  } else {
+    row = (static_cast<size_t>(seq) * g.hkv + kvh) * g.max_seq_len + j;
+  }
+  const size_t el = row * D + 8 * part;
+  const uint2 pa = *reinterpret_cast<const uint2*>(a.ka + el);
+  const uint2 pb = *reinterpret_cast<const uint2*>(a.kb + el);
+  const float e = bf16_lo(a.ks[row]);
+  uint32_t h[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t wa = i < 4 ? pa.x : pa.y;
+    const uint32_t wb = i < 4 ? pb.x : pb.y;
+    const int ca = static_cast<int8_t>((wa >> (8 * (i & 3))) & 0xffu);
+    const int cb = static_cast<int8_t>((wb >> (8 * (i & 3))) & 0xffu);
+    // a + b/256 is exact in FP32, and so is its product with an 8-bit scale
+    const float code = static_cast<float>(ca) + static_cast<float>(cb) * (1.0f / 256.0f);
+    h[i] = f32_to_f16_bits(e * code);
+  }
+  *reinterpret_cast<u32x4*>(a.out + el) =
+      u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+}
+
 }  // namespace
+
+hipError_t launch_q8_stack_keys(const Q8StackArgs& a, int head_dim, hipStream_t stream) {
+  const int cap = view_capacity(a.geo);
+  const int kpb = kFrontThreads / (head_dim / 8);
+  const int per_seq = (cap + kpb - 1) / kpb;
+  const long long blocks = static_cast<long long>(a.geo.num_seqs) * a.geo.hkv * per_seq;
+  if (blocks == 0) return hipSuccess;
+  if (head_dim == 128)
+    hipLaunchKernelGGL(q8_stack_kernel<128>, dim3(static_cast<unsigned>(blocks)),
+                       dim3(kFrontThreads), 0, stream, a, per_seq);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL(q8_stack_kernel<64>, dim3(static_cast<unsigned>(blocks)),
+                       dim3(kFrontThreads), 0, stream, a, per_seq);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
 
 hipError_t launch_v8_write(const V8WriteArgs& a, int head_dim, hipStream_t stream) {
   const long long items = static_cast<long long>(a.n_tok) * a.geo.hkv;

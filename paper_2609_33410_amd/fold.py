@@ -47,6 +47,8 @@ EXPORTED = (
     "fold_q8_decode_rows_per_group",
     "fold_q8_decode_row_groups",
     "fold_q8_decode_split",
+    "fold_q8_stack_keys",
+    "fold_q8_decode_stacked",
     "fold_append_kv",
     "fold_cert_update",
     "fold_draft_plan",
@@ -231,6 +233,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_void_p, P(fold_q8_debug),
                                          ctypes.c_void_p]
+    lib.fold_q8_stack_keys.restype = ctypes.c_int
+    lib.fold_q8_stack_keys.argtypes = [P(fold_kv_view), P(fold_q8_keys), ctypes.c_void_p,
+                                       ctypes.c_void_p]
+    lib.fold_q8_decode_stacked.restype = ctypes.c_int
+    lib.fold_q8_decode_stacked.argtypes = [P(fold_kv_view), P(fold_q8_query), ctypes.c_void_p,
+                                           ctypes.c_float, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_void_p, P(fold_debug), ctypes.c_void_p]
     V = ctypes.c_void_p
     I32 = ctypes.c_int32
     lib.fold_append_kv.restype = ctypes.c_int
@@ -338,10 +348,11 @@ def kv_view(k: torch.Tensor, v: Optional[torch.Tensor], seq_lens: torch.Tensor, 
     ``block_table [num_seqs, max_pages]``; contiguous: ``k, v [num_seqs, Hkv,
     max_seq_len, D]``.  With ``k_is_layout_only`` (two-plane key caches), ``k``
     is a key plane that gives the shape only and the view's key pointer is
-    NULL."""
+    NULL.  A float16 ``k`` is the FP16 keys of a stacked two-plane level
+    (``fold_q8_stack_keys``), read by ``fold_q8_decode_stacked`` only."""
     if k_is_layout_only:
         _need(k, "plane", torch.int8)
-    else:
+    elif k.dtype != torch.float16:
         _need(k, "k", torch.bfloat16)
     if v is not None:
         _need(v, "v", torch.bfloat16)
@@ -985,6 +996,57 @@ def fold_q8_decode_rows_per_group(kv: KV, q: Q8Query) -> int:
 def fold_q8_decode_row_groups(kv: KV, q: Q8Query) -> int:
     qq = q.view()
     return load_library().fold_q8_decode_row_groups(ctypes.byref(kv.view), ctypes.byref(qq))
+
+
+def fold_q8_stack_keys(kv: KV, keys: Q8Keys, k_f16: torch.Tensor, stream=None) -> torch.Tensor:
+    """FP16 keys ``fp16(e (a + b/256))`` of a stacked level's kv sequences, in
+    the element layout of the planes (written once per prefix)."""
+    _need(k_f16, "k_f16", torch.float16)
+    if tuple(k_f16.shape) != tuple(keys.plane_a.shape):
+        raise ValueError(f"k_f16 must be shaped like the planes {tuple(keys.plane_a.shape)}")
+    _need_device([("k_f16", k_f16), ("plane_a", keys.plane_a), ("plane_b", keys.plane_b),
+                  ("scale", keys.scale)] + [(f"view tensor {i}", t) for i, t in
+                                            enumerate(kv.tensors) if t is not None])
+    kk = keys.view()
+    _check(load_library().fold_q8_stack_keys(ctypes.byref(kv.view), ctypes.byref(kk),
+                                             _ptr(k_f16), _stream(stream)))
+    return k_f16
+
+
+def fold_q8_decode_stacked(kv: KV, q: Q8Query, z: torch.Tensor, depth_T: float,
+                           num_splits: int, slot_offset: int, part_A: torch.Tensor,
+                           part_L: torch.Tensor, x_out: Optional[torch.Tensor] = None,
+                           key_gate_out: Optional[torch.Tensor] = None,
+                           page_gate_out: Optional[torch.Tensor] = None,
+                           part_Lcut: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Split scan of a stacked level (more than 32 rows per kv sequence) over
+    the FP16 keys of ``fold_q8_stack_keys`` (``kv.view.k``)."""
+    _need(z, "z", torch.float32)
+    _need(part_A, "part_A", torch.float32)
+    _need(part_L, "part_L", torch.float32)
+    if kv.tensors[0] is None or kv.tensors[0].dtype != torch.float16:
+        raise ValueError("the view's k must be the FP16 keys of fold_q8_stack_keys")
+    if part_Lcut is not None:
+        _need(part_Lcut, "part_Lcut", torch.float32)
+    b, h = int(q.planes.shape[0]), int(q.planes.shape[1])
+    if part_A.dim() != 4 or tuple(part_A.shape[1:3]) != (b, h):
+        raise ValueError(f"part_A must be [slots, {b}, {h}, D], got {tuple(part_A.shape)}")
+    _need_device([("planes", q.planes), ("eta", q.eta), ("z", z), ("part_A", part_A),
+                  ("part_L", part_L), ("part_Lcut", part_Lcut), ("x_out", x_out),
+                  ("key_gate_out", key_gate_out), ("page_gate_out", page_gate_out)]
+                 + [(f"view tensor {i}", t) for i, t in enumerate(kv.tensors)])
+    dbg = None
+    if x_out is not None or key_gate_out is not None or page_gate_out is not None:
+        for t, nm, dt in ((x_out, "x_out", torch.float32), (key_gate_out, "key_gate_out", torch.uint8),
+                          (page_gate_out, "page_gate_out", torch.uint8)):
+            if t is not None:
+                _need(t, nm, dt)
+        dbg = fold_debug(_ptr(x_out), _ptr(key_gate_out), _ptr(page_gate_out))
+    qq = q.view()
+    _check(load_library().fold_q8_decode_stacked(
+        ctypes.byref(kv.view), ctypes.byref(qq), _ptr(z), depth_T, num_splits, slot_offset,
+        int(part_A.shape[0]), _ptr(part_A), _ptr(part_L), _ptr(part_Lcut),
+        None if dbg is None else ctypes.byref(dbg), _stream(stream)))
 
 
 def fold_q8_decode_split(kv: KV, keys: Q8Keys, q: Q8Query, z: torch.Tensor, depth_T: float,

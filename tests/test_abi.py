@@ -198,6 +198,32 @@ def test_block_model_binding_checks_shapes_and_devices():
         F.fold_value_block_mean(kv, good)
 
 
+def test_q8_stacked_rejects_bad_args(lib):
+    from paper_2609_33410_amd.fold import fold_q8_keys, fold_q8_query
+    keys = fold_q8_keys(FAKE, FAKE, FAKE)
+    sk = lib.fold_q8_stack_keys
+    assert sk(ctypes.byref(_kv()), None, FAKE, None) == F.FOLD_E_INVAL
+    assert sk(ctypes.byref(_kv()), ctypes.byref(keys), None, None) == F.FOLD_E_INVAL
+    assert sk(ctypes.byref(_kv()), ctypes.byref(keys), FAKE + 2, None) == F.FOLD_E_INVAL
+    assert sk(ctypes.byref(_kv(head_dim=96)), ctypes.byref(keys), FAKE, None) == F.FOLD_E_INVAL
+    assert sk(ctypes.byref(_kv(num_seqs=0)), ctypes.byref(keys), None, None) == F.FOLD_OK
+    q = fold_q8_query(FAKE, FAKE, None, 2, 8, None)
+    ds = lib.fold_q8_decode_stacked
+
+    def call(kv, qq=q, T=math.inf, z=FAKE, splits=1):
+        return ds(ctypes.byref(kv), ctypes.byref(qq), z, T, splits, 0, 1, FAKE, FAKE, None, None,
+                  None)
+    # 8 heads over 2 kv heads, one request per sequence: 4 rows, not a stacked level
+    assert call(_kv()) == F.FOLD_E_UNSUPPORTED
+    wide = dict(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=16)  # 64 rows per sequence
+    assert call(_kv(v=None, **wide)) == F.FOLD_E_INVAL
+    assert call(_kv(**wide), qq=fold_q8_query(None, FAKE, None, 2, 8, None)) == F.FOLD_E_INVAL
+    assert call(_kv(**wide), z=None) == F.FOLD_E_INVAL
+    assert call(_kv(**wide), T=-1.0) == F.FOLD_E_INVAL
+    assert call(_kv(**wide), splits=0) == F.FOLD_E_INVAL
+    assert call(_kv(k=FAKE + 2, **wide)) == F.FOLD_E_INVAL
+
+
 def test_row_group_queries(lib):
     kv = _kv()
     # GQA group of 4: one matrix-core read group of 16 rows
