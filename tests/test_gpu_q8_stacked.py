@@ -178,3 +178,53 @@ def test_stacked_level_refuses_narrow_levels():
     with pytest.raises(F.FoldError) as e:
         F.fold_q8_decode_stacked(kv0, qq, z, 16.0, 2, 0, pa, pl)
     assert e.value.status == F.FOLD_E_UNSUPPORTED
+
+
+@pytest.mark.parametrize("T", [INF, 16.0])
+def test_workload5_full_size(T):
+    """The full shared-prefix cascade (64 requests x 8 heads over one 16384-key
+    prefix, 1024 own keys each) on a two-plane cache, in the benchmark's launch
+    configuration (32 + 8 splits): the stacked prefix level on FP16 keys, the
+    suffix on the gated two-plane scan, every row against the oracle."""
+    from workloads import make_config
+    wl = make_config(5, device="cuda")
+    dev = wl.q.device
+    keys = _gpu_q8.encode_cache(wl)
+    qq = _gpu_q8.split_query(wl, -4.0)
+    z = _gpu_q8.estimate(wl, keys, qq)
+    levels, _ = _gpu_q8.level_views(wl, keys)
+    lv0 = wl.levels[0]
+    k16 = _stack(wl, keys, lv0)
+    kv0 = _stacked_view(wl, keys, k16, lv0)
+    b, h, d = wl.q.shape
+    s0, s1 = wl.level_splits
+    pa = torch.empty(s0 + s1, b, h, d, device=dev)
+    pl = torch.empty(s0 + s1, b, h, device=dev)
+    x = torch.full((b, h, lv0.max_seq_len), float("nan"), device=dev)
+    pa_d, pl_d = torch.empty_like(pa), torch.empty_like(pl)
+    F.fold_q8_decode_stacked(kv0, qq, z, T, s0, 0, pa, pl)
+    F.fold_q8_decode_stacked(kv0, qq, z, T, s0, 0, pa_d, pl_d, x_out=x)
+    F.fold_q8_decode_split(levels[1], keys, qq, z, T, s1, s0, pa, pl)
+    out = torch.empty(b, h, d, device=dev)
+    F.fold_combine(pa, pl, out)
+    torch.cuda.synchronize()
+    assert torch.equal(pa[:s0], pa_d[:s0])
+    oi = _adapt.oracle_inputs(wl)
+    a_, b_, e_ = (keys.plane_a.cpu().numpy(), keys.plane_b.cpu().numpy(),
+                  keys.scale.cpu().numpy().view(np.uint16))
+    planes = qq.planes.cpu().numpy()
+    qa, qb = planes[:, :, 0], planes[:, :, 1]
+    eta = qq.eta.cpu().numpy()
+    z64 = z.cpu().double().numpy()
+    a0, l0 = q8.decode_level_q8_stacked(q8.stack_queries(qa, qb), eta, q8.stack_keys(a_, b_, e_),
+                                        oi["v_bits"], num_kv_heads=1, page_size=wl.page_size,
+                                        z=z64, T=T, num_splits=s0, imposed_x=x.cpu().numpy(),
+                                        **oi["levels"][0])
+    a1, l1 = q8.decode_level_q8(qa, qb, eta, (a_, b_, e_), oi["v_bits"], num_kv_heads=1,
+                                page_size=wl.page_size, z=z64, T=T,
+                                tau=qq.tau.cpu().numpy(), num_splits=s1, **oi["levels"][1])
+    np.testing.assert_allclose(pl.cpu().double().numpy()[:s0], l0, rtol=2e-5)
+    o_ref, l_ref = oracle.combine(np.concatenate([a0, a1]), np.concatenate([l0, l1]))
+    err = _gpu.row_errors(out.cpu().numpy(), o_ref)
+    print(f"  workload 5 two-plane T={T}: {b * h} rows, max row err = {err.max():.3e}")
+    assert (err <= TOL).all()
