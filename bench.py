@@ -653,6 +653,8 @@ def scan_kernel_name(wl, dense=True):
 def q8_kernel_name(wl, values8):
     """The dense two-plane scan kernel of a single-level workload."""
     v8 = "true" if values8 else "false"
+    if wl.group == 1:
+        return f"decode_q8_split_kernel<{wl.head_dim}, true, false, {v8}, 4>"
     if wl.group <= 8:
         return f"decode_q8_packed_kernel<{wl.head_dim}, 2, true, false, {v8}>"
     return f"decode_q8_kernel<{wl.head_dim}, ..., true, false, {v8}>"

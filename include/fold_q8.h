@@ -181,8 +181,9 @@ fold_status fold_q8_front(const fold_kv_view* kv, const fold_q8_keys* keys, cons
                           int8_t* planes_out, float* eta_out, float* tau_out, float* tau_v_out,
                           const fold_est_params* params, float* z_out, void* stream);
 
-/* Rows per read group (16 or 32) and read groups per (kv sequence, kv head)
- * of fold_q8_decode_split; -1 on an invalid view.  The GQA group size
+/* Rows per read group (1 when one row attends each kv sequence and head, else
+ * 16 or 32) and read groups per (kv sequence, kv head) of
+ * fold_q8_decode_split; -1 on an invalid view.  The GQA group size
  * num_heads / num_kv_heads must be 1, 2, 4, 8, 16 or 32, so that every read
  * group holds whole GQA groups. */
 int32_t fold_q8_decode_rows_per_group(const fold_kv_view* kv, const fold_q8_query* q);

@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libfold.so")
 
 SOURCES = ["decode_split.hip", "decode_mfma.hip", "decode_packed.hip", "decode_stacked.hip", "ref_estimate.hip", "combine.hip",
-           "decode_q8.hip", "decode_q8_packed.hip", "q8_front.hip", "value_model.hip", "step.hip", "noalloc.hip",
+           "decode_q8.hip", "decode_q8_packed.hip", "decode_q8_split.hip", "q8_front.hip", "value_model.hip", "step.hip", "noalloc.hip",
            "fold_api.cpp"]
 
 HIPCC_FLAGS = [

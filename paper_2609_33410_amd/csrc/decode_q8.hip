@@ -531,8 +531,11 @@ hipError_t launch_q8_d(const Q8DecodeArgs& a, unsigned blocks, hipStream_t strea
 }  // namespace
 
 hipError_t launch_q8_decode_packed(const Q8DecodeArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_q8_decode_valu(const Q8DecodeArgs& a, int head_dim, hipStream_t stream);
 
 hipError_t launch_q8_decode(const Q8DecodeArgs& a, int head_dim, hipStream_t stream) {
+  // one row per kv sequence and head: the VALU scan
+  if (a.d.rows_per_group == 1) return launch_q8_decode_valu(a, head_dim, stream);
   // at most eight rows per kv sequence: several chunks per pass
   if (a.d.rows_per_seq <= 8) return launch_q8_decode_packed(a, head_dim, stream);
   const long long blocks = static_cast<long long>(a.d.geo.num_seqs) * a.d.geo.hkv *

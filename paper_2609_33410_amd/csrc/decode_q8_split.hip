@@ -1,0 +1,398 @@
+// Split-KV decode over a two-plane INT8 key cache for one query row per kv
+// sequence and head (MHA), on VALU (Section 4, "Cache format", "Weight-gated
+// reads", "Depth as a dial"; Algorithm 1 with BF16 or 8-bit values).
+//
+// The arithmetic is the two-plane scans' (decode_q8.hip): coarse scores from
+// plane A and the key scales, the live / refine-K / refine-V verdicts on them,
+// plane B only for refined keys, value rows only for live keys, the weight
+// 2^x with every key's weight in L.  With one row the read group is the row,
+// so the verdicts are also the read bits.  The layout is the BF16 MHA scan's
+// (decode_split.hip): no matrix core would have more than one of its sixteen
+// columns busy.
+//
+// Workgroup = (kv sequence, kv head, split), W wave64s sharing the split's
+// 64-key tiles (wave w owns chunk w mod 4 of tiles k == w / 4 (mod W / 4);
+// W = 4 is launched);
+// for a per-request view of at most 64 sequences the longest are dispatched
+// first.  LPK = D/8 lanes hold one key, lane part p owning channels
+// 8p .. 8p+7: one wave-wide load covers KPI = 64/LPK keys of a plane (8 bytes
+// per lane), of the BF16 values (16 bytes) or of an E4M3 value plane (8).
+//
+//   coarse   the lane's c_aa = a . qa and c_ab = a . qb by v_dot4_i32_i8,
+//            added over the key's LPK lanes in FP32 (exact: every partial and
+//            total is an integer below 2^24); xc = (eta e)(c_aa + c_ab/256)
+//            - Z in FP32.
+//   refine   plane B of refined keys only (the others get an offset past the
+//            chunk's buffer resource: no bytes move), c_ba and c_bb the same
+//            way, x = xc + [refine] (eta e)((c_ba + c_bb/256)/256).
+//   values   w = 2^x; a key counts iff x >= -T; L adds every w; A += w v in
+//            FP32.  8-bit values are widened exactly to FP32
+//            (v_cvt_scalef32_pk_f32_fp8), the second plane with scale 1/16,
+//            and A, a sum over p + [refine-V] r/16, is multiplied by 2^e when
+//            written.
+//
+// Pipeline per wave: plane A and the scales of chunk t+2 are requested while
+// chunk t+1 is scored and its plane-B and value rows requested, and chunk t
+// is refined and accumulated.  At T = inf every value row is requested once
+// its chunk is scored (plane B still waits for the refine verdict).
+#include "q8_common.h"
+
+namespace fold {
+namespace {
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ u32x2 buf_load8(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kStreamPolicy));
+}
+
+// Signed INT8 dot product of two 8-byte groups.
+__device__ __forceinline__ int sdot8(u32x2 a, u32x2 b) {
+  return __builtin_amdgcn_sdot4(static_cast<int>(a.y), static_cast<int>(b.y),
+                                __builtin_amdgcn_sdot4(static_cast<int>(a.x), static_cast<int>(b.x),
+                                                       0, false),
+                                false);
+}
+
+template <int D>
+struct Q8VPlaneA {  // a chunk whose plane A and scales are requested
+  static constexpr int NI = kChunk / (64 / (D / 8));
+  Q8Loc loc;
+  u32x2 ka[NI];        // plane A, the lane's 8 channels of key KPI i + kslot
+  uint32_t sc[NI];     // its BF16 scale (low half)
+};
+
+template <int D, bool V8>
+struct Q8VScored {  // a scored chunk whose plane-B and value rows are requested
+  static constexpr int NI = kChunk / (64 / (D / 8));
+  float xc[NI];        // coarse score
+  uint32_t e2[NI / 2]; // the keys' BF16 scales, two per word
+  uint32_t bits;       // bit i: live, 8 + i: refine, 16 + i: refine-V, 24 + i: key exists
+  bool anyref;         // some key of the chunk is refined (wave-uniform)
+  bool anylive;        // some key of the chunk is live (wave-uniform)
+  u32x2 kb[NI];        // plane B of refined keys
+  u32x4 vv[V8 ? 1 : NI];   // BF16 values of live keys
+  u32x2 vp[V8 ? NI : 1];   // first E4M3 plane of live keys
+  u32x2 vr[V8 ? NI : 1];   // second E4M3 plane of refine-V keys
+};
+
+template <int D, bool DENSE, bool DBG, bool V8>
+struct Q8Valu {
+  static constexpr int LPK = D / 8;        // lanes per key row
+  static constexpr int KPI = 64 / LPK;     // keys per wave-wide load
+  static constexpr int NI = kChunk / KPI;  // loads per lane per 16-key chunk
+  using PA = Q8VPlaneA<D>;
+  using SC = Q8VScored<D, V8>;
+
+  const Q8DecodeArgs& a;
+  const ScanGeometry& g;
+  ScanPlace p;
+  int lane, part, kslot, pshift;
+  size_t gate_row;
+  int gate_pages;
+  u32x2 qa, qb;  // query codes of the lane's channels
+  float eta, zr, ntau, ntau_v;
+  bool rok;
+  size_t xrow;
+  float acc[8];
+  float lsum, lcut;
+
+  __device__ Q8Valu(const Q8DecodeArgs& a_) : a(a_), g(a_.d.geo) {}
+
+  // Plane A and the scales of chunk c.
+  __device__ __forceinline__ void load_a(int c, PA& s) const {
+    s.loc = q8_loc(g, p, c, q8_chunk_phys(g, p, c, pshift), pshift);
+    const rsrc_t ra = make_rsrc(a.keys.ka + s.loc.row * D, s.loc.nk * D);
+    const rsrc_t rs = make_rsrc(a.keys.ks + s.loc.row, s.loc.nk * 2);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const uint32_t key = KPI * i + kslot;
+      s.ka[i] = buf_load8(ra, key * D + 8 * part);
+      s.sc[i] = buf_load2(rs, 2 * key);
+    }
+  }
+
+  // Coarse scores and verdicts of chunk c (plane A in in), then the requests
+  // its verdicts allow: plane B of refined keys, value rows of live keys.
+  __device__ __forceinline__ void coarse(int c, const PA& in, SC& s) const {
+    const int key0 = c * kChunk;
+    const int nk = c < p.nchunks ? min(kChunk, p.n - key0) : 0;
+    uint32_t bits = 0;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int kk = KPI * i + kslot;
+      const bool ok = rok && kk < nk;
+      const float caa = group_sum<LPK>(static_cast<float>(sdot8(in.ka[i], qa)));
+      const float cab = group_sum<LPK>(static_cast<float>(sdot8(in.ka[i], qb)));
+      const float e = bf16_lo(in.sc[i]);
+      const float t = caa + cab * (1.0f / 256.0f);
+      if (i & 1)
+        s.e2[i / 2] |= (in.sc[i] & 0xffffu) << 16;
+      else
+        s.e2[i / 2] = in.sc[i] & 0xffffu;
+      const float xc = __builtin_fmaf(eta * e, t, -zr);
+      s.xc[i] = xc;
+      const bool live = ok && (DENSE || xc >= a.d.neg_T);
+      const bool ref = live && xc >= ntau;
+      const bool rv = V8 && live && xc >= ntau_v;
+      bits |= (live ? 1u : 0u) << i;
+      bits |= (ref ? 1u : 0u) << (8 + i);
+      bits |= (rv ? 1u : 0u) << (16 + i);
+      bits |= (ok ? 1u : 0u) << (24 + i);
+      if (DBG && ok && part == 0) {
+        const size_t j = static_cast<size_t>(key0) + kk;
+        if (a.xc_out) a.xc_out[xrow * g.max_seq_len + j] = xc;
+        if (a.d.key_gate_out) a.d.key_gate_out[gate_row * g.max_seq_len + j] = live ? 1 : 0;
+        if (a.refine_gate_out) a.refine_gate_out[gate_row * g.max_seq_len + j] = ref ? 1 : 0;
+        if (V8 && a.refine_v_gate_out)
+          a.refine_v_gate_out[gate_row * g.max_seq_len + j] = rv ? 1 : 0;
+      }
+    }
+    s.bits = bits;
+    s.anylive = __ballot((bits & 0xFFu) != 0) != 0;
+    s.anyref = __ballot((bits & 0xFF00u) != 0) != 0;
+    if (DBG && a.d.page_gate_out && lane == 0 && c < p.nchunks)
+      a.d.page_gate_out[gate_row * gate_pages + c] = s.anylive ? 1 : 0;
+    if (s.anyref) {  // wave-uniform: no request at all when no key is refined
+      const rsrc_t rb = make_rsrc(a.keys.kb + in.loc.row * D, in.loc.nk * D);
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const uint32_t key = KPI * i + kslot;
+        s.kb[i] = buf_load8(rb, (bits >> (8 + i)) & 1u ? key * D + 8 * part : kOutOfRange);
+      }
+    }
+    if (s.anylive) {
+      if constexpr (V8) {
+        const rsrc_t rp = make_rsrc(a.vp + in.loc.row * D, in.loc.nk * D);
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const uint32_t key = KPI * i + kslot;
+          s.vp[i] = buf_load8(rp, (bits >> i) & 1u ? key * D + 8 * part : kOutOfRange);
+        }
+        if (__ballot((bits & 0xFF0000u) != 0) != 0) {
+          const rsrc_t rr = make_rsrc(a.vr + in.loc.row * D, in.loc.nk * D);
+#pragma unroll
+          for (int i = 0; i < NI; ++i) {
+            const uint32_t key = KPI * i + kslot;
+            s.vr[i] = buf_load8(rr, (bits >> (16 + i)) & 1u ? key * D + 8 * part : kOutOfRange);
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < NI; ++i) s.vr[i] = u32x2{0u, 0u};
+        }
+      } else {
+        const rsrc_t rv = make_rsrc(g.v + in.loc.row * D, in.loc.nk * D * 2);
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const uint32_t key = KPI * i + kslot;
+          s.vv[i] = buf_load(rv, (bits >> i) & 1u ? key * 2 * D + 16 * part : kOutOfRange);
+        }
+      }
+    }
+  }
+
+  // Refined scores, weights, L and the accumulation of chunk c.
+  __device__ __forceinline__ void finish(int c, const SC& s) {
+    const int key0 = c * kChunk;
+    float pw[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      float x = s.xc[i];
+      if (s.anyref) {
+        const float cba = group_sum<LPK>(static_cast<float>(sdot8(s.kb[i], qa)));
+        const float cbb = group_sum<LPK>(static_cast<float>(sdot8(s.kb[i], qb)));
+        if ((s.bits >> (8 + i)) & 1u) {
+          const float e = (i & 1) ? bf16_hi(s.e2[i / 2]) : bf16_lo(s.e2[i / 2]);
+          const float tb = cba + cbb * (1.0f / 256.0f);
+          x = x + (eta * e) * (tb * (1.0f / 256.0f));
+        }
+      }
+      const bool ok = (s.bits >> (24 + i)) & 1u;
+      const bool counts = ok && (DENSE || x >= a.d.neg_T);
+      const float w = ok ? exp2_fast(x) : 0.0f;
+      lsum += w;
+      if (!DENSE) lcut += counts ? 0.0f : w;
+      pw[i] = counts ? w : 0.0f;
+      if (DBG && a.d.x_out && ok && part == 0)
+        a.d.x_out[xrow * g.max_seq_len + static_cast<size_t>(key0) + KPI * i + kslot] = x;
+    }
+    if (!s.anylive) return;  // wave-uniform: no value row was read
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      float v[8];
+      if constexpr (V8) {
+        const bool rv = (s.bits >> (16 + i)) & 1u;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int wp = static_cast<int>(h == 0 ? s.vp[i].x : s.vp[i].y);
+          const int wr = static_cast<int>(h == 0 ? s.vr[i].x : s.vr[i].y);
+          const f32x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wp, 1.0f, false);
+          const f32x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wp, 1.0f, true);
+          const f32x2 r0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wr, 0.0625f, false);
+          const f32x2 r1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wr, 0.0625f, true);
+          v[4 * h + 0] = p0.x + (rv ? r0.x : 0.0f);
+          v[4 * h + 1] = p0.y + (rv ? r0.y : 0.0f);
+          v[4 * h + 2] = p1.x + (rv ? r1.x : 0.0f);
+          v[4 * h + 3] = p1.y + (rv ? r1.y : 0.0f);
+        }
+      } else {
+        v[0] = bf16_lo(s.vv[i].x), v[1] = bf16_hi(s.vv[i].x);
+        v[2] = bf16_lo(s.vv[i].y), v[3] = bf16_hi(s.vv[i].y);
+        v[4] = bf16_lo(s.vv[i].z), v[5] = bf16_hi(s.vv[i].z);
+        v[6] = bf16_lo(s.vv[i].w), v[7] = bf16_hi(s.vv[i].w);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += pw[i] * v[e];
+    }
+  }
+};
+
+// Occupancy: at a finite depth 128 registers (four waves per SIMD) hold the
+// two chunk stages without spilling, and the wider memory-level parallelism
+// is what the key-plane stream needs; dense decode keeps three waves per SIMD
+// (four would spill).  Measured on the MHA 4 x 64K-128K decode: 420 us at
+// T = 16 against 517 us at two waves per SIMD.
+template <int D, bool DENSE, bool DBG, bool V8, int W>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(DBG ? 2 : (DENSE ? 3 : 4))))
+void decode_q8_split_kernel(const Q8DecodeArgs a) {
+  using S = Q8Valu<D, DENSE, DBG, V8>;
+  const ScanGeometry& g = a.d.geo;
+  S sc(a);
+  sc.lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  sc.part = sc.lane % S::LPK;
+  sc.kslot = sc.lane / S::LPK;
+  __shared__ int order[kOrderMax];
+  sc.p = a.d.by_length ? scan_place_by_length(a.d, order) : scan_place(a.d);
+  if (sc.p.rg >= sc.p.nrows) return;  // uniform: no row
+  sc.pshift = q8_page_shift(g);
+  sc.gate_row = (static_cast<size_t>(sc.p.seq) * g.hkv + sc.p.kvh) * a.d.row_groups + sc.p.rg;
+  sc.gate_pages = (g.max_seq_len + kChunk - 1) / kChunk;
+  {
+    const RowInfo ri = row_info(g, sc.p.seq, sc.p.kvh, sc.p.rg, sc.p.nrows, sc.p.req0);
+    sc.rok = ri.ok;
+    const size_t row = static_cast<size_t>(ri.req) * g.heads + ri.head;
+    sc.xrow = row;
+    const int8_t* qp = a.qp + (ri.ok ? row : 0) * 2 * D + 8 * sc.part;
+    sc.qa = *reinterpret_cast<const u32x2*>(qp);
+    sc.qb = *reinterpret_cast<const u32x2*>(qp + D);
+    // one row per workgroup: its scalars are wave-uniform
+    auto uni = [](float v) {
+      return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
+    };
+    sc.eta = uni(ri.ok ? a.eta[row] : 0.0f);
+    sc.zr = uni(ri.ok ? a.d.z[row] : 0.0f);
+    sc.ntau = uni(ri.ok ? -a.tau[ri.req] : 0.0f);
+    sc.ntau_v = uni((V8 && ri.ok) ? -a.tau_v[ri.req] : 0.0f);
+  }
+  sc.lsum = 0.0f;
+  sc.lcut = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) sc.acc[e] = 0.0f;
+
+  // chunks of this wave: c_t = c0 + t * cstride, t < m
+  const int cstride = W * a.d.num_splits;
+  const int c0 = 4 * sc.p.split + 4 * a.d.num_splits * (wave >> 2) + (wave & 3);
+  const int m = sc.p.nchunks > c0 ? (sc.p.nchunks - c0 + cstride - 1) / cstride : 0;
+  if (m > 0) {
+    // A0 / A1: plane A of chunks t and t+1 (parity of t); S0 / S1: scored chunks
+    typename S::PA A0, A1;
+    typename S::SC S0, S1;
+    sc.load_a(c0, A0);
+    sc.load_a(c0 + cstride, A1);
+    sc.coarse(c0, A0, S0);
+    for (int t = 0; t < m; t += 2) {
+      // S0: chunk t scored (plane B / values in flight); A1: plane A of t+1
+      sc.load_a(c0 + (t + 2) * cstride, A0);
+      sc.coarse(c0 + (t + 1) * cstride, A1, S1);
+      sc.finish(c0 + t * cstride, S0);
+      if (t + 1 >= m) break;
+      // S1: chunk t+1 scored; A0: plane A of t+2
+      sc.load_a(c0 + (t + 3) * cstride, A1);
+      sc.coarse(c0 + (t + 2) * cstride, A0, S0);
+      sc.finish(c0 + (t + 1) * cstride, S1);
+    }
+  }
+
+  // Reduce over the key slots of the wave (lanes with equal `part`).
+#pragma unroll
+  for (int off = S::LPK; off < 64; off <<= 1) {
+    sc.lsum += __shfl_xor(sc.lsum, off, 64);
+    if (!DENSE) sc.lcut += __shfl_xor(sc.lcut, off, 64);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sc.acc[e] += __shfl_xor(sc.acc[e], off, 64);
+  }
+  __shared__ float red_a[W][D];
+  __shared__ float red_l[W];
+  __shared__ float red_c[W];
+  if (sc.kslot == 0) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) red_a[wave][8 * sc.part + e] = sc.acc[e];
+  }
+  if (sc.lane == 0) {
+    red_l[wave] = sc.lsum;
+    red_c[wave] = sc.lcut;
+  }
+  __syncthreads();
+  if (!sc.rok) return;
+  const size_t slot = static_cast<size_t>(a.d.slot_offset) + sc.p.split;
+  const size_t prow = slot * g.batch * g.heads + sc.xrow;
+  for (int d = threadIdx.x; d < D; d += 64 * W) {
+    float s = red_a[0][d];
+#pragma unroll
+    for (int w = 1; w < W; ++w) s += red_a[w][d];
+    if (V8) s *= a.v_scale;  // 2^e: exact
+    a.d.part_A[prow * D + d] = s;
+    if (d == 0) {
+      float l = red_l[0];
+#pragma unroll
+      for (int w = 1; w < W; ++w) l += red_l[w];
+      a.d.part_L[prow] = l;
+      if (a.d.part_Lcut) {
+        float cm = red_c[0];
+#pragma unroll
+        for (int w = 1; w < W; ++w) cm += red_c[w];
+        a.d.part_Lcut[prow] = cm;
+      }
+    }
+  }
+}
+
+template <int D, bool DENSE, bool V8>
+hipError_t launch_qs_dbg(const Q8DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
+  // four waves per workgroup: with 128-160 registers a compute unit then
+  // holds three or four workgroups (eight-wave workgroups left it one or two:
+  // 517 against 417 us at T = 16 on the MHA 4 x 64K-128K decode)
+  if (dbg)
+    hipLaunchKernelGGL((decode_q8_split_kernel<D, DENSE, true, V8, 4>), dim3(blocks), dim3(256),
+                       0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_q8_split_kernel<D, DENSE, false, V8, 4>), dim3(blocks), dim3(256),
+                       0, stream, a);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_qs(const Q8DecodeArgs& a, unsigned blocks, hipStream_t stream) {
+  const bool dbg = a.d.x_out || a.d.key_gate_out || a.d.page_gate_out || a.xc_out ||
+                   a.refine_gate_out || a.refine_v_gate_out;
+  if (a.d.dense)
+    return a.vp ? launch_qs_dbg<D, true, true>(a, dbg, blocks, stream)
+                : launch_qs_dbg<D, true, false>(a, dbg, blocks, stream);
+  return a.vp ? launch_qs_dbg<D, false, true>(a, dbg, blocks, stream)
+              : launch_qs_dbg<D, false, false>(a, dbg, blocks, stream);
+}
+
+}  // namespace
+
+// Two-plane scan of one row per kv sequence and head (read groups of one row).
+hipError_t launch_q8_decode_valu(const Q8DecodeArgs& a, int head_dim, hipStream_t stream) {
+  const long long blocks = static_cast<long long>(a.d.geo.num_seqs) * a.d.geo.hkv *
+                           a.d.num_splits * a.d.row_groups;
+  if (blocks == 0) return hipSuccess;
+  if (head_dim == 128) return launch_qs<128>(a, static_cast<unsigned>(blocks), stream);
+  if (head_dim == 64) return launch_qs<64>(a, static_cast<unsigned>(blocks), stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace fold

@@ -110,7 +110,7 @@ fold_status check_q8_view(const fold_kv_view* kv, const fold_q8_keys* keys, cons
   return FOLD_OK;
 }
 
-int q8_rows_per_group(int rows) { return rows <= 16 ? 16 : 32; }
+int q8_rows_per_group(int rows) { return rows <= 1 ? 1 : (rows <= 16 ? 16 : 32); }
 
 int rows_per_seq_of(const fold_kv_view* kv, int num_heads) {
   const int group = num_heads / kv->num_kv_heads;
@@ -798,6 +798,8 @@ fold_status fold_q8_decode_split(const fold_kv_view* kv, const fold_q8_keys* key
   a.d.rows_per_seq = rows;
   a.d.rows_per_group = gr;
   a.d.row_groups = groups;
+  a.d.by_length = (gr == 1 && !kv->row_indptr && kv->num_seqs >= 2 &&
+                   kv->num_seqs <= fold::kOrderMax) ? 1 : 0;
   a.keys = {keys->plane_a, keys->plane_b, keys->scale};
   a.qp = q->planes;
   a.eta = q->eta;

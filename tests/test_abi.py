@@ -355,6 +355,10 @@ def test_q8_row_group_queries(lib):
     assert lib.fold_q8_decode_rows_per_group(ctypes.byref(csr), ctypes.byref(q)) == 32
     assert lib.fold_q8_decode_row_groups(ctypes.byref(csr), ctypes.byref(q)) == 16
     assert lib.fold_q8_decode_row_groups(ctypes.byref(_kv(head_dim=5)), ctypes.byref(q)) == -1
+    # one row per kv sequence and head (MHA): read groups of one row
+    mha = _kv(num_kv_heads=8)
+    assert lib.fold_q8_decode_rows_per_group(ctypes.byref(mha), ctypes.byref(q)) == 1
+    assert lib.fold_q8_decode_row_groups(ctypes.byref(mha), ctypes.byref(q)) == 1
 
 
 # ------------------------------------------------------------- the step ----

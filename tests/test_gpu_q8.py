@@ -271,6 +271,17 @@ def test_q8_ragged_edge_lengths(d, group, paged):
         assert torch.isnan(res["out"][0]).all()
 
 
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("splits", [1, 3, 5])
+def test_q8_mha_ragged_longest_first(d, splits):
+    """MHA (one row per kv sequence and head: the VALU two-plane scan) over
+    ragged lengths dispatched longest first, several splits and depths."""
+    wl = make_custom(batch=5, heads=4, kv_heads=4, dim=d, lens=[2100, 1100, 2053, 0, 77],
+                     spike_count=6, n_sink=1, seed=d + splits, device="cuda")
+    for T, kappa in ((INF, 0.0), (16.0, -4.0), (6.0, 2.0)):
+        _full_parity(wl, T, kappa=kappa, splits=[splits])
+
+
 @pytest.mark.parametrize("requests,prefix,splits", [(5, 1488, (3, 2)), (3, 80, (2, 1))])
 def test_q8_cascade_stacked_rows(requests, prefix, splits):
     """Shared-prefix levels: 40 and 24 stacked rows of 8-head GQA groups in
@@ -344,9 +355,13 @@ def test_q8_front_rejects_bad_arguments():
 
 
 # ------------------------------------------------------- invariants ---------
+@pytest.mark.parametrize("cfg", [2, 4])
 @pytest.mark.parametrize("T", [INF, 16.0])
-def test_q8_debug_exports_do_not_change_results(T):
-    wl = make_config(2, batch=4, seq_len=1500, device="cuda")
+def test_q8_debug_exports_do_not_change_results(T, cfg):
+    """Config 2 (GQA, the packed scan) and config 4 shrunk (MHA, the VALU scan
+    with one row per read group)."""
+    wl = make_config(cfg, batch=4 if cfg == 2 else 3, seq_len=1500 if cfg == 2 else 3000,
+                     device="cuda")
     a, keys = _gpu_q8.run(wl, T, debug=False)
     z = a["z"].cuda()
     b, _ = _gpu_q8.run(wl, T, z=z, keys=keys, debug=True)

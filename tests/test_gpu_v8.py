@@ -169,6 +169,15 @@ def test_v8_ragged(d, group):
         _v8_parity(wl, T, splits=[2])
 
 
+@pytest.mark.parametrize("splits", [1, 4])
+def test_v8_mha_ragged_longest_first(splits):
+    """MHA with 8-bit values (the VALU two-plane scan) over ragged lengths."""
+    wl = make_custom(batch=5, heads=4, kv_heads=4, dim=128, lens=[2100, 1100, 2053, 0, 77],
+                     spike_count=6, n_sink=1, seed=40 + splits, device="cuda")
+    for T, kv in ((INF, 0.0), (16.0, -4.0), (5.0, 4.0)):
+        _v8_parity(wl, T, kappa_v=kv, splits=[splits])
+
+
 def test_v8_cascade_groups_keep_their_own_values():
     """Stacked rows of three requests share read groups: each row's second
     value plane counts only where its own GQA group set refine-V."""
@@ -192,8 +201,9 @@ def test_v8_full_refine_equals_bf16_values():
     assert err.max() < 1e-4
 
 
-def test_v8_debug_exports_do_not_change_results():
-    wl = make_config(2, batch=3, seq_len=1500, device="cuda")
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_v8_debug_exports_do_not_change_results(cfg):
+    wl = make_config(cfg, batch=3, seq_len=1500 if cfg == 2 else 3000, device="cuda")
     vals = _gpu_q8.encode_values(wl)
     a, keys = _gpu_q8.run(wl, 16.0, values=vals)
     b, _ = _gpu_q8.run(wl, 16.0, values=vals, keys=keys, z=a["z"].cuda(), debug=True)
