@@ -193,9 +193,9 @@ class Q8Path:
         # stacked level over FP16 keys written once per prefix (BF16 values)
         self.stacked = [None] * len(wl.levels)
         if not values8:
-            qv = F.q_view(wl.q)
             for i, lv in enumerate(wl.levels):
-                if F.fold_decode_rows_per_group(self.levels[i], qv) == 64:
+                reqs = lv.max_reqs_per_seq if lv.row_indptr is not None else 1
+                if reqs * wl.group > 32:  # the stacked-row threshold
                     k16 = torch.empty(self.keys.plane_a.shape, dtype=torch.float16, device=dev)
                     F.fold_q8_stack_keys(self.levels[i], self.keys, k16)
                     self.stacked[i] = F.kv_view(
