@@ -91,6 +91,13 @@ class Path:
                         and lv.num_seqs == b)
         self.arrivals = (torch.zeros(lv.num_seqs, wl.num_kv_heads, dtype=torch.int32, device=dev)
                          if self.fusable else None)
+        # a cascade whose prefix level is stacked (64-row read groups) and whose
+        # suffix level is per request: both levels in one scan launch
+        # (fold_decode_cascade), whose splits[0] slots hold both levels' pairs
+        self.one_scan = (len(wl.levels) == 2 and wl.levels[0].row_indptr is not None
+                         and wl.levels[1].row_indptr is None and wl.levels[1].num_seqs == b
+                         and F.fold_decode_rows_per_group(self.levels[0], self.qv) == 64)
+        self.slots = self.splits[0] if self.one_scan else total
 
     def step(self, T, stream):
         """One whole call: the fused launch where it applies, else the three calls."""
@@ -113,6 +120,15 @@ class Path:
         self.F.fold_ref_estimate(self.flat, self.qv, self.wl.sm_scale, self.z, stream=stream)
 
     def decode(self, T, stream):
+        if self.one_scan:
+            self.F.fold_decode_cascade(self.levels[0], self.levels[1], self.qv, self.wl.sm_scale,
+                                       self.z, T, self.slots, 0, self.part_A[:self.slots],
+                                       self.part_L[:self.slots], stream=stream)
+        else:
+            self.decode_levels(T, stream)
+
+    def decode_levels(self, T, stream):
+        """Every level's scan as its own launch."""
         off = 0
         for kv, s in zip(self.levels, self.splits):
             self.F.fold_decode_split(kv, self.qv, self.wl.sm_scale, self.z, T, s, off,
@@ -120,6 +136,13 @@ class Path:
             off += s
 
     def combine(self, stream):
+        self.F.fold_combine(self.part_A[:self.slots], self.part_L[:self.slots], self.out,
+                            stream=stream)
+
+    def level_launches(self, T, stream):
+        """The call with one scan launch per level (a cascade's alternative)."""
+        self.estimate(stream)
+        self.decode_levels(T, stream)
         self.F.fold_combine(self.part_A, self.part_L, self.out, stream=stream)
 
     def read_fraction(self, T):
@@ -509,10 +532,11 @@ def q8_leg(wl, F, torch, flush, steps, warmup, name=None, values8=False):
     return out
 
 
-def kv_bytes(wl, lam):
+def kv_bytes(wl, lam, slots=None):
     """Algorithmic bytes of one decode scan (all levels): every key row, the
     value rows the read gates keep (fraction lam of read-group key rows), the
-    query rows, references, block-table entries and partials written."""
+    query rows, references, block-table entries and partials written (`slots`
+    of them; one per split of every level unless given)."""
     d = wl.head_dim
     b, h, _ = wl.q.shape
     keys = sum(sum(lv.seq_lens_host) for lv in wl.levels) * wl.num_kv_heads
@@ -521,7 +545,7 @@ def kv_bytes(wl, lam):
     if wl.page_size:
         total += 4 * sum(sum((n + wl.page_size - 1) // wl.page_size for n in lv.seq_lens_host)
                          for lv in wl.levels)
-    total += 4 * sum(wl.level_splits) * b * h * (d + 1)
+    total += 4 * (sum(wl.level_splits) if slots is None else slots) * b * h * (d + 1)
     return total, keys
 
 
@@ -711,6 +735,25 @@ def time_variant(path, T, steps, warmup, flush, torch):
         res["step"] = res["step_three_calls"]
     torch.cuda.synchronize()
     return {k: statistics.median(v) for k, v in res.items()}, res
+
+
+def time_call(fn, T, steps, warmup, flush, torch):
+    """Median duration (ms) of one call fn(T, stream), caches evicted before
+    each, events only around it."""
+    stream = torch.cuda.current_stream()
+    ts = []
+    for it in range(warmup + steps):
+        evict_caches(flush)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn(T, stream)
+        e1.record(stream)
+        if it >= warmup:
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+    torch.cuda.synchronize()
+    return statistics.median(ts)
 
 
 def time_graph(path, T, steps, warmup, flush, torch):
@@ -991,10 +1034,13 @@ def run_workload(i, args, torch, F, make_config, flush, steps, warmup, splits=No
     for T in depths:
         lam = path.read_fraction(T)
         med, _ = time_variant(path, T, steps, warmup, flush, torch)
-        nbytes, keys = kv_bytes(wl, lam)
+        nbytes, keys = kv_bytes(wl, lam, path.slots)
         fbytes = fused_bytes(wl, lam)[0] if path.fusable else None
         out[T] = {"med": med, "lam": lam, "bytes": nbytes, "keys": keys,
-                  "fused_bytes": fbytes, "fusable": path.fusable}
+                  "fused_bytes": fbytes, "fusable": path.fusable, "one_scan": path.one_scan}
+        if path.one_scan:
+            out[T]["level_launches"] = time_call(path.level_launches, T, steps, warmup, flush,
+                                                 torch)
         progress(f"workload {i} T={T:g}: step {med['step'] * 1e3:.1f} us "
                  f"(three calls {med['step_three_calls'] * 1e3:.1f} us)")
     return wl, out
@@ -1025,6 +1071,10 @@ def depth_record(wl, v, T):
     if v["fusable"]:
         rec["fused_bytes"] = int(v["fused_bytes"])
         rec["fused_gbps"] = gbps(v["fused_bytes"], med["step"])
+    if v.get("one_scan"):
+        rec["scan"] = ("fold_decode_cascade: the prefix and suffix levels in one launch, "
+                       "their pairs in the prefix's slots")
+        rec["us_per_call_level_launches"] = round(v["level_launches"] * 1e3, 2)
     return rec
 
 

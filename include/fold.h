@@ -208,6 +208,38 @@ fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, floa
                               void* stream);
 
 /*
+ * fold_decode_cascade - both levels of a shared-prefix cascade in one scan
+ * launch (Section 4, "Value product": pairs add, so a prefix decoded once with
+ * the rows of its requests stacked and each request's own suffix may share a
+ * slot; Appendix E).
+ *   prefix   CSR view whose kv sequences carry more than 32 stacked rows each
+ *            (fold_decode_rows_per_group == 64)
+ *   suffix   per-request view (row_indptr NULL, num_seqs == q->batch) of the
+ *            requests' own keys in the same k / v pages: same k, v,
+ *            num_kv_heads, head_dim, page_size and num_pages, both paged
+ * Split s walks the prefix tiles t with t mod num_splits == s, as
+ * fold_decode_split does, and then the suffix tiles that fall to it.  For a
+ * read group of 64 stacked rows (rows 64 g .. 64 g + 63 of a prefix kv
+ * sequence and kv head), the requests those rows belong to take positions
+ * p = 0, 1, ... in row order; suffix tile u (keys 64 u .. 64 u + 63) of the
+ * request at position p is pair p * U + u, U = ceil(suffix->max_seq_len / 64),
+ * and goes to split (p * U + u) mod num_splits, weighed for that request's
+ * rows only.  Slot slot_offset + s holds the prefix split's pair plus the
+ * pairs of those suffix tiles, so fold_combine over the num_splits slots
+ * finishes the decode.  A split with no keys writes zeros.
+ *   z ... part_Lcut  as fold_decode_split (no debug exports)
+ * FOLD_E_UNSUPPORTED when the prefix is not a stacked level, the two views do
+ * not share their cache arrays and layout, or one workgroup would own more
+ * than 64 tiles (prefix tiles of its split plus its suffix tiles: raise
+ * num_splits).
+ */
+fold_status fold_decode_cascade(const fold_kv_view* prefix, const fold_kv_view* suffix,
+                                const fold_q_view* q, float sm_scale, const float* z,
+                                float depth_T, int32_t num_splits, int32_t slot_offset,
+                                int32_t num_slots, float* part_A, float* part_L,
+                                float* part_Lcut, void* stream);
+
+/*
  * fold_combine - additive combine (Algorithm 1, last step; Section 4): for
  * each row, sum the slots in increasing slot order and take the quotient
  * o = sum A / sum L.  No maximum is compared and nothing is rescaled.

@@ -171,10 +171,12 @@ struct TileW {
   uint64_t mask;
 };
 
-template <int D, bool DENSE, bool DBG, bool CX = false, bool EAGER = false, bool F16 = false>
+template <int D, bool DENSE, bool DBG, bool CX = false, bool EAGER = false, bool F16 = false,
+          bool CASC = false>
 __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const DecodeArgs a) {
   constexpr bool PIPE = DENSE || EAGER;  // the dense pipeline: values fetched with their keys
   constexpr bool DEPTH = !DENSE;         // the depth rule decides the weights
+  static_assert(!CASC || (PIPE && !DBG && !CX && !F16), "cascade: production BF16 variants");
   constexpr int NK = D / 32;          // K-dim steps of the score product
   constexpr int NB = D / 16;          // 16-channel blocks of the value product
   constexpr int KEYB = 2 * D;         // bytes per key row
@@ -202,7 +204,21 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
 
   const int S = a.num_splits;
   const int ntiles = (p.n + kTile - 1) / kTile;
-  const int m = ntiles > p.split ? (ntiles - p.split + S - 1) / S : 0;  // tiles of this split
+  const int m_pre = ntiles > p.split ? (ntiles - p.split + S - 1) / S : 0;  // tiles of this split
+  // CASC: the suffix tiles of the read group's requests follow the prefix
+  // tiles.  Pair q = position * sfx_tiles + tile, over the request positions
+  // the group's rows cover, goes to split q mod S; a suffix tile weighs only
+  // the rows of its own request (the others get Z = +inf for it).
+  int pos_lo = 0, m_sfx = 0;
+  if constexpr (CASC) {
+    const int r0 = p.rg * kStkRows;
+    const int r1 = min(r0 + kStkRows, p.nrows) - 1;
+    pos_lo = r0 / g.group;
+    const int pairs = (r1 / g.group - pos_lo + 1) * a.sfx_tiles;
+    m_sfx = pairs > p.split ? (pairs - p.split + S - 1) / S : 0;
+    if (m_pre + m_sfx > kWaveSize) return;  // uniform; the host admits no such call
+  }
+  const int m = m_pre + m_sfx;  // tiles of this workgroup
   const int my_chunk = wave / 2;  // all of a wave's DMA keys lie in this 16-key chunk of a tile
   auto chunk_of = [&](int j) { return (p.split + j * S) * (kTile / kChunk) + my_chunk; };
 
@@ -211,13 +227,38 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
   // ask for increasing tiles).
   int ptab = 0;
   int ptab_base = -kWaveSize;
+  // CASC: lane j also holds tile j's key count (bits 0-7), the read-group
+  // position of its request (bits 8-15; 255 for a prefix tile: every row) and
+  // the in-page key offset of this wave's chunk (bits 16-31).  A suffix lane
+  // first learns its request (sreq); the request's length and block-table
+  // entry follow from assembly loads (slen, sbt) and are merged in settle_sfx.
+  uint32_t tmeta = 0;
+  int sreq = -1;
+  uint32_t slen = 0, sbt = 0;
   auto load_ptab = [&](int base) {
     ptab_base = base;
     const int jj = base + lane;
     const int c = chunk_of(jj);
-    ptab = jj < m && c < p.nchunks
-               ? g.block_table[static_cast<size_t>(p.seq) * g.max_pages + (c * kChunk) / g.page_size]
-               : 0;
+    if constexpr (CASC) {
+      ptab = 0;
+      tmeta = 0;
+      if (jj < m_pre) {
+        // the tile's key count for every wave; the page only where this
+        // wave's chunk holds keys
+        const int key0 = c * kChunk;
+        const int pidx = key0 / g.page_size;
+        if (c < p.nchunks) ptab = g.block_table[static_cast<size_t>(p.seq) * g.max_pages + pidx];
+        const int t = p.split + jj * S;
+        tmeta = static_cast<uint32_t>(min(kTile, p.n - t * kTile)) | (0xFFu << 8) |
+                (static_cast<uint32_t>(key0 - pidx * g.page_size) << 16);
+      } else if (jj >= m_pre && jj < m) {
+        sreq = ld_uniform(g.row_req, p.req0 + pos_lo + (p.split + (jj - m_pre) * S) / a.sfx_tiles);
+      }
+    } else {
+      ptab = jj < m && c < p.nchunks
+                 ? g.block_table[static_cast<size_t>(p.seq) * g.max_pages + (c * kChunk) / g.page_size]
+                 : 0;
+    }
   };
   auto page_of = [&](int j) -> int {
     if (j >= m || g.page_size <= 0) return 0;
@@ -235,12 +276,56 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
   if (g.page_size > 0 && m > 0) load_ptab(0);
   const RowInfo ri = row_info(g, p.seq, p.kvh, p.rg * kStkRows + 16 * rb + n16, p.nrows, p.req0);
   const size_t qrow = static_cast<size_t>(ri.req) * g.heads + ri.head;
+  // CASC: a suffix lane's request length and block-table entry, loaded from
+  // assembly (a lane without one reads element 0); merged into the tile
+  // table once they have landed.
+  const int pos_row = (p.rg * kStkRows + 16 * rb + n16) / g.group - pos_lo;
+  int u_sfx = 0, pl_sfx = 0;  // this lane's suffix tile and request position
+  auto settle_sfx = [&]() {
+    if constexpr (CASC) {
+      asm volatile("" : "+v"(slen), "+v"(sbt) : : "memory");
+      if (lane >= m_pre && lane < m) {
+        const int n = sreq >= 0 && sreq < g.batch ? clamp_len(static_cast<int>(slen), a.sfx_cap) : 0;
+        const int key0 = u_sfx * kTile + kChunk * my_chunk;
+        const int pidx = key0 / g.page_size;
+        ptab = key0 < n ? static_cast<int>(sbt) : 0;
+        tmeta = static_cast<uint32_t>(max(0, min(kTile, n - u_sfx * kTile))) |
+                (static_cast<uint32_t>(pl_sfx) << 8) |
+                (static_cast<uint32_t>(key0 - pidx * g.page_size) << 16);
+      }
+    }
+  };
   // Block-table entries of tiles 0..4, read (and the page-table load waited
   // for) before the assembly loads below are issued; the empty asm pins that
   // order.
-  const int pg0 = page_of(0), pg1 = page_of(1), pg2 = page_of(2), pg3 = page_of(3),
+  int pg0 = page_of(0), pg1 = page_of(1), pg2 = page_of(2), pg3 = page_of(3),
             pg4 = page_of(4);
   asm volatile("" : : "s"(pg0), "s"(pg1), "s"(pg2), "s"(pg3), "s"(pg4));
+  if constexpr (CASC) {
+    const int32_t* lp = a.sfx_seq_lens;
+    const int32_t* bp = a.sfx_block_table;
+    if (lane >= m_pre && lane < m) {
+      const int qd = p.split + (lane - m_pre) * S;
+      pl_sfx = qd / a.sfx_tiles;
+      u_sfx = qd - pl_sfx * a.sfx_tiles;
+      const int pidx = (u_sfx * kTile + kChunk * my_chunk) / g.page_size;
+      if (sreq >= 0 && sreq < g.batch) {
+        lp += sreq;
+        if (pidx < a.sfx_max_pages) bp += static_cast<size_t>(sreq) * a.sfx_max_pages + pidx;
+      }
+    }
+    slen = gload4(lp);
+    sbt = gload4(bp);
+    if (m_pre < 5 && m > m_pre) {  // a suffix tile among the first five: wait here
+      wait_vmcnt<0>();
+      settle_sfx();
+      pg0 = page_of(0);
+      pg1 = page_of(1);
+      pg2 = page_of(2);
+      pg3 = page_of(3);
+      pg4 = page_of(4);
+    }
+  }
   u32x4 qb[NK];
   uint32_t zbits;
   // F16 (stacked level of a two-plane key cache): the query codes qa, qb of
@@ -324,6 +409,15 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
 
   // Buffer resource words of this wave's chunk of local tile j (K or V).
   auto chunk_words = [&](int j, int phys, bool val) -> u32x4 {
+    if constexpr (CASC) {
+      const uint32_t meta =
+          j < m ? static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(tmeta), j)) : 0u;
+      const int have = min(kChunk, static_cast<int>(meta & 0xFFu) - kChunk * my_chunk);
+      const bool ok = have > 0 && phys >= 0 && phys < g.num_pages;
+      const size_t off = ((static_cast<size_t>(ok ? phys : 0) * g.hkv + p.kvh) * g.page_size +
+                          (meta >> 16)) * D;
+      return rsrc_words((val ? g.v : g.k) + off, ok ? static_cast<uint32_t>(have) * KEYB : 0u);
+    }
     const int c = chunk_of(j);
     uint32_t bytes = 0;
     size_t off = 0;
@@ -380,7 +474,11 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
 
   // Keys of local tile j that exist (64 for every tile but a split's last
   // partial one; 0 or less past the split's end).
-  auto tile_keys = [&](int j) { return min(kTile, p.n - (p.split + j * S) * kTile); };
+  auto tile_keys = [&](int j) {
+    if constexpr (CASC)
+      return j < m ? (__builtin_amdgcn_readlane(static_cast<int>(tmeta), j) & 0xFF) : 0;
+    return min(kTile, p.n - (p.split + j * S) * kTile);
+  };
 
   // Verdicts, L and the product operands of local tile j from its scores; when
   // `need_mask`, this wave's 32-bit live mask over its key half goes to gate[].
@@ -391,6 +489,12 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
     constexpr bool FULL = decltype(full_tag)::value;
     const int key0 = (p.split + j * S) * kTile;
     const int nk = tile_keys(j);
+    float zt = zr;  // CASC: +inf for rows outside a suffix tile's request
+    if constexpr (CASC) {
+      const int code =
+          j < m ? ((__builtin_amdgcn_readlane(static_cast<int>(tmeta), j) >> 8) & 0xFF) : 0xFF;
+      zt = code == 0xFF || code == pos_row ? zr : INFINITY;
+    }
     uint32_t hb[2][4];
     float lf[2][4];
     float cc[2] = {0.0f, 0.0f};  // cut weights of this lane's keys of the half's two chunks
@@ -401,7 +505,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
       for (int i = 0; i < 4; ++i) {
         const int kk = 32 * kh + 16 * st + 4 * grp + i;
         const bool ok = FULL || (ri.ok && kk < nk);
-        const float x = __builtin_fmaf(s[st][i], sscale, -zr);
+        const float x = __builtin_fmaf(s[st][i], sscale, -zt);
         const bool live = ok && (!DEPTH || x >= a.neg_T);
         const float w = FULL ? exp2_fast(x) : (ok ? exp2_fast(x) : 0.0f);
         lsum += w;
@@ -506,6 +610,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
     // a pair whose tile i+1 does not exist
     wait_groups<NLD>(2 * issued - (issued == m ? 1 : 0));
     settle_row();  // Q and Z were issued before K0
+    if (CASC && m_pre >= 5) settle_sfx();  // so were the suffix lanes' loads
     lds_barrier();
     f32x4 s[2];
     qk(0, s);
@@ -692,7 +797,31 @@ hipError_t launch_stk_d(const DecodeArgs& a, bool dbg, unsigned blocks, hipStrea
                  : launch_stk<D, false, false>(a, dbg, blocks, stream);
 }
 
+template <int D>
+hipError_t launch_casc(const DecodeArgs& a, unsigned blocks, hipStream_t stream) {
+  if (a.dense)
+    hipLaunchKernelGGL((decode_stacked_kernel<D, true, false, false, false, false, true>),
+                       dim3(blocks), dim3(kStkThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, false, true, false, true>),
+                       dim3(blocks), dim3(kStkThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_decode_cascade(const DecodeArgs& a, int head_dim, hipStream_t stream) {
+  if (a.rows_per_group != kStkRows || a.qplanes || a.x_out || a.key_gate_out ||
+      a.page_gate_out || a.chunk_cut || a.geo.page_size <= 0 || a.sfx_tiles < 1)
+    return hipErrorInvalidValue;
+  const long long blocks = static_cast<long long>(a.geo.num_seqs) * a.geo.hkv * a.num_splits *
+                           a.row_groups;
+  if (blocks == 0) return hipSuccess;
+  const unsigned nb = static_cast<unsigned>(blocks);
+  if (head_dim == 128) return launch_casc<128>(a, nb, stream);
+  if (head_dim == 64) return launch_casc<64>(a, nb, stream);
+  return hipErrorInvalidValue;
+}
 
 hipError_t launch_decode_stacked(const DecodeArgs& a, int head_dim, hipStream_t stream) {
   if (a.rows_per_group != kStkRows) return hipErrorInvalidValue;

@@ -257,6 +257,49 @@ fold_status fold_decode_split(const fold_kv_view* kv, const fold_q_view* q, floa
   return ok();
 }
 
+fold_status fold_decode_cascade(const fold_kv_view* prefix, const fold_kv_view* suffix,
+                                const fold_q_view* q, float sm_scale, const float* z,
+                                float depth_T, int32_t num_splits, int32_t slot_offset,
+                                int32_t num_slots, float* part_A, float* part_L,
+                                float* part_Lcut, void* stream) {
+  fold::DecodeArgs a;
+  fold_status st = split_args(prefix, q, sm_scale, z, depth_T, num_splits, slot_offset, num_slots,
+                              part_A, part_L, part_Lcut, nullptr, &a);
+  if (st != FOLD_OK) return st;
+  if (!suffix) return fail(FOLD_E_INVAL, "suffix view is required");
+  fold::ScanGeometry sg;
+  st = check_view(suffix, q, &sg, true);
+  if (st != FOLD_OK) return st;
+  if (!prefix->row_indptr || a.rows_per_group != 64)
+    return fail(FOLD_E_UNSUPPORTED, "the prefix must be a CSR level of more than 32 stacked rows "
+                "per kv sequence");
+  if (suffix->row_indptr || suffix->num_seqs != q->batch)
+    return fail(FOLD_E_UNSUPPORTED, "the suffix must be a per-request view of q->batch sequences");
+  if (suffix->k != prefix->k || suffix->v != prefix->v ||
+      suffix->num_kv_heads != prefix->num_kv_heads || suffix->head_dim != prefix->head_dim ||
+      !suffix->block_table || !prefix->block_table || sg.page_size <= 0 ||
+      sg.page_size != a.geo.page_size || sg.num_pages != a.geo.num_pages)
+    return fail(FOLD_E_UNSUPPORTED, "prefix and suffix must share k, v and one paged layout");
+  const long long U = (static_cast<long long>(suffix->max_seq_len) + fold::kTile - 1) / fold::kTile;
+  if (U < 1) return fail(FOLD_E_INVAL, "suffix max_seq_len must be >= 1");
+  const long long G = a.geo.group;
+  const long long positions = std::min<long long>(63 / G + 2, prefix->max_reqs_per_seq);
+  const long long pre_tiles = (static_cast<long long>(prefix->max_seq_len) + fold::kTile - 1) / fold::kTile;
+  const long long per_wg = (pre_tiles + num_splits - 1) / num_splits +
+                           (positions * U + num_splits - 1) / num_splits;
+  if (per_wg > 64)
+    return fail(FOLD_E_UNSUPPORTED, "a workgroup would own up to %lld tiles (at most 64): raise "
+                "num_splits", per_wg);
+  a.sfx_block_table = suffix->block_table;
+  a.sfx_seq_lens = suffix->seq_lens;
+  a.sfx_max_pages = suffix->max_pages_per_seq;
+  a.sfx_cap = fold::view_capacity(sg);
+  a.sfx_tiles = static_cast<int>(U);
+  hipError_t e = fold::launch_decode_cascade(a, prefix->head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FOLD_E_HIP, "cascade launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 fold_status fold_decode_split_blocks(const fold_kv_view* kv, const fold_q_view* q,
                                      float sm_scale, const float* z, float depth_T,
                                      int32_t num_splits, int32_t slot_offset, int32_t num_slots,

@@ -61,6 +61,15 @@ struct DecodeArgs {
   // query codes and the score scale is eta per row (q is not read).
   const int8_t* qplanes = nullptr;  // [batch][heads][2][D]
   const float* qeta = nullptr;      // [batch][heads]
+  // Cascade in one scan (stacked prefix level only): the 64-key tiles of the
+  // suffixes of a read group's requests ride in the prefix workgroups, after
+  // the prefix tiles.  The suffixes are a per-request view over the same
+  // pages (request r's suffix: sfx_seq_lens[r] keys, block-table row r).
+  const int32_t* sfx_block_table = nullptr;  // [batch][sfx_max_pages]
+  const int32_t* sfx_seq_lens = nullptr;     // [batch]
+  int sfx_max_pages = 0;
+  int sfx_cap = 0;    // keys a suffix can hold
+  int sfx_tiles = 0;  // 64-key tiles of the longest suffix (0: no suffix)
 };
 
 struct EstimateArgs {
@@ -263,6 +272,9 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_q8_decode(const Q8DecodeArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_q8_front(const Q8EstimateArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_decode_fused(const FusedArgs& a, int head_dim, hipStream_t stream);
+// Prefix and suffix levels of a shared-prefix cascade in one stacked scan
+// (decode_stacked.hip); every workgroup's tiles must fit one 64-tile window.
+hipError_t launch_decode_cascade(const DecodeArgs& a, int head_dim, hipStream_t stream);
 // The library's fixed device scratch (noalloc.hip): its capacity in bytes, its
 // address on the current device (looked up once per device), and a fill
 // kernel that zeroes n int32 values of it.

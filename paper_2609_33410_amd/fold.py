@@ -39,6 +39,7 @@ EXPORTED = (
     "fold_value_block_mean",
     "fold_value_block_mean_append",
     "fold_decode_split_blocks",
+    "fold_decode_cascade",
     "fold_q8_write_keys",
     "fold_v8_write_values",
     "fold_q8_split_query",
@@ -165,6 +166,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                       ctypes.c_void_p, ctypes.c_void_p, P(fold_debug),
                                       ctypes.c_void_p]
     lib.fold_decode_split_blocks.restype = ctypes.c_int
+    lib.fold_decode_cascade.argtypes = [P(fold_kv_view), P(fold_kv_view), P(fold_q_view),
+                                        ctypes.c_float, ctypes.c_void_p, ctypes.c_float,
+                                        ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_void_p]
+    lib.fold_decode_cascade.restype = ctypes.c_int
     lib.fold_decode_split_blocks.argtypes = [P(fold_kv_view), P(fold_q_view), ctypes.c_float,
                                              ctypes.c_void_p, ctypes.c_float, ctypes.c_int32,
                                              ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
@@ -435,6 +442,28 @@ def fold_decode_split(kv: KV, q: Q, sm_scale: float, z: torch.Tensor, depth_T: f
         ctypes.byref(kv.view), ctypes.byref(q.view), sm_scale, _ptr(z), depth_T, num_splits,
         slot_offset, int(part_A.shape[0]), _ptr(part_A), _ptr(part_L), _ptr(part_Lcut),
         None if dbg is None else ctypes.byref(dbg), _stream(stream)))
+
+
+def fold_decode_cascade(prefix: KV, suffix: KV, q: Q, sm_scale: float, z: torch.Tensor,
+                        depth_T: float, num_splits: int, slot_offset: int, part_A: torch.Tensor,
+                        part_L: torch.Tensor, part_Lcut: Optional[torch.Tensor] = None,
+                        stream=None) -> None:
+    """Prefix level (stacked rows) and per-request suffix level of a cascade in
+    one scan launch; slot ``slot_offset + s`` gets split ``s`` of both."""
+    _need(z, "z", torch.float32)
+    _need(part_A, "part_A", torch.float32)
+    _need(part_L, "part_L", torch.float32)
+    if part_Lcut is not None:
+        _need(part_Lcut, "part_Lcut", torch.float32)
+    _slot_checks(q.tensor, part_A, part_L, part_Lcut, z)
+    _need_device([("q", q.tensor), ("z", z), ("part_A", part_A), ("part_L", part_L),
+                  ("part_Lcut", part_Lcut)]
+                 + [(f"prefix view tensor {i}", t) for i, t in enumerate(prefix.tensors)]
+                 + [(f"suffix view tensor {i}", t) for i, t in enumerate(suffix.tensors)])
+    _check(load_library().fold_decode_cascade(
+        ctypes.byref(prefix.view), ctypes.byref(suffix.view), ctypes.byref(q.view), sm_scale,
+        _ptr(z), depth_T, num_splits, slot_offset, int(part_A.shape[0]), _ptr(part_A),
+        _ptr(part_L), _ptr(part_Lcut), _stream(stream)))
 
 
 def block_count(max_seq_len: int) -> int:

@@ -224,6 +224,32 @@ def test_q8_stacked_rejects_bad_args(lib):
     assert call(_kv(k=FAKE + 2, **wide)) == F.FOLD_E_INVAL
 
 
+def test_cascade_rejects_bad_args(lib):
+    cd = lib.fold_decode_cascade
+    wide = dict(row_indptr=FAKE, row_req=FAKE, max_reqs_per_seq=16)  # 64 rows per sequence
+
+    def call(pre, suf, T=math.inf, z=FAKE, splits=1):
+        return cd(ctypes.byref(pre), None if suf is None else ctypes.byref(suf),
+                  ctypes.byref(_q()), 0.125, z, T, splits, 0, splits, FAKE, FAKE, None, None)
+    assert call(_kv(**wide), None) == F.FOLD_E_INVAL
+    assert call(_kv(**wide), _kv(), z=None) == F.FOLD_E_INVAL
+    assert call(_kv(**wide), _kv(), T=-1.0) == F.FOLD_E_INVAL
+    assert call(_kv(**wide), _kv(seq_lens=None)) == F.FOLD_E_INVAL
+    # the prefix must be a stacked CSR level, the suffix a per-request view
+    assert call(_kv(), _kv()) == F.FOLD_E_UNSUPPORTED
+    assert call(_kv(**wide), _kv(**wide)) == F.FOLD_E_UNSUPPORTED
+    assert call(_kv(**wide), _kv(num_seqs=1)) == F.FOLD_E_UNSUPPORTED
+    # one cache and one paged layout
+    assert call(_kv(**wide), _kv(k=FAKE + 16)) == F.FOLD_E_UNSUPPORTED
+    assert call(_kv(**wide), _kv(v=FAKE + 16)) == F.FOLD_E_UNSUPPORTED
+    assert call(_kv(**wide), _kv(page_size=32, max_pages_per_seq=2)) == F.FOLD_E_UNSUPPORTED
+    assert call(_kv(**wide), _kv(num_pages=9)) == F.FOLD_E_UNSUPPORTED
+    # at most 64 tiles per workgroup: 125 prefix tiles in one split
+    long = dict(wide, max_seq_len=8000, max_pages_per_seq=500)
+    assert call(_kv(**long), _kv()) == F.FOLD_E_UNSUPPORTED
+    assert "raise num_splits" in lib.fold_last_error().decode()
+
+
 def test_row_group_queries(lib):
     kv = _kv()
     # GQA group of 4: one matrix-core read group of 16 rows
