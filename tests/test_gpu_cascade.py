@@ -9,9 +9,10 @@ group of 64 stacked rows.  Bars: every slot's L within rtol 2e-5 (L holds
 every weight, so it does not depend on the verdicts); the output per row
 max-abs error <= 1e-2 * |o_i|_inf against the oracle's own FP64 verdicts,
 plus 2 * 2^-T * max|v| / L / |o|_inf for every key whose FP64 x lies within
-1e-4 of -T (where the kernel's FP32 verdict may differ); and the output
-against the two-launch path (fold_decode_split per level) within 1e-4 of
-|o|_inf, since only the slots' summation order differs.
+1e-4 of -T (where the kernel's FP32 verdict may differ); at finite T every
+slot's cut mass within rtol 2e-5 plus 2^(-T+1e-4) per such key; and the
+output against the two-launch path (fold_decode_split per level) within 1e-4
+of |o|_inf, since only the slots' summation order differs.
 """
 
 import dataclasses
@@ -130,7 +131,16 @@ def _check(wl, T, S, two_launch=True):
         near = _near_counts(wl, oi, z64, T)
         bound = bound + 2.0 * 2.0 ** -T * near * vmax / np.maximum(l_own, 1e-300) \
             / np.maximum(np.abs(o_own).max(axis=-1), 1e-300)
-        assert (pc >= 0).all()
+        # cut mass per slot: the oracle's per-level cut slots composed like L;
+        # a key within NEAR of -T may sit on either side (weight <= 2^-T+NEAR)
+        cuts = [oracle.decode_level(oi["q_bits"], oi["k_bits"], oi["v_bits"],
+                                    num_kv_heads=oi["num_kv_heads"], page_size=oi["page_size"],
+                                    sm_scale=oi["sm_scale"], z=z64, T=T, num_splits=s_,
+                                    with_cut=True, **lv)[2]
+                for lv, s_ in zip(oi["levels"], [S, _tiles(wl.levels[1].max_seq_len)])]
+        _, ec = _expected_slots(wl, opa, np.concatenate(cuts, axis=0), S)
+        slack = 2e-5 * ec + near[None] * 2.0 ** (-T + NEAR)
+        assert (np.abs(pc - ec) <= slack).all()
     else:
         assert (pc == 0).all()
     print(f"    max row err = {err.max():.3e}", flush=True)
