@@ -172,7 +172,7 @@ struct TileW {
 };
 
 template <int D, bool DENSE, bool DBG, bool CX = false, bool EAGER = false, bool F16 = false,
-          bool CASC = false>
+          bool CASC = false, bool LC = true>
 __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const DecodeArgs a) {
   constexpr bool PIPE = DENSE || EAGER;  // the dense pipeline: values fetched with their keys
   constexpr bool DEPTH = !DENSE;         // the depth rule decides the weights
@@ -509,7 +509,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
         const bool live = ok && (!DEPTH || x >= a.neg_T);
         const float w = FULL ? exp2_fast(x) : (ok ? exp2_fast(x) : 0.0f);
         lsum += w;
-        if (DEPTH) lcut += live ? 0.0f : w;
+        if (DEPTH && LC) lcut += live ? 0.0f : w;  // LC: the caller asked for the cut mass
         if (DEPTH && (CX || DBG)) cc[st] += live ? 0.0f : w;
         const float pw = (FULL && !DEPTH) ? w : (live ? w : 0.0f);
         hb[st][i] = __float_as_uint(pw) & 0xffff0000u;
@@ -781,9 +781,12 @@ hipError_t launch_stk(const DecodeArgs& a, bool dbg, unsigned blocks, hipStream_
     if constexpr (!F16)
       hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, true, true>), dim3(blocks),
                          dim3(kStkThreads), 0, stream, a);
-  } else {
+  } else if (a.part_Lcut) {
     hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, false, true, F16>), dim3(blocks),
                        dim3(kStkThreads), 0, stream, a);
+  } else {  // no cut mass wanted: the depth rule only selects the weights
+    hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, false, true, F16, false, false>),
+                       dim3(blocks), dim3(kStkThreads), 0, stream, a);
   }
   return hipGetLastError();
 }
@@ -802,8 +805,11 @@ hipError_t launch_casc(const DecodeArgs& a, unsigned blocks, hipStream_t stream)
   if (a.dense)
     hipLaunchKernelGGL((decode_stacked_kernel<D, true, false, false, false, false, true>),
                        dim3(blocks), dim3(kStkThreads), 0, stream, a);
-  else
+  else if (a.part_Lcut)
     hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, false, true, false, true>),
+                       dim3(blocks), dim3(kStkThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_stacked_kernel<D, false, false, false, true, false, true, false>),
                        dim3(blocks), dim3(kStkThreads), 0, stream, a);
   return hipGetLastError();
 }
