@@ -1097,7 +1097,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(every GPU box here has one GPU; the sharding of this path is design only)",
+              "(the path runs on one GPU; how it would shard is a design, not code)",
               file=sys.stderr)
         sys.exit(2)
     import torch
