@@ -189,6 +189,27 @@ def test_cascade_ragged_suffixes_and_row_order():
         _check(wl, T, 4)
 
 
+def test_cascade_two_prefix_sequences():
+    """A prefix view of two kv sequences (over the same pages) that serve two
+    disjoint request sets, one of them in permuted order: read groups and
+    request positions are per prefix sequence."""
+    wl = make_cascade(requests=12, heads=8, kv_heads=1, dim=128, prefix_len=1024,
+                      suffix_len=96, splits=(4, 1), seed=11, device="cuda")
+    dev = wl.q.device
+    pre = wl.levels[0]
+    bt = pre.block_table.expand(2, -1).contiguous()
+    indptr = torch.tensor([0, 5, 12], dtype=torch.int32, device=dev)
+    req = torch.tensor([0, 1, 2, 3, 4, 11, 6, 9, 8, 5, 10, 7], dtype=torch.int32, device=dev)
+    n = pre.seq_lens_host[0]
+    pre = dataclasses.replace(pre, block_table=bt,
+                              seq_lens=torch.tensor([n, n], dtype=torch.int32, device=dev),
+                              seq_lens_host=[n, n], row_indptr=indptr, row_req=req,
+                              max_reqs_per_seq=7)
+    wl = dataclasses.replace(wl, levels=[pre, wl.levels[1]])
+    for T in (INF, 16.0, 6.0):
+        _check(wl, T, 4)
+
+
 @pytest.mark.parametrize("T", [INF, 16.0])
 def test_cascade_workload5_full(T):
     """The 64 x (16384 + 1024)-key cascade with 32 splits: 8 prefix and 4
