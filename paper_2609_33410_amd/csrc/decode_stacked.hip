@@ -41,6 +41,13 @@
 // mass per row, the summed weights of its cut keys, is also written to
 // chunk_cut.
 //
+// CASC (fold_decode_cascade): after the prefix tiles of its split, a
+// workgroup scans the suffix tiles of its read group's requests that fall to
+// the split, through the same pipeline, and adds them to the same slot (pairs
+// add; Section 4, "Value product").  A suffix tile weighs only the rows of
+// its own request.  LC: the finite-depth cut mass is accumulated only when
+// the caller asked for it (part_Lcut).
+//
 // Pipelines.  Dense (T = inf): keys run one tile ahead of values; while the
 // product of tile t runs on the matrix cores, the weights of tile t+1 are
 // formed, and keys of t+4 / values of t+3 are in flight (four stages each).
@@ -204,7 +211,7 @@ __global__ __launch_bounds__(kStkThreads) void decode_stacked_kernel(const Decod
 
   const int S = a.num_splits;
   const int ntiles = (p.n + kTile - 1) / kTile;
-  const int m_pre = ntiles > p.split ? (ntiles - p.split + S - 1) / S : 0;  // tiles of this split
+  const int m_pre = ntiles > p.split ? (ntiles - p.split + S - 1) / S : 0;  // prefix tiles of the split
   // CASC: the suffix tiles of the read group's requests follow the prefix
   // tiles.  Pair q = position * sfx_tiles + tile, over the request positions
   // the group's rows cover, goes to split q mod S; a suffix tile weighs only
