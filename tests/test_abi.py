@@ -250,6 +250,21 @@ def test_cascade_rejects_bad_args(lib):
     assert "raise num_splits" in lib.fold_last_error().decode()
 
 
+def test_cascade_binding_checks_devices_and_slots():
+    import torch
+    t = _fused_tensors()
+    kv = F.kv_view(t["k"], t["v"], t["seq_lens"], num_kv_heads=t["k"].shape[1], max_seq_len=32,
+                   block_table=t["block_table"])
+    qv = F.q_view(t["q"])
+    b, h = t["q"].shape[:2]
+    z = torch.zeros(b, h)
+    pa, pl = torch.zeros(2, b, h, 128), torch.zeros(2, b, h)
+    with pytest.raises(ValueError):
+        F.fold_decode_cascade(kv, kv, qv, 0.1, z, 16.0, 2, 0, pa, pl[:1])
+    with pytest.raises(ValueError, match="device tensor"):
+        F.fold_decode_cascade(kv, kv, qv, 0.1, z, 16.0, 2, 0, pa, pl)
+
+
 def test_row_group_queries(lib):
     kv = _kv()
     # GQA group of 4: one matrix-core read group of 16 rows
