@@ -60,6 +60,47 @@ def test_graph_replays_match_eager(cfg, T):
 
 
 @pytest.mark.parametrize("T", [math.inf, 16.0])
+def test_graph_replays_of_the_cascade_scan(T):
+    """Estimate, the one-launch cascade scan and the combine captured in one
+    graph: every replay gives the eager bits, with eager steps in between."""
+    import paper_2609_33410_amd as F
+
+    wl = make_config(5, device="cuda", batch=8, seq_len=3000)
+    levels, flat = _gpu.kv_views(wl)
+    qv = F.q_view(wl.q)
+    b, h, d = wl.q.shape
+    s = wl.level_splits[0]
+    z = torch.empty(b, h, dtype=torch.float32, device="cuda")
+    part_a = torch.empty(s, b, h, d, dtype=torch.float32, device="cuda")
+    part_l = torch.empty(s, b, h, dtype=torch.float32, device="cuda")
+    out = torch.empty(b, h, d, dtype=torch.float32, device="cuda")
+
+    def step(stream):
+        F.fold_ref_estimate(flat, qv, wl.sm_scale, z, stream=stream)
+        F.fold_decode_cascade(levels[0], levels[1], qv, wl.sm_scale, z, T, s, 0, part_a, part_l,
+                              stream=stream)
+        F.fold_combine(part_a, part_l, out, stream=stream)
+
+    step(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    eager = out.clone()
+    assert torch.isfinite(eager).all()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(torch.cuda.current_stream())
+    for it in range(3):
+        out.fill_(float("nan"))
+        part_a.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), f"replay {it} differs from the eager step"
+        step(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager)
+
+
+@pytest.mark.parametrize("T", [math.inf, 16.0])
 def test_graph_replays_of_the_fused_call(T):
     """The one-launch decode captured in a graph: every replay gives the eager
     bits and leaves the arrival counts at zero (they reset themselves, so the
