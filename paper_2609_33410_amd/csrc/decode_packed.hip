@@ -94,7 +94,7 @@ struct PackedScan {
   float zp;          // its reference
   f32x4 acc[NB];
   float lsum, lcut;
-  float xs[4];       // packed x of the last scored step (-inf for no key); dense: its weights
+  float xs[4];       // packed weights of the last scored step entering A (0: cut or no key)
   uint32_t ms[PK];   // value-read masks of its chunks
 
   __device__ PackedScan(const DecodeArgs& a_) : a(a_), g(a_.geo) {}
@@ -181,7 +181,7 @@ struct PackedScan {
       w[i] = exp2_fast(x);
       if (!DENSE) lcut += live ? 0.0f : w[i];
       if (!DENSE && (CX || DBG)) cc += live ? 0.0f : w[i];
-      xs[i] = DENSE ? w[i] : x;  // dense: the product takes the weights as they are
+      xs[i] = live ? w[i] : 0.0f;  // the product takes these weights as they are
       bits |= live ? (1u << i) : 0u;
       if (DBG && a.x_out && ok) a.x_out[prow * g.max_seq_len + cl * kChunk + kk] = x;
     }
@@ -244,14 +244,8 @@ struct PackedScan {
     uint32_t hi[4], lo[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float pw;
-      if constexpr (DENSE) {  // the weights of the scored step (0 for no key)
-        pw = dpp_move<Q == 0 ? kDppIdentity : kDppRowShl + Q * BW, banks<0>()>(0.0f, xs[i]);
-      } else {
-        const float x = dpp_move<Q == 0 ? kDppIdentity : kDppRowShl + Q * BW, banks<0>()>(
-            -INFINITY, xs[i]);
-        pw = x >= a.neg_T ? exp2_fast(x) : 0.0f;
-      }
+      const float pw =
+          dpp_move<Q == 0 ? kDppIdentity : kDppRowShl + Q * BW, banks<0>()>(0.0f, xs[i]);
       hi[i] = __float_as_uint(pw) & 0xffff0000u;
       lo[i] = f32_to_bf16_rne(pw - __uint_as_float(hi[i]));
     }

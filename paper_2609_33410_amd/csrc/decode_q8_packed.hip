@@ -343,13 +343,8 @@ struct Q8Packed {
     float res[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float pw;
-      if constexpr (DENSE) {  // xs: the packed weights of the step (0 for no key)
-        pw = dpp_movf<from_packed<Q>(), banks<0>()>(0.0f, xs[i]);
-      } else {
-        const float x = dpp_movf<from_packed<Q>(), banks<0>()>(-INFINITY, xs[i]);
-        pw = x >= a.d.neg_T ? exp2_fast(x) : 0.0f;
-      }
+      // the packed weights entering A (0 for a cut key or none)
+      const float pw = dpp_movf<from_packed<Q>(), banks<0>()>(0.0f, xs[i]);
       hi[i] = __float_as_uint(pw) & 0xffff0000u;
       res[i] = pw - __uint_as_float(hi[i]);
     }
@@ -388,23 +383,22 @@ struct Q8Packed {
         if ((refl >> i) & 1u) x[i] = xc[i] + (etap * e[i]) * (tbp[i] * (1.0f / 256.0f));
     }
     const int cl = chunk_of(step, slot);
-    float wv[4];  // dense: the weights go to the products as they are
+    float wv[4];  // the weights entering A (0 for a cut key): the products take them as they are
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const float w = exp2_fast(x[i]);
-      wv[i] = w;
+      wv[i] = DENSE || x[i] >= a.d.neg_T ? w : 0.0f;
       lsum += w;
       if (!DENSE) lcut += x[i] >= a.d.neg_T ? 0.0f : w;
       if (DBG && a.d.x_out && ((okl >> i) & 1u))
         a.d.x_out[prow * g.max_seq_len + cl * kChunk + 4 * grp + i] = x[i];
     }
     if (anyv) {
-      const float (&pin)[4] = DENSE ? wv : x;
-      product_chunk<0>(pin, V[0], R[0]);
-      if constexpr (PK >= 2) product_chunk<1>(pin, V[1], R[1]);
+      product_chunk<0>(wv, V[0], R[0]);
+      if constexpr (PK >= 2) product_chunk<1>(wv, V[1], R[1]);
       if constexpr (PK == 4) {
-        product_chunk<2>(pin, V[2], R[2]);
-        product_chunk<3>(pin, V[3], R[3]);
+        product_chunk<2>(wv, V[2], R[2]);
+        product_chunk<3>(wv, V[3], R[3]);
       }
     }
   }
