@@ -1,7 +1,10 @@
 // The reference estimate of one (request, kv head) (Section 3, "Choosing the
-// reference"), as a device routine of four wave64s: the estimate kernel runs
-// it once per workgroup, the fused decode as the prologue of every split's
-// workgroup, so that both give Z the same bits.
+// reference"), as a device routine of NT / 64 wave64s (four by default; the
+// fused front takes eight for groups of more than four rows): the estimate
+// kernel runs it once per workgroup, the fused decode as the prologue of
+// every split's workgroup.  Each row is reduced by one wave and each 16-sample
+// tile scored by one MFMA chain, whatever the wave count, so all give Z the
+// same bits.
 //
 // The sampled keys are the first `sink` keys, the last `recent` keys and the
 // centre of each of `strata` contiguous strata of the keys in between (every
@@ -143,7 +146,7 @@ __device__ __forceinline__ float refine_threshold(float kappa, int nr) {
 // codes are the same bits), into qs / etas in LDS and, when write_out, to
 // qa8.qp_out / eta_out and the request's thresholds.  The caller puts a
 // barrier before reading qs / etas.
-template <int D>
+template <int D, int NT = kThreads>
 __device__ __forceinline__ void front_split_rows(const Q8EstimateArgs& qa8, int req, int kvh,
                                                  int8_t (*qs)[2 * D], float* etas,
                                                  bool write_out) {
@@ -151,7 +154,7 @@ __device__ __forceinline__ void front_split_rows(const Q8EstimateArgs& qa8, int 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int G = g.group;
-  for (int r = wave; r < G; r += kThreads / 64) {
+  for (int r = wave; r < G; r += NT / 64) {
     const size_t row = static_cast<size_t>(req) * g.heads + kvh * G + r;
     double x[D / 64];
 #pragma unroll
@@ -183,14 +186,14 @@ __device__ __forceinline__ void front_split_rows(const Q8EstimateArgs& qa8, int 
   }
 }
 
-// Z of the GQA rows of (req, kvh), computed by all four waves of the
+// Z of the GQA rows of (req, kvh), computed by all NT / 64 waves of the
 // workgroup (it contains barriers).  sc: the workgroup's LDS score buffer.
 // qs / etas: the LDS query codes and scales of the fused front (FRONT only).
 // Z goes to a.z_out when write_z and to z_lds[r] when z_lds is not null.
 // issued() runs once per wave of a non-empty row, right after the wave's
 // first sample loads are issued: a caller's loads issued there fly while the
 // estimate waits for its keys.
-template <int D, bool Q8, bool FRONT, typename Issued>
+template <int D, bool Q8, bool FRONT, int NT = kThreads, typename Issued>
 __device__ __forceinline__ void estimate_rows(const Q8EstimateArgs& qa8, int req, int kvh,
                                               float (*sc)[kMaxEstSamples],
                                               const int8_t (*qs)[2 * D], const float* etas,
@@ -198,7 +201,7 @@ __device__ __forceinline__ void estimate_rows(const Q8EstimateArgs& qa8, int req
   const EstimateArgs& a = qa8.e;
   constexpr int NK = Q8 ? D / 64 : D / 32;  // 16-byte key loads per lane per sample tile
   constexpr int kTilesPerPass = 4;      // sample tiles per wave whose loads fly together
-  constexpr int kScanWavesEst = kThreads / 64;
+  constexpr int kScanWavesEst = NT / 64;
   const ScanGeometry& g = a.geo;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -208,7 +211,7 @@ __device__ __forceinline__ void estimate_rows(const Q8EstimateArgs& qa8, int req
   int n = 0;
   if (req < g.num_seqs) n = clamp_len(ld_uniform(g.seq_lens, req), view_capacity(g));
   if (n == 0) {
-    for (int r = threadIdx.x; r < G; r += kThreads) {
+    for (int r = threadIdx.x; r < G; r += NT) {
       if (write_z) a.z_out[static_cast<size_t>(req) * g.heads + kvh * G + r] = 0.0f;
       if (z_lds) z_lds[r] = 0.0f;
     }
@@ -356,7 +359,7 @@ __device__ __forceinline__ void estimate_rows(const Q8EstimateArgs& qa8, int req
   constexpr int kPerLane = kMaxEstSamples / 64;
   const int nu_all = (m + 63) / 64;
   const int nu = (a.strata + 63) / 64;
-  for (int r = wave; r < G; r += kThreads / 64) {
+  for (int r = wave; r < G; r += NT / 64) {
     float mx = -INFINITY;
 #pragma unroll
     for (int u = 0; u < kPerLane; ++u) {
