@@ -19,9 +19,10 @@
 // per lane), of the BF16 values (16 bytes) or of an E4M3 value plane (8).
 //
 //   coarse   the lane's c_aa = a . qa and c_ab = a . qb by v_dot4_i32_i8,
-//            added over the key's LPK lanes in FP32 (exact: every partial and
-//            total is an integer below 2^24); xc = (eta e)(c_aa + c_ab/256)
-//            - Z in FP32.
+//            its 256 c_aa + c_ab added over the key's LPK lanes in int32
+//            (exact: below 2^30 in magnitude) and rounded to FP32 once, so
+//            the coarse logit c_aa + c_ab/256 is the FP32 sum of the two
+//            exact integer totals; xc = (eta e)(c_aa + c_ab/256) - Z in FP32.
 //   refine   plane B of refined keys only (the others get an offset past the
 //            chunk's buffer resource: no bytes move), c_ba and c_bb the same
 //            way, x = xc + [refine] (eta e)((c_ba + c_bb/256)/256).
@@ -54,6 +55,26 @@ __device__ __forceinline__ int sdot8(u32x2 a, u32x2 b) {
                                 false);
 }
 
+// c_xa + c_xb / 256 for one key, from the lane's 8 channels of a plane and of
+// the two query code vectors: 256 c_xa + c_xb is summed over the key's LANES
+// lanes in int32 (every partial is at most 8 * 128 * 128 in magnitude, so
+// the total stays below 2^30) and rounded to FP32 once.  Scaling by 256 is
+// exact, so this is the FP32 sum of the exact totals c_xa and c_xb / 256.
+template <int LANES>
+__device__ __forceinline__ float coarse_logit(u32x2 k, u32x2 qa, u32x2 qb) {
+  static_assert(LANES == 8 || LANES == 16, "a key on 8 or 16 lanes");
+  int v = __builtin_amdgcn_sdot4(static_cast<int>(k.y), static_cast<int>(qb.y),
+                                 __builtin_amdgcn_sdot4(static_cast<int>(k.x),
+                                                        static_cast<int>(qb.x),
+                                                        sdot8(k, qa) * 256, false),
+                                 false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);  // row_half_mirror
+  if constexpr (LANES == 16) v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
+  return static_cast<float>(v) * (1.0f / 256.0f);
+}
+
 template <int D>
 struct Q8VPlaneA {  // a chunk whose plane A and scales are requested
   static constexpr int NI = kChunk / (64 / (D / 8));
@@ -70,6 +91,7 @@ struct Q8VScored {  // a scored chunk whose plane-B and value rows are requested
   uint32_t bits;       // bit i: live, 8 + i: refine, 16 + i: refine-V, 24 + i: key exists
   bool anyref;         // some key of the chunk is refined (wave-uniform)
   bool anylive;        // some key of the chunk is live (wave-uniform)
+  bool anyrv;          // some key of the chunk is refine-V (wave-uniform)
   u32x2 kb[NI];        // plane B of refined keys
   u32x4 vv[V8 ? 1 : NI];   // BF16 values of live keys
   u32x2 vp[V8 ? NI : 1];   // first E4M3 plane of live keys
@@ -122,10 +144,8 @@ struct Q8Valu {
     for (int i = 0; i < NI; ++i) {
       const int kk = KPI * i + kslot;
       const bool ok = rok && kk < nk;
-      const float caa = group_sum<LPK>(static_cast<float>(sdot8(in.ka[i], qa)));
-      const float cab = group_sum<LPK>(static_cast<float>(sdot8(in.ka[i], qb)));
+      const float t = coarse_logit<LPK>(in.ka[i], qa, qb);
       const float e = bf16_lo(in.sc[i]);
-      const float t = caa + cab * (1.0f / 256.0f);
       if (i & 1)
         s.e2[i / 2] |= (in.sc[i] & 0xffffu) << 16;
       else
@@ -151,6 +171,7 @@ struct Q8Valu {
     s.bits = bits;
     s.anylive = __ballot((bits & 0xFFu) != 0) != 0;
     s.anyref = __ballot((bits & 0xFF00u) != 0) != 0;
+    s.anyrv = V8 && __ballot((bits & 0xFF0000u) != 0) != 0;
     if (DBG && a.d.page_gate_out && lane == 0 && c < p.nchunks)
       a.d.page_gate_out[gate_row * gate_pages + c] = s.anylive ? 1 : 0;
     if (s.anyref) {  // wave-uniform: no request at all when no key is refined
@@ -169,16 +190,13 @@ struct Q8Valu {
           const uint32_t key = KPI * i + kslot;
           s.vp[i] = buf_load8(rp, (bits >> i) & 1u ? key * D + 8 * part : kOutOfRange);
         }
-        if (__ballot((bits & 0xFF0000u) != 0) != 0) {
+        if (s.anyrv) {
           const rsrc_t rr = make_rsrc(a.vr + in.loc.row * D, in.loc.nk * D);
 #pragma unroll
           for (int i = 0; i < NI; ++i) {
             const uint32_t key = KPI * i + kslot;
             s.vr[i] = buf_load8(rr, (bits >> (16 + i)) & 1u ? key * D + 8 * part : kOutOfRange);
           }
-        } else {
-#pragma unroll
-          for (int i = 0; i < NI; ++i) s.vr[i] = u32x2{0u, 0u};
         }
       } else {
         const rsrc_t rv = make_rsrc(g.v + in.loc.row * D, in.loc.nk * D * 2);
@@ -199,11 +217,9 @@ struct Q8Valu {
     for (int i = 0; i < NI; ++i) {
       float x = s.xc[i];
       if (s.anyref) {
-        const float cba = group_sum<LPK>(static_cast<float>(sdot8(s.kb[i], qa)));
-        const float cbb = group_sum<LPK>(static_cast<float>(sdot8(s.kb[i], qb)));
+        const float tb = coarse_logit<LPK>(s.kb[i], qa, qb);
         if ((s.bits >> (8 + i)) & 1u) {
           const float e = (i & 1) ? bf16_hi(s.e2[i / 2]) : bf16_lo(s.e2[i / 2]);
-          const float tb = cba + cbb * (1.0f / 256.0f);
           x = x + (eta * e) * (tb * (1.0f / 256.0f));
         }
       }
@@ -217,32 +233,44 @@ struct Q8Valu {
         a.d.x_out[xrow * g.max_seq_len + static_cast<size_t>(key0) + KPI * i + kslot] = x;
     }
     if (!s.anylive) return;  // wave-uniform: no value row was read
+    if constexpr (V8) {
+      accumulate_v8(s, pw);
+    } else {
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      float v[8];
-      if constexpr (V8) {
-        const bool rv = (s.bits >> (16 + i)) & 1u;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int wp = static_cast<int>(h == 0 ? s.vp[i].x : s.vp[i].y);
-          const int wr = static_cast<int>(h == 0 ? s.vr[i].x : s.vr[i].y);
-          const f32x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wp, 1.0f, false);
-          const f32x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wp, 1.0f, true);
-          const f32x2 r0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wr, 0.0625f, false);
-          const f32x2 r1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wr, 0.0625f, true);
-          v[4 * h + 0] = p0.x + (rv ? r0.x : 0.0f);
-          v[4 * h + 1] = p0.y + (rv ? r0.y : 0.0f);
-          v[4 * h + 2] = p1.x + (rv ? r1.x : 0.0f);
-          v[4 * h + 3] = p1.y + (rv ? r1.y : 0.0f);
-        }
-      } else {
+      for (int i = 0; i < NI; ++i) {
+        float v[8];
         v[0] = bf16_lo(s.vv[i].x), v[1] = bf16_hi(s.vv[i].x);
         v[2] = bf16_lo(s.vv[i].y), v[3] = bf16_hi(s.vv[i].y);
         v[4] = bf16_lo(s.vv[i].z), v[5] = bf16_hi(s.vv[i].z);
         v[6] = bf16_lo(s.vv[i].w), v[7] = bf16_hi(s.vv[i].w);
-      }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += pw[i] * v[e];
+        for (int e = 0; e < 8; ++e) acc[e] += pw[i] * v[e];
+      }
+    }
+  }
+
+  // A += w (p + [refine-V] r / 16) over the chunk's live keys.  The second
+  // plane is widened only in chunks with a refine-V key; there a key without
+  // the bit read its plane-R bytes at an offset past the buffer, so its r is
+  // +0 and adding it changes nothing.
+  __device__ __forceinline__ void accumulate_v8(const SC& s, const float (&pw)[NI]) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int wp = static_cast<int>(h == 0 ? s.vp[i].x : s.vp[i].y);
+        const f32x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wp, 1.0f, false);
+        const f32x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wp, 1.0f, true);
+        float v[4] = {p0.x, p0.y, p1.x, p1.y};
+        if (s.anyrv) {  // wave-uniform
+          const int wr = static_cast<int>(h == 0 ? s.vr[i].x : s.vr[i].y);
+          const f32x2 r0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wr, 0.0625f, false);
+          const f32x2 r1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wr, 0.0625f, true);
+          v[0] += r0.x, v[1] += r0.y, v[2] += r1.x, v[3] += r1.y;
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[4 * h + e] += pw[i] * v[e];
+      }
     }
   }
 };
