@@ -14,9 +14,13 @@
 // 64-key tiles (wave w owns chunk w mod 4 of tiles k == w / 4 (mod W / 4);
 // W = 4 is launched);
 // for a per-request view of at most 64 sequences the longest are dispatched
-// first.  LPK = D/8 lanes hold one key, lane part p owning channels
-// 8p .. 8p+7: one wave-wide load covers KPI = 64/LPK keys of a plane (8 bytes
-// per lane), of the BF16 values (16 bytes) or of an E4M3 value plane (8).
+// first.  LPK = D/16 lanes hold one key, lane part p owning channels
+// 16p .. 16p+15 of the key planes and of the E4M3 value planes (16 bytes per
+// lane) and, with BF16 values, channels 8p .. 8p+7 and D/2 + 8p .. +7 (one
+// 16-byte load per half row, so that the key's lanes read contiguous bytes);
+// one wave-wide load covers KPI = 64/LPK keys.  Sixteen channels per lane
+// keep the lane-sum chains short: the scan is bound by instruction issue
+// more than by bytes.
 //
 //   coarse   the lane's c_aa = a . qa and c_ab = a . qb by v_dot4_i32_i8,
 //            its 256 c_aa + c_ab added over the key's LPK lanes in int32
@@ -43,64 +47,55 @@ namespace {
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ u32x2 buf_load8(rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kStreamPolicy));
+// Signed INT8 dot product of two 16-byte groups, added to acc.
+__device__ __forceinline__ int sdot16(u32x4 a, u32x4 b, int acc) {
+  acc = __builtin_amdgcn_sdot4(static_cast<int>(a.x), static_cast<int>(b.x), acc, false);
+  acc = __builtin_amdgcn_sdot4(static_cast<int>(a.y), static_cast<int>(b.y), acc, false);
+  acc = __builtin_amdgcn_sdot4(static_cast<int>(a.z), static_cast<int>(b.z), acc, false);
+  return __builtin_amdgcn_sdot4(static_cast<int>(a.w), static_cast<int>(b.w), acc, false);
 }
 
-// Signed INT8 dot product of two 8-byte groups.
-__device__ __forceinline__ int sdot8(u32x2 a, u32x2 b) {
-  return __builtin_amdgcn_sdot4(static_cast<int>(a.y), static_cast<int>(b.y),
-                                __builtin_amdgcn_sdot4(static_cast<int>(a.x), static_cast<int>(b.x),
-                                                       0, false),
-                                false);
-}
-
-// c_xa + c_xb / 256 for one key, from the lane's 8 channels of a plane and of
-// the two query code vectors: 256 c_xa + c_xb is summed over the key's LANES
-// lanes in int32 (every partial is at most 8 * 128 * 128 in magnitude, so
-// the total stays below 2^30) and rounded to FP32 once.  Scaling by 256 is
-// exact, so this is the FP32 sum of the exact totals c_xa and c_xb / 256.
+// c_xa + c_xb / 256 for one key, from the lane's 16 channels of a plane and
+// of the two query code vectors: 256 c_xa + c_xb is summed over the key's
+// LANES lanes in int32 (|c_xa|, |c_xb| <= D * 128 * 128 <= 2^21, so the total
+// stays below 2^30) and rounded to FP32 once.  Scaling by 256 is exact, so
+// this is the FP32 sum of the exact totals c_xa and c_xb / 256.
 template <int LANES>
-__device__ __forceinline__ float coarse_logit(u32x2 k, u32x2 qa, u32x2 qb) {
-  static_assert(LANES == 8 || LANES == 16, "a key on 8 or 16 lanes");
-  int v = __builtin_amdgcn_sdot4(static_cast<int>(k.y), static_cast<int>(qb.y),
-                                 __builtin_amdgcn_sdot4(static_cast<int>(k.x),
-                                                        static_cast<int>(qb.x),
-                                                        sdot8(k, qa) * 256, false),
-                                 false);
-  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
-  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
-  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);  // row_half_mirror
-  if constexpr (LANES == 16) v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
+__device__ __forceinline__ float coarse_logit(u32x4 k, u32x4 qa, u32x4 qb) {
+  static_assert(LANES == 4 || LANES == 8, "a key on 4 or 8 lanes");
+  int v = sdot16(k, qb, sdot16(k, qa, 0) * 256);
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+  if constexpr (LANES == 8) v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);  // row_half_mirror
   return static_cast<float>(v) * (1.0f / 256.0f);
 }
 
 template <int D>
 struct Q8VPlaneA {  // a chunk whose plane A and scales are requested
-  static constexpr int NI = kChunk / (64 / (D / 8));
+  static constexpr int NI = kChunk / (64 / (D / 16));
   Q8Loc loc;
-  u32x2 ka[NI];        // plane A, the lane's 8 channels of key KPI i + kslot
+  u32x4 ka[NI];        // plane A, the lane's 16 channels of key KPI i + kslot
   uint32_t sc[NI];     // its BF16 scale (low half)
 };
 
 template <int D, bool V8>
 struct Q8VScored {  // a scored chunk whose plane-B and value rows are requested
-  static constexpr int NI = kChunk / (64 / (D / 8));
+  static constexpr int NI = kChunk / (64 / (D / 16));
   float xc[NI];        // coarse score
-  uint32_t e2[NI / 2]; // the keys' BF16 scales, two per word
+  float es[NI];        // the key's scale
   uint32_t bits;       // bit i: live, 8 + i: refine, 16 + i: refine-V, 24 + i: key exists
   bool anyref;         // some key of the chunk is refined (wave-uniform)
   bool anylive;        // some key of the chunk is live (wave-uniform)
   bool anyrv;          // some key of the chunk is refine-V (wave-uniform)
-  u32x2 kb[NI];        // plane B of refined keys
-  u32x4 vv[V8 ? 1 : NI];   // BF16 values of live keys
-  u32x2 vp[V8 ? NI : 1];   // first E4M3 plane of live keys
-  u32x2 vr[V8 ? NI : 1];   // second E4M3 plane of refine-V keys
+  u32x4 kb[NI];        // plane B of refined keys
+  u32x4 vv[V8 ? 1 : NI][2];  // BF16 values of live keys (channels 8p .. +7, D/2 + 8p .. +7)
+  u32x4 vp[V8 ? NI : 1];     // first E4M3 plane of live keys
+  u32x4 vr[V8 ? NI : 1];     // second E4M3 plane of refine-V keys
 };
 
 template <int D, bool DENSE, bool DBG, bool V8>
 struct Q8Valu {
-  static constexpr int LPK = D / 8;        // lanes per key row
+  static constexpr int LPK = D / 16;       // lanes per key row
   static constexpr int KPI = 64 / LPK;     // keys per wave-wide load
   static constexpr int NI = kChunk / KPI;  // loads per lane per 16-key chunk
   using PA = Q8VPlaneA<D>;
@@ -112,11 +107,13 @@ struct Q8Valu {
   int lane, part, kslot, pshift;
   size_t gate_row;
   int gate_pages;
-  u32x2 qa, qb;  // query codes of the lane's channels
+  u32x4 qa, qb;  // query codes of the lane's channels
   float eta, zr, ntau, ntau_v;
   bool rok;
   size_t xrow;
-  float acc[8];
+  // A over the lane's channels: 16p + e (8-bit values) or, with BF16 values,
+  // 8p + e and D/2 + 8p + e (e < 8) for acc[e] and acc[8 + e]
+  float acc[16];
   float lsum, lcut;
 
   __device__ Q8Valu(const Q8DecodeArgs& a_) : a(a_), g(a_.d.geo) {}
@@ -129,7 +126,7 @@ struct Q8Valu {
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const uint32_t key = KPI * i + kslot;
-      s.ka[i] = buf_load8(ra, key * D + 8 * part);
+      s.ka[i] = buf_load(ra, key * D + 16 * part);
       s.sc[i] = buf_load2(rs, 2 * key);
     }
   }
@@ -146,10 +143,7 @@ struct Q8Valu {
       const bool ok = rok && kk < nk;
       const float t = coarse_logit<LPK>(in.ka[i], qa, qb);
       const float e = bf16_lo(in.sc[i]);
-      if (i & 1)
-        s.e2[i / 2] |= (in.sc[i] & 0xffffu) << 16;
-      else
-        s.e2[i / 2] = in.sc[i] & 0xffffu;
+      s.es[i] = e;
       const float xc = __builtin_fmaf(eta * e, t, -zr);
       s.xc[i] = xc;
       const bool live = ok && (DENSE || xc >= a.d.neg_T);
@@ -179,7 +173,7 @@ struct Q8Valu {
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const uint32_t key = KPI * i + kslot;
-        s.kb[i] = buf_load8(rb, (bits >> (8 + i)) & 1u ? key * D + 8 * part : kOutOfRange);
+        s.kb[i] = buf_load(rb, (bits >> (8 + i)) & 1u ? key * D + 16 * part : kOutOfRange);
       }
     }
     if (s.anylive) {
@@ -188,14 +182,14 @@ struct Q8Valu {
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
           const uint32_t key = KPI * i + kslot;
-          s.vp[i] = buf_load8(rp, (bits >> i) & 1u ? key * D + 8 * part : kOutOfRange);
+          s.vp[i] = buf_load(rp, (bits >> i) & 1u ? key * D + 16 * part : kOutOfRange);
         }
         if (s.anyrv) {
           const rsrc_t rr = make_rsrc(a.vr + in.loc.row * D, in.loc.nk * D);
 #pragma unroll
           for (int i = 0; i < NI; ++i) {
             const uint32_t key = KPI * i + kslot;
-            s.vr[i] = buf_load8(rr, (bits >> (16 + i)) & 1u ? key * D + 8 * part : kOutOfRange);
+            s.vr[i] = buf_load(rr, (bits >> (16 + i)) & 1u ? key * D + 16 * part : kOutOfRange);
           }
         }
       } else {
@@ -203,7 +197,11 @@ struct Q8Valu {
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
           const uint32_t key = KPI * i + kslot;
-          s.vv[i] = buf_load(rv, (bits >> i) & 1u ? key * 2 * D + 16 * part : kOutOfRange);
+          // each load reads one half of the row, 16 bytes per lane, so
+          // the key's lanes cover 8 * 16 contiguous bytes per instruction
+          const uint32_t off = (bits >> i) & 1u ? key * 2 * D + 16 * part : kOutOfRange;
+          s.vv[i][0] = buf_load(rv, off);
+          s.vv[i][1] = buf_load(rv, off + static_cast<uint32_t>(D));
         }
       }
     }
@@ -218,10 +216,7 @@ struct Q8Valu {
       float x = s.xc[i];
       if (s.anyref) {
         const float tb = coarse_logit<LPK>(s.kb[i], qa, qb);
-        if ((s.bits >> (8 + i)) & 1u) {
-          const float e = (i & 1) ? bf16_hi(s.e2[i / 2]) : bf16_lo(s.e2[i / 2]);
-          x = x + (eta * e) * (tb * (1.0f / 256.0f));
-        }
+        if ((s.bits >> (8 + i)) & 1u) x = x + (eta * s.es[i]) * (tb * (1.0f / 256.0f));
       }
       const bool ok = (s.bits >> (24 + i)) & 1u;
       const bool counts = ok && (DENSE || x >= a.d.neg_T);
@@ -238,13 +233,17 @@ struct Q8Valu {
     } else {
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
-        float v[8];
-        v[0] = bf16_lo(s.vv[i].x), v[1] = bf16_hi(s.vv[i].x);
-        v[2] = bf16_lo(s.vv[i].y), v[3] = bf16_hi(s.vv[i].y);
-        v[4] = bf16_lo(s.vv[i].z), v[5] = bf16_hi(s.vv[i].z);
-        v[6] = bf16_lo(s.vv[i].w), v[7] = bf16_hi(s.vv[i].w);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] += pw[i] * v[e];
+        for (int h = 0; h < 2; ++h) {
+          const u32x4 w = s.vv[i][h];
+          float v[8];
+          v[0] = bf16_lo(w.x), v[1] = bf16_hi(w.x);
+          v[2] = bf16_lo(w.y), v[3] = bf16_hi(w.y);
+          v[4] = bf16_lo(w.z), v[5] = bf16_hi(w.z);
+          v[6] = bf16_lo(w.w), v[7] = bf16_hi(w.w);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[8 * h + e] += pw[i] * v[e];
+        }
       }
     }
   }
@@ -257,13 +256,13 @@ struct Q8Valu {
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int wp = static_cast<int>(h == 0 ? s.vp[i].x : s.vp[i].y);
+      for (int h = 0; h < 4; ++h) {
+        const int wp = static_cast<int>(s.vp[i][h]);
         const f32x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wp, 1.0f, false);
         const f32x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wp, 1.0f, true);
         float v[4] = {p0.x, p0.y, p1.x, p1.y};
         if (s.anyrv) {  // wave-uniform
-          const int wr = static_cast<int>(h == 0 ? s.vr[i].x : s.vr[i].y);
+          const int wr = static_cast<int>(s.vr[i][h]);
           const f32x2 r0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wr, 0.0625f, false);
           const f32x2 r1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wr, 0.0625f, true);
           v[0] += r0.x, v[1] += r0.y, v[2] += r1.x, v[3] += r1.y;
@@ -275,11 +274,10 @@ struct Q8Valu {
   }
 };
 
-// Occupancy: at a finite depth 128 registers (four waves per SIMD) hold the
-// two chunk stages without spilling, and the wider memory-level parallelism
-// is what the key-plane stream needs; dense decode keeps three waves per SIMD
-// (four would spill).  Measured on the MHA 4 x 64K-128K decode: 420 us at
-// T = 16 against 517 us at two waves per SIMD.
+// Occupancy: the two chunk stages fit in 128 registers (about 120 at D = 128),
+// four waves per SIMD at every depth; with two waves per SIMD the key-plane
+// stream lacked memory-level parallelism (517 against 420 us at T = 16 on the
+// MHA 4 x 64K-128K decode, eight channels per lane).
 template <int D, bool DENSE, bool DBG, bool V8, int W>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(DBG ? 2 : (DENSE ? 3 : 4))))
 void decode_q8_split_kernel(const Q8DecodeArgs a) {
@@ -301,9 +299,9 @@ void decode_q8_split_kernel(const Q8DecodeArgs a) {
     sc.rok = ri.ok;
     const size_t row = static_cast<size_t>(ri.req) * g.heads + ri.head;
     sc.xrow = row;
-    const int8_t* qp = a.qp + (ri.ok ? row : 0) * 2 * D + 8 * sc.part;
-    sc.qa = *reinterpret_cast<const u32x2*>(qp);
-    sc.qb = *reinterpret_cast<const u32x2*>(qp + D);
+    const int8_t* qp = a.qp + (ri.ok ? row : 0) * 2 * D + 16 * sc.part;
+    sc.qa = *reinterpret_cast<const u32x4*>(qp);
+    sc.qb = *reinterpret_cast<const u32x4*>(qp + D);
     // one row per workgroup: its scalars are wave-uniform
     auto uni = [](float v) {
       return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
@@ -316,7 +314,7 @@ void decode_q8_split_kernel(const Q8DecodeArgs a) {
   sc.lsum = 0.0f;
   sc.lcut = 0.0f;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) sc.acc[e] = 0.0f;
+  for (int e = 0; e < 16; ++e) sc.acc[e] = 0.0f;
 
   // chunks of this wave: c_t = c0 + t * cstride, t < m
   const int cstride = W * a.d.num_splits;
@@ -348,14 +346,17 @@ void decode_q8_split_kernel(const Q8DecodeArgs a) {
     sc.lsum += __shfl_xor(sc.lsum, off, 64);
     if (!DENSE) sc.lcut += __shfl_xor(sc.lcut, off, 64);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) sc.acc[e] += __shfl_xor(sc.acc[e], off, 64);
+    for (int e = 0; e < 16; ++e) sc.acc[e] += __shfl_xor(sc.acc[e], off, 64);
   }
   __shared__ float red_a[W][D];
   __shared__ float red_l[W];
   __shared__ float red_c[W];
   if (sc.kslot == 0) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) red_a[wave][8 * sc.part + e] = sc.acc[e];
+    for (int e = 0; e < 16; ++e) {
+      const int ch = V8 ? 16 * sc.part + e : (e < 8 ? 8 * sc.part + e : D / 2 + 8 * sc.part + e - 8);
+      red_a[wave][ch] = sc.acc[e];
+    }
   }
   if (sc.lane == 0) {
     red_l[wave] = sc.lsum;
@@ -388,9 +389,9 @@ void decode_q8_split_kernel(const Q8DecodeArgs a) {
 
 template <int D, bool DENSE, bool V8>
 hipError_t launch_qs_dbg(const Q8DecodeArgs& a, bool dbg, unsigned blocks, hipStream_t stream) {
-  // four waves per workgroup: with 128-160 registers a compute unit then
-  // holds three or four workgroups (eight-wave workgroups left it one or two:
-  // 517 against 417 us at T = 16 on the MHA 4 x 64K-128K decode)
+  // four waves per workgroup: a compute unit then holds four workgroups
+  // (eight-wave workgroups at 135 registers left it one or two: 517 against
+  // 417 us at T = 16 on the MHA 4 x 64K-128K decode)
   if (dbg)
     hipLaunchKernelGGL((decode_q8_split_kernel<D, DENSE, true, V8, 4>), dim3(blocks), dim3(256),
                        0, stream, a);
