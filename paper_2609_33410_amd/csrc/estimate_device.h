@@ -87,36 +87,51 @@ __device__ __forceinline__ void net_stage(float& v0, float& v1, int lane) {
 
 // Ascending sort of 128 values held two per lane (element 2 lane + u): a
 // bitonic network in its mirror form, so that every comparator keeps the
-// minimum at the lower index and each block merge starts with a flip.
-__device__ __forceinline__ void sort128(float& v0, float& v1, int lane) {
-  sort_pair(v0, v1);
-  net_stage<1, true>(v0, v1, lane);
-  sort_pair(v0, v1);
-  net_stage<3, true>(v0, v1, lane);
-  net_stage<1, false>(v0, v1, lane);
-  sort_pair(v0, v1);
-  net_stage<7, true>(v0, v1, lane);
-  net_stage<2, false>(v0, v1, lane);
-  net_stage<1, false>(v0, v1, lane);
-  sort_pair(v0, v1);
-  net_stage<15, true>(v0, v1, lane);
-  net_stage<4, false>(v0, v1, lane);
-  net_stage<2, false>(v0, v1, lane);
-  net_stage<1, false>(v0, v1, lane);
-  sort_pair(v0, v1);
-  net_stage<31, true>(v0, v1, lane);
-  net_stage<8, false>(v0, v1, lane);
-  net_stage<4, false>(v0, v1, lane);
-  net_stage<2, false>(v0, v1, lane);
-  net_stage<1, false>(v0, v1, lane);
-  sort_pair(v0, v1);
-  net_stage<63, true>(v0, v1, lane);
-  net_stage<16, false>(v0, v1, lane);
-  net_stage<8, false>(v0, v1, lane);
-  net_stage<4, false>(v0, v1, lane);
-  net_stage<2, false>(v0, v1, lane);
-  net_stage<1, false>(v0, v1, lane);
-  sort_pair(v0, v1);
+// minimum at the lower index and each block merge starts with a flip.  K
+// independent rows go through each stage side by side, so that a wave
+// sorting two rows overlaps their dependency chains.
+template <int K, int L, bool FLIP>
+__device__ __forceinline__ void net_stage_k(float (&v0)[K], float (&v1)[K], int lane) {
+#pragma unroll
+  for (int k = 0; k < K; ++k) net_stage<L, FLIP>(v0[k], v1[k], lane);
+}
+
+template <int K>
+__device__ __forceinline__ void sort_pair_k(float (&v0)[K], float (&v1)[K]) {
+#pragma unroll
+  for (int k = 0; k < K; ++k) sort_pair(v0[k], v1[k]);
+}
+
+template <int K>
+__device__ __forceinline__ void sort128(float (&v0)[K], float (&v1)[K], int lane) {
+  sort_pair_k<K>(v0, v1);
+  net_stage_k<K, 1, true>(v0, v1, lane);
+  sort_pair_k<K>(v0, v1);
+  net_stage_k<K, 3, true>(v0, v1, lane);
+  net_stage_k<K, 1, false>(v0, v1, lane);
+  sort_pair_k<K>(v0, v1);
+  net_stage_k<K, 7, true>(v0, v1, lane);
+  net_stage_k<K, 2, false>(v0, v1, lane);
+  net_stage_k<K, 1, false>(v0, v1, lane);
+  sort_pair_k<K>(v0, v1);
+  net_stage_k<K, 15, true>(v0, v1, lane);
+  net_stage_k<K, 4, false>(v0, v1, lane);
+  net_stage_k<K, 2, false>(v0, v1, lane);
+  net_stage_k<K, 1, false>(v0, v1, lane);
+  sort_pair_k<K>(v0, v1);
+  net_stage_k<K, 31, true>(v0, v1, lane);
+  net_stage_k<K, 8, false>(v0, v1, lane);
+  net_stage_k<K, 4, false>(v0, v1, lane);
+  net_stage_k<K, 2, false>(v0, v1, lane);
+  net_stage_k<K, 1, false>(v0, v1, lane);
+  sort_pair_k<K>(v0, v1);
+  net_stage_k<K, 63, true>(v0, v1, lane);
+  net_stage_k<K, 16, false>(v0, v1, lane);
+  net_stage_k<K, 8, false>(v0, v1, lane);
+  net_stage_k<K, 4, false>(v0, v1, lane);
+  net_stage_k<K, 2, false>(v0, v1, lane);
+  net_stage_k<K, 1, false>(v0, v1, lane);
+  sort_pair_k<K>(v0, v1);
 }
 
 // Key index of sample t of a row of n keys (the sink, the recent keys, then
@@ -359,7 +374,90 @@ __device__ __forceinline__ void estimate_rows(const Q8EstimateArgs& qa8, int req
   constexpr int kPerLane = kMaxEstSamples / 64;
   const int nu_all = (m + 63) / 64;
   const int nu = (a.strata + 63) / 64;
-  for (int r = wave; r < G; r += NT / 64) {
+  const int nkept = a.strata - a.trim_lo - a.trim_hi;
+  // Z of K rows of this wave.  With K = 2 the two rows' independent chains
+  // run side by side; each row's operations and their order are those of a
+  // row alone, so Z has the same bits either way.  Stratified rows sort their
+  // (at most 128) centre scores across the wave, two per lane (element
+  // e = 2 * lane + u), padded with +inf; sorted positions
+  // [trim_lo, strata - trim_hi) are kept.  A fixed network: the kept
+  // multiset, hence the sum, does not depend on tie order.
+  auto rows_z = [&](auto kk, const int* rs) {
+    constexpr int K = decltype(kk)::value;
+    float mx[K], ex[K], mass[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      mx[k] = -INFINITY;
+#pragma unroll
+      for (int u = 0; u < kPerLane; ++u) {
+        const int t = lane + 64 * u;
+        if (u < nu_all && t < m) mx[k] = fmaxf(mx[k], sc[rs[k]][t]);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) mx[k] = wave_max_dpp(mx[k]);
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      ex[k] = 0.0f;
+#pragma unroll
+      for (int u = 0; u < kPerLane; ++u) {
+        const int t = lane + 64 * u;
+        if (u < nu_all && t < n_exact) ex[k] += exp2_fast(sc[rs[k]][t] - mx[k]);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) ex[k] = wave_sum_dpp(ex[k]);
+#pragma unroll
+    for (int k = 0; k < K; ++k) mass[k] = 0.0f;
+    if (stratified) {
+      float v0[K], v1[K], kept[K];
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const float* cs = &sc[rs[k]][a.sink + a.recent];
+        v0[k] = 2 * lane < a.strata ? cs[2 * lane] : INFINITY;
+        v1[k] = 2 * lane + 1 < a.strata ? cs[2 * lane + 1] : INFINITY;
+      }
+      sort128<K>(v0, v1, lane);
+      const int hi_pos = a.strata - a.trim_hi;
+      const int e0 = 2 * lane, e1 = 2 * lane + 1;
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        kept[k] = 0.0f;
+        if (e0 >= a.trim_lo && e0 < hi_pos) kept[k] += exp2_fast(v0[k] - mx[k]);
+        if (e1 >= a.trim_lo && e1 < hi_pos) kept[k] += exp2_fast(v1[k] - mx[k]);
+      }
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        kept[k] = wave_sum_dpp(kept[k]);
+        mass[k] = (static_cast<float>(rmid) / static_cast<float>(nkept)) * kept[k];
+      }
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const float z = mx[k] + log2_fast(ex[k] + mass[k]);
+        if (write_z) a.z_out[static_cast<size_t>(req) * g.heads + kvh * G + rs[k]] = z;
+        if (z_lds) z_lds[rs[k]] = z;
+      }
+    }
+  };
+  constexpr int NW = NT / 64;
+  if (!stratified || a.strata <= 128) {
+    int r = wave;
+    for (; r + NW < G; r += 2 * NW) {
+      const int rs[2] = {r, r + NW};
+      rows_z(std::integral_constant<int, 2>{}, rs);
+    }
+    if (r < G) {
+      const int rs[1] = {r};
+      rows_z(std::integral_constant<int, 1>{}, rs);
+    }
+    return;
+  }
+  // Larger stratifications: remove the trim_hi largest and the trim_lo
+  // smallest centre scores one at a time (among equal scores the lowest
+  // stratum index goes first), then add what is left.
+  for (int r = wave; r < G; r += NW) {
     float mx = -INFINITY;
 #pragma unroll
     for (int u = 0; u < kPerLane; ++u) {
@@ -374,61 +472,40 @@ __device__ __forceinline__ void estimate_rows(const Q8EstimateArgs& qa8, int req
       if (u < nu_all && t < n_exact) ex += exp2_fast(sc[r][t] - mx);
     }
     ex = wave_sum_dpp(ex);
-    float mass = 0.0f;
-    if (stratified) {
-      const float* cs = &sc[r][a.sink + a.recent];
-      float kept = 0.0f;
-      if (a.strata <= 128) {
-        // Sort the (at most 128) centre scores across the wave, two per lane
-        // (element e = 2 * lane + u), padded with +inf; sorted positions
-        // [trim_lo, strata - trim_hi) are kept.  A fixed network: the kept
-        // multiset, hence the sum, does not depend on tie order.
-        float v0 = 2 * lane < a.strata ? cs[2 * lane] : INFINITY;
-        float v1 = 2 * lane + 1 < a.strata ? cs[2 * lane + 1] : INFINITY;
-        sort128(v0, v1, lane);
-        const int hi_pos = a.strata - a.trim_hi;
-        const int e0 = 2 * lane, e1 = 2 * lane + 1;
-        if (e0 >= a.trim_lo && e0 < hi_pos) kept += exp2_fast(v0 - mx);
-        if (e1 >= a.trim_lo && e1 < hi_pos) kept += exp2_fast(v1 - mx);
-      } else {
-        // Larger stratifications: remove the trim_hi largest and the trim_lo
-        // smallest scores one at a time (among equal scores the lowest
-        // stratum index goes first), then add what is left.
-        float sv[kPerLane];
-        bool keep[kPerLane];
+    const float* cs = &sc[r][a.sink + a.recent];
+    float kept = 0.0f;
+    float sv[kPerLane];
+    bool keep[kPerLane];
 #pragma unroll
-        for (int u = 0; u < kPerLane; ++u) {
-          const int b = lane + 64 * u;
-          keep[u] = u < nu && b < a.strata;
-          sv[u] = keep[u] ? cs[b] : 0.0f;
-        }
-        for (int k = 0; k < a.trim_hi + a.trim_lo; ++k) {
-          const bool top = k < a.trim_hi;  // uniform
-          float ext = -INFINITY;
-#pragma unroll
-          for (int u = 0; u < kPerLane; ++u)
-            if (u < nu && keep[u]) ext = fmaxf(ext, top ? sv[u] : -sv[u]);
-          ext = wave_max_dpp(ext);
-          if (!top) ext = -ext;
-          bool removed = false;  // uniform
-#pragma unroll
-          for (int u = 0; u < kPerLane; ++u) {
-            if (u >= nu || removed) break;
-            const uint64_t hit = __ballot(keep[u] && sv[u] == ext);
-            if (hit) {
-              if (lane == __builtin_ctzll(hit)) keep[u] = false;
-              removed = true;
-            }
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < kPerLane; ++u)
-          if (u < nu && keep[u]) kept += exp2_fast(sv[u] - mx);
-      }
-      kept = wave_sum_dpp(kept);
-      const int nkept = a.strata - a.trim_lo - a.trim_hi;
-      mass = (static_cast<float>(rmid) / static_cast<float>(nkept)) * kept;
+    for (int u = 0; u < kPerLane; ++u) {
+      const int b = lane + 64 * u;
+      keep[u] = u < nu && b < a.strata;
+      sv[u] = keep[u] ? cs[b] : 0.0f;
     }
+    for (int k = 0; k < a.trim_hi + a.trim_lo; ++k) {
+      const bool top = k < a.trim_hi;  // uniform
+      float ext = -INFINITY;
+#pragma unroll
+      for (int u = 0; u < kPerLane; ++u)
+        if (u < nu && keep[u]) ext = fmaxf(ext, top ? sv[u] : -sv[u]);
+      ext = wave_max_dpp(ext);
+      if (!top) ext = -ext;
+      bool removed = false;  // uniform
+#pragma unroll
+      for (int u = 0; u < kPerLane; ++u) {
+        if (u >= nu || removed) break;
+        const uint64_t hit = __ballot(keep[u] && sv[u] == ext);
+        if (hit) {
+          if (lane == __builtin_ctzll(hit)) keep[u] = false;
+          removed = true;
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kPerLane; ++u)
+      if (u < nu && keep[u]) kept += exp2_fast(sv[u] - mx);
+    kept = wave_sum_dpp(kept);
+    const float mass = (static_cast<float>(rmid) / static_cast<float>(nkept)) * kept;
     if (lane == 0) {
       const float z = mx + log2_fast(ex + mass);
       if (write_z) a.z_out[static_cast<size_t>(req) * g.heads + kvh * G + r] = z;
